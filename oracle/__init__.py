@@ -1,0 +1,22 @@
+"""CPU float64 oracle of the PCPP per-patch hot path.
+
+TEST INFRASTRUCTURE ONLY: imported by the test suite, the smoke check and the
+benchmark's CPU-baseline leg, never by the library or its Python binding.
+"""
+
+from .pcpp_oracle import (  # noqa: F401
+    CTX_EPS,
+    as_f64,
+    assemble_context,
+    context_rows,
+    context_token_ids,
+    from_bf16_bits,
+    gelu,
+    geglu,
+    group_norm,
+    layer_norm,
+    linear,
+    mha,
+    partial_attention,
+    transformer_block,
+)

@@ -1,0 +1,253 @@
+"""Seeded synthetic inputs for the PCPP hot path.
+
+This module only draws numbers and lays them out; it holds none of the
+method's arithmetic (no context selection, no attention, no normalisation).
+Both the GPU path's tests and the CPU oracle consume what it returns, so it
+imports nothing else from this package and nothing from the oracle.
+
+Workload shapes follow the SDXL U-Net's self-attention layers: an image of
+R x R pixels has an R/8 latent, whose first transformer level runs on an
+(R/16) x (R/16) token grid with 640 channels (10 heads of 64) and whose
+second level runs on (R/32) x (R/32) tokens with 1280 channels (20 heads).
+The patch split follows Sec. 3.1: n row bands of height h = H/n, full width.
+
+Every tensor is drawn on the full token grid, patch by patch, from its own
+counter-keyed stream (seed, patch, tensor kind), so patch j's arrays are the
+same whichever patch is the local one.  Fresh activations are N(0, 1); the
+stale copy a neighbour holds from the previous step is fresh + sigma * N(0, 1)
+with sigma = 0.05 (the step-to-step drift the method relies on, Sec. 1).
+"""
+
+from __future__ import annotations
+
+import dataclasses
+from typing import Dict, Optional
+
+import numpy as np
+
+BASE_SEED = 2412029620
+
+DTYPE_F32 = "f32"
+DTYPE_BF16 = "bf16"
+
+
+@dataclasses.dataclass(frozen=True)
+class AttnConfig:
+    """Geometry of one partially conditioned self-attention call."""
+
+    name: str
+    H: int            # token-grid height of this layer
+    W: int            # token-grid width
+    n: int            # number of row patches
+    i: int            # 0-based local patch index (row band i, top band is 0)
+    p: float          # partial value: fraction of a neighbour's height used
+    heads: int
+    d: int            # head dim
+    dtype: str
+    seed_id: int
+    batch: int = 1
+    step: int = 0
+
+    @property
+    def C(self) -> int:
+        return self.heads * self.d
+
+    @property
+    def h(self) -> int:
+        return self.H // self.n
+
+    @property
+    def n_q(self) -> int:
+        return self.h * self.W
+
+
+@dataclasses.dataclass(frozen=True)
+class BlockConfig:
+    """One SDXL-shaped transformer block (GroupNorm, proj_in, self-attn,
+    cross-attn, GEGLU feed-forward, proj_out) around a partial self-attn."""
+
+    name: str
+    attn: AttnConfig
+    n_text: int = 77
+    text_dim: int = 2048
+    ff_inner: int = 2560
+    gn_groups: int = 32
+    seed_id: int = 5
+
+
+def _cfg(name, H, W, n, i, p, heads, d, dtype, seed_id):
+    return AttnConfig(name=name, H=H, W=W, n=n, i=i, p=p, heads=heads, d=d,
+                      dtype=dtype, seed_id=seed_id)
+
+
+# The five workloads: a tiny fp32 case, and SDXL level-1 / level-2 shapes at
+# 1024 px and 2048 px.  The 2048 px level-1 case is run at p = 0.25 and 0.5.
+ATTN_CONFIGS: Dict[str, AttnConfig] = {
+    c.name: c
+    for c in [
+        _cfg("tiny_f32", 16, 16, 4, 1, 0.25, 2, 64, DTYPE_F32, 1),
+        _cfg("sdxl1024_l1", 64, 64, 4, 1, 0.25, 10, 64, DTYPE_BF16, 2),
+        _cfg("sdxl2048_l1_p25", 128, 128, 8, 3, 0.25, 10, 64, DTYPE_BF16, 3),
+        _cfg("sdxl2048_l1_p50", 128, 128, 8, 3, 0.5, 10, 64, DTYPE_BF16, 3),
+        _cfg("sdxl2048_l2_edge", 64, 64, 8, 0, 0.25, 20, 64, DTYPE_BF16, 4),
+    ]
+}
+
+BLOCK_CONFIG = BlockConfig(
+    name="sdxl2048_block",
+    attn=_cfg("sdxl2048_block_attn", 128, 128, 8, 3, 0.25, 10, 64, DTYPE_BF16, 5),
+)
+
+# Input variants.
+#   "unit"      : Q, K, V ~ N(0,1); the kernel's 1/sqrt(d) makes logits unit-std
+#   "prescaled" : Q, K, V ~ N(0,1)/sqrt(d) as well (near-uniform softmax)
+#   "sharp"     : Q ~ 4 N(0,1) (logits four times wider)
+#   "stale_eq_fresh": no step-to-step drift (stale copies equal fresh ones)
+VARIANTS = ("unit", "prescaled", "sharp", "stale_eq_fresh")
+
+_KIND = {"q": 1, "k": 2, "v": 3, "k_drift": 4, "v_drift": 5, "q_drift": 6}
+
+
+def _stream(seed: int, *key: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, *key])))
+
+
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round to bfloat16 (round to nearest even via float32) and return the
+    16-bit patterns as uint16.  NaN inputs are not expected here."""
+    f = np.ascontiguousarray(x, dtype=np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return u.astype(np.uint16)
+
+
+def store(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Cast a float64 draw to its stored form: float32, or bf16 bit patterns."""
+    if dtype == DTYPE_F32:
+        return np.ascontiguousarray(x, dtype=np.float32)
+    if dtype == DTYPE_BF16:
+        return bf16_bits(x)
+    raise ValueError(dtype)
+
+
+def patch_tensor(cfg: AttnConfig, patch: int, kind: str, stale: bool,
+                 variant: str = "unit", seed: Optional[int] = None) -> np.ndarray:
+    """float64 [batch, h*W, C] draw of tensor `kind` ('q', 'k' or 'v') for row
+    band `patch`, fresh (this step) or stale (the previous step's copy)."""
+    if variant not in VARIANTS:
+        raise ValueError(variant)
+    s = BASE_SEED + cfg.seed_id if seed is None else seed
+    shape = (cfg.batch, cfg.h * cfg.W, cfg.C)
+    x = _stream(s, patch, _KIND[kind]).standard_normal(shape)
+    if stale and variant != "stale_eq_fresh":
+        x = x + 0.05 * _stream(s, patch, _KIND[kind + "_drift"]).standard_normal(shape)
+    if variant == "prescaled":
+        x = x / np.sqrt(cfg.d)
+    elif variant == "sharp" and kind == "q":
+        x = 4.0 * x
+    return x
+
+
+def attention_inputs(cfg: AttnConfig, variant: str = "unit",
+                     seed: Optional[int] = None) -> Dict[str, Optional[np.ndarray]]:
+    """Stored-dtype inputs of one partial-attention call on patch cfg.i.
+
+    Returns q, k_fresh, v_fresh: the local patch's fresh tensors
+    [batch, h*W, C]; k_up, v_up: the whole stale patch above (or None for the
+    top patch); k_dn, v_dn: the whole stale patch below (or None for the
+    bottom patch).  Which rows of the neighbours are read is the method's
+    business, not the generator's.
+    """
+    i = cfg.i
+    out: Dict[str, Optional[np.ndarray]] = {}
+    out["q"] = store(patch_tensor(cfg, i, "q", False, variant, seed), cfg.dtype)
+    out["k_fresh"] = store(patch_tensor(cfg, i, "k", False, variant, seed), cfg.dtype)
+    out["v_fresh"] = store(patch_tensor(cfg, i, "v", False, variant, seed), cfg.dtype)
+    for tag, j in (("up", i - 1), ("dn", i + 1)):
+        if 0 <= j < cfg.n:
+            out["k_" + tag] = store(patch_tensor(cfg, j, "k", True, variant, seed), cfg.dtype)
+            out["v_" + tag] = store(patch_tensor(cfg, j, "v", True, variant, seed), cfg.dtype)
+        else:
+            out["k_" + tag] = None
+            out["v_" + tag] = None
+    return out
+
+
+# --------------------------------------------------------------------------
+# Transformer-block inputs (random-init weights of the SDXL block shapes).
+# --------------------------------------------------------------------------
+
+BLOCK_WEIGHT_NAMES = (
+    "gn_gamma", "gn_beta",
+    "proj_in_w", "proj_in_b",
+    "ln1_gamma", "ln1_beta",
+    "attn1_qkv_w",
+    "attn1_out_w", "attn1_out_b",
+    "ln2_gamma", "ln2_beta",
+    "attn2_q_w", "attn2_kv_w",
+    "attn2_out_w", "attn2_out_b",
+    "ln3_gamma", "ln3_beta",
+    "ff1_w", "ff1_b",
+    "ff2_w", "ff2_b",
+    "proj_out_w", "proj_out_b",
+)
+
+
+def block_weight_shapes(bc: BlockConfig) -> Dict[str, tuple]:
+    C = bc.attn.C
+    F = bc.ff_inner
+    T = bc.text_dim
+    return {
+        "gn_gamma": (C,), "gn_beta": (C,),
+        "proj_in_w": (C, C), "proj_in_b": (C,),
+        "ln1_gamma": (C,), "ln1_beta": (C,),
+        # rows [0,C) = W_q, [C,2C) = W_k, [2C,3C) = W_v   (nn.Linear layout: [out, in])
+        "attn1_qkv_w": (3 * C, C),
+        "attn1_out_w": (C, C), "attn1_out_b": (C,),
+        "ln2_gamma": (C,), "ln2_beta": (C,),
+        "attn2_q_w": (C, C),
+        # rows [0,C) = W_k, [C,2C) = W_v over the text features
+        "attn2_kv_w": (2 * C, T),
+        "attn2_out_w": (C, C), "attn2_out_b": (C,),
+        "ln3_gamma": (C,), "ln3_beta": (C,),
+        # rows [0,F) = value half, [F,2F) = gate half of GEGLU
+        "ff1_w": (2 * F, C), "ff1_b": (2 * F,),
+        "ff2_w": (C, F), "ff2_b": (C,),
+        "proj_out_w": (C, C), "proj_out_b": (C,),
+    }
+
+
+def block_inputs(bc: BlockConfig = BLOCK_CONFIG, seed: Optional[int] = None,
+                 batch: int = 1) -> Dict[str, Optional[np.ndarray]]:
+    """bf16 inputs of one transformer-block call on patch bc.attn.i.
+
+    x [batch, h*W, C] ~ N(0,1); text [batch, n_text, text_dim] ~ N(0,1);
+    linear weights ~ N(0, 1/fan_in); biases ~ 0.02 N(0,1); norm scales
+    ~ 1 + 0.1 N(0,1), shifts ~ 0.1 N(0,1); the neighbours' stale K and V
+    (whole patches above / below, [batch, h*W, C]) ~ N(0,1), the scale of the
+    block's own K/V projections of a layer-normed input.
+    """
+    cfg = bc.attn
+    s = BASE_SEED + bc.seed_id if seed is None else seed
+    C = cfg.C
+    nq = cfg.h * cfg.W
+    out: Dict[str, Optional[np.ndarray]] = {}
+    out["x"] = bf16_bits(_stream(s, 100).standard_normal((batch, nq, C)))
+    out["text"] = bf16_bits(_stream(s, 101).standard_normal((batch, bc.n_text, bc.text_dim)))
+    for idx, (name, shape) in enumerate(block_weight_shapes(bc).items()):
+        g = _stream(s, 200 + idx)
+        if name.endswith("_w"):
+            w = g.standard_normal(shape) / np.sqrt(shape[1])
+        elif name.endswith("_b") or name.endswith("_beta"):
+            w = (0.02 if name.endswith("_b") else 0.1) * g.standard_normal(shape)
+        else:  # *_gamma
+            w = 1.0 + 0.1 * g.standard_normal(shape)
+        out[name] = bf16_bits(w)
+    for tag, j, key in (("up", cfg.i - 1, 300), ("dn", cfg.i + 1, 310)):
+        if 0 <= j < cfg.n:
+            out["k_" + tag] = bf16_bits(_stream(s, key).standard_normal((batch, nq, C)))
+            out["v_" + tag] = bf16_bits(_stream(s, key + 1).standard_normal((batch, nq, C)))
+        else:
+            out["k_" + tag] = None
+            out["v_" + tag] = None
+    return out

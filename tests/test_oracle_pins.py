@@ -1,0 +1,306 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics,
+not by the oracle itself (CPU only).
+
+  P1  Eq. 1 index set: brute force from the three cases, exact rationals
+  P2  attention for any p: torch's scaled_dot_product_attention in float64
+      over the brute-force-gathered context
+  P3  p = 0: patch-local attention
+  P4  p = 1 with stale == fresh: full-image attention restricted to the
+      patch (n <= 3) / attention over the fresh three-band window (n >= 4)
+  P5  softmax rows sum to one; joint K/V permutation invariance
+  P7  Q = 0 gives the mean of V; constant V; a single key
+  P8  stale rows outside the window cannot reach the output
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+from paper_2412_02962_amd import synth
+from tests.oracle_pins_util import eq1_token_ids_brute, full_grid
+
+
+def _sdpa_torch(q, k, v, heads):
+    """torch float64 SDPA on [B, N, C] arrays (library routine)."""
+    B, nq, C = q.shape
+    d = C // heads
+
+    def split(x):
+        return torch.from_numpy(x).reshape(B, x.shape[1], heads, d).permute(0, 2, 1, 3)
+
+    o = F.scaled_dot_product_attention(split(q), split(k), split(v))
+    return o.permute(0, 2, 1, 3).reshape(B, nq, C).numpy()
+
+
+def _small_cfg(H=16, W=8, n=4, i=1, p=0.25, heads=2, d=16, seed_id=11):
+    return synth.AttnConfig(name="pin", H=H, W=W, n=n, i=i, p=p, heads=heads, d=d,
+                            dtype="f32", seed_id=seed_id)
+
+
+def _inputs64(cfg, variant="unit"):
+    i = cfg.i
+    g = {
+        "q": synth.patch_tensor(cfg, i, "q", False, variant),
+        "k_fresh": synth.patch_tensor(cfg, i, "k", False, variant),
+        "v_fresh": synth.patch_tensor(cfg, i, "v", False, variant),
+    }
+    for tag, j in (("up", i - 1), ("dn", i + 1)):
+        if 0 <= j < cfg.n:
+            g["k_" + tag] = synth.patch_tensor(cfg, j, "k", True, variant)
+            g["v_" + tag] = synth.patch_tensor(cfg, j, "v", True, variant)
+        else:
+            g["k_" + tag] = None
+            g["v_" + tag] = None
+    return g
+
+
+def _oracle(cfg, g, **kw):
+    return oracle.partial_attention(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads,
+                                    g["q"], g["k_fresh"], g["v_fresh"], g["k_up"],
+                                    g["v_up"], g["k_dn"], g["v_dn"], **kw)
+
+
+# ----------------------------------------------------------------- P1 ------
+
+def test_p1_index_set_brute_force_grid():
+    ps = [round(0.05 * k, 2) for k in range(21)]
+    for H in (1, 2, 4, 8, 12, 16, 24, 32, 40, 64):
+        for n in range(1, 9):
+            if H % n:
+                continue
+            for i in range(n):
+                for p in ps:
+                    W = 3
+                    got = oracle.context_token_ids(H, W, n, i, p)
+                    want = eq1_token_ids_brute(H, W, n, i, p)
+                    assert np.array_equal(got, want), (H, n, i, p)
+
+
+def test_p1_non_integer_rows_follow_floor():
+    # p*h fractional: p = 0.3 and 0.8 (the paper's values) at h = 32, 16, 30
+    for p in (0.3, 0.8, 0.29, 0.33):
+        for h in (16, 30, 32, 100):
+            n = 4
+            got = oracle.context_token_ids(h * n, 2, n, 1, p)
+            want = eq1_token_ids_brute(h * n, 2, n, 1, p)
+            assert np.array_equal(got, want), (p, h)
+
+
+def test_p1_closed_form_context_sizes():
+    want = {"tiny_f32": (4, 1, 1, 96), "sdxl1024_l1": (16, 4, 4, 1536),
+            "sdxl2048_l1_p25": (16, 4, 4, 3072), "sdxl2048_l1_p50": (16, 8, 8, 4096),
+            "sdxl2048_l2_edge": (8, 0, 2, 640)}
+    for name, (h, up, dn, nkv) in want.items():
+        c = synth.ATTN_CONFIGS[name]
+        hh, u, dd, rows = oracle.context_rows(c.H, c.n, c.i, c.p)
+        assert (hh, u, dd, rows * c.W) == (h, up, dn, nkv), name
+
+
+@pytest.mark.parametrize("bad", [
+    dict(H=10, n=4, i=0, p=0.5),      # H not a multiple of n
+    dict(H=8, n=4, i=4, p=0.5),       # patch index out of range
+    dict(H=8, n=4, i=-1, p=0.5),
+    dict(H=8, n=4, i=0, p=-0.01),     # p outside [0, 1]
+    dict(H=8, n=4, i=0, p=1.01),
+    dict(H=8, n=4, i=0, p=float("nan")),
+    dict(H=8, n=0, i=0, p=0.5),
+])
+def test_p1_rejects_bad_geometry(bad):
+    with pytest.raises(ValueError):
+        oracle.context_rows(**bad)
+
+
+def test_p1_assembled_rows_come_from_the_right_bands():
+    cfg = _small_cfg(H=16, W=4, n=4, i=2, p=0.5)
+    # tag each token with its global id so the assembled context reveals origin
+    h, W = cfg.h, cfg.W
+    ids = np.arange(cfg.H * W, dtype=np.float64)
+    band = lambda j: ids[j * h * W:(j + 1) * h * W].reshape(1, -1, 1)
+    kc = oracle.assemble_context(cfg.H, W, cfg.n, cfg.i, cfg.p, band(2), band(1), band(3))
+    want = eq1_token_ids_brute(cfg.H, W, cfg.n, cfg.i, cfg.p)
+    assert np.array_equal(kc.reshape(-1).astype(np.int64), want)
+
+
+# ----------------------------------------------------------------- P2 ------
+
+@pytest.mark.parametrize("geo", [
+    dict(H=16, W=8, n=4, i=1, p=0.25),
+    dict(H=16, W=8, n=4, i=0, p=0.5),
+    dict(H=16, W=8, n=4, i=3, p=0.75),
+    dict(H=12, W=5, n=3, i=1, p=1.0),
+    dict(H=8, W=6, n=2, i=1, p=0.3),
+    dict(H=9, W=7, n=1, i=0, p=0.5),
+])
+@pytest.mark.parametrize("variant", ["unit", "sharp"])
+def test_p2_matches_library_sdpa_on_brute_force_context(geo, variant):
+    cfg = _small_cfg(**geo)
+    g = _inputs64(cfg, variant)
+    got = _oracle(cfg, g)
+    kfull = full_grid(cfg, "k", cfg.i, variant, synth)
+    vfull = full_grid(cfg, "v", cfg.i, variant, synth)
+    ids = eq1_token_ids_brute(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p)
+    want = _sdpa_torch(g["q"], kfull[:, ids], vfull[:, ids], cfg.heads)
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-12)
+
+
+def test_p2_batch_entries_are_independent():
+    cfg = synth.AttnConfig(name="pinb", H=8, W=4, n=2, i=0, p=0.5, heads=2, d=8,
+                           dtype="f32", seed_id=12, batch=3)
+    g = _inputs64(cfg)
+    got = _oracle(cfg, g)
+    for b in range(3):
+        gb = {k: (None if v is None else v[b:b + 1]) for k, v in g.items()}
+        np.testing.assert_allclose(_oracle(cfg, gb), got[b:b + 1], rtol=0, atol=1e-14)
+
+
+# ----------------------------------------------------------------- P3 ------
+
+@pytest.mark.parametrize("i", [0, 1, 3])
+def test_p3_p0_is_patch_local_attention(i):
+    cfg = _small_cfg(i=i, p=0.0)
+    g = _inputs64(cfg)
+    got = _oracle(cfg, g)
+    want = _sdpa_torch(g["q"], g["k_fresh"], g["v_fresh"], cfg.heads)
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-12)
+
+
+# ----------------------------------------------------------------- P4 ------
+
+@pytest.mark.parametrize("n,i", [(2, 0), (2, 1), (3, 1), (3, 0)])
+def test_p4_full_context_small_n_is_full_image_attention(n, i):
+    cfg = _small_cfg(H=12 if n == 3 else 8, W=5, n=n, i=i, p=1.0)
+    g = _inputs64(cfg, "stale_eq_fresh")
+    got = _oracle(cfg, g)
+    kfull = full_grid(cfg, "k", cfg.i, "stale_eq_fresh", synth)
+    vfull = full_grid(cfg, "v", cfg.i, "stale_eq_fresh", synth)
+    qfull = full_grid(cfg, "q", cfg.i, "stale_eq_fresh", synth)
+    full_out = _sdpa_torch(qfull, kfull, vfull, cfg.heads)
+    rows = slice(i * cfg.h * cfg.W, (i + 1) * cfg.h * cfg.W)
+    if (n == 3 and i == 0):
+        # the top patch of three sees only bands 0 and 1: not the full image
+        assert not np.allclose(got, full_out[:, rows], atol=1e-6)
+    else:
+        np.testing.assert_allclose(got, full_out[:, rows], rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("i", [1, 2, 4])
+def test_p4_full_context_large_n_is_three_band_window(i):
+    cfg = _small_cfg(H=24, W=4, n=6, i=i, p=1.0)
+    g = _inputs64(cfg, "stale_eq_fresh")
+    got = _oracle(cfg, g)
+    kfull = full_grid(cfg, "k", cfg.i, "stale_eq_fresh", synth)
+    vfull = full_grid(cfg, "v", cfg.i, "stale_eq_fresh", synth)
+    win = slice((i - 1) * cfg.h * cfg.W, (i + 2) * cfg.h * cfg.W)
+    want = _sdpa_torch(g["q"], kfull[:, win], vfull[:, win], cfg.heads)
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-12)
+
+
+def test_n1_is_full_image_attention():
+    # warm-up steps attend to the whole image: the one-patch case
+    cfg = _small_cfg(H=8, W=8, n=1, i=0, p=0.7)
+    g = _inputs64(cfg)
+    want = _sdpa_torch(g["q"], g["k_fresh"], g["v_fresh"], cfg.heads)
+    np.testing.assert_allclose(_oracle(cfg, g), want, rtol=0, atol=1e-12)
+
+
+# ----------------------------------------------------------------- P5 ------
+
+def test_p5_softmax_rows_sum_to_one():
+    cfg = _small_cfg(p=0.5)
+    g = _inputs64(cfg, "sharp")
+    _, probs = _oracle(cfg, g, return_probs=True)
+    assert np.all(probs >= 0)
+    np.testing.assert_allclose(probs.sum(axis=-1), 1.0, rtol=0, atol=1e-12)
+
+
+def test_p5_kv_permutation_invariance():
+    cfg = _small_cfg(p=0.75, i=2)
+    g = _inputs64(cfg)
+    kc = oracle.assemble_context(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, g["k_fresh"], g["k_up"], g["k_dn"])
+    vc = oracle.assemble_context(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, g["v_fresh"], g["v_up"], g["v_dn"])
+    perm = np.random.default_rng(0).permutation(kc.shape[1])
+    a = oracle.mha(g["q"], kc, vc, cfg.heads)
+    b = oracle.mha(g["q"], kc[:, perm], vc[:, perm], cfg.heads)
+    np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
+    # and a wrong pairing (K permuted alone) must change the result
+    c = oracle.mha(g["q"], kc[:, perm], vc, cfg.heads)
+    assert np.abs(a - c).max() > 1e-3
+
+
+# ----------------------------------------------------------------- P7 ------
+
+def test_p7_zero_query_gives_mean_of_context_values():
+    cfg = _small_cfg(p=0.5, i=1)
+    g = _inputs64(cfg)
+    g["q"] = np.zeros_like(g["q"])
+    vc = oracle.assemble_context(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, g["v_fresh"], g["v_up"], g["v_dn"])
+    got = _oracle(cfg, g)
+    want = np.broadcast_to(vc.mean(axis=1, keepdims=True), got.shape)
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-13)
+
+
+def test_p7_constant_values_pass_through():
+    cfg = _small_cfg(p=0.5, i=2)
+    g = _inputs64(cfg, "sharp")
+    const = np.linspace(-2, 3, cfg.C)
+    for key in ("v_fresh", "v_up", "v_dn"):
+        g[key] = np.broadcast_to(const, g[key].shape).copy()
+    got = _oracle(cfg, g)
+    np.testing.assert_allclose(got, np.broadcast_to(const, got.shape), rtol=0, atol=1e-13)
+
+
+def test_p7_single_key_returns_its_value():
+    cfg = synth.AttnConfig(name="one", H=1, W=1, n=1, i=0, p=0.0, heads=2, d=4, dtype="f32", seed_id=13)
+    g = _inputs64(cfg)
+    np.testing.assert_allclose(_oracle(cfg, g), g["v_fresh"], rtol=0, atol=0)
+
+
+# ----------------------------------------------------------------- P8 ------
+
+def test_p8_stale_rows_outside_window_are_never_read():
+    cfg = _small_cfg(H=16, W=4, n=4, i=1, p=0.25)
+    g = _inputs64(cfg)
+    ref = _oracle(cfg, g)
+    h, W = cfg.h, cfg.W
+    r = 1
+    poisoned = {k: (None if v is None else v.copy()) for k, v in g.items()}
+    # patch above: only its last r rows are context; poison the rest
+    poisoned["k_up"][:, :(h - r) * W] = np.nan
+    poisoned["v_up"][:, :(h - r) * W] = np.nan
+    # patch below: only its first r rows are context
+    poisoned["k_dn"][:, r * W:] = np.nan
+    poisoned["v_dn"][:, r * W:] = np.nan
+    got = _oracle(cfg, poisoned)
+    assert np.array_equal(got, ref)
+
+
+def test_p8_stale_rows_inside_window_are_read():
+    cfg = _small_cfg(H=16, W=4, n=4, i=1, p=0.25)
+    g = _inputs64(cfg)
+    ref = _oracle(cfg, g)
+    h, W = cfg.h, cfg.W
+    for key, row in (("v_up", h - 1), ("v_dn", 0), ("k_up", h - 1), ("k_dn", 0)):
+        gg = {k: (None if v is None else v.copy()) for k, v in g.items()}
+        gg[key][:, row * W:(row + 1) * W] += 1.0
+        assert np.abs(_oracle(cfg, gg) - ref).max() > 1e-4, key
+
+
+def test_bf16_widening_is_exact():
+    vals = np.array([0.0, -0.0, 1.0, -2.5, 3.140625, 1e-30, 65280.0, -2.0 ** -126])
+    bits = synth.bf16_bits(vals)
+    back = oracle.from_bf16_bits(bits)
+    # every value above is representable in bf16 except 1e-30, which rounds
+    exact = np.array([True, True, True, True, True, False, True, True])
+    assert np.array_equal(back[exact], vals[exact])
+    assert abs(back[5] - 1e-30) / 1e-30 < 2 ** -8
+    # widening agrees with torch's bfloat16 -> float64 conversion
+    t = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(t, back)
+    # rounding is to nearest even, as torch's float32 -> bfloat16 cast
+    x = np.random.default_rng(1).standard_normal(10000) * 10
+    tb = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(synth.bf16_bits(x), tb)
