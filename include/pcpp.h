@@ -1,0 +1,225 @@
+/*
+ * pcpp.h - C ABI of the PCPP per-patch hot path on AMD Instinct MI355X (gfx950).
+ *
+ * Partially Conditioned Patch Parallelism (arXiv 2412.02962) splits the
+ * H x W latent feature map into n horizontal bands of h = H/n rows (Sec. 3.1)
+ * and runs each band on its own device.  In every self-attention layer the
+ * band's queries attend to its own fresh keys/values plus the stale keys and
+ * values (previous diffusion step) of only the boundary rows of its two
+ * neighbours: the lower p*h rows of the band above and the upper p*h rows of
+ * the band below (Eq. 1, Sec. 3.3, Fig. 3).  This library computes one
+ * device's share of that work for one band; the neighbours' stale tensors are
+ * inputs supplied by the caller.
+ *
+ * Conventions shared by every entry point
+ *   - Tensors are row-major and contiguous.  Token tensors are [B, N, C] with
+ *     C = heads * head_dim; head a owns channels [a*head_dim, (a+1)*head_dim).
+ *     Tokens of a band are ordered row by row (token = row * W + col).
+ *   - Tensor pointers are DEVICE pointers owned by the caller.  The library
+ *     never frees, retains or writes through an input pointer, and holds no
+ *     global mutable state.
+ *   - Neighbour buffers hold the WHOLE neighbouring band, [B, h*W, C], as
+ *     received from that neighbour; only its boundary rows are read.  A
+ *     missing neighbour (top or bottom band) or a zero row count allows NULL.
+ *   - `stream` is a hipStream_t passed as void* (NULL = default stream).
+ *     Compute entry points are asynchronous: they validate, enqueue kernels
+ *     and return.  The caller must not modify inputs, and must not read
+ *     outputs, before the stream has passed the call.
+ *   - Return value: PCPP_OK (0) or a negative PCPP_E* code.  Every argument
+ *     is validated before anything is enqueued; on an error nothing is
+ *     launched and no output is touched.  No exception crosses the ABI.
+ *   - Element types: PCPP_DTYPE_BF16 (bfloat16 storage, float32
+ *     accumulation) or PCPP_DTYPE_F32 (float32 throughout).
+ */
+#ifndef PCPP_H
+#define PCPP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PCPP_VERSION 1
+
+/* Status codes. */
+#define PCPP_OK          0
+#define PCPP_EINVAL     -1   /* bad geometry, p outside [0,1] or NaN, NULL where data is needed */
+#define PCPP_ENOTSUP    -2   /* head_dim or dtype the kernels do not implement */
+#define PCPP_EWORKSPACE -3   /* workspace missing or smaller than *_workspace_size() */
+#define PCPP_EHIP       -4   /* a HIP runtime call or kernel launch failed */
+
+/* Element types. */
+#define PCPP_DTYPE_F32  0
+#define PCPP_DTYPE_BF16 1
+
+/*
+ * Geometry of one self-attention layer on one band (Sec. 3.1).
+ *   H, W       token grid of this layer (H rows, W columns), H % n_patches == 0
+ *   n_patches  number of bands n >= 1; n = 1 is full-image attention, the
+ *              synchronous warm-up steps of the method (Sec. 3.2)
+ *   patch_idx  0-based band index i in [0, n); band 0 is the top band
+ *              (the paper numbers bands from 1)
+ *   partial    p in [0, 1]: fraction of a neighbour's height used as context;
+ *              rows taken r = min(h, floor(p*h + 1e-9))
+ *   heads, head_dim  multi-head layout, C = heads * head_dim
+ *   batch      B >= 1 independent images (one classifier-free-guidance branch
+ *              per image)
+ *   step       diffusion step t >= 0; validated and otherwise unused: the
+ *              result is a function of the inputs and geometry only
+ *   dtype      PCPP_DTYPE_BF16 or PCPP_DTYPE_F32
+ */
+typedef struct pcpp_geom {
+    int32_t H;
+    int32_t W;
+    int32_t n_patches;
+    int32_t patch_idx;
+    double  partial;
+    int32_t heads;
+    int32_t head_dim;
+    int32_t batch;
+    int32_t step;
+    int32_t dtype;
+    int32_t reserved;   /* must be 0 */
+} pcpp_geom_t;
+
+/* Library version (PCPP_VERSION). */
+int pcpp_version(void);
+
+/* Static description of a status code; never NULL. */
+const char* pcpp_strerror(int status);
+
+/*
+ * Eq. 1 context geometry (host only, no GPU work).
+ * Outputs (any may be NULL): h = H/n; up = rows taken from band i-1 (0 for
+ * the top band); dn = rows taken from band i+1 (0 for the bottom band);
+ * n_kv = (up + h + dn) * W keys per image.
+ * Errors: PCPP_EINVAL for NULL g, n < 1, H % n != 0, i outside [0,n),
+ * p outside [0,1] or NaN, W < 1, batch < 1, step < 0, or a non-zero
+ * reserved field.
+ */
+int pcpp_context_rows(const pcpp_geom_t* g, int32_t* h, int32_t* up,
+                      int32_t* dn, int32_t* n_kv);
+
+/*
+ * Key/value context assembly (Eq. 1, Fig. 3).
+ *   k_fresh, v_fresh  [B, h*W, C] this band's keys/values of the current step
+ *   k_up, v_up        [B, h*W, C] stale band i-1 (its last `up` rows are read)
+ *   k_dn, v_dn        [B, h*W, C] stale band i+1 (its first `dn` rows are read)
+ *   idx_out           [n_kv] int32, device: global token ids row*W + col of
+ *                     the context in ascending order (rows i*h-up ..
+ *                     (i+1)*h+dn-1, every column); may be NULL
+ *   k_ctx, v_ctx      [B, n_kv, C] device outputs in that token order, or
+ *                     both NULL to build the index set only
+ * Element type from g->dtype; all tensors share it.  Neighbour pointers may
+ * be NULL when the matching row count is 0.  Outputs must not overlap inputs.
+ */
+int pcpp_gather_context(const pcpp_geom_t* g,
+                        const void* k_fresh, const void* v_fresh,
+                        const void* k_up, const void* v_up,
+                        const void* k_dn, const void* v_dn,
+                        int32_t* idx_out, void* k_ctx, void* v_ctx,
+                        void* stream);
+
+/*
+ * Bytes of device workspace pcpp_partial_attention needs for geometry g
+ * (0 when none is needed; the split-key-range path stores float32 partial
+ * outputs and row statistics there).  Returns 0 for an invalid g.
+ */
+size_t pcpp_partial_attention_workspace_size(const pcpp_geom_t* g);
+
+/*
+ * Partially conditioned self-attention of band i (Sec. 3.3, Fig. 3).
+ * Per image and head a: S = Q_a K_ctx,a^T / sqrt(head_dim) over the n_kv
+ * context keys (stale rows above, fresh band, stale rows below), row
+ * softmax, O_a = softmax(S) V_ctx,a.  No mask, no bias.
+ *   q                 [B, h*W, C] queries of this band (never exchanged)
+ *   k_fresh, v_fresh  [B, h*W, C]
+ *   k_up, v_up, k_dn, v_dn  whole stale neighbour bands as above
+ *   out               [B, h*W, C], same dtype as the inputs
+ *   workspace         device scratch of ws_bytes >= the workspace size
+ *                     (may be NULL when that size is 0); not preserved
+ * Supported: head_dim == 64 for both dtypes.  bf16 runs on the MFMA path
+ * (float32 accumulation and softmax, probabilities rounded to bf16 as the
+ * operand of the P*V product); f32 runs a float32 path.
+ */
+int pcpp_partial_attention(const pcpp_geom_t* g, const void* q,
+                           const void* k_fresh, const void* v_fresh,
+                           const void* k_up, const void* v_up,
+                           const void* k_dn, const void* v_dn,
+                           void* out, void* workspace, size_t ws_bytes,
+                           void* stream);
+
+/*
+ * Weights of one SDXL-shaped transformer block (device pointers, bf16,
+ * nn.Linear layout [out, in]).  C = heads * head_dim, F = ff_inner,
+ * T = text_dim.
+ */
+typedef struct pcpp_block_weights {
+    const void* gn_gamma;      /* [C] GroupNorm scale (eps 1e-6)            */
+    const void* gn_beta;       /* [C]                                        */
+    const void* proj_in_w;     /* [C, C]                                     */
+    const void* proj_in_b;     /* [C]                                        */
+    const void* ln1_gamma;     /* [C] LayerNorm before self-attn (eps 1e-5)  */
+    const void* ln1_beta;      /* [C]                                        */
+    const void* attn1_qkv_w;   /* [3C, C] rows: W_q, then W_k, then W_v       */
+    const void* attn1_out_w;   /* [C, C]                                     */
+    const void* attn1_out_b;   /* [C]                                        */
+    const void* ln2_gamma;     /* [C] LayerNorm before cross-attn            */
+    const void* ln2_beta;      /* [C]                                        */
+    const void* attn2_q_w;     /* [C, C]                                     */
+    const void* attn2_kv_w;    /* [2C, T] rows: W_k, then W_v (text side)    */
+    const void* attn2_out_w;   /* [C, C]                                     */
+    const void* attn2_out_b;   /* [C]                                        */
+    const void* ln3_gamma;     /* [C] LayerNorm before the feed-forward      */
+    const void* ln3_beta;      /* [C]                                        */
+    const void* ff1_w;         /* [2F, C] rows [0,F) value, [F,2F) gate      */
+    const void* ff1_b;         /* [2F]                                       */
+    const void* ff2_w;         /* [C, F]                                     */
+    const void* ff2_b;         /* [C]                                        */
+    const void* proj_out_w;    /* [C, C]                                     */
+    const void* proj_out_b;    /* [C]                                        */
+    int32_t ff_inner;          /* F >= 1, multiple of 64                     */
+    int32_t gn_groups;         /* groups dividing C                          */
+} pcpp_block_weights_t;
+
+/* Bytes of device workspace pcpp_transformer_block needs (0 if g invalid). */
+size_t pcpp_transformer_block_workspace_size(const pcpp_geom_t* g,
+                                             const pcpp_block_weights_t* w,
+                                             int32_t n_text, int32_t text_dim);
+
+/*
+ * One SDXL-shaped transformer block on band i, bf16 storage with float32
+ * accumulation (the method applies to the self-attention only, Sec. 3.3;
+ * GroupNorm here uses the band's own statistics):
+ *   t  = GroupNorm(x)                       (gn_groups groups, eps 1e-6)
+ *   h  = t proj_in^T + b
+ *   n1 = LayerNorm(h);  q,k,v = n1 W_q^T, n1 W_k^T, n1 W_v^T
+ *   h += PartialAttention(q, k, v, k_up, v_up, k_dn, v_dn) W_o^T + b
+ *   n2 = LayerNorm(h);  h += Attention(n2 W_q2^T, text W_k2^T, text W_v2^T) W_o2^T + b
+ *   n3 = LayerNorm(h);  [a, g] = n3 ff1^T + b;  h += (a * GELU(g)) ff2^T + b
+ *   y  = h proj_out^T + b + x
+ *   x            [B, h*W, C] bf16 band tokens
+ *   text         [B, n_text, text_dim] bf16 conditioning features
+ *   k_up .. v_dn stale neighbour keys/values as in pcpp_partial_attention
+ *   y            [B, h*W, C] bf16 output
+ *   k_fresh_out, v_fresh_out  [B, h*W, C] bf16: this band's keys/values of
+ *                the step, what the neighbours read as stale context at the
+ *                next step (Sec. 3.2); either may be NULL
+ *   workspace    device scratch, ws_bytes >= the workspace size
+ * Requires dtype PCPP_DTYPE_BF16, head_dim 64, C % 64 == 0, text_dim % 64 == 0.
+ */
+int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w,
+                           const void* x, const void* text, int32_t n_text,
+                           int32_t text_dim,
+                           const void* k_up, const void* v_up,
+                           const void* k_dn, const void* v_dn,
+                           void* y, void* k_fresh_out, void* v_fresh_out,
+                           void* workspace, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PCPP_H */

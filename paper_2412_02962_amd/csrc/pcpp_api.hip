@@ -1,0 +1,195 @@
+// C ABI entry points of the PCPP library: argument validation, Eq. 1
+// geometry, and kernel launches on the caller's stream.
+//
+// Everything here runs on the host.  Validation completes before anything
+// is enqueued, so an error return leaves the outputs untouched.
+
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+
+#include "../../include/pcpp.h"
+#include "api_internal.h"
+#include "kernels.h"
+
+#define PCPP_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace pcpp {
+
+// Sec. 3.1: h = H/n.  Eq. 1: r = p*h rows from each existing neighbour; a
+// fractional p*h is floored (the small epsilon keeps decimal fractions such
+// as p = 0.29, h = 100 at their exact value).
+int validate_geom(const pcpp_geom_t* g, Geo* out) {
+    if (g == nullptr) return PCPP_EINVAL;
+    if (g->reserved != 0) return PCPP_EINVAL;
+    if (g->n_patches < 1 || g->H < 1 || g->W < 1) return PCPP_EINVAL;
+    if (g->H % g->n_patches != 0) return PCPP_EINVAL;
+    if (g->patch_idx < 0 || g->patch_idx >= g->n_patches) return PCPP_EINVAL;
+    if (!(g->partial >= 0.0 && g->partial <= 1.0)) return PCPP_EINVAL;  // NaN fails too
+    if (g->heads < 1 || g->head_dim < 1 || g->batch < 1 || g->step < 0) return PCPP_EINVAL;
+    if ((int64_t)g->H * g->W > INT32_MAX / 2) return PCPP_EINVAL;
+    if ((int64_t)g->heads * g->head_dim > (1 << 20)) return PCPP_EINVAL;
+    Geo r;
+    r.h = g->H / g->n_patches;
+    double rows = floor(g->partial * (double)r.h + 1e-9);
+    int32_t ctx = rows >= (double)r.h ? r.h : (int32_t)rows;
+    r.up = g->patch_idx > 0 ? ctx : 0;
+    r.dn = g->patch_idx < g->n_patches - 1 ? ctx : 0;
+    r.nq = r.h * g->W;
+    r.n_kv = (r.up + r.h + r.dn) * g->W;
+    r.C = g->heads * g->head_dim;
+    r.esize = g->dtype == PCPP_DTYPE_BF16 ? 2 : 4;
+    if (out) *out = r;
+    return PCPP_OK;
+}
+
+KvSource make_kv_source(const pcpp_geom_t* g, const Geo& r, const void* k_fresh, const void* v_fresh,
+                        const void* k_up, const void* v_up, const void* k_dn, const void* v_dn) {
+    KvSource s;
+    const int64_t band = (int64_t)r.nq * r.C;  // elements of one whole band
+    const int64_t skip_up = (int64_t)(r.h - r.up) * g->W * r.C * r.esize;
+    s.k[0] = r.up > 0 ? (const char*)k_up + skip_up : nullptr;
+    s.v[0] = r.up > 0 ? (const char*)v_up + skip_up : nullptr;
+    s.k[1] = k_fresh;
+    s.v[1] = v_fresh;
+    s.k[2] = r.dn > 0 ? k_dn : nullptr;
+    s.v[2] = r.dn > 0 ? v_dn : nullptr;
+    s.bstride[0] = s.bstride[1] = s.bstride[2] = band;
+    s.end0 = r.up * g->W;
+    s.end1 = (r.up + r.h) * g->W;
+    s.n_kv = r.n_kv;
+    return s;
+}
+
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Shared argument checks of the attention entry point.
+static int check_attention(const pcpp_geom_t* g, Geo* r, const void* q, const void* k_fresh,
+                           const void* v_fresh, const void* k_up, const void* v_up, const void* k_dn,
+                           const void* v_dn, const void* out) {
+    int st = validate_geom(g, r);
+    if (st != PCPP_OK) return st;
+    if (g->dtype != PCPP_DTYPE_BF16 && g->dtype != PCPP_DTYPE_F32) return PCPP_ENOTSUP;
+    if (g->head_dim != 64) return PCPP_ENOTSUP;
+    if (!q || !k_fresh || !v_fresh || !out) return PCPP_EINVAL;
+    if (r->up > 0 && (!k_up || !v_up)) return PCPP_EINVAL;
+    if (r->dn > 0 && (!k_dn || !v_dn)) return PCPP_EINVAL;
+    if (g->heads > 65535 || g->batch > 65535) return PCPP_EINVAL;
+    const void* ptrs[8] = {q, k_fresh, v_fresh, k_up, v_up, k_dn, v_dn, out};
+    for (const void* p : ptrs)
+        if (p && !aligned16(p)) return PCPP_EINVAL;
+    return PCPP_OK;
+}
+
+AttnParams make_attn_params(const pcpp_geom_t* g, const Geo& r, const void* q, void* out,
+                            const KvSource& kv) {
+    AttnParams p;
+    p.q = q;
+    p.out = out;
+    p.q_bstride = (int64_t)r.nq * r.C;
+    p.nq = r.nq;
+    p.C = r.C;
+    p.heads = g->heads;
+    p.batch = g->batch;
+    p.kv = kv;
+    p.scale = (float)(1.0 / sqrt((double)g->head_dim));
+    p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)g->head_dim));
+    p.splits = 1;
+    p.tiles_per_split = 1 << 30;
+    p.ws_o = nullptr;
+    p.ws_ml = nullptr;
+    return p;
+}
+
+}  // namespace pcpp
+
+using namespace pcpp;
+
+PCPP_EXPORT int pcpp_version(void) { return PCPP_VERSION; }
+
+PCPP_EXPORT const char* pcpp_strerror(int status) {
+    switch (status) {
+        case PCPP_OK: return "ok";
+        case PCPP_EINVAL: return "invalid argument (geometry, partial value, pointer or alignment)";
+        case PCPP_ENOTSUP: return "unsupported head_dim, dtype or shape";
+        case PCPP_EWORKSPACE: return "workspace missing or too small";
+        case PCPP_EHIP: return "HIP runtime or kernel launch failure";
+        default: return "unknown status";
+    }
+}
+
+PCPP_EXPORT int pcpp_context_rows(const pcpp_geom_t* g, int32_t* h, int32_t* up, int32_t* dn,
+                                  int32_t* n_kv) {
+    Geo r;
+    int st = validate_geom(g, &r);
+    if (st != PCPP_OK) return st;
+    if (h) *h = r.h;
+    if (up) *up = r.up;
+    if (dn) *dn = r.dn;
+    if (n_kv) *n_kv = r.n_kv;
+    return PCPP_OK;
+}
+
+PCPP_EXPORT int pcpp_gather_context(const pcpp_geom_t* g, const void* k_fresh, const void* v_fresh,
+                                    const void* k_up, const void* v_up, const void* k_dn,
+                                    const void* v_dn, int32_t* idx_out, void* k_ctx, void* v_ctx,
+                                    void* stream) {
+    Geo r;
+    int st = validate_geom(g, &r);
+    if (st != PCPP_OK) return st;
+    if (g->dtype != PCPP_DTYPE_BF16 && g->dtype != PCPP_DTYPE_F32) return PCPP_ENOTSUP;
+    if ((k_ctx == nullptr) != (v_ctx == nullptr)) return PCPP_EINVAL;
+    if (k_ctx == nullptr && idx_out == nullptr) return PCPP_EINVAL;  // nothing to do
+    if (k_ctx != nullptr) {
+        if (!k_fresh || !v_fresh) return PCPP_EINVAL;
+        if (r.up > 0 && (!k_up || !v_up)) return PCPP_EINVAL;
+        if (r.dn > 0 && (!k_dn || !v_dn)) return PCPP_EINVAL;
+    }
+    if (g->batch > 65535) return PCPP_EINVAL;
+    GatherParams p;
+    p.src = make_kv_source(g, r, k_fresh, v_fresh, k_up, v_up, k_dn, v_dn);
+    p.k_ctx = k_ctx;
+    p.v_ctx = v_ctx;
+    p.idx = idx_out;
+    p.idx_base = (g->patch_idx * r.h - r.up) * g->W;
+    p.C = r.C;
+    p.batch = g->batch;
+    p.esize = r.esize;
+    return launch_gather(p, (hipStream_t)stream) == hipSuccess ? PCPP_OK : PCPP_EHIP;
+}
+
+PCPP_EXPORT size_t pcpp_partial_attention_workspace_size(const pcpp_geom_t* g) {
+    Geo r;
+    if (validate_geom(g, &r) != PCPP_OK) return 0;
+    if (g->dtype != PCPP_DTYPE_BF16 || g->head_dim != 64) return 0;
+    return plan_attention_bf16(r.nq, r.n_kv, g->heads, g->batch, r.C).ws_bytes;
+}
+
+PCPP_EXPORT int pcpp_partial_attention(const pcpp_geom_t* g, const void* q, const void* k_fresh,
+                                       const void* v_fresh, const void* k_up, const void* v_up,
+                                       const void* k_dn, const void* v_dn, void* out, void* workspace,
+                                       size_t ws_bytes, void* stream) {
+    Geo r;
+    int st = check_attention(g, &r, q, k_fresh, v_fresh, k_up, v_up, k_dn, v_dn, out);
+    if (st != PCPP_OK) return st;
+    KvSource kv = make_kv_source(g, r, k_fresh, v_fresh, k_up, v_up, k_dn, v_dn);
+    AttnParams p = make_attn_params(g, r, q, out, kv);
+    hipError_t e;
+    if (g->dtype == PCPP_DTYPE_BF16) {
+        AttnPlan pl = plan_attention_bf16(r.nq, r.n_kv, g->heads, g->batch, r.C);
+        if (pl.ws_bytes > 0) {
+            if (workspace == nullptr || ws_bytes < pl.ws_bytes) return PCPP_EWORKSPACE;
+            if (!aligned16(workspace)) return PCPP_EINVAL;
+        }
+        p.splits = pl.splits;
+        p.tiles_per_split = pl.tiles_per_split;
+        p.ws_o = (float*)workspace;
+        p.ws_ml = pl.ws_bytes > 0 ? (float*)((char*)workspace + (size_t)pl.splits * g->batch * r.nq * r.C *
+                                                                    sizeof(float))
+                                  : nullptr;
+        e = launch_attention_bf16(p, (hipStream_t)stream);
+    } else {
+        e = launch_attention_f32(p, (hipStream_t)stream);
+    }
+    return e == hipSuccess ? PCPP_OK : PCPP_EHIP;
+}

@@ -1,0 +1,173 @@
+"""ctypes binding of libpcpp.so: the C ABI declared in include/pcpp.h, with
+the same function names.  Argument marshalling only (device pointers from
+torch tensors, the current HIP stream); every step of the computation runs
+in the library's HIP kernels.  There is no fallback: if the shared library is
+missing or does not load, importing this module raises."""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpcpp.so")
+
+PCPP_OK = 0
+PCPP_EINVAL = -1
+PCPP_ENOTSUP = -2
+PCPP_EWORKSPACE = -3
+PCPP_EHIP = -4
+
+PCPP_DTYPE_F32 = 0
+PCPP_DTYPE_BF16 = 1
+
+
+class PcppError(RuntimeError):
+    def __init__(self, fn, status):
+        self.status = status
+        super().__init__(f"{fn} failed with status {status}: {pcpp_strerror(status)}")
+
+
+class pcpp_geom_t(ctypes.Structure):
+    _fields_ = [
+        ("H", ctypes.c_int32), ("W", ctypes.c_int32),
+        ("n_patches", ctypes.c_int32), ("patch_idx", ctypes.c_int32),
+        ("partial", ctypes.c_double),
+        ("heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+        ("batch", ctypes.c_int32), ("step", ctypes.c_int32),
+        ("dtype", ctypes.c_int32), ("reserved", ctypes.c_int32),
+    ]
+
+
+_BLOCK_PTR_FIELDS = (
+    "gn_gamma", "gn_beta", "proj_in_w", "proj_in_b", "ln1_gamma", "ln1_beta",
+    "attn1_qkv_w", "attn1_out_w", "attn1_out_b", "ln2_gamma", "ln2_beta",
+    "attn2_q_w", "attn2_kv_w", "attn2_out_w", "attn2_out_b", "ln3_gamma",
+    "ln3_beta", "ff1_w", "ff1_b", "ff2_w", "ff2_b", "proj_out_w", "proj_out_b",
+)
+
+
+class pcpp_block_weights_t(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in _BLOCK_PTR_FIELDS] + [
+        ("ff_inner", ctypes.c_int32), ("gn_groups", ctypes.c_int32)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built: run __graft_entry__.build() "
+                          "(or python paper_2412_02962_amd/build.py); there is no fallback path")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    gp = ctypes.POINTER(pcpp_geom_t)
+    wp = ctypes.POINTER(pcpp_block_weights_t)
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    sig = {
+        "pcpp_version": (ctypes.c_int, []),
+        "pcpp_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+        "pcpp_context_rows": (ctypes.c_int, [gp, i32p, i32p, i32p, i32p]),
+        "pcpp_gather_context": (ctypes.c_int, [gp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+        "pcpp_partial_attention_workspace_size": (sz, [gp]),
+        "pcpp_partial_attention": (ctypes.c_int, [gp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "pcpp_transformer_block_workspace_size": (sz, [gp, wp, i32, i32]),
+        "pcpp_transformer_block": (ctypes.c_int, [gp, wp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp,
+                                                  vp, sz, vp]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    return lib
+
+
+_lib = _load()
+EXPORTED = (
+    "pcpp_version", "pcpp_strerror", "pcpp_context_rows", "pcpp_gather_context",
+    "pcpp_partial_attention_workspace_size", "pcpp_partial_attention",
+    "pcpp_transformer_block_workspace_size", "pcpp_transformer_block",
+)
+
+
+def lib():
+    return _lib
+
+
+def make_geom(H, W, n_patches, patch_idx, partial, heads, head_dim=64, batch=1, step=0,
+              dtype=PCPP_DTYPE_BF16, reserved=0) -> pcpp_geom_t:
+    return pcpp_geom_t(H, W, n_patches, patch_idx, float(partial), heads, head_dim, batch, step,
+                       dtype, reserved)
+
+
+def _ptr(t) -> Optional[int]:
+    """Device address of a tensor (or a raw int address); None -> NULL."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is not None:
+        return stream if isinstance(stream, int) else stream.cuda_stream
+    import torch  # device memory and streams only
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _check(fn, st):
+    if st != PCPP_OK:
+        raise PcppError(fn, st)
+
+
+def pcpp_version() -> int:
+    return _lib.pcpp_version()
+
+
+def pcpp_strerror(status: int) -> str:
+    return _lib.pcpp_strerror(status).decode()
+
+
+def pcpp_context_rows(g: pcpp_geom_t):
+    """(h, up, dn, n_kv) of Eq. 1; raises PcppError on invalid geometry."""
+    h, up, dn, nkv = (ctypes.c_int32() for _ in range(4))
+    _check("pcpp_context_rows", _lib.pcpp_context_rows(ctypes.byref(g), ctypes.byref(h), ctypes.byref(up),
+                                                       ctypes.byref(dn), ctypes.byref(nkv)))
+    return h.value, up.value, dn.value, nkv.value
+
+
+def pcpp_gather_context(g, k_fresh, v_fresh, k_up, v_up, k_dn, v_dn, idx_out, k_ctx, v_ctx, stream=None):
+    _check("pcpp_gather_context", _lib.pcpp_gather_context(
+        ctypes.byref(g), _ptr(k_fresh), _ptr(v_fresh), _ptr(k_up), _ptr(v_up), _ptr(k_dn), _ptr(v_dn),
+        _ptr(idx_out), _ptr(k_ctx), _ptr(v_ctx), _stream(stream)))
+
+
+def pcpp_partial_attention_workspace_size(g) -> int:
+    return _lib.pcpp_partial_attention_workspace_size(ctypes.byref(g))
+
+
+def pcpp_partial_attention(g, q, k_fresh, v_fresh, k_up, v_up, k_dn, v_dn, out, workspace=None,
+                           ws_bytes=0, stream=None):
+    _check("pcpp_partial_attention", _lib.pcpp_partial_attention(
+        ctypes.byref(g), _ptr(q), _ptr(k_fresh), _ptr(v_fresh), _ptr(k_up), _ptr(v_up), _ptr(k_dn),
+        _ptr(v_dn), _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def make_block_weights(tensors: dict, ff_inner: int, gn_groups: int) -> pcpp_block_weights_t:
+    w = pcpp_block_weights_t()
+    for name in _BLOCK_PTR_FIELDS:
+        setattr(w, name, _ptr(tensors.get(name)))
+    w.ff_inner = ff_inner
+    w.gn_groups = gn_groups
+    return w
+
+
+def pcpp_transformer_block_workspace_size(g, w, n_text, text_dim) -> int:
+    return _lib.pcpp_transformer_block_workspace_size(ctypes.byref(g), ctypes.byref(w), n_text, text_dim)
+
+
+def pcpp_transformer_block(g, w, x, text, n_text, text_dim, k_up, v_up, k_dn, v_dn, y, k_fresh_out,
+                           v_fresh_out, workspace, ws_bytes, stream=None):
+    _check("pcpp_transformer_block", _lib.pcpp_transformer_block(
+        ctypes.byref(g), ctypes.byref(w), _ptr(x), _ptr(text), n_text, text_dim, _ptr(k_up), _ptr(v_up),
+        _ptr(k_dn), _ptr(v_dn), _ptr(y), _ptr(k_fresh_out), _ptr(v_fresh_out), _ptr(workspace), ws_bytes,
+        _stream(stream)))

@@ -1,0 +1,130 @@
+"""The C ABI library loads, exports every function include/pcpp.h declares,
+and its host-side logic (Eq. 1 geometry, argument validation) behaves as
+documented.  No compute call is made: every call here fails validation
+before anything would be enqueued, or is host-only."""
+
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pcpp.h")
+
+
+def _declared():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(pcpp_[a-z_]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_function():
+    from paper_2412_02962_amd import pcpp
+    names = _declared()
+    assert len(names) >= 8
+    lib = ctypes.CDLL(pcpp.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(pcpp.EXPORTED) == names
+
+
+def test_version_and_strerror():
+    from paper_2412_02962_amd import pcpp
+    assert pcpp.pcpp_version() == 1
+    for code in (0, -1, -2, -3, -4, -99):
+        assert isinstance(pcpp.pcpp_strerror(code), str) and pcpp.pcpp_strerror(code)
+
+
+def test_context_rows_agree_with_oracle_over_grid():
+    # two independent implementations of Sec. 3.1 / Eq. 1 (C++ and Python)
+    from paper_2412_02962_amd import pcpp
+    ps = [0.0, 0.05, 0.1, 0.25, 0.29, 0.3, 0.33, 0.5, 0.67, 0.75, 0.8, 0.99, 1.0]
+    for H in (1, 4, 8, 16, 30, 64, 100, 128, 240):
+        for n in range(1, 9):
+            if H % n:
+                continue
+            for i in range(n):
+                for p in ps:
+                    g = pcpp.make_geom(H, 7, n, i, p, 2)
+                    h, up, dn, nkv = pcpp.pcpp_context_rows(g)
+                    oh, oup, odn, rows = oracle.context_rows(H, n, i, p)
+                    assert (h, up, dn, nkv) == (oh, oup, odn, rows * 7), (H, n, i, p)
+
+
+@pytest.mark.parametrize("over", [
+    dict(H=10, n_patches=4), dict(patch_idx=4), dict(patch_idx=-1), dict(partial=-0.1),
+    dict(partial=1.5), dict(partial=math.nan), dict(n_patches=0), dict(W=0), dict(batch=0),
+    dict(step=-1), dict(heads=0), dict(reserved=1),
+])
+def test_context_rows_rejects_invalid_geometry(over):
+    from paper_2412_02962_amd import pcpp
+    kw = dict(H=16, W=8, n_patches=4, patch_idx=1, partial=0.25, heads=2)
+    kw.update(over)
+    with pytest.raises(pcpp.PcppError) as e:
+        pcpp.pcpp_context_rows(pcpp.make_geom(**kw))
+    assert e.value.status == pcpp.PCPP_EINVAL
+
+
+FAKE = 1 << 20  # an aligned non-null address; never dereferenced (validation fails first)
+
+
+def _attn(pcpp, g, **ptrs):
+    a = dict(q=FAKE, kf=FAKE, vf=FAKE, ku=FAKE, vu=FAKE, kd=FAKE, vd=FAKE, out=FAKE, ws=None, wsb=0)
+    a.update(ptrs)
+    return pcpp.lib().pcpp_partial_attention(ctypes.byref(g), a["q"], a["kf"], a["vf"], a["ku"], a["vu"],
+                                             a["kd"], a["vd"], a["out"], a["ws"], a["wsb"], None)
+
+
+def test_attention_validation_errors_before_launch():
+    from paper_2412_02962_amd import pcpp
+    g = pcpp.make_geom(128, 128, 8, 3, 0.25, 10)
+    assert _attn(pcpp, pcpp.make_geom(128, 128, 8, 3, 0.25, 10, head_dim=128)) == pcpp.PCPP_ENOTSUP
+    assert _attn(pcpp, pcpp.make_geom(128, 128, 8, 3, 0.25, 10, dtype=7)) == pcpp.PCPP_ENOTSUP
+    assert _attn(pcpp, g, q=None) == pcpp.PCPP_EINVAL
+    assert _attn(pcpp, g, out=None) == pcpp.PCPP_EINVAL
+    assert _attn(pcpp, g, ku=None) == pcpp.PCPP_EINVAL        # needed: up = 4 rows
+    assert _attn(pcpp, g, vd=None) == pcpp.PCPP_EINVAL
+    assert _attn(pcpp, g, q=FAKE + 2) == pcpp.PCPP_EINVAL     # misaligned
+    assert _attn(pcpp, pcpp.make_geom(128, 128, 8, 3, float("nan"), 10)) == pcpp.PCPP_EINVAL
+    ws = pcpp.pcpp_partial_attention_workspace_size(g)
+    if ws > 0:
+        assert _attn(pcpp, g, ws=None, wsb=0) == pcpp.PCPP_EWORKSPACE
+        assert _attn(pcpp, g, ws=FAKE, wsb=ws - 1) == pcpp.PCPP_EWORKSPACE
+
+
+def test_workspace_size_is_zero_for_invalid_or_f32():
+    from paper_2412_02962_amd import pcpp
+    assert pcpp.pcpp_partial_attention_workspace_size(pcpp.make_geom(10, 8, 4, 0, 0.5, 2)) == 0
+    assert pcpp.pcpp_partial_attention_workspace_size(
+        pcpp.make_geom(16, 16, 4, 1, 0.25, 2, dtype=pcpp.PCPP_DTYPE_F32)) == 0
+
+
+def test_gather_validation_errors_before_launch():
+    from paper_2412_02962_amd import pcpp
+    lib = pcpp.lib()
+    g = pcpp.make_geom(16, 16, 4, 1, 0.25, 2)
+    call = lambda *a: lib.pcpp_gather_context(ctypes.byref(g), *a, None)
+    # nothing requested
+    assert call(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None) == pcpp.PCPP_EINVAL
+    # one of the two outputs only
+    assert call(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, None) == pcpp.PCPP_EINVAL
+    # neighbour data missing while rows are needed
+    assert call(FAKE, FAKE, None, FAKE, FAKE, FAKE, None, FAKE, FAKE) == pcpp.PCPP_EINVAL
+    bad = pcpp.make_geom(16, 16, 4, 9, 0.25, 2)
+    assert lib.pcpp_gather_context(ctypes.byref(bad), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                   FAKE, None) == pcpp.PCPP_EINVAL
+
+
+def test_binding_refuses_to_load_without_library(tmp_path, monkeypatch):
+    import importlib.util
+    src = os.path.join(ROOT, "paper_2412_02962_amd", "pcpp.py")
+    dst = tmp_path / "pcpp.py"
+    dst.write_text(open(src).read())
+    spec = importlib.util.spec_from_file_location("pcpp_nolib", str(dst))
+    mod = importlib.util.module_from_spec(spec)
+    with pytest.raises(ImportError):
+        spec.loader.exec_module(mod)

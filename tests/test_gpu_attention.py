@@ -1,0 +1,192 @@
+"""GPU parity of pcpp_partial_attention and pcpp_gather_context against the
+float64 oracle, through the C ABI, on seeded synthetic inputs."""
+
+import dataclasses
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2412_02962_amd import synth
+from tests import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+
+def _cfg(name, **over):
+    return dataclasses.replace(synth.ATTN_CONFIGS[name], **over)
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+@pytest.mark.parametrize("name", list(synth.ATTN_CONFIGS))
+@pytest.mark.parametrize("variant", ["unit", "prescaled", "sharp"])
+def test_attention_matches_oracle_on_workloads(name, variant):
+    cfg = synth.ATTN_CONFIGS[name]
+    _say("attention", name, variant)
+    inp = synth.attention_inputs(cfg, variant)
+    got = gu.to_f64(gu.run_attention(cfg, inp))
+    want = gu.oracle_attention(cfg, inp)
+    mx, mean = gu.assert_close(cfg, got, want, f"{name}/{variant}")
+    rel = np.linalg.norm(got - want) / np.linalg.norm(want)
+    print(f"{name}/{variant}: max {mx:.2e} mean {mean:.2e} rel {rel:.2e}")
+    assert rel < (1e-5 if cfg.dtype == "f32" else 1e-2)
+
+
+@pytest.mark.parametrize("geo", [
+    dict(H=12, W=20, n=3, i=1, p=0.5),      # ragged: 80 queries, 120 keys
+    dict(H=12, W=20, n=3, i=0, p=1.0),      # top band, whole neighbour
+    dict(H=12, W=20, n=3, i=2, p=0.34),     # bottom band, fractional p*h
+    dict(H=1, W=1, n=1, i=0, p=0.0),        # one query, one key
+    dict(H=6, W=7, n=1, i=0, p=0.5),        # n = 1: full-image attention
+    dict(H=32, W=48, n=2, i=1, p=0.3),      # the paper's 2-band split, p*h fractional
+    dict(H=64, W=64, n=4, i=2, p=0.0),      # p = 0: band-local attention
+    dict(H=40, W=72, n=4, i=1, p=0.8),      # the paper's p for 8 devices
+])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_attention_edge_geometries(geo, dtype):
+    cfg = synth.AttnConfig(name="edge", heads=3, d=64, dtype=dtype, seed_id=40, **geo)
+    _say("edge", geo, dtype)
+    inp = synth.attention_inputs(cfg, "sharp")
+    got = gu.to_f64(gu.run_attention(cfg, inp))
+    gu.assert_close(cfg, got, gu.oracle_attention(cfg, inp), str(geo))
+
+
+@pytest.mark.parametrize("batch", [2, 3])
+def test_attention_batched(batch):
+    cfg = _cfg("sdxl1024_l1", batch=batch, H=32, W=32)
+    _say("batched", batch)
+    inp = synth.attention_inputs(cfg)
+    got = gu.to_f64(gu.run_attention(cfg, inp))
+    gu.assert_close(cfg, got, gu.oracle_attention(cfg, inp), "batched")
+
+
+def test_attention_f32_at_workload_shape():
+    cfg = _cfg("sdxl1024_l1", dtype="f32")
+    _say("f32 at 1024px level-1 shape")
+    inp = synth.attention_inputs(cfg)
+    got = gu.to_f64(gu.run_attention(cfg, inp))
+    gu.assert_close(cfg, got, gu.oracle_attention(cfg, inp), "f32 big")
+
+
+def test_step_does_not_change_the_result():
+    import torch
+    cfg = synth.ATTN_CONFIGS["sdxl1024_l1"]
+    _say("step independence")
+    inp = synth.attention_inputs(cfg)
+    a = gu.run_attention(cfg, inp, g=gu.geom(cfg, step=0))
+    b = gu.run_attention(cfg, inp, g=gu.geom(cfg, step=37))
+    assert torch.equal(a, b)
+
+
+def test_stale_rows_outside_window_never_read():
+    cfg = synth.ATTN_CONFIGS["sdxl2048_l1_p25"]
+    _say("NaN outside window")
+    inp = synth.attention_inputs(cfg)
+    ref = gu.run_attention(cfg, inp)
+    h, W, C = cfg.h, cfg.W, cfg.C
+    r = 4
+    bad = dict(inp)
+    nan = np.uint16(0x7FC0)
+    for key in ("k_up", "v_up"):
+        x = inp[key].copy()
+        x[:, :(h - r) * W] = nan
+        bad[key] = x
+    for key in ("k_dn", "v_dn"):
+        x = inp[key].copy()
+        x[:, r * W:] = nan
+        bad[key] = x
+    got = gu.run_attention(cfg, bad)
+    assert bool((got == ref).all())
+
+
+def test_split_and_unsplit_paths_agree_with_oracle():
+    cfg = synth.ATTN_CONFIGS["sdxl2048_l1_p50"]
+    inp = synth.attention_inputs(cfg)
+    want = gu.oracle_attention(cfg, inp)
+    old = os.environ.get("PCPP_ATTN_SPLITS")
+    try:
+        for s in ("1", "3", "7"):
+            _say("splits", s)
+            os.environ["PCPP_ATTN_SPLITS"] = s
+            gu.assert_close(cfg, gu.to_f64(gu.run_attention(cfg, inp)), want, f"splits={s}")
+    finally:
+        if old is None:
+            os.environ.pop("PCPP_ATTN_SPLITS", None)
+        else:
+            os.environ["PCPP_ATTN_SPLITS"] = old
+
+
+def test_virtual_patches_each_match_oracle():
+    # every band of one image, run one after another on the same GPU
+    base = synth.AttnConfig(name="virt", H=32, W=24, n=4, i=0, p=0.5, heads=2, d=64, dtype="bf16", seed_id=41)
+    for i in range(base.n):
+        cfg = dataclasses.replace(base, i=i)
+        _say("virtual band", i)
+        inp = synth.attention_inputs(cfg)
+        gu.assert_close(cfg, gu.to_f64(gu.run_attention(cfg, inp)), gu.oracle_attention(cfg, inp), f"band {i}")
+
+
+def test_largest_workload_sampled_rows():
+    # 3840 px level-1 grid (240 x 240, 640 channels) on 2 bands, p = 0.3:
+    # 28800 queries x 37440 keys; the oracle checks a sample of query rows
+    cfg = synth.AttnConfig(name="3840", H=240, W=240, n=2, i=0, p=0.3, heads=10, d=64, dtype="bf16",
+                           seed_id=42)
+    _say("3840px level-1, sampled")
+    inp = synth.attention_inputs(cfg)
+    got = gu.to_f64(gu.run_attention(cfg, inp))
+    rows = np.sort(np.random.default_rng(5).choice(cfg.n_q, 96, replace=False))
+    f = {k: oracle.as_f64(v, cfg.dtype) for k, v in inp.items()}
+    want = oracle.partial_attention(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, f["q"][:, rows],
+                                    f["k_fresh"], f["v_fresh"], f["k_up"], f["v_up"], f["k_dn"], f["v_dn"])
+    gu.assert_close(cfg, got[:, rows], want, "3840 sampled")
+
+
+@pytest.mark.parametrize("name", list(synth.ATTN_CONFIGS))
+def test_gather_is_bit_exact(name):
+    import torch
+    from paper_2412_02962_amd import pcpp
+    cfg = synth.ATTN_CONFIGS[name]
+    _say("gather", name)
+    inp = synth.attention_inputs(cfg)
+    g = gu.geom(cfg)
+    h, up, dn, nkv = pcpp.pcpp_context_rows(g)
+    d = {k: gu.to_dev(v, cfg.dtype) for k, v in inp.items()}
+    idx = torch.full((nkv,), -1, dtype=torch.int32, device=gu.DEV)
+    kc = torch.empty((cfg.batch, nkv, cfg.C), dtype=d["k_fresh"].dtype, device=gu.DEV)
+    vc = torch.empty_like(kc)
+    pcpp.pcpp_gather_context(g, d["k_fresh"], d["v_fresh"], d["k_up"], d["v_up"], d["k_dn"], d["v_dn"],
+                             idx, kc, vc)
+    torch.cuda.synchronize()
+    want_idx = oracle.context_token_ids(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p)
+    assert np.array_equal(idx.cpu().numpy(), want_idx)
+    for got, key in ((kc, "k"), (vc, "v")):
+        want = oracle.assemble_context(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, inp[key + "_fresh"],
+                                       inp[key + "_up"], inp[key + "_dn"])
+        raw = got.cpu()
+        raw = raw.view(torch.int16).numpy().view(np.uint16) if cfg.dtype == "bf16" else raw.numpy()
+        assert np.array_equal(raw, want), key
+
+
+def test_gather_index_only_and_unaligned_width():
+    import torch
+    from paper_2412_02962_amd import pcpp
+    cfg = synth.AttnConfig(name="g", H=15, W=3, n=5, i=2, p=0.67, heads=1, d=4, dtype="bf16", seed_id=43)
+    _say("gather odd sizes")
+    inp = synth.attention_inputs(cfg)
+    g = gu.geom(cfg)
+    _, _, _, nkv = pcpp.pcpp_context_rows(g)
+    d = {k: gu.to_dev(v, cfg.dtype) for k, v in inp.items()}
+    idx = torch.full((nkv,), -1, dtype=torch.int32, device=gu.DEV)
+    pcpp.pcpp_gather_context(g, None, None, None, None, None, None, idx, None, None)
+    kc = torch.empty((1, nkv, cfg.C), dtype=torch.bfloat16, device=gu.DEV)
+    vc = torch.empty_like(kc)
+    pcpp.pcpp_gather_context(g, d["k_fresh"], d["v_fresh"], d["k_up"], d["v_up"], d["k_dn"], d["v_dn"],
+                             None, kc, vc)
+    torch.cuda.synchronize()
+    assert np.array_equal(idx.cpu().numpy(), oracle.context_token_ids(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p))
+    want = oracle.assemble_context(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, inp["v_fresh"], inp["v_up"], inp["v_dn"])
+    assert np.array_equal(vc.cpu().view(torch.int16).numpy().view(np.uint16), want)
