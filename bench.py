@@ -132,8 +132,10 @@ def main():
     stream = torch.cuda.current_stream()
 
     def step():
+        # stream=None: the launch goes to torch's current stream, which is the
+        # capture stream inside torch.cuda.graph()
         pcpp.pcpp_partial_attention(g, d["q"], d["k_fresh"], d["v_fresh"], d["k_up"], d["v_up"], d["k_dn"],
-                                    d["v_dn"], out, ws, wsb, stream)
+                                    d["v_dn"], out, ws, wsb, None)
 
     for _ in range(args.warmup):
         step()

@@ -4,10 +4,12 @@
 // 2412.02962): per image and head, softmax(Q K_ctx^T / sqrt(64)) V_ctx over
 // the fresh band plus the stale boundary rows of the neighbours, read in
 // place from the three sources.  One thread owns one query and keeps its
-// 64-dim query and output in registers; 32-key tiles of K and V are staged
+// 64-dim query and output in registers; 16-key tiles of K and V are staged
 // in LDS and read by every thread of the block (LDS broadcast).  Scores of a
-// tile are computed first, then one online-softmax update per tile with the
-// accurate expf.  Meant for small problems and float32 accuracy, not speed.
+// tile are computed first, then one online-softmax update per tile.  Logits,
+// softmax weights, their sum and the weighted sum of values accumulate in
+// float64 (the float32 inputs widen exactly), so the only float32 rounding is
+// the final store.  Meant for small problems and float32 accuracy, not speed.
 
 #include <math.h>
 
@@ -20,7 +22,7 @@ namespace {
 
 constexpr int D = 64;
 constexpr int BQ = 128;
-constexpr int BKV = 32;
+constexpr int BKV = 16;
 
 __device__ __forceinline__ const float* kv_ptr_f32(const KvSource& s, bool v, int b, int j, int C,
                                                    int head_off) {
@@ -43,13 +45,14 @@ __global__ __launch_bounds__(BQ) void attn_f32_kernel(AttnParams p) {
     float qv[D];
     const float* qp = (const float*)p.q + (int64_t)b * p.q_bstride + (int64_t)qrow * p.C + head_off;
 #pragma unroll
-    for (int e = 0; e < D; ++e) qv[e] = qp[e] * p.scale;
+    for (int e = 0; e < D; ++e) qv[e] = qp[e];
+    const double scale = (double)p.scale;
 
-    float o[D];
+    double o[D];
 #pragma unroll
-    for (int e = 0; e < D; ++e) o[e] = 0.f;
-    float m_run = -INFINITY;
-    float l_run = 0.f;
+    for (int e = 0; e < D; ++e) o[e] = 0.0;
+    double m_run = -INFINITY;
+    double l_run = 0.0;
 
     const int n_kv = p.kv.n_kv;
     for (int base = 0; base < n_kv; base += BKV) {
@@ -62,35 +65,35 @@ __global__ __launch_bounds__(BQ) void attn_f32_kernel(AttnParams p) {
         }
         __syncthreads();
         const int cnt = min(BKV, n_kv - base);
-        float s[BKV];
-        float mx = -INFINITY;
+        double s[BKV];
+        double mx = -INFINITY;
 #pragma unroll
         for (int r = 0; r < BKV; ++r) {
-            float acc = 0.f;
+            double acc = 0.0;
 #pragma unroll
-            for (int e = 0; e < D; ++e) acc = fmaf(qv[e], ks[r][e], acc);
-            s[r] = r < cnt ? acc : -INFINITY;
-            mx = fmaxf(mx, s[r]);
+            for (int e = 0; e < D; ++e) acc = fma((double)qv[e], (double)ks[r][e], acc);
+            s[r] = r < cnt ? acc * scale : -INFINITY;
+            mx = fmax(mx, s[r]);
         }
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = expf(m_run - m_new);
+        const double m_new = fmax(m_run, mx);
+        const double alpha = exp(m_run - m_new);
         l_run *= alpha;
 #pragma unroll
         for (int e = 0; e < D; ++e) o[e] *= alpha;
 #pragma unroll
         for (int r = 0; r < BKV; ++r) {
-            float w = expf(s[r] - m_new);
+            double w = exp(s[r] - m_new);
             l_run += w;
 #pragma unroll
-            for (int e = 0; e < D; ++e) o[e] = fmaf(w, vs[r][e], o[e]);
+            for (int e = 0; e < D; ++e) o[e] = fma(w, (double)vs[r][e], o[e]);
         }
         m_run = m_new;
     }
     if (q >= p.nq) return;
-    const float inv = 1.0f / l_run;
+    const double inv = 1.0 / l_run;
     float* op = (float*)p.out + (int64_t)b * p.q_bstride + (int64_t)q * p.C + head_off;
 #pragma unroll
-    for (int e = 0; e < D; ++e) op[e] = o[e] * inv;
+    for (int e = 0; e < D; ++e) op[e] = (float)(o[e] * inv);
 }
 
 }  // namespace
