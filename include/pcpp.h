@@ -208,7 +208,11 @@ size_t pcpp_transformer_block_workspace_size(const pcpp_geom_t* g,
  *                the step, what the neighbours read as stale context at the
  *                next step (Sec. 3.2); either may be NULL
  *   workspace    device scratch, ws_bytes >= the workspace size
- * Requires dtype PCPP_DTYPE_BF16, head_dim 64, C % 64 == 0, text_dim % 64 == 0.
+ * Requires dtype PCPP_DTYPE_BF16 and head_dim 64 (PCPP_ENOTSUP otherwise),
+ * C <= 2048 (PCPP_ENOTSUP), text_dim >= 32 with text_dim % 32 == 0,
+ * n_text >= 1, ff_inner % 64 == 0, C % gn_groups == 0 (PCPP_EINVAL).  All
+ * pointers, weights included, must be 16-byte aligned (PCPP_EINVAL).
+ * Workspace contents are scratch and not preserved between calls.
  */
 int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w,
                            const void* x, const void* text, int32_t n_text,

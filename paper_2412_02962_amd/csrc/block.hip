@@ -1,17 +1,284 @@
-// Placeholder: the transformer-block entry points are added with the GEMM,
-// normalisation and cross-attention kernels.
+// pcpp_transformer_block: one SDXL-shaped transformer block on one band,
+// built from the library's kernels (GroupNorm, LayerNorm, MFMA GEMMs with
+// fused epilogues, and the attention kernel used twice: partially
+// conditioned self-attention over the band plus its neighbours' stale
+// boundary rows, Sec. 3.3 of arXiv 2412.02962, and cross-attention to the
+// text features).
+//
+// Data flow (per call, all images of the batch stacked as GEMM rows):
+//   t   = GroupNorm(x)                         bf16
+//   h   = t Wpi^T + b                          fp32 residual stream
+//   n   = LayerNorm(h)                         bf16
+//   q,k,v = n Wqkv^T                           bf16 (k, v also exported)
+//   a   = PartialAttention(q, k, v, stale)     bf16
+//   h  += a Wo^T + b                           fp32 (epilogue residual)
+//   n   = LayerNorm(h);  q2 = n Wq2^T;  k2,v2 = text Wkv^T
+//   a   = Attention(q2, k2, v2);  h += a Wo2^T + b
+//   n   = LayerNorm(h);  u = GEGLU(n Wff1^T + b)   (epilogue value*GELU(gate))
+//   h  += u Wff2^T + b
+//   y   = h Wpo^T + b + x                      bf16 (fp32 h rounded on load)
+
+#include <stdint.h>
+
 #include "../../include/pcpp.h"
+#include "api_internal.h"
+#include "gemm.h"
+#include "kernels.h"
 
 #define PCPP_EXPORT extern "C" __attribute__((visibility("default")))
 
-PCPP_EXPORT size_t pcpp_transformer_block_workspace_size(const pcpp_geom_t*, const pcpp_block_weights_t*,
-                                                         int32_t, int32_t) {
-    return 0;
+namespace pcpp {
+
+namespace {
+
+struct BlockLayout {
+    size_t t16, hid, q16, k16, v16, a16, k2, v2, u16, attn_ws, gn, total;
+    size_t attn_ws_bytes;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int validate_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, int32_t n_text, int32_t text_dim,
+                   Geo* r) {
+    int st = validate_geom(g, r);
+    if (st != PCPP_OK) return st;
+    if (g->dtype != PCPP_DTYPE_BF16 || g->head_dim != 64) return PCPP_ENOTSUP;
+    if (w == nullptr) return PCPP_EINVAL;
+    if (n_text < 1 || text_dim < 32 || text_dim % 32 != 0) return PCPP_EINVAL;
+    if (w->ff_inner < 64 || w->ff_inner % 64 != 0) return PCPP_EINVAL;
+    if (w->gn_groups < 1 || r->C % w->gn_groups != 0) return PCPP_EINVAL;
+    if (r->C > 2048) return PCPP_ENOTSUP;  // LayerNorm keeps a row in registers
+    if (g->heads > 65535 || g->batch > 65535) return PCPP_EINVAL;
+    return PCPP_OK;
 }
 
-PCPP_EXPORT int pcpp_transformer_block(const pcpp_geom_t*, const pcpp_block_weights_t*, const void*,
-                                       const void*, int32_t, int32_t, const void*, const void*,
-                                       const void*, const void*, void*, void*, void*, void*, size_t,
-                                       void*) {
-    return PCPP_ENOTSUP;
+BlockLayout layout(const pcpp_geom_t* g, const Geo& r, const pcpp_block_weights_t* w, int32_t n_text) {
+    BlockLayout L;
+    const size_t rows = (size_t)g->batch * r.nq;
+    const size_t C = r.C;
+    const AttnPlan ps = plan_attention_bf16(r.nq, r.n_kv, g->heads, g->batch, r.C);
+    const AttnPlan pc = plan_attention_bf16(r.nq, n_text, g->heads, g->batch, r.C);
+    L.attn_ws_bytes = ps.ws_bytes > pc.ws_bytes ? ps.ws_bytes : pc.ws_bytes;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off += align256(bytes);
+        return o;
+    };
+    L.t16 = take(rows * C * 2);
+    L.hid = take(rows * C * 4);
+    L.q16 = take(rows * C * 2);
+    L.k16 = take(rows * C * 2);
+    L.v16 = take(rows * C * 2);
+    L.a16 = take(rows * C * 2);
+    L.k2 = take((size_t)g->batch * n_text * C * 2);
+    L.v2 = take((size_t)g->batch * n_text * C * 2);
+    L.u16 = take(rows * (size_t)w->ff_inner * 2);
+    L.attn_ws = take(L.attn_ws_bytes);
+    L.gn = take(group_norm_ws_bytes(g->batch, w->gn_groups));
+    L.total = off;
+    return L;
+}
+
+GemmParams gemm(const void* a, int64_t lda, bool a_f32, const void* wt, const void* bias, int M, int N, int K,
+                void* out, int64_t ldo, bool out_f32) {
+    GemmParams p;
+    p.a = a;
+    p.lda = lda;
+    p.a_f32 = a_f32 ? 1 : 0;
+    p.w = (const __bf16*)wt;
+    p.bias = (const __bf16*)bias;
+    p.M = M;
+    p.N = N;
+    p.K = K;
+    p.geglu = 0;
+    p.F = 0;
+    p.resid = nullptr;
+    p.ldr = 0;
+    p.resid_f32 = 0;
+    p.out[0] = out;
+    p.out[1] = p.out[2] = nullptr;
+    p.seg = N;
+    p.ldo = ldo;
+    p.out_f32 = out_f32 ? 1 : 0;
+    return p;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+}  // namespace pcpp
+
+using namespace pcpp;
+
+PCPP_EXPORT size_t pcpp_transformer_block_workspace_size(const pcpp_geom_t* g, const pcpp_block_weights_t* w,
+                                                         int32_t n_text, int32_t text_dim) {
+    Geo r;
+    if (validate_block(g, w, n_text, text_dim, &r) != PCPP_OK) return 0;
+    return layout(g, r, w, n_text).total;
+}
+
+PCPP_EXPORT int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, const void* x,
+                                       const void* text, int32_t n_text, int32_t text_dim, const void* k_up,
+                                       const void* v_up, const void* k_dn, const void* v_dn, void* y,
+                                       void* k_fresh_out, void* v_fresh_out, void* workspace, size_t ws_bytes,
+                                       void* stream) {
+    Geo r;
+    int st = validate_block(g, w, n_text, text_dim, &r);
+    if (st != PCPP_OK) return st;
+    const void* wptrs[] = {w->gn_gamma, w->gn_beta, w->proj_in_w, w->proj_in_b, w->ln1_gamma, w->ln1_beta,
+                           w->attn1_qkv_w, w->attn1_out_w, w->attn1_out_b, w->ln2_gamma, w->ln2_beta,
+                           w->attn2_q_w, w->attn2_kv_w, w->attn2_out_w, w->attn2_out_b, w->ln3_gamma,
+                           w->ln3_beta, w->ff1_w, w->ff1_b, w->ff2_w, w->ff2_b, w->proj_out_w, w->proj_out_b};
+    for (const void* p : wptrs)
+        if (p == nullptr || !aligned16(p)) return PCPP_EINVAL;
+    if (!x || !text || !y) return PCPP_EINVAL;
+    if (r.up > 0 && (!k_up || !v_up)) return PCPP_EINVAL;
+    if (r.dn > 0 && (!k_dn || !v_dn)) return PCPP_EINVAL;
+    const void* aptrs[] = {x, text, y, k_up, v_up, k_dn, v_dn, k_fresh_out, v_fresh_out};
+    for (const void* p : aptrs)
+        if (p && !aligned16(p)) return PCPP_EINVAL;
+    const BlockLayout L = layout(g, r, w, n_text);
+    if (workspace == nullptr || ws_bytes < L.total) return PCPP_EWORKSPACE;
+    if (!aligned16(workspace)) return PCPP_EINVAL;
+
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    const int B = g->batch, N = r.nq, C = r.C, F = w->ff_inner, T = n_text;
+    const int rows = B * N;
+    __bf16* t16 = (__bf16*)(ws + L.t16);
+    float* hid = (float*)(ws + L.hid);
+    __bf16* q16 = (__bf16*)(ws + L.q16);
+    __bf16* k16 = k_fresh_out ? (__bf16*)k_fresh_out : (__bf16*)(ws + L.k16);
+    __bf16* v16 = v_fresh_out ? (__bf16*)v_fresh_out : (__bf16*)(ws + L.v16);
+    __bf16* a16 = (__bf16*)(ws + L.a16);
+    __bf16* k2 = (__bf16*)(ws + L.k2);
+    __bf16* v2 = (__bf16*)(ws + L.v2);
+    __bf16* u16 = (__bf16*)(ws + L.u16);
+    void* attn_ws = ws + L.attn_ws;
+    hipError_t e = hipSuccess;
+#define PCPP_CHECK(call)                  \
+    do {                                  \
+        e = (call);                       \
+        if (e != hipSuccess) return PCPP_EHIP; \
+    } while (0)
+
+    // GroupNorm over the band's tokens, then proj_in into the fp32 stream.
+    GroupNormParams gp;
+    gp.x = (const __bf16*)x;
+    gp.y = t16;
+    gp.gamma = (const __bf16*)w->gn_gamma;
+    gp.beta = (const __bf16*)w->gn_beta;
+    gp.stats = (float*)(ws + L.gn);
+    gp.B = B;
+    gp.N = N;
+    gp.C = C;
+    gp.G = w->gn_groups;
+    gp.chunks = 8;
+    gp.eps = 1e-6f;
+    PCPP_CHECK(launch_group_norm(gp, s));
+    PCPP_CHECK(launch_gemm(gemm(t16, C, false, w->proj_in_w, w->proj_in_b, rows, C, C, hid, C, true), s));
+
+    LayerNormParams lp;
+    lp.x = hid;
+    lp.y = t16;
+    lp.rows = rows;
+    lp.C = C;
+    lp.eps = 1e-5f;
+
+    // Self-attention: Q, K, V of the band; K and V are the band's export.
+    lp.gamma = (const __bf16*)w->ln1_gamma;
+    lp.beta = (const __bf16*)w->ln1_beta;
+    PCPP_CHECK(launch_layer_norm(lp, s));
+    {
+        GemmParams qkv = gemm(t16, C, false, w->attn1_qkv_w, nullptr, rows, 3 * C, C, q16, C, false);
+        qkv.out[1] = k16;
+        qkv.out[2] = v16;
+        qkv.seg = C;
+        PCPP_CHECK(launch_gemm(qkv, s));
+    }
+    {
+        KvSource kv = make_kv_source(g, r, k16, v16, k_up, v_up, k_dn, v_dn);
+        AttnParams ap = make_attn_params(g, r, q16, a16, kv);
+        AttnPlan pl = plan_attention_bf16(N, r.n_kv, g->heads, B, C);
+        ap.splits = pl.splits;
+        ap.tiles_per_split = pl.tiles_per_split;
+        ap.ws_o = (float*)attn_ws;
+        ap.ws_ml = (float*)((char*)attn_ws + (size_t)pl.splits * B * N * C * sizeof(float));
+        PCPP_CHECK(launch_attention_bf16(ap, s));
+    }
+    {
+        GemmParams o = gemm(a16, C, false, w->attn1_out_w, w->attn1_out_b, rows, C, C, hid, C, true);
+        o.resid = hid;
+        o.ldr = C;
+        o.resid_f32 = 1;
+        PCPP_CHECK(launch_gemm(o, s));
+    }
+
+    // Cross-attention to the text features.
+    lp.gamma = (const __bf16*)w->ln2_gamma;
+    lp.beta = (const __bf16*)w->ln2_beta;
+    PCPP_CHECK(launch_layer_norm(lp, s));
+    PCPP_CHECK(launch_gemm(gemm(t16, C, false, w->attn2_q_w, nullptr, rows, C, C, q16, C, false), s));
+    {
+        GemmParams kv = gemm(text, text_dim, false, w->attn2_kv_w, nullptr, B * T, 2 * C, text_dim, k2, C, false);
+        kv.out[1] = v2;
+        kv.seg = C;
+        PCPP_CHECK(launch_gemm(kv, s));
+    }
+    {
+        KvSource kv;
+        kv.k[0] = kv.k[2] = nullptr;
+        kv.v[0] = kv.v[2] = nullptr;
+        kv.k[1] = k2;
+        kv.v[1] = v2;
+        kv.bstride[0] = kv.bstride[1] = kv.bstride[2] = (int64_t)T * C;
+        kv.end0 = 0;
+        kv.end1 = T;
+        kv.n_kv = T;
+        AttnParams ap = make_attn_params(g, r, q16, a16, kv);
+        AttnPlan pl = plan_attention_bf16(N, T, g->heads, B, C);
+        ap.splits = pl.splits;
+        ap.tiles_per_split = pl.tiles_per_split;
+        ap.ws_o = (float*)attn_ws;
+        ap.ws_ml = (float*)((char*)attn_ws + (size_t)pl.splits * B * N * C * sizeof(float));
+        PCPP_CHECK(launch_attention_bf16(ap, s));
+    }
+    {
+        GemmParams o = gemm(a16, C, false, w->attn2_out_w, w->attn2_out_b, rows, C, C, hid, C, true);
+        o.resid = hid;
+        o.ldr = C;
+        o.resid_f32 = 1;
+        PCPP_CHECK(launch_gemm(o, s));
+    }
+
+    // GEGLU feed-forward.
+    lp.gamma = (const __bf16*)w->ln3_gamma;
+    lp.beta = (const __bf16*)w->ln3_beta;
+    PCPP_CHECK(launch_layer_norm(lp, s));
+    {
+        GemmParams ff = gemm(t16, C, false, w->ff1_w, w->ff1_b, rows, F, C, u16, F, false);
+        ff.geglu = 1;
+        ff.F = F;
+        PCPP_CHECK(launch_gemm(ff, s));
+    }
+    {
+        GemmParams o = gemm(u16, F, false, w->ff2_w, w->ff2_b, rows, C, F, hid, C, true);
+        o.resid = hid;
+        o.ldr = C;
+        o.resid_f32 = 1;
+        PCPP_CHECK(launch_gemm(o, s));
+    }
+
+    // proj_out plus the block input.
+    {
+        GemmParams o = gemm(hid, C, true, w->proj_out_w, w->proj_out_b, rows, C, C, y, C, false);
+        o.resid = x;
+        o.ldr = C;
+        o.resid_f32 = 0;
+        PCPP_CHECK(launch_gemm(o, s));
+    }
+#undef PCPP_CHECK
+    return PCPP_OK;
 }

@@ -1,0 +1,57 @@
+// Internal interface of the block's GEMM and normalisation kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pcpp {
+
+// Y[m, n] = X[m, :] . W[n, :] (+ bias[n]) (+ resid[m, n]), optionally
+// value * GELU(gate) with the gate taken from W rows F + n.
+struct GemmParams {
+    const void* a;        // X [M, K], row stride lda (bf16, or fp32 if a_f32)
+    int64_t lda;
+    int32_t a_f32;
+    const __bf16* w;      // W [rows, K] bf16, nn.Linear layout
+    const __bf16* bias;   // [rows] or null
+    int32_t M, N, K;      // N = output columns
+    int32_t geglu;        // 1: output n = (acc_n + b_n) * GELU(acc_{F+n} + b_{F+n})
+    int32_t F;            // gate row offset for geglu
+    const void* resid;    // [M, N] row stride ldr, or null
+    int64_t ldr;
+    int32_t resid_f32;
+    void* out[3];         // output segments: column n goes to out[n / seg] column n % seg
+    int32_t seg;
+    int64_t ldo;          // row stride of each output segment
+    int32_t out_f32;
+};
+
+bool gemm_shape_ok(const GemmParams& p);
+hipError_t launch_gemm(const GemmParams& p, hipStream_t s);
+
+// GroupNorm with statistics over one image's tokens (per image and group):
+// writes bf16 y = (x - mean) * rsqrt(var + eps) * gamma + beta.
+struct GroupNormParams {
+    const __bf16* x;      // [B, N, C]
+    __bf16* y;            // [B, N, C]
+    const __bf16* gamma;
+    const __bf16* beta;
+    float* stats;         // workspace [B, G, chunks, 3]
+    int32_t B, N, C, G, chunks;
+    float eps;
+};
+size_t group_norm_ws_bytes(int B, int G);
+hipError_t launch_group_norm(GroupNormParams p, hipStream_t s);
+
+// LayerNorm over the channel axis of fp32 rows, bf16 output.
+struct LayerNormParams {
+    const float* x;       // [rows, C]
+    __bf16* y;            // [rows, C]
+    const __bf16* gamma;
+    const __bf16* beta;
+    int32_t rows, C;
+    float eps;
+};
+hipError_t launch_layer_norm(const LayerNormParams& p, hipStream_t s);
+
+}  // namespace pcpp

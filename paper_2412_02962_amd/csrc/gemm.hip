@@ -1,0 +1,246 @@
+// bf16 GEMM on gfx950 MFMA for the transformer block's linear layers:
+//   Y[m, n] = sum_k X[m, k] * W[n, k]  (+ bias[n]) (+ residual[m, n])
+// with W in nn.Linear layout [out, in].  Optional GEGLU epilogue: the
+// workgroup computes the value columns n and the gate columns F + n of the
+// same outputs and writes value * GELU(gate) (exact erf GELU).
+//
+// The product is computed transposed, Y^T = W X^T, with 32x32x16 MFMAs so
+// each lane ends up holding four consecutive output features of one token:
+// stores are 8-byte (bf16) or 16-byte (fp32) vectors along the row.
+// Tiles: BK = 32, LDS rows padded to 40 elements (conflict-free 16-byte
+// operand reads), register-staged double buffering of the next K slice.
+// X may be bf16 or fp32 (fp32 is rounded to bf16 while staging).
+
+#include <math.h>
+
+#include "common.h"
+#include "gemm.h"
+
+namespace pcpp {
+
+namespace {
+
+constexpr int BK = 32;
+constexpr int LSTR = 40;  // LDS row stride in elements
+
+__device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
+
+typedef const __attribute__((address_space(1))) u32x4* gchunk;
+
+template <int WMB, int WNB, bool AF32>
+__global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
+    constexpr int BM = 2 * 32 * WMB;           // tokens per workgroup
+    constexpr int BNW = 2 * 32 * WNB;          // W-tile rows per workgroup
+    constexpr int A_CHUNKS = BM * BK / 8;      // 16-byte bf16 chunks of the X tile
+    constexpr int W_CHUNKS = BNW * BK / 8;
+    constexpr int A_PER = (A_CHUNKS + 255) / 256;
+    constexpr int W_PER = (W_CHUNKS + 255) / 256;
+
+    __shared__ __attribute__((aligned(16))) bf16 a_lds[2][BM * LSTR];
+    __shared__ __attribute__((aligned(16))) bf16 w_lds[2][BNW * LSTR];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave & 1;
+    const int wn = wave >> 1;
+    const int col = lane & 31;
+    const int half = lane >> 5;
+    const int m0 = blockIdx.x * BM;
+    // output columns per workgroup: BNW, or BNW/2 with the GEGLU pairing
+    const int bn_out = p.geglu ? BNW / 2 : BNW;
+    const int n0 = blockIdx.y * bn_out;
+
+    // global W row of W-tile row r
+    auto w_row = [&](int r) -> int {
+        if (!p.geglu) return n0 + r;
+        return r < BNW / 2 ? n0 + r : p.F + n0 + (r - BNW / 2);
+    };
+
+    u32x4 a_reg[A_PER * (AF32 ? 2 : 1)];
+    u32x4 w_reg[W_PER];
+
+    auto load = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < A_PER; ++i) {
+            const int c = tid + 256 * i;
+            const int r = c >> 2, kc = (c & 3) * 8;
+            const int m = m0 + r;
+            const u32x4 z = {0u, 0u, 0u, 0u};
+            if (c < A_CHUNKS && m < p.M) {
+                if (AF32) {
+                    gchunk src = (gchunk)((const float*)p.a + (int64_t)m * p.lda + k0 + kc);
+                    a_reg[2 * i] = src[0];
+                    a_reg[2 * i + 1] = src[1];
+                } else {
+                    a_reg[i] = *(gchunk)((const bf16*)p.a + (int64_t)m * p.lda + k0 + kc);
+                }
+            } else {
+                if (AF32) {
+                    a_reg[2 * i] = z;
+                    a_reg[2 * i + 1] = z;
+                } else {
+                    a_reg[i] = z;
+                }
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < W_PER; ++i) {
+            const int c = tid + 256 * i;
+            const int r = c >> 2, kc = (c & 3) * 8;
+            if (c < W_CHUNKS) w_reg[i] = *(gchunk)(p.w + (int64_t)w_row(r) * p.K + k0 + kc);
+        }
+    };
+    auto store = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < A_PER; ++i) {
+            const int c = tid + 256 * i;
+            if (c >= A_CHUNKS) continue;
+            const int r = c >> 2, kc = (c & 3) * 8;
+            u32x4 v;
+            if (AF32) {
+                f32x4 lo = __builtin_bit_cast(f32x4, a_reg[2 * i]);
+                f32x4 hi = __builtin_bit_cast(f32x4, a_reg[2 * i + 1]);
+                bf16x8 b = {f32_to_bf16(lo[0]), f32_to_bf16(lo[1]), f32_to_bf16(lo[2]), f32_to_bf16(lo[3]),
+                            f32_to_bf16(hi[0]), f32_to_bf16(hi[1]), f32_to_bf16(hi[2]), f32_to_bf16(hi[3])};
+                v = __builtin_bit_cast(u32x4, b);
+            } else {
+                v = a_reg[i];
+            }
+            *(u32x4*)(a_lds[buf] + r * LSTR + kc) = v;
+        }
+#pragma unroll
+        for (int i = 0; i < W_PER; ++i) {
+            const int c = tid + 256 * i;
+            if (c >= W_CHUNKS) continue;
+            const int r = c >> 2, kc = (c & 3) * 8;
+            *(u32x4*)(w_lds[buf] + r * LSTR + kc) = w_reg[i];
+        }
+    };
+
+    f32x16 acc[WNB][WMB];
+#pragma unroll
+    for (int i = 0; i < WNB; ++i)
+#pragma unroll
+        for (int j = 0; j < WMB; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    // W-tile row offset of this wave's n-block i
+    auto wrow_off = [&](int i) -> int { return p.geglu ? 32 * wn + (BNW / 2) * i : (BNW / 2) * wn + 32 * i; };
+
+    const int nk = p.K / BK;
+    load(0);
+    store(0);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+        const int buf = kt & 1;
+        if (kt + 1 < nk) load((kt + 1) * BK);
+#pragma unroll
+        for (int kk = 0; kk < BK / 16; ++kk) {
+            bf16x8 wop[WNB], aop[WMB];
+#pragma unroll
+            for (int i = 0; i < WNB; ++i)
+                wop[i] = *(const bf16x8*)(w_lds[buf] + (wrow_off(i) + col) * LSTR + 16 * kk + 8 * half);
+#pragma unroll
+            for (int j = 0; j < WMB; ++j)
+                aop[j] = *(const bf16x8*)(a_lds[buf] + (32 * WMB * wm + 32 * j + col) * LSTR + 16 * kk + 8 * half);
+#pragma unroll
+            for (int i = 0; i < WNB; ++i)
+#pragma unroll
+                for (int j = 0; j < WMB; ++j) acc[i][j] = mfma32x32x16(wop[i], aop[j], acc[i][j]);
+        }
+        if (kt + 1 < nk) store(buf ^ 1);
+        __syncthreads();
+    }
+
+    // Epilogue: lane holds token m = m-block base + col and features
+    // n-block base + 8*c + 4*half + (0..3) in registers 4c..4c+3.
+    const int n_blocks_out = p.geglu ? 1 : WNB;
+#pragma unroll
+    for (int i = 0; i < n_blocks_out; ++i) {
+#pragma unroll
+        for (int j = 0; j < WMB; ++j) {
+            const int m = m0 + 32 * WMB * wm + 32 * j + col;
+            if (m >= p.M) continue;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int nloc = p.geglu ? 32 * wn + 8 * c + 4 * half : (BNW / 2) * wn + 32 * i + 8 * c + 4 * half;
+                const int n = n0 + nloc;
+                float v[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * c + e];
+                if (p.bias != nullptr) {
+                    bf16x4 bv = *(const bf16x4*)(p.bias + n);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] += bf16_to_f32(bv[e]);
+                }
+                if (WNB == 2 && p.geglu) {
+                    float g[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) g[e] = acc[WNB - 1][j][4 * c + e];
+                    if (p.bias != nullptr) {
+                        bf16x4 bg = *(const bf16x4*)(p.bias + p.F + n);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) g[e] += bf16_to_f32(bg[e]);
+                    }
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] *= gelu_erf(g[e]);
+                }
+                if (p.resid != nullptr) {
+                    if (p.resid_f32) {
+                        f32x4 rv = *(const f32x4*)((const float*)p.resid + (int64_t)m * p.ldr + n);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) v[e] += rv[e];
+                    } else {
+                        bf16x4 rv = *(const bf16x4*)((const bf16*)p.resid + (int64_t)m * p.ldr + n);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) v[e] += bf16_to_f32(rv[e]);
+                    }
+                }
+                const int seg = n / p.seg;
+                const int ns = n - seg * p.seg;
+                void* dst = p.out[seg];
+                if (p.out_f32) {
+                    f32x4 o = {v[0], v[1], v[2], v[3]};
+                    *(f32x4*)((float*)dst + (int64_t)m * p.ldo + ns) = o;
+                } else {
+                    bf16x4 o = {f32_to_bf16(v[0]), f32_to_bf16(v[1]), f32_to_bf16(v[2]), f32_to_bf16(v[3])};
+                    *(bf16x4*)((bf16*)dst + (int64_t)m * p.ldo + ns) = o;
+                }
+            }
+        }
+    }
+}
+
+template <int WMB, int WNB>
+hipError_t launch_shape(const GemmParams& p, hipStream_t s) {
+    constexpr int BM = 64 * WMB;
+    const int bn_out = p.geglu ? 32 * WNB : 64 * WNB;
+    dim3 grid((p.M + BM - 1) / BM, p.N / bn_out);
+    if (p.a_f32)
+        gemm_kernel<WMB, WNB, true><<<grid, 256, 0, s>>>(p);
+    else
+        gemm_kernel<WMB, WNB, false><<<grid, 256, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bool gemm_shape_ok(const GemmParams& p) {
+    if (p.K % BK != 0 || p.M < 1 || p.N < 1) return false;
+    if (p.geglu) return p.N % 64 == 0;  // two n-blocks of 32 per workgroup pair
+    return p.N % 64 == 0 && p.seg % 4 == 0;
+}
+
+hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
+    // 128x128 tiles when they still give about a workgroup per compute unit,
+    // else 64x128 / 64x64.
+    if (p.geglu) return launch_shape<2, 2>(p, s);
+    const int64_t t128 = (int64_t)((p.M + 127) / 128) * (p.N / 128);
+    if (p.N % 128 == 0 && t128 >= 200) return launch_shape<2, 2>(p, s);
+    if (p.N % 128 == 0 && (int64_t)((p.M + 63) / 64) * (p.N / 128) >= 160) return launch_shape<1, 2>(p, s);
+    return launch_shape<1, 1>(p, s);
+}
+
+}  // namespace pcpp

@@ -128,3 +128,60 @@ def test_binding_refuses_to_load_without_library(tmp_path, monkeypatch):
     mod = importlib.util.module_from_spec(spec)
     with pytest.raises(ImportError):
         spec.loader.exec_module(mod)
+
+
+def _block_args(pcpp, **over):
+    w = pcpp.pcpp_block_weights_t()
+    for name, _ in pcpp.pcpp_block_weights_t._fields_[:-2]:
+        setattr(w, name, FAKE)
+    w.ff_inner = 2560
+    w.gn_groups = 32
+    a = dict(g=pcpp.make_geom(128, 128, 8, 3, 0.25, 10), w=w, x=FAKE, text=FAKE, nt=77, td=2048,
+             ku=FAKE, vu=FAKE, kd=FAKE, vd=FAKE, y=FAKE, ko=None, vo=None, ws=FAKE, wsb=1 << 40)
+    a.update(over)
+    return a
+
+
+def _block(pcpp, a):
+    return pcpp.lib().pcpp_transformer_block(
+        ctypes.byref(a["g"]), ctypes.byref(a["w"]), a["x"], a["text"], a["nt"], a["td"], a["ku"], a["vu"],
+        a["kd"], a["vd"], a["y"], a["ko"], a["vo"], a["ws"], a["wsb"], None)
+
+
+def test_block_validation_errors_before_launch():
+    from paper_2412_02962_amd import pcpp
+    E, N, W = pcpp.PCPP_EINVAL, pcpp.PCPP_ENOTSUP, pcpp.PCPP_EWORKSPACE
+    assert _block(pcpp, _block_args(pcpp, g=pcpp.make_geom(128, 128, 8, 3, 0.25, 10, head_dim=80))) == N
+    assert _block(pcpp, _block_args(pcpp, g=pcpp.make_geom(128, 128, 8, 3, 0.25, 10,
+                                                           dtype=pcpp.PCPP_DTYPE_F32))) == N
+    assert _block(pcpp, _block_args(pcpp, x=None)) == E
+    assert _block(pcpp, _block_args(pcpp, text=None)) == E
+    assert _block(pcpp, _block_args(pcpp, ku=None)) == E
+    assert _block(pcpp, _block_args(pcpp, td=100)) == E           # not a multiple of 32
+    assert _block(pcpp, _block_args(pcpp, nt=0)) == E
+    a = _block_args(pcpp)
+    a["w"].ff_inner = 100
+    assert _block(pcpp, a) == E
+    a = _block_args(pcpp)
+    a["w"].gn_groups = 7                                             # 640 % 7 != 0
+    assert _block(pcpp, a) == E
+    a = _block_args(pcpp)
+    a["w"].ff2_w = None
+    assert _block(pcpp, a) == E
+    a = _block_args(pcpp)
+    a["w"].proj_in_w = FAKE + 8                                      # misaligned weight
+    assert _block(pcpp, a) == E
+    need = pcpp.pcpp_transformer_block_workspace_size(a["g"], _block_args(pcpp)["w"], 77, 2048)
+    assert need > 0
+    assert _block(pcpp, _block_args(pcpp, ws=None)) == W
+    assert _block(pcpp, _block_args(pcpp, wsb=need - 1)) == W
+
+
+def test_block_workspace_size_scales_with_batch_and_rejects_invalid():
+    from paper_2412_02962_amd import pcpp
+    w = _block_args(pcpp)["w"]
+    one = pcpp.pcpp_transformer_block_workspace_size(pcpp.make_geom(128, 128, 8, 3, 0.25, 10), w, 77, 2048)
+    two = pcpp.pcpp_transformer_block_workspace_size(pcpp.make_geom(128, 128, 8, 3, 0.25, 10, batch=2), w, 77,
+                                                     2048)
+    assert 0 < one < two <= 2 * one + 4096
+    assert pcpp.pcpp_transformer_block_workspace_size(pcpp.make_geom(10, 128, 8, 3, 0.25, 10), w, 77, 2048) == 0

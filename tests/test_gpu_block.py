@@ -1,0 +1,116 @@
+"""GPU parity of pcpp_transformer_block against the float64 oracle block,
+through the C ABI, on seeded random-init SDXL-shaped weights.
+
+Tolerance: the GPU block stores the activations that feed each GEMM in bf16
+(GroupNorm/LayerNorm outputs, Q/K/V, attention outputs, the GEGLU hidden
+state) and rounds the output to bf16; the residual stream and every
+accumulation stay in float32.  Each bf16 rounding is a relative error of at
+most 2^-8 of that tensor.  The output rounding alone is up to 2^-8 |y|; the
+six rounded intermediates add errors of the same relative size to the
+branch outputs, which enter y through the residual sum.  The bound used is
+|dy| <= 2^-8 |y| + 6 * 2^-8 * rms(y) per element, with a mean absolute error
+below 2^-8 * rms(y).  The exported K and V sit behind three roundings (the
+GroupNorm output, the LayerNorm output and K/V themselves), so they use the
+same form with 3 in place of 6.  (The 2e-2 / 2e-3 tolerances of the
+attention kernel apply to attention outputs, whose magnitude is the
+weighted mean of values; K and V are unit-scale projections.)
+"""
+
+import dataclasses
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2412_02962_amd import synth
+from tests import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+def _run_block(bc, inp, batch, want_kv=True):
+    import torch
+    from paper_2412_02962_amd import pcpp
+    cfg = bc.attn
+    dev = gu.DEV
+    d = {k: gu.to_dev(v, "bf16") for k, v in inp.items()}
+    g = pcpp.make_geom(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, cfg.d, batch, 0, pcpp.PCPP_DTYPE_BF16)
+    w = pcpp.make_block_weights(d, bc.ff_inner, bc.gn_groups)
+    y = torch.empty_like(d["x"])
+    k_out = torch.empty_like(d["x"]) if want_kv else None
+    v_out = torch.empty_like(d["x"]) if want_kv else None
+    wsb = pcpp.pcpp_transformer_block_workspace_size(g, w, bc.n_text, bc.text_dim)
+    assert wsb > 0
+    ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    pcpp.pcpp_transformer_block(g, w, d["x"], d["text"], bc.n_text, bc.text_dim, d["k_up"], d["v_up"],
+                                d["k_dn"], d["v_dn"], y, k_out, v_out, ws, wsb)
+    torch.cuda.synchronize()
+    return y, k_out, v_out
+
+
+def _oracle_block(bc, inp):
+    cfg = bc.attn
+    f = {k: (None if v is None else oracle.from_bf16_bits(v)) for k, v in inp.items()}
+    wts = {k: f[k] for k in synth.block_weight_shapes(bc)}
+    return oracle.transformer_block(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, wts, f["x"], f["text"],
+                                    f["k_up"], f["v_up"], f["k_dn"], f["v_dn"], gn_groups=bc.gn_groups)
+
+
+def _check(y, want, stages=6, tag="block"):
+    err = np.abs(y - want)
+    rms = float(np.sqrt(np.mean(want ** 2)))
+    bound = 2.0 ** -8 * np.abs(want) + stages * 2.0 ** -8 * rms
+    worst = float((err / bound).max())
+    mean = float(err.mean())
+    print(f"{tag}: max-abs {err.max():.3e}, worst err/bound {worst:.3f}, mean-abs {mean:.3e}, rms {rms:.3f}")
+    assert worst <= 1.0, f"{tag}: max error exceeds bound by {worst:.2f}x"
+    assert mean <= 2.0 ** -8 * rms, f"{tag}: mean-abs {mean:.3e} > {2.0 ** -8 * rms:.3e}"
+
+
+def _check_kv(got, want, tag):
+    _check(got, want, stages=3, tag=tag)
+
+
+def test_block_matches_oracle_at_2048px():
+    bc = synth.BLOCK_CONFIG
+    _say("block", bc.name)
+    inp = synth.block_inputs(bc)
+    y, k, v = _run_block(bc, inp, 1)
+    want_y, want_k, want_v = _oracle_block(bc, inp)
+    _check(gu.to_f64(y), want_y)
+    _check_kv(gu.to_f64(k), want_k, "k export")
+    _check_kv(gu.to_f64(v), want_v, "v export")
+
+
+@pytest.mark.parametrize("geo", [
+    dict(H=12, W=20, n=3, i=1, p=0.5, heads=2),     # 80 tokens, ragged tiles
+    dict(H=16, W=16, n=4, i=0, p=0.25, heads=3),    # top band, C = 192
+    dict(H=16, W=16, n=4, i=3, p=1.0, heads=2),     # bottom band, whole neighbour
+])
+@pytest.mark.parametrize("batch", [1, 2])
+def test_block_small_shapes(geo, batch):
+    attn = synth.AttnConfig(name="blk", d=64, dtype="bf16", seed_id=50, **geo)
+    bc = synth.BlockConfig(name="blk", attn=attn, n_text=7, text_dim=96, ff_inner=128,
+                           gn_groups=4, seed_id=51)
+    _say("block small", geo, batch)
+    inp = synth.block_inputs(bc, batch=batch)
+    y, k, v = _run_block(bc, inp, batch)
+    want_y, want_k, want_v = _oracle_block(bc, inp)
+    _check(gu.to_f64(y), want_y)
+    _check_kv(gu.to_f64(k), want_k, "k export")
+    _check_kv(gu.to_f64(v), want_v, "v export")
+
+
+def test_block_without_kv_export_gives_same_output():
+    import torch
+    attn = synth.AttnConfig(name="blk", H=16, W=16, n=4, i=1, p=0.5, heads=2, d=64, dtype="bf16", seed_id=52)
+    bc = synth.BlockConfig(name="blk", attn=attn, n_text=5, text_dim=64, ff_inner=192, gn_groups=8, seed_id=53)
+    _say("block no export")
+    inp = synth.block_inputs(bc)
+    y1, _, _ = _run_block(bc, inp, 1, want_kv=True)
+    y2, _, _ = _run_block(bc, inp, 1, want_kv=False)
+    assert torch.equal(y1, y2)
