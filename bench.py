@@ -93,6 +93,103 @@ def cpu_baseline(cfg, inputs, budget_s=12.0):
                       f"{el:.1f} s, {el / n * 1e3:.1f} ms/step"}
 
 
+def block_flops(bc, n_kv):
+    """Algorithmic FLOPs of one transformer-block call (GEMMs + attention cores)."""
+    cfg = bc.attn
+    N, C, F, T, Td = cfg.n_q * cfg.batch, cfg.C, bc.ff_inner, bc.n_text * cfg.batch, bc.text_dim
+    gemm = 2.0 * N * C * (C + 3 * C + C + C + C + 2 * F + C) + 2.0 * N * F * C + 2.0 * T * Td * 2 * C
+    attn = 4.0 * N * n_kv * C + 4.0 * N * bc.n_text * C
+    return gemm + attn
+
+
+def graph_time_us(torch, fn, K, use_graph=True):
+    """Average microseconds per call of fn: K calls captured in one HIP graph
+    and replayed (or K eager calls)."""
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    if not use_graph:
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(K):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / K * 1e3
+    gr = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gr):
+        for _ in range(K):
+            fn()
+    gr.replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    gr.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / K * 1e3
+
+
+def extras(torch, pcpp, synth, dev, use_graph=True, reps=200):
+    """Context lines: materialised gather (GB/s vs HBM peak), the p = 0.5
+    variant of the 2048 px level-1 workload, and the full block."""
+    import numpy as np
+
+    def to_dev(x):
+        return None if x is None else torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(
+            torch.bfloat16).to(dev)
+
+    out = {}
+    cfg = synth.ATTN_CONFIGS[WORKLOAD]
+    d = {k: to_dev(v) for k, v in synth.attention_inputs(cfg).items()}
+    g = pcpp.make_geom(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, cfg.d, 1, 0, pcpp.PCPP_DTYPE_BF16)
+    _, _, _, n_kv = pcpp.pcpp_context_rows(g)
+    idx = torch.empty(n_kv, dtype=torch.int32, device=dev)
+    kc = torch.empty((1, n_kv, cfg.C), dtype=torch.bfloat16, device=dev)
+    vc = torch.empty_like(kc)
+    us = graph_time_us(torch, lambda: pcpp.pcpp_gather_context(g, d["k_fresh"], d["v_fresh"], d["k_up"], d["v_up"],
+                                                               d["k_dn"], d["v_dn"], idx, kc, vc), reps, use_graph)
+    gbytes = 2 * 2 * n_kv * cfg.C * 2 + 4 * n_kv
+    out["gather_us"] = round(us, 3)
+    out["gather_GBps"] = round(gbytes / us / 1e3, 1)
+    out["gather_frac_hbm"] = round(gbytes / us / 1e3 / PEAK_HBM_GBS, 4)
+
+    c50 = synth.ATTN_CONFIGS["sdxl2048_l1_p50"]
+    d50 = {k: to_dev(v) for k, v in synth.attention_inputs(c50).items()}
+    g50 = pcpp.make_geom(c50.H, c50.W, c50.n, c50.i, c50.p, c50.heads, c50.d, 1, 0, pcpp.PCPP_DTYPE_BF16)
+    _, _, _, nkv50 = pcpp.pcpp_context_rows(g50)
+    o50 = torch.empty_like(d50["q"])
+    w50 = pcpp.pcpp_partial_attention_workspace_size(g50)
+    ws50 = torch.empty(max(w50, 1), dtype=torch.uint8, device=dev)
+    us = graph_time_us(torch, lambda: pcpp.pcpp_partial_attention(g50, d50["q"], d50["k_fresh"], d50["v_fresh"],
+                                                                  d50["k_up"], d50["v_up"], d50["k_dn"],
+                                                                  d50["v_dn"], o50, ws50, w50), reps, use_graph)
+    out["p50_us"] = round(us, 3)
+    out["p50_TFLOPs"] = round(attn_flops(c50, nkv50) / us / 1e6, 1)
+
+    bc = synth.BLOCK_CONFIG
+    bcfg = bc.attn
+    bi = {k: to_dev(v) for k, v in synth.block_inputs(bc).items()}
+    gb = pcpp.make_geom(bcfg.H, bcfg.W, bcfg.n, bcfg.i, bcfg.p, bcfg.heads, bcfg.d, 1, 0, pcpp.PCPP_DTYPE_BF16)
+    _, _, _, nkvb = pcpp.pcpp_context_rows(gb)
+    wts = pcpp.make_block_weights(bi, bc.ff_inner, bc.gn_groups)
+    y = torch.empty_like(bi["x"])
+    ko = torch.empty_like(bi["x"])
+    vo = torch.empty_like(bi["x"])
+    wsb = pcpp.pcpp_transformer_block_workspace_size(gb, wts, bc.n_text, bc.text_dim)
+    wsb_t = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    us = graph_time_us(torch, lambda: pcpp.pcpp_transformer_block(gb, wts, bi["x"], bi["text"], bc.n_text,
+                                                                  bc.text_dim, bi["k_up"], bi["v_up"], bi["k_dn"],
+                                                                  bi["v_dn"], y, ko, vo, wsb_t, wsb), max(reps // 4, 1),
+                        use_graph)
+    out["block_us"] = round(us, 3)
+    out["block_TFLOPs"] = round(block_flops(bc, nkvb) / us / 1e6, 1)
+    out["block_gflop"] = round(block_flops(bc, nkvb) / 1e9, 2)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -101,6 +198,7 @@ def main():
     ap.add_argument("--workload", default=WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead of a graph")
+    ap.add_argument("--no-extras", action="store_true", help="skip the gather / p=0.5 / block context lines")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -199,6 +297,8 @@ def main():
         "extra": {"pct_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2), "eager_ms_per_call": round(eager_ms, 4),
                   "workspace_bytes": wsb, "gflop_per_step": round(flops / 1e9, 3)},
     }
+    if not args.no_extras:
+        res["extra"].update(extras(torch, pcpp, synth, dev, graph is not None, min(K, 200)))
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, inputs)
     print(json.dumps(res), flush=True)

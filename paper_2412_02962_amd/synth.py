@@ -15,7 +15,8 @@ Every tensor is drawn on the full token grid, patch by patch, from its own
 counter-keyed stream (seed, patch, tensor kind), so patch j's arrays are the
 same whichever patch is the local one.  Fresh activations are N(0, 1); the
 stale copy a neighbour holds from the previous step is fresh + sigma * N(0, 1)
-with sigma = 0.05 (the step-to-step drift the method relies on, Sec. 1).
+with sigma = 0.05 (the small step-to-step change the method relies on,
+abstract and Sec. 2.2).
 """
 
 from __future__ import annotations
