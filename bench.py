@@ -162,7 +162,7 @@ def extras(torch, pcpp, synth, dev, use_graph=True, reps=200):
     _, _, _, nkv50 = pcpp.pcpp_context_rows(g50)
     o50 = torch.empty_like(d50["q"])
     w50 = pcpp.pcpp_partial_attention_workspace_size(g50)
-    ws50 = torch.empty(max(w50, 1), dtype=torch.uint8, device=dev)
+    ws50 = torch.zeros(max(w50, 1), dtype=torch.uint8, device=dev)
     us = graph_time_us(torch, lambda: pcpp.pcpp_partial_attention(g50, d50["q"], d50["k_fresh"], d50["v_fresh"],
                                                                   d50["k_up"], d50["v_up"], d50["k_dn"],
                                                                   d50["v_dn"], o50, ws50, w50), reps, use_graph)
@@ -179,7 +179,7 @@ def extras(torch, pcpp, synth, dev, use_graph=True, reps=200):
     ko = torch.empty_like(bi["x"])
     vo = torch.empty_like(bi["x"])
     wsb = pcpp.pcpp_transformer_block_workspace_size(gb, wts, bc.n_text, bc.text_dim)
-    wsb_t = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    wsb_t = torch.zeros(wsb, dtype=torch.uint8, device=dev)
     us = graph_time_us(torch, lambda: pcpp.pcpp_transformer_block(gb, wts, bi["x"], bi["text"], bc.n_text,
                                                                   bc.text_dim, bi["k_up"], bi["v_up"], bi["k_dn"],
                                                                   bi["v_dn"], y, ko, vo, wsb_t, wsb), max(reps // 4, 1),
@@ -226,7 +226,7 @@ def main():
     h, up, dn, n_kv = pcpp.pcpp_context_rows(g)
     out = torch.empty_like(d["q"])
     wsb = pcpp.pcpp_partial_attention_workspace_size(g)
-    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    ws = torch.zeros(max(wsb, 1), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
     def step():

@@ -123,9 +123,17 @@ int pcpp_gather_context(const pcpp_geom_t* g,
                         void* stream);
 
 /*
- * Bytes of device workspace pcpp_partial_attention needs for geometry g
- * (0 when none is needed; the split-key-range path stores float32 partial
- * outputs and row statistics there).  Returns 0 for an invalid g.
+ * Bytes of device workspace pcpp_partial_attention needs for geometry g on
+ * the current device (bf16 path: per-query-block work counters plus float32
+ * partial outputs and row statistics of query blocks whose keys are split
+ * across workgroups; 0 for the f32 path).  Returns 0 for an invalid g.
+ *
+ * Workspace contract: the buffer must be zero-filled before its first use
+ * (e.g. hipMemset once after allocation).  Every call leaves its counters
+ * zero again and the layout does not depend on the geometry, so the same
+ * buffer (of the largest size needed) serves any number of later calls of
+ * any geometry on that device, graph replays included, without clearing.
+ * Calls that share one workspace must be ordered on one stream.
  */
 size_t pcpp_partial_attention_workspace_size(const pcpp_geom_t* g);
 
@@ -139,7 +147,8 @@ size_t pcpp_partial_attention_workspace_size(const pcpp_geom_t* g);
  *   k_up, v_up, k_dn, v_dn  whole stale neighbour bands as above
  *   out               [B, h*W, C], same dtype as the inputs
  *   workspace         device scratch of ws_bytes >= the workspace size
- *                     (may be NULL when that size is 0); not preserved
+ *                     (may be NULL when that size is 0), zero-filled before
+ *                     its first use (see the workspace contract above)
  * Supported: head_dim == 64 for both dtypes.  bf16 runs on the MFMA path
  * (float32 accumulation and softmax, probabilities rounded to bf16 as the
  * operand of the P*V product); f32 runs a float32 path.
@@ -184,7 +193,9 @@ typedef struct pcpp_block_weights {
     int32_t gn_groups;         /* groups dividing C                          */
 } pcpp_block_weights_t;
 
-/* Bytes of device workspace pcpp_transformer_block needs (0 if g invalid). */
+/* Bytes of device workspace pcpp_transformer_block needs (0 if g invalid).
+ * Same contract as the attention workspace: zero-filled before first use,
+ * reusable afterwards without clearing. */
 size_t pcpp_transformer_block_workspace_size(const pcpp_geom_t* g,
                                              const pcpp_block_weights_t* w,
                                              int32_t n_text, int32_t text_dim);
@@ -212,7 +223,7 @@ size_t pcpp_transformer_block_workspace_size(const pcpp_geom_t* g,
  * C <= 2048 (PCPP_ENOTSUP), text_dim >= 32 with text_dim % 32 == 0,
  * n_text >= 1, ff_inner % 64 == 0, C % gn_groups == 0 (PCPP_EINVAL).  All
  * pointers, weights included, must be 16-byte aligned (PCPP_EINVAL).
- * Workspace contents are scratch and not preserved between calls.
+ * The workspace follows the contract above (zero-filled before first use).
  */
 int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w,
                            const void* x, const void* text, int32_t n_text,

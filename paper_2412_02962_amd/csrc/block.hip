@@ -52,13 +52,35 @@ int validate_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, int32_t 
     return PCPP_OK;
 }
 
+AttnParams self_attn_params(const pcpp_geom_t* g, const Geo& r, const void* q, void* out, const void* k,
+                            const void* v, const void* k_up, const void* v_up, const void* k_dn, const void* v_dn,
+                            void*) {
+    return make_attn_params(g, r, q, out, make_kv_source(g, r, k, v, k_up, v_up, k_dn, v_dn));
+}
+
+// Cross-attention: one key segment of n_text tokens per image.
+AttnParams cross_attn_params(const pcpp_geom_t* g, const Geo& r, const void* q, void* out, const void* k2,
+                             const void* v2, int32_t n_text) {
+    KvSource kv;
+    kv.k[0] = kv.k[2] = nullptr;
+    kv.v[0] = kv.v[2] = nullptr;
+    kv.k[1] = k2;
+    kv.v[1] = v2;
+    kv.bstride[0] = kv.bstride[1] = kv.bstride[2] = (int64_t)n_text * r.C;
+    kv.end0 = 0;
+    kv.end1 = n_text;
+    kv.n_kv = n_text;
+    return make_attn_params(g, r, q, out, kv);
+}
+
 BlockLayout layout(const pcpp_geom_t* g, const Geo& r, const pcpp_block_weights_t* w, int32_t n_text) {
     BlockLayout L;
     const size_t rows = (size_t)g->batch * r.nq;
     const size_t C = r.C;
-    const AttnPlan ps = plan_attention_bf16(r.nq, r.n_kv, g->heads, g->batch, r.C);
-    const AttnPlan pc = plan_attention_bf16(r.nq, n_text, g->heads, g->batch, r.C);
-    L.attn_ws_bytes = ps.ws_bytes > pc.ws_bytes ? ps.ws_bytes : pc.ws_bytes;
+    const size_t ps = attention_bf16_ws_bytes(self_attn_params(g, r, nullptr, nullptr, nullptr, nullptr,
+                                                                 nullptr, nullptr, nullptr, nullptr, nullptr));
+    const size_t pc = attention_bf16_ws_bytes(cross_attn_params(g, r, nullptr, nullptr, nullptr, nullptr, n_text));
+    L.attn_ws_bytes = ps > pc ? ps : pc;
     size_t off = 0;
     auto take = [&](size_t bytes) {
         size_t o = off;
@@ -199,14 +221,8 @@ PCPP_EXPORT int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_we
         PCPP_CHECK(launch_gemm(qkv, s));
     }
     {
-        KvSource kv = make_kv_source(g, r, k16, v16, k_up, v_up, k_dn, v_dn);
-        AttnParams ap = make_attn_params(g, r, q16, a16, kv);
-        AttnPlan pl = plan_attention_bf16(N, r.n_kv, g->heads, B, C);
-        ap.splits = pl.splits;
-        ap.tiles_per_split = pl.tiles_per_split;
-        ap.ws_o = (float*)attn_ws;
-        ap.ws_ml = (float*)((char*)attn_ws + (size_t)pl.splits * B * N * C * sizeof(float));
-        PCPP_CHECK(launch_attention_bf16(ap, s));
+        AttnParams ap = self_attn_params(g, r, q16, a16, k16, v16, k_up, v_up, k_dn, v_dn, nullptr);
+        PCPP_CHECK(launch_attention_bf16(ap, attn_ws, L.attn_ws_bytes, s));
     }
     {
         GemmParams o = gemm(a16, C, false, w->attn1_out_w, w->attn1_out_b, rows, C, C, hid, C, true);
@@ -228,22 +244,8 @@ PCPP_EXPORT int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_we
         PCPP_CHECK(launch_gemm(kv, s));
     }
     {
-        KvSource kv;
-        kv.k[0] = kv.k[2] = nullptr;
-        kv.v[0] = kv.v[2] = nullptr;
-        kv.k[1] = k2;
-        kv.v[1] = v2;
-        kv.bstride[0] = kv.bstride[1] = kv.bstride[2] = (int64_t)T * C;
-        kv.end0 = 0;
-        kv.end1 = T;
-        kv.n_kv = T;
-        AttnParams ap = make_attn_params(g, r, q16, a16, kv);
-        AttnPlan pl = plan_attention_bf16(N, T, g->heads, B, C);
-        ap.splits = pl.splits;
-        ap.tiles_per_split = pl.tiles_per_split;
-        ap.ws_o = (float*)attn_ws;
-        ap.ws_ml = (float*)((char*)attn_ws + (size_t)pl.splits * B * N * C * sizeof(float));
-        PCPP_CHECK(launch_attention_bf16(ap, s));
+        AttnParams ap = cross_attn_params(g, r, q16, a16, k2, v2, T);
+        PCPP_CHECK(launch_attention_bf16(ap, attn_ws, L.attn_ws_bytes, s));
     }
     {
         GemmParams o = gemm(a16, C, false, w->attn2_out_w, w->attn2_out_b, rows, C, C, hid, C, true);

@@ -32,21 +32,12 @@ struct AttnParams {
     KvSource kv;
     float scale_log2;     // log2(e) / sqrt(head_dim)
     float scale;          // 1 / sqrt(head_dim)
-    int32_t splits;       // key-range splits (1 = no workspace)
-    int32_t tiles_per_split;  // 64-key tiles per split
-    float* ws_o;          // [splits, B, nq, C] normalised partial outputs
-    float* ws_ml;         // [splits, B, heads, nq, 2] (row max in log2 units, row sum)
 };
 
-// Planning of the bf16 path: number of key-range splits for a geometry.
-struct AttnPlan {
-    int32_t splits;
-    int32_t tiles_per_split;
-    size_t ws_bytes;
-};
-AttnPlan plan_attention_bf16(int32_t nq, int32_t n_kv, int32_t heads, int32_t batch, int32_t C);
-
-hipError_t launch_attention_bf16(const AttnParams& p, hipStream_t stream);
+// bf16 path: workspace bytes it needs (work counters and float32 partial
+// results of query blocks split across workgroups) and the launch.
+size_t attention_bf16_ws_bytes(const AttnParams& p);
+hipError_t launch_attention_bf16(const AttnParams& p, void* ws, size_t ws_bytes, hipStream_t stream);
 hipError_t launch_attention_f32(const AttnParams& p, hipStream_t stream);
 
 // Context assembly: contiguous segment copies plus the index set.

@@ -48,8 +48,8 @@ KvSource make_kv_source(const pcpp_geom_t* g, const Geo& r, const void* k_fresh,
     KvSource s;
     const int64_t band = (int64_t)r.nq * r.C;  // elements of one whole band
     const int64_t skip_up = (int64_t)(r.h - r.up) * g->W * r.C * r.esize;
-    s.k[0] = r.up > 0 ? (const char*)k_up + skip_up : nullptr;
-    s.v[0] = r.up > 0 ? (const char*)v_up + skip_up : nullptr;
+    s.k[0] = (r.up > 0 && k_up) ? (const char*)k_up + skip_up : nullptr;
+    s.v[0] = (r.up > 0 && v_up) ? (const char*)v_up + skip_up : nullptr;
     s.k[1] = k_fresh;
     s.v[1] = v_fresh;
     s.k[2] = r.dn > 0 ? k_dn : nullptr;
@@ -94,10 +94,6 @@ AttnParams make_attn_params(const pcpp_geom_t* g, const Geo& r, const void* q, v
     p.kv = kv;
     p.scale = (float)(1.0 / sqrt((double)g->head_dim));
     p.scale_log2 = (float)(1.4426950408889634 / sqrt((double)g->head_dim));
-    p.splits = 1;
-    p.tiles_per_split = 1 << 30;
-    p.ws_o = nullptr;
-    p.ws_ml = nullptr;
     return p;
 }
 
@@ -162,7 +158,8 @@ PCPP_EXPORT size_t pcpp_partial_attention_workspace_size(const pcpp_geom_t* g) {
     Geo r;
     if (validate_geom(g, &r) != PCPP_OK) return 0;
     if (g->dtype != PCPP_DTYPE_BF16 || g->head_dim != 64) return 0;
-    return plan_attention_bf16(r.nq, r.n_kv, g->heads, g->batch, r.C).ws_bytes;
+    KvSource kv = make_kv_source(g, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
+    return attention_bf16_ws_bytes(make_attn_params(g, r, nullptr, nullptr, kv));
 }
 
 PCPP_EXPORT int pcpp_partial_attention(const pcpp_geom_t* g, const void* q, const void* k_fresh,
@@ -176,18 +173,10 @@ PCPP_EXPORT int pcpp_partial_attention(const pcpp_geom_t* g, const void* q, cons
     AttnParams p = make_attn_params(g, r, q, out, kv);
     hipError_t e;
     if (g->dtype == PCPP_DTYPE_BF16) {
-        AttnPlan pl = plan_attention_bf16(r.nq, r.n_kv, g->heads, g->batch, r.C);
-        if (pl.ws_bytes > 0) {
-            if (workspace == nullptr || ws_bytes < pl.ws_bytes) return PCPP_EWORKSPACE;
-            if (!aligned16(workspace)) return PCPP_EINVAL;
-        }
-        p.splits = pl.splits;
-        p.tiles_per_split = pl.tiles_per_split;
-        p.ws_o = (float*)workspace;
-        p.ws_ml = pl.ws_bytes > 0 ? (float*)((char*)workspace + (size_t)pl.splits * g->batch * r.nq * r.C *
-                                                                    sizeof(float))
-                                  : nullptr;
-        e = launch_attention_bf16(p, (hipStream_t)stream);
+        const size_t need = attention_bf16_ws_bytes(p);
+        if (workspace == nullptr || ws_bytes < need) return PCPP_EWORKSPACE;
+        if (!aligned16(workspace)) return PCPP_EINVAL;
+        e = launch_attention_bf16(p, workspace, ws_bytes, (hipStream_t)stream);
     } else {
         e = launch_attention_f32(p, (hipStream_t)stream);
     }

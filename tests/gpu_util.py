@@ -49,7 +49,7 @@ def run_attention(cfg, inputs, g=None, stream=None):
     d = {k: to_dev(v, cfg.dtype) for k, v in inputs.items()}
     out = torch.empty_like(d["q"])
     ws_bytes = pcpp.pcpp_partial_attention_workspace_size(g)
-    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=DEV)
+    ws = torch.zeros(max(ws_bytes, 1), dtype=torch.uint8, device=DEV)
     pcpp.pcpp_partial_attention(g, d["q"], d["k_fresh"], d["v_fresh"], d["k_up"], d["v_up"], d["k_dn"],
                                 d["v_dn"], out, ws, ws_bytes, stream)
     torch.cuda.synchronize()

@@ -2,7 +2,6 @@
 float64 oracle, through the C ABI, on seeded synthetic inputs."""
 
 import dataclasses
-import os
 
 import numpy as np
 import pytest
@@ -103,21 +102,57 @@ def test_stale_rows_outside_window_never_read():
     assert bool((got == ref).all())
 
 
-def test_split_and_unsplit_paths_agree_with_oracle():
-    cfg = synth.ATTN_CONFIGS["sdxl2048_l1_p50"]
+def test_workspace_reuse_across_geometries():
+    # one zero-filled workspace serves calls of different geometries in a row:
+    # the per-block work counters must come back to zero after every call
+    import torch
+    from paper_2412_02962_amd import pcpp
+    names = ["sdxl2048_l1_p50", "sdxl1024_l1", "sdxl2048_l2_edge", "sdxl2048_l1_p50", "sdxl1024_l1"]
+    cfgs = [synth.ATTN_CONFIGS[n] for n in names]
+    need = max(pcpp.pcpp_partial_attention_workspace_size(gu.geom(c)) for c in cfgs)
+    ws = torch.zeros(need, dtype=torch.uint8, device=gu.DEV)
+    for n, cfg in zip(names, cfgs):
+        _say("reuse", n)
+        inp = synth.attention_inputs(cfg)
+        d = {k: gu.to_dev(v, cfg.dtype) for k, v in inp.items()}
+        out = torch.empty_like(d["q"])
+        pcpp.pcpp_partial_attention(gu.geom(cfg), d["q"], d["k_fresh"], d["v_fresh"], d["k_up"], d["v_up"],
+                                    d["k_dn"], d["v_dn"], out, ws, need)
+        torch.cuda.synchronize()
+        gu.assert_close(cfg, gu.to_f64(out), gu.oracle_attention(cfg, inp), f"reuse {n}")
+
+
+def test_graph_replays_match_eager():
+    import torch
+    from paper_2412_02962_amd import pcpp
+    cfg = synth.ATTN_CONFIGS["sdxl2048_l1_p25"]
+    _say("graph replays")
     inp = synth.attention_inputs(cfg)
-    want = gu.oracle_attention(cfg, inp)
-    old = os.environ.get("PCPP_ATTN_SPLITS")
-    try:
-        for s in ("1", "3", "7"):
-            _say("splits", s)
-            os.environ["PCPP_ATTN_SPLITS"] = s
-            gu.assert_close(cfg, gu.to_f64(gu.run_attention(cfg, inp)), want, f"splits={s}")
-    finally:
-        if old is None:
-            os.environ.pop("PCPP_ATTN_SPLITS", None)
-        else:
-            os.environ["PCPP_ATTN_SPLITS"] = old
+    d = {k: gu.to_dev(v, cfg.dtype) for k, v in inp.items()}
+    g = gu.geom(cfg)
+    wsb = pcpp.pcpp_partial_attention_workspace_size(g)
+    ws = torch.zeros(wsb, dtype=torch.uint8, device=gu.DEV)
+    out = torch.empty_like(d["q"])
+
+    def call():
+        pcpp.pcpp_partial_attention(g, d["q"], d["k_fresh"], d["v_fresh"], d["k_up"], d["v_up"], d["k_dn"],
+                                    d["v_dn"], out, ws, wsb)
+
+    call()
+    torch.cuda.synchronize()
+    eager = out.clone()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        call()
+    for rep in range(3):
+        out.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager), f"replay {rep} differs"
+        call()  # eager work between replays on the same workspace
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager)
 
 
 def test_virtual_patches_each_match_oracle():

@@ -45,7 +45,7 @@ def _run_block(bc, inp, batch, want_kv=True):
     v_out = torch.empty_like(d["x"]) if want_kv else None
     wsb = pcpp.pcpp_transformer_block_workspace_size(g, w, bc.n_text, bc.text_dim)
     assert wsb > 0
-    ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    ws = torch.zeros(wsb, dtype=torch.uint8, device=dev)
     pcpp.pcpp_transformer_block(g, w, d["x"], d["text"], bc.n_text, bc.text_dim, d["k_up"], d["v_up"],
                                 d["k_dn"], d["v_dn"], y, k_out, v_out, ws, wsb)
     torch.cuda.synchronize()
