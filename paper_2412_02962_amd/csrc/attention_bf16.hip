@@ -3,42 +3,46 @@
 // Computes, per image and head, softmax(Q K_ctx^T / sqrt(64)) V_ctx where
 // the key/value context is the band's fresh tokens plus the stale boundary
 // rows of its neighbours (Sec. 3.3 and Eq. 1 of arXiv 2412.02962).  The three
-// key/value sources are read in place (no assembled copy): every key row of a
-// 32-key tile picks its source from its token index.
+// key/value sources are read in place (no assembled copy): a 64-key tile that
+// lies inside one source is fetched from that source's base; a tile that
+// straddles two sources (or the end) picks the source row by row.
 //
-// Work decomposition.  A unit is one 32-key tile of one 64-query block of one
-// (image, head).  The query blocks are dealt out to the XCDs in contiguous
-// ranges (consecutive blocks share a head, hence keys, in that XCD's L2);
-// inside an XCD the units of its blocks, in (block, tile) order, are cut into
-// equal contiguous ranges, one per workgroup, two workgroups per compute
-// unit.  Workgroup w runs on XCD w % n_xcd (the hardware deals workgroups out
-// round-robin), so every workgroup that shares a block shares an L2: a block
-// split between workgroups is merged through that L2 with ordinary stores and
-// one counter per split block (the last contributor to arrive merges and
-// resets the counter to zero), without any cache-wide writeback.
+// Work decomposition.  A block is 128 queries of one (image, head); its key
+// tiles are cut into k equal pieces (k = 2 * compute units / blocks, so that
+// every compute unit holds two workgroups at once) and a workgroup computes
+// one piece of one block.  The blocks are dealt out to the XCDs in
+// contiguous ranges and all pieces of a block run on one XCD: workgroup w
+// runs on XCD w % n_xcd (the hardware deals workgroups out round-robin), so
+// the pieces of a block are merged through that XCD's L2 with ordinary
+// stores and one counter per block (the last piece to arrive merges and
+// resets the counter to zero).  Pieces of the blocks of one head start on
+// the same key tiles, so their tiles are fetched from HBM once and then hit
+// in the L2.
 //
-// Inside a workgroup: 4 wavefronts, one per SIMD, split the tiles of the
-// current block; each streams its own tiles through a private LDS ring (two K
-// and two V slots, filled with direct global->LDS loads) and synchronises
-// with nobody until the block's tiles are done, so the two workgroups on a
-// compute unit interleave MFMA and softmax work freely.  The wavefronts'
-// partial results are then merged through LDS.
+// Inside a workgroup the four wavefronts (one per SIMD) own 32 queries each
+// and walk the same key tiles, staged once per workgroup in LDS by direct
+// global->LDS loads into three K and three V slots (tile t+2's keys and tile
+// t+1's values load while tile t is computed; one barrier per tile).  The
+// second workgroup of the compute unit puts a second wavefront on every SIMD.
 //
-// Per 32-key tile and wavefront (64 queries = two 32-query column blocks):
-//   S^T = K Q^T      8 MFMA 32x32x16; K from LDS, Q^T in registers.  The
-//                    transposed product leaves each lane with one query and
-//                    16 of the tile's keys: a row max needs one exchange
-//                    with the partner lane (lane ^ 32), the row sum none.
+// Software pipeline over 32-key half-tiles h.  Step h holds S(h) (scores of
+// half h) and P(h-1) (bf16 probabilities of half h-1) in registers and
+// interleaves, one matrix product at a time, the VALU softmax of S(h) with
+// the 8 MFMA 32x32x16 of O^T += V(h-1)^T P(h-1)^T and S(h+1)^T = K(h+1) Q^T;
+// the LDS operands of step h+1 are read during step h.
+//   S^T = K Q^T      K from LDS, Q^T in registers.  The transposed product
+//                    leaves each lane with one query and 16 keys of the
+//                    half: a row max needs one exchange with the partner
+//                    lane (lane ^ 32), the row sum none.
 //   online softmax   in log2 units, p = exp2(s*log2(e)/8 - m) against the
-//                    running max m; the tile max is only taken (and m
+//                    running max m; the half's max is only taken (and m
 //                    raised, O and l rescaled) when a lane's probabilities
-//                    of the tile sum to 2^20 or more, so p < 2^20.
-//   O^T += V^T P^T   8 MFMA 32x32x16; P^T is the B operand taken straight
-//                    from the S^T accumulators (inside each 16-key step the
-//                    key order is permuted the same way on both operands);
-//                    V^T comes from the row-major V tile through the
-//                    transposing LDS read ds_read_b64_tr_b16.
-// Tile x-1's P V MFMAs run while the softmax of tile x is computed.
+//                    of the half sum to 2^20 or more, so p < 2^20.
+//   O^T += V^T P^T   P^T is the B operand taken straight from the S^T
+//                    accumulators (inside each 16-key step the key order is
+//                    permuted the same way on both operands); V^T comes from
+//                    the row-major V tile through the transposing LDS read
+//                    ds_read_b64_tr_b16.
 // Row sums accumulate the bf16 probabilities with v_dot2 against (1, 1), so
 // numerator and denominator see the same rounded weights.
 
@@ -52,44 +56,44 @@ namespace pcpp {
 namespace {
 
 constexpr int D = 64;
-constexpr int TILE = 32;                   // keys per tile
-constexpr int QB = 64;                     // queries per block
-constexpr int NW = 4;                      // wavefronts per workgroup
+constexpr int KT = 64;                      // keys per tile
+constexpr int QW = 32;                      // queries per wavefront
+constexpr int NW = 4;                       // wavefronts per workgroup
+constexpr int QB = QW * NW;                 // queries per block
 constexpr int NTHREADS = 64 * NW;
 constexpr int WG_PER_CU = 2;
-constexpr int TILE_BYTES = TILE * D * 2;   // 4 KB of K or of V
-constexpr int LOADS_PER_TILE = TILE_BYTES / 1024;  // 1 KB direct-to-LDS loads
-constexpr int OSTR = 68;                   // merge buffer row stride (floats)
-constexpr int RING_BYTES = NW * TILE_BYTES > QB * OSTR * 4 ? NW * TILE_BYTES : QB * OSTR * 4;
-constexpr float P_LIMIT = 1048576.0f;      // 2^20: bound on a lane's probability sum per tile
-constexpr int PIECE_SLOTS = 2;             // partial-result slots per workgroup
-constexpr int MIN_TILES_PER_WAVE = 4;
-constexpr int CUS_PER_XCD = 32;            // gfx950
+constexpr int TILE_BYTES = KT * D * 2;      // 8 KB of K or of V
+constexpr int SLOTS = 3;                    // LDS slots for K tiles, and for V tiles
+constexpr int V_REGION = SLOTS * TILE_BYTES;
+constexpr float P_LIMIT = 1048576.0f;       // 2^20: bound on a lane's probability sum per half-tile
+constexpr int MIN_TILES_PER_PIECE = 2;
+constexpr int CUS_PER_XCD = 32;             // gfx950
 
-static_assert(WG_PER_CU * (4 * RING_BYTES + NW * QB * 2 * 4 + 16) <= 160 * 1024,
-              "two workgroups share a compute unit's LDS");
+static_assert(WG_PER_CU * 2 * V_REGION + 64 <= 160 * 1024, "two workgroups share a compute unit's LDS");
+static_assert(TILE_BYTES / 1024 == 2 * NW, "each wavefront stages two 1 KB pieces of a K (and a V) tile");
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef const __attribute__((address_space(1))) void* gptr_t;
 typedef __attribute__((address_space(3))) void* lptr_t;
 
 // LDS swizzles: 16-byte chunk c of tile row r is stored at slot c ^ mask(r).
-// K rows are read 16 bytes per lane by 16 consecutive rows at one chunk; V
-// rows by four rows x 32 bytes per 16 lanes (transposing read).
+// K rows are read 16 bytes per lane by 32 consecutive rows at one chunk; V
+// rows by four rows x 32 bytes per 16 lanes (transposing read).  Both masks
+// repeat every 16 rows, so a half-tile (32 rows) offset keeps them.
 __device__ __forceinline__ int k_mask(int r) { return (r >> 1) & 7; }
 __device__ __forceinline__ int v_mask(int r) { return ((r >> 1) & 3) << 1; }
 
 struct Sched {
     int32_t n_xcd;      // XCDs; workgroup w runs on XCD w % n_xcd
-    int32_t per_xcd;    // workgroups per XCD
-    int32_t n_tiles;    // key tiles per query block
-    int32_t nqb;        // query blocks per (image, head)
-    int64_t n_blocks;   // query blocks in total
-    int32_t whole;      // 1: ranges hold whole blocks only (no merging across workgroups)
+    int32_t bpx;        // blocks per XCD (the last XCD may hold fewer)
+    int32_t k;          // pieces per block
+    int32_t n_tiles;    // key tiles per block
+    int32_t nqb;        // blocks per (image, head)
+    int32_t n_blocks;   // blocks in total
     int* xcc_of;        // [grid]: XCC id + 1 each workgroup ran on (diagnostic)
-    int* counters;      // [grid]: zero at launch, left zero
-    float* part_o;      // [grid * PIECE_SLOTS][QB][D]
-    float* part_ml;     // [grid * PIECE_SLOTS][QB][2]
+    int* counters;      // [n_blocks]: zero at launch, left zero
+    float* part_o;      // [grid][QB * D] partial outputs of pieces
+    float* part_ml;     // [grid][QB][2] their row statistics
 };
 
 __device__ __forceinline__ int64_t pick(int j, int end0, int end1, int64_t a0, int64_t a1, int64_t a2) {
@@ -97,34 +101,22 @@ __device__ __forceinline__ int64_t pick(int j, int end0, int end1, int64_t a0, i
     return j < end0 ? a0 : a12;
 }
 
-// Transposing LDS reads of one V^T operand (rows p and p + 8 rows), in
-// inline assembly: the compiler sees no address for them, so it does not
-// order them after the direct-to-LDS loads still in flight into other ring
-// slots.  Their results are complete only after lds_wait().
-__device__ __forceinline__ void lds_read_tr2(const char* p, u32x2& lo, u32x2& hi) {
-    const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)p;
-    asm volatile("ds_read_b64_tr_b16 %0, %2\n\tds_read_b64_tr_b16 %1, %2 offset:1024"
-                 : "=&v"(lo), "=&v"(hi)
-                 : "v"(a));
-}
-// Waits for every outstanding LDS read; the operands tie the wait to the
-// registers the reads wrote.
-__device__ __forceinline__ void lds_wait(u32x2 (&v)[8]) {
-    asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]), "+v"(v[7]));
-}
-// The four 16-byte K reads of one score product (chunks c0, c0+2, c0+4,
-// c0+6 of a row, each at its swizzled slot), in inline assembly for the
-// same reason, followed by their wait.
-__device__ __forceinline__ void lds_read_k4(const char* row, int c0, int mask, u32x4 (&k)[4]) {
-    const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)row;
-    const uint32_t a0 = a + (((c0 + 0) ^ mask) << 4), a1 = a + (((c0 + 2) ^ mask) << 4);
-    const uint32_t a2 = a + (((c0 + 4) ^ mask) << 4), a3 = a + (((c0 + 6) ^ mask) << 4);
-    asm volatile(
-        "ds_read_b128 %0, %4\n\tds_read_b128 %1, %5\n\tds_read_b128 %2, %6\n\tds_read_b128 %3, %7\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(k[0]), "=&v"(k[1]), "=&v"(k[2]), "=&v"(k[3])
-        : "v"(a0), "v"(a1), "v"(a2), "v"(a3));
+// LDS operands of one pipeline step: K of a half-tile (four 16-byte chunks
+// per lane) and V^T of a half-tile (32-dim block mb, 16-key step st).
+struct Operands {
+    bf16x8 k[4];
+    bf16x8 v[2][2];  // [mb][st]
+};
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+// Two transposing reads (rows p and p + 8 of a V tile) form one V^T operand.
+__device__ __forceinline__ bf16x8 read_vt(const char* p) {
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 1024));
+    const short __attribute__((ext_vector_type(8))) w = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(bf16x8, w);
 }
 
 // Value of lanes l and l ^ 32 combined, without an LDS round trip.
@@ -137,25 +129,18 @@ __device__ __forceinline__ float sum_xor32(float v) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Workgroup of XCD-local index j owns units [T*j/J, T*(j+1)/J) of its XCD's
-// T units (or, with whole blocks, the blocks [B*j/J, B*(j+1)/J)).
-__device__ __forceinline__ int64_t range_start(int64_t T, int64_t nblk, int n_tiles, int j, int J, bool whole) {
-    return whole ? nblk * j / J * n_tiles : T * j / J;
-}
-// Workgroup whose range holds unit u (ranges may be empty when J > T).
-__device__ __forceinline__ int owner_of(int64_t u, int64_t T, int J) { return (int)(((u + 1) * J - 1) / T); }
+#define SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
 
 __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnParams p, Sched sc) {
-    // Separate arrays per ring slot: with distinct objects the compiler can
-    // tell a direct-to-LDS load into one slot from reads of another and does
-    // not make those reads wait for the loads.  Wavefront w uses bytes
-    // [w*4K, (w+1)*4K) of each; after a block the four arrays are the four
-    // wavefronts' merge buffers.
-    __shared__ __attribute__((aligned(16))) char kring0[RING_BYTES];
-    __shared__ __attribute__((aligned(16))) char kring1[RING_BYTES];
-    __shared__ __attribute__((aligned(16))) char vring0[RING_BYTES];
-    __shared__ __attribute__((aligned(16))) char vring1[RING_BYTES];
-    __shared__ __attribute__((aligned(16))) float ml_lds[NW * QB * 2];  // (m, l) per wavefront and query
+    // Three K and three V slots, each its own object: a direct-to-LDS load
+    // in flight into one slot is then known not to touch the others, and the
+    // compiler orders LDS reads of the other slots freely.
+    __shared__ __attribute__((aligned(16))) char ks0[TILE_BYTES];
+    __shared__ __attribute__((aligned(16))) char ks1[TILE_BYTES];
+    __shared__ __attribute__((aligned(16))) char ks2[TILE_BYTES];
+    __shared__ __attribute__((aligned(16))) char vs0[TILE_BYTES];
+    __shared__ __attribute__((aligned(16))) char vs1[TILE_BYTES];
+    __shared__ __attribute__((aligned(16))) char vs2[TILE_BYTES];
     __shared__ int flag_lds;
 
     const int tid = threadIdx.x;
@@ -165,63 +150,76 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
     const int half = lane >> 5;
     const int C = p.C;
     const int kv_end = p.kv.n_kv;
+    const int end0 = p.kv.end0, end1 = p.kv.end1;
     const float sl2 = p.scale_log2;
     const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
     const int n_tiles = sc.n_tiles;
 
     const int x = blockIdx.x % sc.n_xcd;
     const int j = blockIdx.x / sc.n_xcd;
-    const int J = sc.per_xcd;
+    const int bl = j / sc.k;            // block, XCD-local
+    const int piece = j - bl * sc.k;
+    const int blk = x * sc.bpx + bl;
+    if (bl >= sc.bpx || blk >= sc.n_blocks) return;  // idle slot of the last XCD (uniform)
     if (tid == 0) sc.xcc_of[blockIdx.x] = (__builtin_amdgcn_s_getreg(0xf814) & 15) + 1;  // HW_REG_XCC_ID
+    const int t0 = (int)((int64_t)n_tiles * piece / sc.k);
+    const int t1 = (int)((int64_t)n_tiles * (piece + 1) / sc.k);
 
-    const int64_t bx0 = sc.n_blocks * x / sc.n_xcd;
-    const int64_t nblk = sc.n_blocks * (x + 1) / sc.n_xcd - bx0;
-    const int64_t T = nblk * n_tiles;
-    const bool whole = sc.whole != 0;
-    const int64_t s_j = range_start(T, nblk, n_tiles, j, J, whole);
-    const int64_t e_j = range_start(T, nblk, n_tiles, j + 1, J, whole);
+    // Staging geometry: wavefront w fills the 1 KB pieces 2w and 2w+1 of a
+    // tile (rows 8*piece .. +8); lane l fills LDS slot l & 7 of row
+    // 8*piece + (l >> 3) with the global chunk the swizzle puts there.
+    int ld_row[2];
+    uint32_t ld_koff[2], ld_voff[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int r = 8 * (2 * wave + i) + (lane >> 3);
+        ld_row[i] = r;
+        ld_koff[i] = (uint32_t)(r * C * 2 + (((lane & 7) ^ k_mask(r)) << 4));
+        ld_voff[i] = (uint32_t)(r * C * 2 + (((lane & 7) ^ v_mask(r)) << 4));
+    }
 
-    // transposing-read lane geometry inside a V tile
-    const int jj = lane & 15;
-    const int tr_row = 4 * half + (jj >> 2);
-    const int tr_e = 16 * ((lane >> 4) & 1) + 4 * (jj & 3);
-    const int wbase = wave * TILE_BYTES;
+    // K operand reads (within a half-tile of a K slot): row col, chunks
+    // 2*kk + half at their swizzled slots.
+    int k_rel[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) k_rel[kk] = col * 128 + (((2 * kk + half) ^ k_mask(col)) << 4);
+    // Transposing V reads (within a half-tile of a V slot), per 32-dim block
+    // mb and 16-key step st.
+    int v_rel[2];
+    {
+        const int jj = lane & 15;
+        const int tr_row = 4 * half + (jj >> 2);
+        const int tr_e = 16 * ((lane >> 4) & 1) + 4 * (jj & 3);
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+            const int e = 32 * mb + tr_e;
+            v_rel[mb] = tr_row * 128 + (((e >> 3) ^ v_mask(tr_row)) << 4) + ((e & 7) << 1);
+        }
+    }
+    // Operands of key half kb of the tile in slot kt, and of value half vb
+    // of the tile in slot vt.
+    auto read_step = [&](const char* kt, int kb, const char* vt, int vb, Operands& o) {
+        const char* kh = kt + kb * (TILE_BYTES / 2);
+        const char* vh = vt + vb * (TILE_BYTES / 2);
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) o.k[kk] = *(const bf16x8*)(kh + k_rel[kk]);
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int st = 0; st < 2; ++st) o.v[mb][st] = read_vt(vh + v_rel[mb] + st * 2048);
+    };
 
-    // Lane offsets (bytes) of the direct-to-LDS loads inside a tile: lane l
-    // loads row 8i + (l >> 3), chunk (l & 7) ^ mask(row).  The K mask of
-    // row 8i + r is k_mask(r) ^ 4 for odd i; the V mask does not depend on i.
-    const int ld_r = lane >> 3, ld_pos = lane & 7;
-    const uint32_t lane_off_k0 = ld_r * C * 2 + ((ld_pos ^ k_mask(ld_r)) << 4);
-    const uint32_t lane_off_k1 = ld_r * C * 2 + ((ld_pos ^ k_mask(ld_r) ^ 4) << 4);
-    const uint32_t lane_off_v = ld_r * C * 2 + ((ld_pos ^ v_mask(ld_r)) << 4);
-
-    // lane geometry of the merge: query ql of the block, dims [d0, d0 + 16)
-    const int ql = 16 * wave + (lane >> 2);
-    const int d0 = 16 * (lane & 3);
-
-    for (int64_t u = s_j; u < e_j;) {
-        const int64_t bl = u / n_tiles;  // block, XCD-local
-        const int t0 = (int)(u - bl * n_tiles);
-        const int64_t bend = (bl + 1) * n_tiles;
-        const int t1 = (int)((e_j < bend ? e_j : bend) - bl * n_tiles);
-        const bool first_seg = u == s_j;
-        u = bl * n_tiles + t1;
-        const int64_t blk = bx0 + bl;
-        const int qb = (int)(blk % sc.nqb);
-        const int64_t bh = blk / sc.nqb;
-        const int head = (int)(bh % p.heads);
-        const int b = (int)(bh / p.heads);
+    {
+        const int qb = blk % sc.nqb;
+        const int bh = blk / sc.nqb;
+        const int head = bh % p.heads;
+        const int b = bh / p.heads;
         const int head_off = head * D;
 
-        // this wavefront's tiles [w0, w0 + n)
-        const int nseg = t1 - t0;
-        const int w0 = t0 + nseg * wave / NW;
-        const int n = t0 + nseg * (wave + 1) / NW - w0;
-
-        // Row bases (bytes), pre-offset so that key row j of a segment is base + j*C*2.
+        // Source bases (bytes), pre-offset so that key row j of a segment is base + j*C*2.
         const int64_t o0 = (int64_t)b * p.kv.bstride[0] + head_off;
-        const int64_t o1 = (int64_t)b * p.kv.bstride[1] - (int64_t)p.kv.end0 * C + head_off;
-        const int64_t o2 = (int64_t)b * p.kv.bstride[2] - (int64_t)p.kv.end1 * C + head_off;
+        const int64_t o1 = (int64_t)b * p.kv.bstride[1] - (int64_t)end0 * C + head_off;
+        const int64_t o2 = (int64_t)b * p.kv.bstride[2] - (int64_t)end1 * C + head_off;
         const int64_t ka0 = (int64_t)(uintptr_t)p.kv.k[0] + o0 * 2;
         const int64_t ka1 = (int64_t)(uintptr_t)p.kv.k[1] + o1 * 2;
         const int64_t ka2 = (int64_t)(uintptr_t)p.kv.k[2] + o2 * 2;
@@ -229,351 +227,291 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
         const int64_t va1 = (int64_t)(uintptr_t)p.kv.v[1] + o1 * 2;
         const int64_t va2 = (int64_t)(uintptr_t)p.kv.v[2] + o2 * 2;
 
-        // Stage tile t (32 rows x 128 bytes) into dst: four 1 KB loads of
-        // eight rows each; lane l fills LDS chunk l & 7 of its row with the
-        // global chunk that the swizzle puts there.  A tile inside one key
-        // source takes a scalar base and the fixed lane offsets; a tile that
-        // straddles two sources or the end picks the source row by row.
-        auto issue_tile = [&](int t_in, char* dst, bool is_v) {
+        // Stage tile t of K (is_v = false) or V into the slot at dst.
+        auto issue = [&](int t_in, char* slot, bool is_v) {
             const int t = __builtin_amdgcn_readfirstlane(t_in);
-            const int j0 = t * TILE, j1 = j0 + TILE;
-            const bool one_src = j1 <= kv_end && (j1 <= p.kv.end0 || j0 >= p.kv.end0) &&
-                                 (j1 <= p.kv.end1 || j0 >= p.kv.end1);
+            char* dst = slot + 2 * wave * 1024;
+            const uint32_t* off = is_v ? ld_voff : ld_koff;
+            const int j0 = t * KT, j1 = j0 + KT;
+            const bool one_src = j1 <= kv_end && (j1 <= end0 || j0 >= end0) && (j1 <= end1 || j0 >= end1);
             if (one_src) {
-                const int64_t base = (is_v ? pick(j0, p.kv.end0, p.kv.end1, va0, va1, va2)
-                                           : pick(j0, p.kv.end0, p.kv.end1, ka0, ka1, ka2)) +
+                const int64_t base = (is_v ? pick(j0, end0, end1, va0, va1, va2) : pick(j0, end0, end1, ka0, ka1, ka2)) +
                                      (int64_t)j0 * C * 2;
 #pragma unroll
-                for (int i = 0; i < LOADS_PER_TILE; ++i) {
-                    const uint32_t off = is_v ? lane_off_v : (i & 1) ? lane_off_k1 : lane_off_k0;
-                    const char* g = (const char*)(uintptr_t)(base + (int64_t)i * 8 * C * 2) + off;
-                    __builtin_amdgcn_global_load_lds((gptr_t)g, (lptr_t)(dst + wbase + i * 1024), 16, 0, 0);
-                }
+                for (int i = 0; i < 2; ++i)
+                    __builtin_amdgcn_global_load_lds((gptr_t)((const char*)(uintptr_t)base + off[i]),
+                                                     (lptr_t)(dst + i * 1024), 16, 0, 0);
                 return;
             }
-            const int rr = lane >> 3;
-            const int pos = lane & 7;
 #pragma unroll
-            for (int i = 0; i < LOADS_PER_TILE; ++i) {
-                const int row = 8 * i + rr;
-                const int c = pos ^ (is_v ? v_mask(row) : k_mask(row));
-                int jk = t * TILE + row;
+            for (int i = 0; i < 2; ++i) {
+                int jk = j0 + ld_row[i];
                 jk = jk < kv_end ? jk : kv_end - 1;
-                const int64_t base = is_v ? pick(jk, p.kv.end0, p.kv.end1, va0, va1, va2)
-                                          : pick(jk, p.kv.end0, p.kv.end1, ka0, ka1, ka2);
-                const int64_t addr = base + (int64_t)jk * C * 2 + c * 16;
-                __builtin_amdgcn_global_load_lds((gptr_t)(uintptr_t)addr, (lptr_t)(dst + wbase + i * 1024), 16, 0, 0);
+                const int64_t base = (is_v ? pick(jk, end0, end1, va0, va1, va2) : pick(jk, end0, end1, ka0, ka1, ka2)) +
+                                     ((int64_t)jk - ld_row[i]) * C * 2;
+                __builtin_amdgcn_global_load_lds((gptr_t)((const char*)(uintptr_t)base + off[i]),
+                                                 (lptr_t)(dst + i * 1024), 16, 0, 0);
             }
         };
 
-        // Q^T operands of the block's 64 queries.
-        const int q_base = qb * QB;
-        bf16x8 qop[2][4];
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb) {
-            const int qrow = min(q_base + 32 * cb + col, p.nq - 1);
+        // Prologue: K of tiles t0 and t0+1 and V of tile t0, then Q^T.
+        issue(t0, ks0, false);
+        issue(t0, vs0, true);
+        if (t0 + 1 < t1) issue(t0 + 1, ks1, false);
+        // Q^T operands of the wavefront's 32 queries.
+        const int q_base = qb * QB + QW * wave;
+        bf16x8 qop[4];
+        {
+            const int qrow = min(q_base + col, p.nq - 1);
             const bf16* qp = (const bf16*)p.q + (int64_t)b * p.q_bstride + (int64_t)qrow * C + head_off + 8 * half;
 #pragma unroll
-            for (int kk = 0; kk < 4; ++kk) qop[cb][kk] = *(const bf16x8*)(qp + 16 * kk);
+            for (int kk = 0; kk < 4; ++kk) qop[kk] = *(const bf16x8*)(qp + 16 * kk);
         }
 
-        f32x16 o[2][2];
-        float m_run[2], l_run[2];
+        f32x16 o[2];
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb) {
+        for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-            for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) o[cb][mb][r] = 0.f;
-            m_run[cb] = -INFINITY;
-            l_run[cb] = 0.f;
-        }
+            for (int r = 0; r < 16; ++r) o[mb][r] = 0.f;
+        // Running max (log2 units) and the lane's share of the row sum.
+        float m_run = -INFINITY, l_run = 0.f;
 
-        // Raw scores of tile t for the 64 queries (two 32-query column
-        // blocks), masked past the last key.
-        auto qk = [&](int t, const char* kring, f32x16* sc2, bool may_mask) {
-            u32x4 kr[4];
-            lds_read_k4(kring + wbase + col * 128, half, k_mask(col), kr);
-            bf16x8 kop[4];
+        // Mask the scores of half-tile h past the last key.
+        auto mask_half = [&](int h, f32x16& sv) {
+            if ((h >> 1) * KT + KT > kv_end) {
 #pragma unroll
-            for (int kk = 0; kk < 4; ++kk) kop[kk] = __builtin_bit_cast(bf16x8, kr[kk]);
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-                for (int rr = 0; rr < 16; ++rr) sc2[cb][rr] = 0.f;
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-                for (int cb = 0; cb < 2; ++cb) sc2[cb] = mfma32x32x16(kop[kk], qop[cb][kk], sc2[cb]);
-            if (may_mask) {
-#pragma unroll
-                for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-                    for (int rr = 0; rr < 16; ++rr) {
-                        const int jk = t * TILE + 8 * (rr >> 2) + 4 * half + (rr & 3);
-                        if (jk >= kv_end) sc2[cb][rr] = -INFINITY;
-                    }
-            }
-        };
-
-        // Online softmax.  Probabilities are taken against the running max,
-        // p = exp2(s*log2(e)/8 - m), and summed per lane in the bf16 values
-        // the P V product uses.  Only when a lane's 16 probabilities of the
-        // tile sum to 2^20 or more (or to inf / NaN: the first tile, where m
-        // is -inf) is the tile's max taken, m raised to it, O and l rescaled
-        // and the probabilities recomputed.  So p < 2^20 always, and the max
-        // reduction is off the common path.
-        auto tile_probs = [&](const f32x16* sc2, int cb, bf16x8 (*pb)[2], float& lt) {
-            const float mneg = -m_run[cb];
-#pragma unroll
-            for (int rr = 0; rr < 16; ++rr)
-                pb[cb][rr >> 3][rr & 7] = f32_to_bf16(fast_exp2(fmaf(sc2[cb][rr], sl2, mneg)));
-            float s0 = 0.f, s1 = 0.f;
-#pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                bf16x2 p0 = {pb[cb][0][2 * w], pb[cb][0][2 * w + 1]};
-                bf16x2 p1 = {pb[cb][1][2 * w], pb[cb][1][2 * w + 1]};
-                s0 = __builtin_amdgcn_fdot2_f32_bf16(p0, ones, s0, false);
-                s1 = __builtin_amdgcn_fdot2_f32_bf16(p1, ones, s1, false);
-            }
-            lt = s0 + s1;
-        };
-        auto probs = [&](const f32x16* sc2, bf16x8 (*pb)[2]) {
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb) {
-                float lt;
-                tile_probs(sc2, cb, pb, lt);
-                if (__any(!(lt < P_LIMIT))) {
-                    float m4[4];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        m4[i] = fmaxf(fmaxf(sc2[cb][4 * i], sc2[cb][4 * i + 1]), fmaxf(sc2[cb][4 * i + 2], sc2[cb][4 * i + 3]));
-                    const float mx = max_xor32(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]))) * sl2;
-                    const float m_new = fmaxf(m_run[cb], mx);
-                    const float alpha = fast_exp2(m_run[cb] - m_new);
-                    m_run[cb] = m_new;
-                    l_run[cb] *= alpha;
-#pragma unroll
-                    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-                        for (int rr = 0; rr < 16; ++rr) o[cb][mb][rr] *= alpha;
-                    tile_probs(sc2, cb, pb, lt);
-                }
-                l_run[cb] += lt;
-            }
-        };
-
-        // O^T += V^T P^T for the tile in vring.
-        auto pv = [&](const char* vring, bf16x8 (*pb)[2]) {
-            const char* vt = vring + wbase;
-            u32x2 vr[8];
-#pragma unroll
-            for (int st = 0; st < 2; ++st) {
-                const int row = 16 * st + tr_row;
-#pragma unroll
-                for (int mb = 0; mb < 2; ++mb) {
-                    const int e = 32 * mb + tr_e;
-                    const char* vp = vt + row * 128 + (((e >> 3) ^ v_mask(row)) << 4) + ((e & 7) << 1);
-                    lds_read_tr2(vp, vr[4 * st + 2 * mb], vr[4 * st + 2 * mb + 1]);
+                for (int rr = 0; rr < 16; ++rr) {
+                    const int jk = (h >> 1) * KT + 32 * (h & 1) + 8 * (rr >> 2) + 4 * half + (rr & 3);
+                    if (jk >= kv_end) sv[rr] = -INFINITY;
                 }
             }
-            lds_wait(vr);
-#pragma unroll
-            for (int st = 0; st < 2; ++st)
-#pragma unroll
-                for (int mb = 0; mb < 2; ++mb) {
-                    const u32x2 lo = vr[4 * st + 2 * mb], hi = vr[4 * st + 2 * mb + 1];
-                    const u32x4 v4 = {lo[0], lo[1], hi[0], hi[1]};
-                    const bf16x8 vop = __builtin_bit_cast(bf16x8, v4);
-#pragma unroll
-                    for (int cb = 0; cb < 2; ++cb) o[cb][mb] = mfma32x32x16(vop, pb[cb][st], o[cb][mb]);
-                }
         };
 
-        // Software pipeline over the wavefront's n tiles.  Round x computes
-        // the scores of tile x and then tile x-1's P V product (MFMA), while
-        // tile x's softmax (VALU) overlaps the latter; only tile x-1's bf16
-        // probabilities carry over.  K(x+1) is loaded from the start of round
-        // x into the K slot tile x-1 used, V(x+1) from the end of round x into
-        // the V slot tile x-1 used; round x therefore only waits for K(x)
-        // (and everything before it), with V(x) in flight.
-        auto round_step = [&](int xr, const char* kcur, char* knext, char* vprev, bf16x8 (*pb_prev)[2],
-                              bf16x8 (*pb_cur)[2]) {
-            if (xr < n) {
-                __builtin_amdgcn_s_waitcnt(0xF70 | LOADS_PER_TILE);  // vmcnt(4): K(x) has landed
-                if (xr + 1 < n) issue_tile(w0 + xr + 1, knext, false);
-            } else {
-                __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): V(n-1) has landed
-            }
-            const int t = w0 + xr;
-            f32x16 s_cur[2];
-            if (xr < n) qk(t, kcur, s_cur, t * TILE + TILE > kv_end);
-            if (xr >= 1) pv(vprev, pb_prev);
-            if (xr < n) probs(s_cur, pb_cur);
-            if (xr + 1 < n) issue_tile(w0 + xr + 1, vprev, true);
-        };
-        if (n > 0) {
-            bf16x8 pb0[2][2], pb1[2][2];
-            issue_tile(w0, kring0, false);
-            issue_tile(w0, vring0, true);
-            for (int xr = 0; xr <= n; xr += 2) {
-                round_step(xr, kring0, kring1, vring1, pb1, pb0);
-                if (xr + 1 <= n) round_step(xr + 1, kring1, kring0, vring0, pb0, pb1);
-            }
-        }
+        __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): this thread's staging loads and Q have landed
+        __syncthreads();
 
-        // ---- merge the wavefronts' partial results through LDS ----
-        float l_tot[2];
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb) l_tot[cb] = sum_xor32(l_run[cb]);
-        if (half == 0) {
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb) {
-                float* ml = ml_lds + (wave * QB + 32 * cb + col) * 2;
-                ml[0] = m_run[cb];
-                ml[1] = l_tot[cb];
-            }
-        }
-        __syncthreads();  // every wavefront is done with its ring; (m, l) are visible
-        // merged max and sum of query q of the block over the wavefronts
-        auto block_ml = [&](int q, float& M, float& L) {
-            M = -INFINITY;
-#pragma unroll
-            for (int k = 0; k < NW; ++k) {
-                const float* ml = ml_lds + (k * QB + q) * 2;
-                if (ml[1] > 0.f) M = fmaxf(M, ml[0]);
-            }
-            L = 0.f;
-#pragma unroll
-            for (int k = 0; k < NW; ++k) {
-                const float* ml = ml_lds + (k * QB + q) * 2;
-                if (ml[1] > 0.f) L += ml[1] * fast_exp2(ml[0] - M);
-            }
-        };
+        // S(2 t0) from key half 0 of tile t0; operands of step 2 t0: key half
+        // 1 of tile t0 and, standing in for the absent half 2 t0 - 1, value
+        // half 0 of tile t0 (multiplied by all-zero probabilities).
+        f32x16 s_a, s_b;
+        Operands op_a, op_b;
         {
-            char* mybuf = wave == 0 ? kring0 : wave == 1 ? kring1 : wave == 2 ? vring0 : vring1;
+            Operands o0;
+            read_step(ks0, 0, vs0, 0, o0);
 #pragma unroll
-            for (int cb = 0; cb < 2; ++cb) {
-                float M, L;
-                block_ml(32 * cb + col, M, L);
-                const float w_own = l_tot[cb] > 0.f ? fast_exp2(m_run[cb] - M) * __builtin_amdgcn_rcpf(L) : 0.f;
+            for (int kk = 0; kk < 4; ++kk) s_a = mfma32x32x16(o0.k[kk], qop[kk], kk == 0 ? f32x16{} : s_a);
+            mask_half(2 * t0, s_a);
+        }
+        read_step(ks0, 1, vs0, 0, op_a);
+        bf16x8 p_a[2], p_b[2];
+#pragma unroll
+        for (int st = 0; st < 2; ++st)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) p_b[st][e] = (bf16)0.0f;
+
+        // One pipeline step h: softmax of s_cur -> p_cur, interleaved with
+        // O^T += V(h-1)^T p_prev^T and s_nxt = K(h+1) Q^T from op_cur; the
+        // operands of step h+1 are read into op_nxt first.
+        auto step = [&](int h, f32x16& s_cur, f32x16& s_nxt, bf16x8 (&p_prev)[2], bf16x8 (&p_cur)[2],
+                        Operands& op_cur, Operands& op_nxt, const char* nk, int nk_half, const char* nv, int nv_half) {
+            SCHED_FENCE();
+            read_step(nk, nk_half, nv, nv_half, op_nxt);
+            float acc0 = 0.f, acc1 = 0.f;
+            float mneg = -m_run;
+            // probabilities of elements 2i, 2i+1 and their bf16 sum
+            auto pair = [&](int i) {
+                const float e0 = fast_exp2(fmaf(s_cur[2 * i], sl2, mneg));
+                const float e1 = fast_exp2(fmaf(s_cur[2 * i + 1], sl2, mneg));
+                const bf16x2 pk = {f32_to_bf16(e0), f32_to_bf16(e1)};
+                p_cur[i >> 2][2 * (i & 3)] = pk[0];
+                p_cur[i >> 2][2 * (i & 3) + 1] = pk[1];
+                if (i & 1)
+                    acc1 = __builtin_amdgcn_fdot2_f32_bf16(pk, ones, acc1, false);
+                else
+                    acc0 = __builtin_amdgcn_fdot2_f32_bf16(pk, ones, acc0, false);
+            };
+            SCHED_FENCE();
+            pair(0);
+            pair(1);
+            SCHED_FENCE();
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int st = i >> 2, mb = (i >> 1) & 1;
+                if ((i & 1) == 0) {
+                    o[mb] = mfma32x32x16(op_cur.v[mb][st], p_prev[st], o[mb]);
+                } else {
+                    const int kk = i >> 1;
+                    s_nxt = mfma32x32x16(op_cur.k[kk], qop[kk], kk == 0 ? f32x16{} : s_nxt);
+                }
+                SCHED_FENCE();
+                if (i < 6) pair(i + 2);
+                SCHED_FENCE();
+            }
+            float lt = acc0 + acc1;
+            if (__any(!(lt < P_LIMIT))) {
+                // Only when a lane's 16 probabilities of the half sum to 2^20
+                // or more (or to inf / NaN: the first half, where m is -inf)
+                // is the half's max taken, m raised to it, O and l rescaled
+                // and the probabilities recomputed.
+                float m4[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    m4[i] = fmaxf(fmaxf(s_cur[4 * i], s_cur[4 * i + 1]), fmaxf(s_cur[4 * i + 2], s_cur[4 * i + 3]));
+                const float mx = max_xor32(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]))) * sl2;
+                const float m_new = fmaxf(m_run, mx);
+                const float alpha = fast_exp2(m_run - m_new);
+                m_run = m_new;
+                mneg = -m_new;
+                l_run *= alpha;
 #pragma unroll
                 for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-                    for (int c4 = 0; c4 < 4; ++c4) {
-                        float* dst = (float*)mybuf + (32 * cb + col) * OSTR + 32 * mb + 8 * c4 + 4 * half;
-                        const f32x4 v = {o[cb][mb][4 * c4] * w_own, o[cb][mb][4 * c4 + 1] * w_own,
-                                         o[cb][mb][4 * c4 + 2] * w_own, o[cb][mb][4 * c4 + 3] * w_own};
-                        *(f32x4*)dst = v;
-                    }
-            }
-        }
-        __syncthreads();
-        // normalised output of the workgroup's piece for (ql, [d0, d0+16))
-        float acc[16];
-        {
-            const int off = ql * OSTR + d0;
-            const float* b0 = (const float*)kring0 + off;
-            const float* b1 = (const float*)kring1 + off;
-            const float* b2 = (const float*)vring0 + off;
-            const float* b3 = (const float*)vring1 + off;
+                    for (int rr = 0; rr < 16; ++rr) o[mb][rr] *= alpha;
+                acc0 = 0.f;
+                acc1 = 0.f;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const f32x4 v = *(const f32x4*)(b0 + 4 * i) + *(const f32x4*)(b1 + 4 * i) +
-                                *(const f32x4*)(b2 + 4 * i) + *(const f32x4*)(b3 + 4 * i);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) acc[4 * i + e] = v[e];
+                for (int i = 0; i < 8; ++i) pair(i);
+                lt = acc0 + acc1;
             }
-        }
-        float M_own, L_own;
-        block_ml(ql, M_own, L_own);
-        const int q_out = q_base + ql;
-        bf16* out_row = (bf16*)p.out + (int64_t)b * p.q_bstride + (int64_t)q_out * C + head_off + d0;
-        auto store_out = [&](const float* a, float scale) {
-            if (q_out >= p.nq) return;
-            bf16x8 v0, v1;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                v0[e] = f32_to_bf16(a[e] * scale);
-                v1[e] = f32_to_bf16(a[8 + e] * scale);
-            }
-            *(bf16x8*)out_row = v0;
-            *(bf16x8*)(out_row + 8) = v1;
+            l_run += lt;
+            mask_half(h + 1, s_nxt);
         };
 
-        if (t0 == 0 && t1 == n_tiles) {
-            store_out(acc, 1.0f);
-        } else {
-            // A piece of a block that other workgroups of this XCD share.
-            const int64_t slot = (int64_t)(x * J + j) * PIECE_SLOTS + (first_seg ? 0 : 1);
-            float* po = sc.part_o + (slot * QB + ql) * D + d0;
+        // Period of tile pt: its two halves.  Slots: K(pt) in kc, K(pt+1) in
+        // kn, V(pt) in vc; K(pt+2) and V(pt+1) are staged into kl and vl.
+        auto period = [&](int pt, char* kc, char* kn, char* kl, char* vc, char* vl) {
+            if (pt > t0) {
+                __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): K(pt+1) and V(pt) have landed
+                __syncthreads();                    // for everyone; slots of K(pt-1), V(pt-2) are free
+            }
+            if (pt + 2 < t1) issue(pt + 2, kl, false);
+            if (pt + 1 < t1) issue(pt + 1, vl, true);
+            // keys of tile pt+1 (or, past the end, tile pt again: products discarded)
+            const char* kk = pt + 1 < t1 ? kn : kc;
+            step(2 * pt, s_a, s_b, p_b, p_a, op_a, op_b, kk, 0, vc, 0);
+            step(2 * pt + 1, s_b, s_a, p_a, p_b, op_b, op_a, kk, 1, vc, 1);
+        };
+        for (int pt = t0; pt < t1; pt += 3) {
+            period(pt, ks0, ks1, ks2, vs0, vs1);
+            if (pt + 1 < t1) period(pt + 1, ks1, ks2, ks0, vs1, vs2);
+            if (pt + 2 < t1) period(pt + 2, ks2, ks0, ks1, vs2, vs0);
+        }
+        // Drain: O^T += V(2 t1 - 1)^T P(2 t1 - 1)^T, operands in op_a.
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const f32x4 v = {acc[4 * i], acc[4 * i + 1], acc[4 * i + 2], acc[4 * i + 3]};
-                *(f32x4*)(po + 4 * i) = v;
-            }
-            if ((lane & 3) == 0) {
-                float* pml = sc.part_ml + (slot * QB + ql) * 2;
-                pml[0] = M_own;
-                pml[1] = L_own;
-            }
-            __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): this thread's stores reached the L2
-            __syncthreads();
-            const int64_t blk_u0 = bl * n_tiles;
-            const int jf = owner_of(blk_u0, T, J);
-            const int jl = owner_of(blk_u0 + n_tiles - 1, T, J);
-            if (tid == 0) {
-                // Count tiles: the contribution that completes the block's
-                // n_tiles merges.  The counter lives at the index of the
-                // block's first workgroup, unique among split blocks.
-                int* counter = sc.counters + x * J + jf;
-                const int prev = __hip_atomic_fetch_add(counter, t1 - t0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-                const int last = prev + (t1 - t0) == n_tiles;
-                if (last) __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-                flag_lds = last;
-            }
-            __syncthreads();
-            if (flag_lds) {
-                // Every piece, this workgroup's own included, is read back
-                // from the workspace and summed in workgroup order, so the
-                // result does not depend on which contributor arrived last.
-                float Mx = -INFINITY;
-                for (int jo = jf; jo <= jl; ++jo) {
-                    const int64_t so = range_start(T, nblk, n_tiles, jo, J, false);
-                    if (so == range_start(T, nblk, n_tiles, jo + 1, J, false)) continue;
-                    const int64_t sl = (int64_t)(x * J + jo) * PIECE_SLOTS + (so >= blk_u0 ? 0 : 1);
-                    Mx = fmaxf(Mx, sc.part_ml[(sl * QB + ql) * 2]);
+        for (int st = 0; st < 2; ++st)
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb) o[mb] = mfma32x32x16(op_a.v[mb][st], p_b[st], o[mb]);
+
+        // ---- block epilogue ----
+        const float l_tot = sum_xor32(l_run);
+        const int q_out = q_base + col;
+        bf16* out_row = (bf16*)p.out + (int64_t)b * p.q_bstride + (int64_t)min(q_out, p.nq - 1) * C + head_off + 4 * half;
+        // Lane (col, half) holds dims 32*mb + 8*g + 4*half + {0..3} of query col in o[mb][4g..4g+3].
+        auto store_out = [&](const f32x16 (&a)[2], float scale) {
+            if (q_out >= p.nq) return;
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    bf16x4 v;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = f32_to_bf16(a[mb][4 * g + e] * scale);
+                    *(bf16x4*)(out_row + 32 * mb + 8 * g) = v;
                 }
-                float wsum = 0.f;
-                float res[16];
+        };
+
+        if (sc.k == 1) {
+            store_out(o, l_tot > 0.f ? 1.0f / l_tot : 0.f);
+            return;
+        }
+        // A piece of a block whose other pieces run on this XCD: store the
+        // unnormalised O^T accumulators and (m, l), lane-major, then count.
+        {
+            float* po = sc.part_o + (int64_t)blockIdx.x * (QB * D) + wave * (QW * D) + lane * 4;
 #pragma unroll
-                for (int e = 0; e < 16; ++e) res[e] = 0.f;
-                for (int jo = jf; jo <= jl; ++jo) {
-                    const int64_t so = range_start(T, nblk, n_tiles, jo, J, false);
-                    if (so == range_start(T, nblk, n_tiles, jo + 1, J, false)) continue;
-                    const int64_t sl = (int64_t)(x * J + jo) * PIECE_SLOTS + (so >= blk_u0 ? 0 : 1);
-                    const float* pml = sc.part_ml + (sl * QB + ql) * 2;
-                    const float wk = pml[1] * fast_exp2(pml[0] - Mx);
-                    wsum += wk;
-                    const float* pk = sc.part_o + (sl * QB + ql) * D + d0;
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const f32x4 v = *(const f32x4*)(pk + 4 * i);
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) res[4 * i + e] += wk * v[e];
-                    }
-                }
-                store_out(res, 1.0f / wsum);
+            for (int c = 0; c < 8; ++c) {
+                const int mb = c >> 2, g = c & 3;
+                const f32x4 v = {o[mb][4 * g], o[mb][4 * g + 1], o[mb][4 * g + 2], o[mb][4 * g + 3]};
+                *(f32x4*)(po + c * 256) = v;
+            }
+            if (half == 0) {
+                float* pml = sc.part_ml + ((int64_t)blockIdx.x * QB + QW * wave + col) * 2;
+                pml[0] = m_run;
+                pml[1] = l_tot;
             }
         }
-        __syncthreads();  // merge buffers and (m, l) are free for the next block
+        __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): this thread's stores reached the L2
+        __syncthreads();
+        if (tid == 0) {
+            int* counter = sc.counters + blk;
+            const int prev = __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            const int last = prev == sc.k - 1;
+            if (last) __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            flag_lds = last;
+        }
+        __syncthreads();
+        if (!flag_lds) return;
+        // Last piece: combine all k pieces in piece order (this one from
+        // registers, the others from the workspace) with a running max, one
+        // code path for every piece, so the result does not depend on which
+        // piece arrived last.  The next piece's loads are issued before the
+        // current one is combined.
+        float M = -INFINITY, L = 0.f;
+        f32x16 res[2];
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) res[mb][r] = 0.f;
+        auto load_piece = [&](int pi, f32x16 (&pc)[2], float& mk, float& lk) {
+            const int w = (bl * sc.k + pi) * sc.n_xcd + x;
+            if (w == (int)blockIdx.x) {
+                pc[0] = o[0];
+                pc[1] = o[1];
+                mk = m_run;
+                lk = l_tot;
+                return;
+            }
+            const float* pml = sc.part_ml + ((int64_t)w * QB + QW * wave + col) * 2;
+            mk = pml[0];
+            lk = pml[1];
+            const float* pk = sc.part_o + (int64_t)w * (QB * D) + wave * (QW * D) + lane * 4;
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                const f32x4 v = *(const f32x4*)(pk + c * 256);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) pc[c >> 2][4 * (c & 3) + e] = v[e];
+            }
+        };
+        f32x16 pc_a[2], pc_b[2];
+        float m_a, l_a, m_b, l_b;
+        auto combine = [&](const f32x16 (&pc)[2], float mk, float lk) {
+            const float Mn = fmaxf(M, mk);
+            const float a = fast_exp2(M - Mn);
+            const float w = fast_exp2(mk - Mn);
+            L = __builtin_fmaf(lk, w, L * a);
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) res[mb][r] = __builtin_fmaf(pc[mb][r], w, res[mb][r] * a);
+            M = Mn;
+        };
+        load_piece(0, pc_a, m_a, l_a);
+        for (int pi = 0; pi < sc.k; pi += 2) {
+            if (pi + 1 < sc.k) load_piece(pi + 1, pc_b, m_b, l_b);
+            combine(pc_a, m_a, l_a);
+            if (pi + 1 < sc.k) {
+                if (pi + 2 < sc.k) load_piece(pi + 2, pc_a, m_a, l_a);
+                combine(pc_b, m_b, l_b);
+            }
+        }
+        store_out(res, L > 0.f ? 1.0f / L : 0.f);
     }
 }
 
 struct Plan {
-    int32_t n_xcd, per_xcd, grid, max_grid, n_tiles, nqb, whole;
-    int64_t n_blocks;
+    int32_t n_xcd, bpx, k, grid, max_grid, n_tiles, nqb, n_blocks;
     size_t off_xcc, off_counters, off_o, off_ml, ws_bytes;
+    bool fits;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -588,39 +526,39 @@ int device_cus() {
 
 // Two workgroups per compute unit.  The workspace layout depends only on the
 // compute unit count: [XCC record: max_grid ints][counters: max_grid ints]
-// [partial outputs: max_grid x 2 slots][partial row statistics: same].
+// [partial outputs: max_grid pieces][partial row statistics: same].  Pieces
+// are only used when k > 1, which keeps the grid within max_grid.
 Plan make_plan(const AttnParams& p) {
     Plan pl;
     const int cus = device_cus();
     pl.max_grid = WG_PER_CU * cus;
-    pl.n_tiles = (p.kv.n_kv + TILE - 1) / TILE;
+    pl.n_tiles = (p.kv.n_kv + KT - 1) / KT;
     pl.nqb = (p.nq + QB - 1) / QB;
-    pl.n_blocks = (int64_t)p.batch * p.heads * pl.nqb;
-    // Merging across workgroups needs the XCD layout of a gfx950 device
-    // (32 compute units per XCD); otherwise every range holds whole blocks.
+    const int64_t n_blocks = (int64_t)p.batch * p.heads * pl.nqb;
+    pl.n_blocks = (int32_t)(n_blocks < INT32_MAX ? n_blocks : INT32_MAX);
+    // Merging pieces needs the XCD layout of a gfx950 device (32 compute
+    // units per XCD); otherwise every workgroup computes whole blocks.
     const bool xcd_known = cus % CUS_PER_XCD == 0;
     pl.n_xcd = xcd_known ? cus / CUS_PER_XCD : 1;
-    pl.whole = xcd_known ? 0 : 1;
-    const int64_t blk_per_xcd = (pl.n_blocks + pl.n_xcd - 1) / pl.n_xcd;
-    int64_t per = pl.max_grid / pl.n_xcd;
-    if (pl.whole) {
-        if (per > blk_per_xcd) per = blk_per_xcd;
-    } else {
-        const int64_t need = (blk_per_xcd * pl.n_tiles + NW * MIN_TILES_PER_WAVE - 1) / (NW * MIN_TILES_PER_WAVE);
-        if (per > need) per = need;
-    }
-    if (per < 1) per = 1;
-    pl.per_xcd = (int32_t)per;
-    pl.grid = pl.n_xcd * pl.per_xcd;
+    const int64_t bpx = (n_blocks + pl.n_xcd - 1) / pl.n_xcd;
+    int64_t k = xcd_known ? pl.max_grid / (pl.n_xcd * bpx) : 1;
+    const int64_t k_tiles = pl.n_tiles / MIN_TILES_PER_PIECE;
+    if (k > k_tiles) k = k_tiles;
+    if (k < 1) k = 1;
+    pl.k = (int32_t)k;
+    pl.bpx = (int32_t)(bpx < INT32_MAX ? bpx : INT32_MAX);
+    const int64_t grid = (int64_t)pl.n_xcd * bpx * k;
+    pl.grid = (int32_t)(grid < INT32_MAX ? grid : INT32_MAX);
+    pl.fits = grid < INT32_MAX && n_blocks < INT32_MAX / 2;
     size_t off = 0;
     pl.off_xcc = off;
     off += align256((size_t)pl.max_grid * sizeof(int));
     pl.off_counters = off;
     off += align256((size_t)pl.max_grid * sizeof(int));
     pl.off_o = off;
-    off += align256((size_t)pl.max_grid * PIECE_SLOTS * QB * D * sizeof(float));
+    off += align256((size_t)pl.max_grid * QB * D * sizeof(float));
     pl.off_ml = off;
-    off += align256((size_t)pl.max_grid * PIECE_SLOTS * QB * 2 * sizeof(float));
+    off += align256((size_t)pl.max_grid * QB * 2 * sizeof(float));
     pl.ws_bytes = off;
     return pl;
 }
@@ -632,15 +570,14 @@ size_t attention_bf16_ws_bytes(const AttnParams& p) { return make_plan(p).ws_byt
 hipError_t launch_attention_bf16(const AttnParams& p, void* ws, size_t ws_bytes, hipStream_t stream) {
     const Plan pl = make_plan(p);
     if (ws == nullptr || ws_bytes < pl.ws_bytes) return hipErrorInvalidValue;
-    // unit positions times workgroup counts stay far inside int64
-    if ((double)pl.n_blocks * pl.n_tiles * (pl.per_xcd + 1) > 4.0e18) return hipErrorInvalidValue;
+    if (!pl.fits) return hipErrorInvalidValue;
     Sched sc;
     sc.n_xcd = pl.n_xcd;
-    sc.per_xcd = pl.per_xcd;
+    sc.bpx = pl.bpx;
+    sc.k = pl.k;
     sc.n_tiles = pl.n_tiles;
     sc.nqb = pl.nqb;
     sc.n_blocks = pl.n_blocks;
-    sc.whole = pl.whole;
     sc.xcc_of = (int*)((char*)ws + pl.off_xcc);
     sc.counters = (int*)((char*)ws + pl.off_counters);
     sc.part_o = (float*)((char*)ws + pl.off_o);
