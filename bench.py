@@ -39,6 +39,10 @@ def attn_bytes(cfg, n_kv):
     return 2.0 * cfg.batch * cfg.C * (2 * cfg.n_q + 2 * n_kv)
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_bf16_sdxl2048_l1_p25_traffic.txt")
+CALIB_BYTES = 256 << 20      # plain device-to-device copy used to scale the memory counters
+
+
 def kernel_source_hash():
     p = os.path.join(ROOT, "paper_2412_02962_amd", "csrc", "attention_bf16.hip")
     return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
@@ -47,7 +51,7 @@ def kernel_source_hash():
 def load_traffic():
     """HBM traffic per launch from the committed rocprofv3 counter summary,
     only if it was taken on the current kernel source."""
-    p = os.path.join(ROOT, "profiles", "attn_bf16_sdxl2048_l1_p25_traffic.txt")
+    p = TRAFFIC_FILE
     if not os.path.exists(p):
         return None
     kv = {}
@@ -190,6 +194,80 @@ def extras(torch, pcpp, synth, dev, use_graph=True, reps=200):
     return out
 
 
+def pmc_run(args):
+    """Workload for one rocprofv3 --pmc pass: a plain copy of CALIB_BYTES
+    (calibrates the counters), then the timed workload's attention call
+    repeated, nothing else."""
+    import numpy as np
+    import torch
+
+    from paper_2412_02962_amd import pcpp, synth
+
+    dev = "cuda:0"
+    src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    cfg = synth.ATTN_CONFIGS[args.workload]
+    d = {k: (None if v is None else torch.from_numpy(np.ascontiguousarray(v).view(np.int16)).view(torch.bfloat16).to(dev))
+         for k, v in synth.attention_inputs(cfg).items()}
+    g = pcpp.make_geom(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, cfg.d, cfg.batch, 0, pcpp.PCPP_DTYPE_BF16)
+    out = torch.empty_like(d["q"])
+    wsb = pcpp.pcpp_partial_attention_workspace_size(g)
+    ws = torch.zeros(max(wsb, 1), dtype=torch.uint8, device=dev)
+    for _ in range(args.steps):
+        pcpp.pcpp_partial_attention(g, d["q"], d["k_fresh"], d["v_fresh"], d["k_up"], d["v_up"], d["k_dn"],
+                                    d["v_dn"], out, ws, wsb, None)
+    torch.cuda.synchronize()
+    print("pmc run done", flush=True)
+
+
+def pmc_summarize(fetch_dir, write_dir):
+    """Writes the traffic summary from two rocprofv3 --pmc outputs
+    (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch), each scaled by what the
+    same counter reads for the calibration copy."""
+    import csv
+    import glob
+
+    def per_kernel(d, counter):
+        f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+        vals = {}
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] != counter:
+                continue
+            vals.setdefault(r["Kernel_Name"], {}).setdefault(r["Dispatch_Id"], 0.0)
+            vals[r["Kernel_Name"]][r["Dispatch_Id"]] += float(r["Counter_Value"])
+        return vals
+
+    out = {}
+    for d, counter in ((fetch_dir, "FETCH_SIZE"), (write_dir, "WRITE_SIZE")):
+        v = per_kernel(d, counter)
+        copy = [x for k, x in v.items() if "copy" in k.lower() or "elementwise" in k.lower()]
+        attn = [x for k, x in v.items() if "attn_bf16_kernel" in k]
+        copy_kib = max(max(x.values()) for x in copy)     # the 256 MiB copy dispatches
+        attn_kib = sorted(attn[0].values())
+        med = attn_kib[len(attn_kib) // 2]
+        scale = copy_kib / (CALIB_BYTES / 1024.0)
+        out[counter] = (med, copy_kib, scale)
+    fetch, write = out["FETCH_SIZE"], out["WRITE_SIZE"]
+    hbm = fetch[0] / fetch[2] * 1024.0 + write[0] / write[2] * 1024.0
+    text = (
+        "# Memory traffic of attn_bf16_kernel, 2048 px level-1 workload (one launch)\n"
+        "# FETCH_SIZE and WRITE_SIZE are KiB per dispatch (L2 misses to the memory fabric), each divided by\n"
+        "# its reading for a plain 256 MiB device-to-device copy over the copy's true size.\n"
+        f"fetch_kib_per_launch: {fetch[0]:.1f}\n"
+        f"write_kib_per_launch: {write[0]:.1f}\n"
+        f"copy_fetch_kib: {fetch[1]:.1f}\n"
+        f"copy_write_kib: {write[1]:.1f}\n"
+        f"fetch_scale: {fetch[2]:.4f}\n"
+        f"write_scale: {write[2]:.4f}\n"
+        f"hbm_bytes_per_launch: {hbm:.0f}\n"
+        f"kernel_source_sha256_16: {kernel_source_hash()}\n")
+    open(TRAFFIC_FILE, "w").write(text)
+    print(text)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -199,7 +277,17 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead of a graph")
     ap.add_argument("--no-extras", action="store_true", help="skip the gather / p=0.5 / block context lines")
+    ap.add_argument("--pmc-run", action="store_true",
+                    help="counter-collection workload: a calibration copy, then --steps attention calls")
+    ap.add_argument("--pmc-summarize", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write the traffic summary from two rocprofv3 --pmc output folders")
     args = ap.parse_args()
+    if args.pmc_summarize:
+        pmc_summarize(*args.pmc_summarize)
+        return
+    if args.pmc_run:
+        pmc_run(args)
+        return
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the per-band hot path); --gpus {args.gpus} is not supported. "
