@@ -16,7 +16,7 @@
 //   a   = Attention(q2, k2, v2);  h += a Wo2^T + b
 //   n   = LayerNorm(h);  u = GEGLU(n Wff1^T + b)   (epilogue value*GELU(gate))
 //   h  += u Wff2^T + b
-//   y   = h Wpo^T + b + x                      bf16 (fp32 h rounded on load)
+//   y   = h Wpo^T + b + x                      bf16 (h rounded to bf16 by FF-out)
 
 #include <stdint.h>
 
@@ -123,6 +123,7 @@ GemmParams gemm(const void* a, int64_t lda, bool a_f32, const void* wt, const vo
     p.seg = N;
     p.ldo = ldo;
     p.out_f32 = out_f32 ? 1 : 0;
+    p.out_bf16 = nullptr;
     return p;
 }
 
@@ -265,17 +266,22 @@ PCPP_EXPORT int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_we
         ff.F = F;
         PCPP_CHECK(launch_gemm(ff, s));
     }
+    // FF-out also writes the stream rounded to bf16 (into t16, free by now),
+    // the operand proj_out reads.
+    const bool copy16 = C % 64 == 0 && F % 64 == 0;
     {
         GemmParams o = gemm(u16, F, false, w->ff2_w, w->ff2_b, rows, C, F, hid, C, true);
         o.resid = hid;
         o.ldr = C;
         o.resid_f32 = 1;
+        if (copy16) o.out_bf16 = t16;
         PCPP_CHECK(launch_gemm(o, s));
     }
 
     // proj_out plus the block input.
     {
-        GemmParams o = gemm(hid, C, true, w->proj_out_w, w->proj_out_b, rows, C, C, y, C, false);
+        GemmParams o = copy16 ? gemm(t16, C, false, w->proj_out_w, w->proj_out_b, rows, C, C, y, C, false)
+                              : gemm(hid, C, true, w->proj_out_w, w->proj_out_b, rows, C, C, y, C, false);
         o.resid = x;
         o.ldr = C;
         o.resid_f32 = 0;

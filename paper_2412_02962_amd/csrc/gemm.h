@@ -24,6 +24,7 @@ struct GemmParams {
     int32_t seg;
     int64_t ldo;          // row stride of each output segment
     int32_t out_f32;
+    void* out_bf16;       // optional bf16 copy of the output [M, N] (row stride ldo), or null
 };
 
 bool gemm_shape_ok(const GemmParams& p);

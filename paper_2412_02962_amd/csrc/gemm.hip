@@ -27,6 +27,11 @@ __device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + e
 
 typedef const __attribute__((address_space(1))) u32x4* gchunk;
 
+template <int V>
+struct IC {
+    static constexpr int value = V;
+};
+
 template <int WMB, int WNB, bool AF32>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
     constexpr int BM = 2 * 32 * WMB;           // tokens per workgroup
@@ -213,6 +218,231 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Pipelined variant for bf16 X and K % 64 == 0: X and W tiles (BK = 64) go
+// straight from global memory into LDS (direct global->LDS loads, NS stages
+// in flight), MFMA operands are read with explicit LDS waits one k-step
+// ahead.  LDS rows are 128 bytes with the 16-byte chunk c of row r stored at
+// slot c ^ ((r >> 1) & 7), so 32 consecutive rows read at one chunk are
+// conflict-free.  Workgroup: 4 wavefronts in a 2 x 2 layout, each
+// computing (BM/2) tokens x (BN/2) W rows.
+// ---------------------------------------------------------------------------
+
+constexpr int DBK = 64;
+
+typedef const __attribute__((address_space(1))) void* gvoid;
+typedef __attribute__((address_space(3))) void* lvoid;
+
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_b128(uint32_t a) {
+    u32x4 r;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(a), "n"(OFF));
+    return r;
+}
+
+template <int BM, int BN, int NS, bool GEGLU>
+__global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
+    constexpr int WMB = BM / 64;                      // 32-token blocks per wavefront
+    constexpr int WNB = BN / 64;                      // 32-row W blocks per wavefront
+    constexpr int XP = BM / 32;                       // 1 KB X pieces per wavefront per k-tile
+    constexpr int WP = BN / 32;
+    constexpr int PT = XP + WP;                       // loads per thread per k-tile
+    constexpr int STAGE = (BM + BN) * DBK * 2;        // bytes per stage
+    constexpr int NOPS = WNB + WMB;                   // operand reads per k-step
+    static_assert(!GEGLU || WNB == 2, "GEGLU pairs a value block with a gate block");
+    __shared__ __attribute__((aligned(16))) char lds[NS * STAGE];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave & 1;
+    const int wn = wave >> 1;
+    const int col = lane & 31;
+    const int half = lane >> 5;
+    const int m0 = blockIdx.x * BM;
+    const int bn_out = GEGLU ? BN / 2 : BN;
+    const int n0 = blockIdx.y * bn_out;
+    const int nk = p.K / DBK;
+
+    // Per-lane global source of each staged piece (row 8q + (lane >> 3),
+    // chunk (lane & 7) ^ swizzle), k offset added per k-tile.
+    const char* xsrc[XP];
+    const char* wsrc[WP];
+#pragma unroll
+    for (int i = 0; i < XP; ++i) {
+        const int r = 8 * (wave + 4 * i) + (lane >> 3);
+        const int m = min(m0 + r, p.M - 1);
+        const int c = (lane & 7) ^ ((r >> 1) & 7);
+        xsrc[i] = (const char*)p.a + ((int64_t)m * p.lda + 8 * c) * 2;
+    }
+#pragma unroll
+    for (int i = 0; i < WP; ++i) {
+        const int r = 8 * (wave + 4 * i) + (lane >> 3);
+        const int wr = GEGLU ? (r < BN / 2 ? n0 + r : p.F + n0 + (r - BN / 2)) : n0 + r;
+        const int c = (lane & 7) ^ ((r >> 1) & 7);
+        wsrc[i] = (const char*)p.w + ((int64_t)wr * p.K + 8 * c) * 2;
+    }
+    auto issue = [&](int kt, int stage) {
+        char* st = lds + stage * STAGE;
+        const int koff = kt * DBK * 2;
+#pragma unroll
+        for (int i = 0; i < XP; ++i)
+            __builtin_amdgcn_global_load_lds((gvoid)(xsrc[i] + koff), (lvoid)(st + (wave + 4 * i) * 1024), 16, 0, 0);
+#pragma unroll
+        for (int i = 0; i < WP; ++i)
+            __builtin_amdgcn_global_load_lds((gvoid)(wsrc[i] + koff), (lvoid)(st + BM * 128 + (wave + 4 * i) * 1024),
+                                             16, 0, 0);
+    };
+
+    // Operand read addresses: row col of each 32-row block, chunk 2kk + half.
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
+    const int cmask = (col >> 1) & 7;
+    uint32_t chunk_off[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) chunk_off[kk] = ((2 * kk + half) ^ cmask) << 4;
+    // W rows of block i: value/gate pairing for GEGLU, else contiguous per wavefront.
+    const uint32_t w_row0 = BM * 128 + (GEGLU ? 32 * wn : (BN / 2) * wn) * 128 + col * 128;
+    const uint32_t x_row0 = ((BM / 2) * wm + col) * 128;
+    constexpr int W_BLOCK_STRIDE = GEGLU ? (BN / 2) * 128 : 32 * 128;
+
+    struct Ops {
+        u32x4 w[WNB];
+        u32x4 x[WMB];
+    };
+    auto read_ops = [&](uint32_t sbase, int kk, Ops& o) {
+        const uint32_t wa = sbase + w_row0 + chunk_off[kk];
+        const uint32_t xa = sbase + x_row0 + chunk_off[kk];
+        o.w[0] = lds_b128<0>(wa);
+        if constexpr (WNB > 1) o.w[1] = lds_b128<W_BLOCK_STRIDE>(wa);
+        o.x[0] = lds_b128<0>(xa);
+        if constexpr (WMB > 1) o.x[1] = lds_b128<32 * 128>(xa);
+    };
+    auto wait_ops = [&](Ops& o, auto n_tag) {
+        constexpr int N = decltype(n_tag)::value;
+        if constexpr (WNB == 2 && WMB == 2)
+            asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(o.w[0]), "+v"(o.w[1]), "+v"(o.x[0]), "+v"(o.x[1]) : "n"(N));
+        else if constexpr (WNB == 2)
+            asm volatile("s_waitcnt lgkmcnt(%3)" : "+v"(o.w[0]), "+v"(o.w[1]), "+v"(o.x[0]) : "n"(N));
+        else if constexpr (WMB == 2)
+            asm volatile("s_waitcnt lgkmcnt(%3)" : "+v"(o.w[0]), "+v"(o.x[0]), "+v"(o.x[1]) : "n"(N));
+        else
+            asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(o.w[0]), "+v"(o.x[0]) : "n"(N));
+    };
+
+    f32x16 acc[WNB][WMB];
+#pragma unroll
+    for (int i = 0; i < WNB; ++i)
+#pragma unroll
+        for (int j = 0; j < WMB; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+        if (s < nk) issue(s, s);
+    for (int kt = 0; kt < nk; ++kt) {
+        // k-tiles issued after kt so far: min(nk - 1 - kt, NS - 2), PT loads each
+        const int later = min(nk - 1 - kt, NS - 2);
+        if (NS >= 4 && later >= 2)
+            __builtin_amdgcn_s_waitcnt(0xF70 | (2 * PT));
+        else if (later >= 1)
+            __builtin_amdgcn_s_waitcnt(0xF70 | PT);
+        else
+            __builtin_amdgcn_s_waitcnt(0xF70);
+        __builtin_amdgcn_s_barrier();  // everyone's pieces of tile kt landed; the stage of tile kt-1 is free
+        if (kt + NS - 1 < nk) issue(kt + NS - 1, (kt + NS - 1) % NS);
+        const uint32_t sbase = lds0 + (kt % NS) * STAGE;
+        Ops o[2];
+        read_ops(sbase, 0, o[0]);
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            Ops& cur = o[kk & 1];
+            if (kk < 3) {
+                read_ops(sbase, kk + 1, o[(kk + 1) & 1]);
+                wait_ops(cur, IC<NOPS>{});
+            } else {
+                wait_ops(cur, IC<0>{});
+            }
+#pragma unroll
+            for (int i = 0; i < WNB; ++i)
+#pragma unroll
+                for (int j = 0; j < WMB; ++j)
+                    acc[i][j] = mfma32x32x16(__builtin_bit_cast(bf16x8, cur.w[i]), __builtin_bit_cast(bf16x8, cur.x[j]),
+                                             acc[i][j]);
+        }
+    }
+
+    // Epilogue: lane holds token (m-block base + col) and W rows
+    // (n-block base + 8c + 4*half + 0..3) in registers 4c..4c+3.
+    constexpr int NBO = GEGLU ? 1 : WNB;
+#pragma unroll
+    for (int i = 0; i < NBO; ++i) {
+#pragma unroll
+        for (int j = 0; j < WMB; ++j) {
+            const int m = m0 + (BM / 2) * wm + 32 * j + col;
+            if (m >= p.M) continue;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int nloc = GEGLU ? 32 * wn + 8 * c + 4 * half : (BN / 2) * wn + 32 * i + 8 * c + 4 * half;
+                const int n = n0 + nloc;
+                float v[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * c + e];
+                if (p.bias != nullptr) {
+                    bf16x4 bv = *(const bf16x4*)(p.bias + n);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] += bf16_to_f32(bv[e]);
+                }
+                if constexpr (GEGLU) {
+                    float g[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) g[e] = acc[1][j][4 * c + e];
+                    if (p.bias != nullptr) {
+                        bf16x4 bg = *(const bf16x4*)(p.bias + p.F + n);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) g[e] += bf16_to_f32(bg[e]);
+                    }
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] *= gelu_erf(g[e]);
+                }
+                if (p.resid != nullptr) {
+                    if (p.resid_f32) {
+                        f32x4 rv = *(const f32x4*)((const float*)p.resid + (int64_t)m * p.ldr + n);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) v[e] += rv[e];
+                    } else {
+                        bf16x4 rv = *(const bf16x4*)((const bf16*)p.resid + (int64_t)m * p.ldr + n);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) v[e] += bf16_to_f32(rv[e]);
+                    }
+                }
+                const int seg = n / p.seg;
+                const int ns = n - seg * p.seg;
+                void* dst = p.out[seg];
+                if (p.out_f32) {
+                    f32x4 o = {v[0], v[1], v[2], v[3]};
+                    *(f32x4*)((float*)dst + (int64_t)m * p.ldo + ns) = o;
+                } else {
+                    bf16x4 o = {f32_to_bf16(v[0]), f32_to_bf16(v[1]), f32_to_bf16(v[2]), f32_to_bf16(v[3])};
+                    *(bf16x4*)((bf16*)dst + (int64_t)m * p.ldo + ns) = o;
+                }
+                if (p.out_bf16 != nullptr) {
+                    bf16x4 o = {f32_to_bf16(v[0]), f32_to_bf16(v[1]), f32_to_bf16(v[2]), f32_to_bf16(v[3])};
+                    *(bf16x4*)((bf16*)p.out_bf16 + (int64_t)m * p.ldo + n) = o;
+                }
+            }
+        }
+    }
+}
+
+template <int BM, int BN, int NS, bool GEGLU>
+hipError_t launch_dma(const GemmParams& p, hipStream_t s) {
+    const int bn_out = GEGLU ? BN / 2 : BN;
+    dim3 grid((p.M + BM - 1) / BM, p.N / bn_out);
+    gemm_dma_kernel<BM, BN, NS, GEGLU><<<grid, 256, 0, s>>>(p);
+    return hipGetLastError();
+}
+
 template <int WMB, int WNB>
 hipError_t launch_shape(const GemmParams& p, hipStream_t s) {
     constexpr int BM = 64 * WMB;
@@ -234,6 +464,19 @@ bool gemm_shape_ok(const GemmParams& p) {
 }
 
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
+    // bf16 X with K % 64 == 0: the pipelined kernel, with the largest tile
+    // that still gives about a workgroup per compute unit.
+    if (!p.a_f32 && p.K % DBK == 0 && p.seg % 4 == 0) {
+        if (p.geglu) {
+            if (p.N % 64 == 0) return launch_dma<128, 128, 3, true>(p, s);
+        } else {
+            const int64_t mt128 = (p.M + 127) / 128, mt64 = (p.M + 63) / 64;
+            if (p.N % 128 == 0 && mt128 * (p.N / 128) >= 200) return launch_dma<128, 128, 3, false>(p, s);
+            if (p.N % 128 == 0 && mt64 * (p.N / 128) >= 200) return launch_dma<64, 128, 4, false>(p, s);
+            if (p.N % 64 == 0) return launch_dma<64, 64, 4, false>(p, s);
+        }
+    }
+    if (p.out_bf16 != nullptr) return hipErrorInvalidValue;  // only the pipelined kernel writes a bf16 copy
     // 128x128 tiles when they still give about a workgroup per compute unit,
     // else 64x128 / 64x64.
     if (p.geglu) return launch_shape<2, 2>(p, s);
