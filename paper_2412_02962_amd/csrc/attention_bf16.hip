@@ -7,24 +7,23 @@
 // lies inside one source is fetched from that source's base; a tile that
 // straddles two sources (or the end) picks the source row by row.
 //
-// Work decomposition.  A block is 128 queries of one (image, head); its key
-// tiles are cut into k equal pieces (k = 2 * compute units / blocks, so that
-// every compute unit holds two workgroups at once) and a workgroup computes
-// one piece of one block.  The blocks are dealt out to the XCDs in
-// contiguous ranges and all pieces of a block run on one XCD: workgroup w
-// runs on XCD w % n_xcd (the hardware deals workgroups out round-robin), so
-// the pieces of a block are merged through that XCD's L2 with ordinary
-// stores and one counter per block (the last piece to arrive merges and
-// resets the counter to zero).  Pieces of the blocks of one head start on
-// the same key tiles, so their tiles are fetched from HBM once and then hit
-// in the L2.
+// Work decomposition.  A block is 256 queries of one (image, head); its key
+// tiles are cut into k equal pieces (k = compute units / blocks, so that
+// every compute unit holds one workgroup) and a workgroup computes one piece
+// of one block.  The blocks are dealt out to the XCDs in contiguous ranges
+// and all pieces of a block run on one XCD: workgroup w runs on XCD w % n_xcd
+// (the hardware deals workgroups out round-robin), so the pieces of a block
+// are merged through that XCD's L2 with ordinary stores and one counter per
+// block (the last piece to arrive merges and resets the counter to zero).
+// Pieces of the blocks of one head start on the same key tiles, so their
+// tiles are fetched from HBM once and then hit in the L2.
 //
-// Inside a workgroup the four wavefronts (one per SIMD) own 32 queries each
+// Inside a workgroup the eight wavefronts (two per SIMD) own 32 queries each
 // and walk the same key tiles, staged once per workgroup in LDS by direct
-// global->LDS loads into three K and three V slots (tile t+2's keys and tile
-// t+1's values load while tile t is computed; one barrier per tile).  The
-// second workgroup of the compute unit puts a second wavefront on every SIMD.
-//
+// global->LDS loads into four K and four V slots (tile t+3's keys and tile
+// t+2's values load while tile t is computed; one barrier per tile, which
+// keeps the two wavefronts of a SIMD in step).
+
 // Software pipeline over 32-key half-tiles h.  Step h holds S(h) (scores of
 // half h) and P(h-1) (bf16 probabilities of half h-1) in registers and
 // interleaves, one matrix product at a time, the VALU softmax of S(h) with
@@ -58,23 +57,40 @@ namespace {
 constexpr int D = 64;
 constexpr int KT = 64;                      // keys per tile
 constexpr int QW = 32;                      // queries per wavefront
-constexpr int NW = 4;                       // wavefronts per workgroup
+#ifndef PCPP_ATTN_WAVES
+#define PCPP_ATTN_WAVES 8
+#endif
+constexpr int NW = PCPP_ATTN_WAVES;         // wavefronts per workgroup
 constexpr int QB = QW * NW;                 // queries per block
 constexpr int NTHREADS = 64 * NW;
-constexpr int WG_PER_CU = 2;
+constexpr int WG_PER_CU = 8 / NW;           // two wavefronts per SIMD
 constexpr int TILE_BYTES = KT * D * 2;      // 8 KB of K or of V
-constexpr int SLOTS = 3;                    // LDS slots for K tiles, and for V tiles
+constexpr int SLOTS = 4;                    // LDS slots for K tiles, and for V tiles
 constexpr int V_REGION = SLOTS * TILE_BYTES;
 constexpr float P_LIMIT = 1048576.0f;       // 2^20: bound on a lane's probability sum per half-tile
 constexpr int MIN_TILES_PER_PIECE = 2;
 constexpr int CUS_PER_XCD = 32;             // gfx950
 
-static_assert(WG_PER_CU * 2 * V_REGION + 64 <= 160 * 1024, "two workgroups share a compute unit's LDS");
-static_assert(TILE_BYTES / 1024 == 2 * NW, "each wavefront stages two 1 KB pieces of a K (and a V) tile");
+constexpr int PIECES = TILE_BYTES / 1024 / NW;  // 1 KB pieces of a tile each wavefront stages
+static_assert(WG_PER_CU * 2 * V_REGION + 64 <= 160 * 1024, "the workgroups of a compute unit share its LDS");
+static_assert(PIECES >= 1 && PIECES * NW * 1024 == TILE_BYTES, "the wavefronts stage whole 1 KB pieces of a tile");
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef const __attribute__((address_space(1))) void* gptr_t;
 typedef __attribute__((address_space(3))) void* lptr_t;
+
+// 16 bytes per lane from global memory straight into LDS: lane l's bytes land
+// at lds + 16 l (lds is the wave-uniform LDS byte address).  Written as inline
+// assembly so that the compiler does not track the LDS write: its own tracking
+// of such writes covers at most a few LDS buffers and otherwise waits for every
+// staging load in flight before any LDS read.  The kernel orders these writes
+// before the reads itself, with vmcnt waits and barriers.  Loads complete in
+// order, so the compiler's own vmcnt waits for register loads stay safe: they
+// only become more conservative.
+__device__ __forceinline__ void dma16(const void* g, const char* lds) {
+    const uint32_t a = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lptr_t)lds);
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(a) : "memory");
+}
 
 // LDS swizzles: 16-byte chunk c of tile row r is stored at slot c ^ mask(r).
 // K rows are read 16 bytes per lane by 32 consecutive rows at one chunk; V
@@ -138,9 +154,11 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
     __shared__ __attribute__((aligned(16))) char ks0[TILE_BYTES];
     __shared__ __attribute__((aligned(16))) char ks1[TILE_BYTES];
     __shared__ __attribute__((aligned(16))) char ks2[TILE_BYTES];
+    __shared__ __attribute__((aligned(16))) char ks3[TILE_BYTES];
     __shared__ __attribute__((aligned(16))) char vs0[TILE_BYTES];
     __shared__ __attribute__((aligned(16))) char vs1[TILE_BYTES];
     __shared__ __attribute__((aligned(16))) char vs2[TILE_BYTES];
+    __shared__ __attribute__((aligned(16))) char vs3[TILE_BYTES];
     __shared__ int flag_lds;
 
     const int tid = threadIdx.x;
@@ -168,11 +186,11 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
     // Staging geometry: wavefront w fills the 1 KB pieces 2w and 2w+1 of a
     // tile (rows 8*piece .. +8); lane l fills LDS slot l & 7 of row
     // 8*piece + (l >> 3) with the global chunk the swizzle puts there.
-    int ld_row[2];
-    uint32_t ld_koff[2], ld_voff[2];
+    int ld_row[PIECES];
+    uint32_t ld_koff[PIECES], ld_voff[PIECES];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int r = 8 * (2 * wave + i) + (lane >> 3);
+    for (int i = 0; i < PIECES; ++i) {
+        const int r = 8 * (PIECES * wave + i) + (lane >> 3);
         ld_row[i] = r;
         ld_koff[i] = (uint32_t)(r * C * 2 + (((lane & 7) ^ k_mask(r)) << 4));
         ld_voff[i] = (uint32_t)(r * C * 2 + (((lane & 7) ^ v_mask(r)) << 4));
@@ -230,7 +248,7 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
         // Stage tile t of K (is_v = false) or V into the slot at dst.
         auto issue = [&](int t_in, char* slot, bool is_v) {
             const int t = __builtin_amdgcn_readfirstlane(t_in);
-            char* dst = slot + 2 * wave * 1024;
+            char* dst = slot + PIECES * wave * 1024;
             const uint32_t* off = is_v ? ld_voff : ld_koff;
             const int j0 = t * KT, j1 = j0 + KT;
             const bool one_src = j1 <= kv_end && (j1 <= end0 || j0 >= end0) && (j1 <= end1 || j0 >= end1);
@@ -238,19 +256,17 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
                 const int64_t base = (is_v ? pick(j0, end0, end1, va0, va1, va2) : pick(j0, end0, end1, ka0, ka1, ka2)) +
                                      (int64_t)j0 * C * 2;
 #pragma unroll
-                for (int i = 0; i < 2; ++i)
-                    __builtin_amdgcn_global_load_lds((gptr_t)((const char*)(uintptr_t)base + off[i]),
-                                                     (lptr_t)(dst + i * 1024), 16, 0, 0);
+                for (int i = 0; i < PIECES; ++i)
+                    dma16((const char*)(uintptr_t)base + off[i], dst + i * 1024);
                 return;
             }
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
+            for (int i = 0; i < PIECES; ++i) {
                 int jk = j0 + ld_row[i];
                 jk = jk < kv_end ? jk : kv_end - 1;
                 const int64_t base = (is_v ? pick(jk, end0, end1, va0, va1, va2) : pick(jk, end0, end1, ka0, ka1, ka2)) +
                                      ((int64_t)jk - ld_row[i]) * C * 2;
-                __builtin_amdgcn_global_load_lds((gptr_t)((const char*)(uintptr_t)base + off[i]),
-                                                 (lptr_t)(dst + i * 1024), 16, 0, 0);
+                dma16((const char*)(uintptr_t)base + off[i], dst + i * 1024);
             }
         };
 
@@ -288,7 +304,10 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
         };
 
         __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): this thread's staging loads and Q have landed
-        __syncthreads();
+        __builtin_amdgcn_s_barrier();
+        // K of tile t0+2 and V of tile t0+1 load during the first period.
+        if (t0 + 2 < t1) issue(t0 + 2, ks2, false);
+        if (t0 + 1 < t1) issue(t0 + 1, vs1, true);
 
         // S(2 t0) from key half 0 of tile t0; operands of step 2 t0: key half
         // 1 of tile t0 and, standing in for the absent half 2 t0 - 1, value
@@ -378,23 +397,44 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
         };
 
         // Period of tile pt: its two halves.  Slots: K(pt) in kc, K(pt+1) in
-        // kn, V(pt) in vc; K(pt+2) and V(pt+1) are staged into kl and vl.
+        // kn, V(pt) in vc; K(pt+3) and V(pt+2) are staged into kl and vl, so
+        // every tile has two periods to arrive.
         auto period = [&](int pt, char* kc, char* kn, char* kl, char* vc, char* vl) {
+            // Two wavefronts share each SIMD and the barrier waits for the
+            // slower one; issue favours the older wavefront at equal
+            // priority.  Raising the priority for the first half-tile and
+            // dropping it for the second lets the one behind catch up.
+            __builtin_amdgcn_s_setprio(1);
             if (pt > t0) {
-                __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): K(pt+1) and V(pt) have landed
-                __syncthreads();                    // for everyone; slots of K(pt-1), V(pt-2) are free
+                // The previous period staged K(pt+2) (if it exists) and
+                // V(pt+1) (if it exists), PIECES loads per thread each; the
+                // loads before them, K(pt+1) and V(pt) among them, must land.
+                if (pt + 2 < t1)
+                    __builtin_amdgcn_s_waitcnt(0xF70 | (2 * PIECES));
+                else if (pt + 1 < t1)
+                    __builtin_amdgcn_s_waitcnt(0xF70 | PIECES);
+                else
+                    __builtin_amdgcn_s_waitcnt(0xF70);
+                // Everyone's loads have landed and nobody reads the slots of
+                // K(pt-1) and V(pt-2) any more.  A bare barrier: a fence would
+                // also wait for the loads still in flight.
+                __builtin_amdgcn_s_barrier();
             }
-            if (pt + 2 < t1) issue(pt + 2, kl, false);
-            if (pt + 1 < t1) issue(pt + 1, vl, true);
-            // keys of tile pt+1 (or, past the end, tile pt again: products discarded)
-            const char* kk = pt + 1 < t1 ? kn : kc;
-            step(2 * pt, s_a, s_b, p_b, p_a, op_a, op_b, kk, 0, vc, 0);
-            step(2 * pt + 1, s_b, s_a, p_a, p_b, op_b, op_a, kk, 1, vc, 1);
+            if (pt + 3 < t1) issue(pt + 3, kl, false);
+            if (pt + 2 < t1) issue(pt + 2, vl, true);
+            // Keys of tile pt+1.  Past the end the slot holds stale bytes that
+            // no load is writing; their products are never used.  (A select
+            // between slots here would hide from the compiler which slot is
+            // read, and it would then wait for every staging load in flight.)
+            step(2 * pt, s_a, s_b, p_b, p_a, op_a, op_b, kn, 0, vc, 0);
+            __builtin_amdgcn_s_setprio(0);
+            step(2 * pt + 1, s_b, s_a, p_a, p_b, op_b, op_a, kn, 1, vc, 1);
         };
-        for (int pt = t0; pt < t1; pt += 3) {
-            period(pt, ks0, ks1, ks2, vs0, vs1);
-            if (pt + 1 < t1) period(pt + 1, ks1, ks2, ks0, vs1, vs2);
-            if (pt + 2 < t1) period(pt + 2, ks2, ks0, ks1, vs2, vs0);
+        for (int pt = t0; pt < t1; pt += 4) {
+            period(pt, ks0, ks1, ks3, vs0, vs2);
+            if (pt + 1 < t1) period(pt + 1, ks1, ks2, ks0, vs1, vs3);
+            if (pt + 2 < t1) period(pt + 2, ks2, ks3, ks1, vs2, vs0);
+            if (pt + 3 < t1) period(pt + 3, ks3, ks0, ks2, vs3, vs1);
         }
         // Drain: O^T += V(2 t1 - 1)^T P(2 t1 - 1)^T, operands in op_a.
 #pragma unroll
