@@ -136,9 +136,10 @@ def graph_time_us(torch, fn, K, use_graph=True):
     return e0.elapsed_time(e1) / K * 1e3
 
 
-def extras(torch, pcpp, synth, dev, use_graph=True, reps=200):
+def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
     """Context lines: materialised gather (GB/s vs HBM peak), the p = 0.5
-    variant of the 2048 px level-1 workload, and the full block."""
+    variant of the 2048 px level-1 workload, the level-2 shapes, and the full
+    block."""
     import numpy as np
 
     def to_dev(x):
@@ -172,6 +173,32 @@ def extras(torch, pcpp, synth, dev, use_graph=True, reps=200):
                                                                   d50["v_dn"], o50, ws50, w50), reps, use_graph)
     out["p50_us"] = round(us, 3)
     out["p50_TFLOPs"] = round(attn_flops(c50, nkv50) / us / 1e6, 1)
+
+    # SDXL's other self-attention shape at 2048 px: the 64 x 64 level-2 grid,
+    # 1280 channels (20 heads), same 8 bands and p; the edge band (one
+    # neighbour) and an interior band.  Derived, labelled as such: the
+    # self-attention share of one whole U-Net step for one band, 10 level-1
+    # layers + 60 level-2 layers (SDXL's transformer depths).
+    l2 = {}
+    for name, band in (("edge", None), ("interior", 3)):
+        c2 = synth.ATTN_CONFIGS["sdxl2048_l2_edge"]
+        if band is not None:
+            import dataclasses
+            c2 = dataclasses.replace(c2, i=band)
+        d2 = {k: to_dev(v) for k, v in synth.attention_inputs(c2).items()}
+        g2 = pcpp.make_geom(c2.H, c2.W, c2.n, c2.i, c2.p, c2.heads, c2.d, 1, 0, pcpp.PCPP_DTYPE_BF16)
+        _, _, _, nkv2 = pcpp.pcpp_context_rows(g2)
+        o2 = torch.empty_like(d2["q"])
+        w2 = pcpp.pcpp_partial_attention_workspace_size(g2)
+        ws2 = torch.zeros(max(w2, 1), dtype=torch.uint8, device=dev)
+        us = graph_time_us(torch, lambda: pcpp.pcpp_partial_attention(g2, d2["q"], d2["k_fresh"], d2["v_fresh"],
+                                                                      d2["k_up"], d2["v_up"], d2["k_dn"],
+                                                                      d2["v_dn"], o2, ws2, w2), reps, use_graph)
+        l2[name] = us
+        out[f"l2_{name}_us"] = round(us, 3)
+        out[f"l2_{name}_keys"] = nkv2
+        out[f"l2_{name}_TFLOPs"] = round(attn_flops(c2, nkv2) / us / 1e6, 1)
+    out["derived_unet_selfattn_ms_per_band_step"] = round((10 * out_l1_us + 60 * l2["interior"]) / 1e3, 4)
 
     bc = synth.BLOCK_CONFIG
     bcfg = bc.attn
@@ -351,6 +378,16 @@ def main():
     ms_total = ev0.elapsed_time(ev1)
     ms_step = ms_total / K
 
+    # per-launch durations: an event pair around each of 200 eager launches
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(200)]
+    for e0, e1 in evs:
+        e0.record(stream)
+        step()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    per = sorted(e0.elapsed_time(e1) * 1e3 for e0, e1 in evs)
+    pct = {q: round(per[min(len(per) - 1, int(q / 100 * len(per)))], 3) for q in (10, 50, 90)}
+
     # eager rate as context (includes host launch overhead of the ctypes call)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -383,10 +420,11 @@ def main():
                      "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
                      "algorithmic_bytes": abytes, "kernel_avg_us": round(ms_step * 1e3, 3)},
         "extra": {"pct_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2), "eager_ms_per_call": round(eager_ms, 4),
-                  "workspace_bytes": wsb, "gflop_per_step": round(flops / 1e9, 3)},
+                  "workspace_bytes": wsb, "gflop_per_step": round(flops / 1e9, 3),
+                  "launch_us_p10": pct[10], "launch_us_p50": pct[50], "launch_us_p90": pct[90]},
     }
     if not args.no_extras:
-        res["extra"].update(extras(torch, pcpp, synth, dev, graph is not None, min(K, 200)))
+        res["extra"].update(extras(torch, pcpp, synth, dev, ms_step * 1e3, graph is not None, min(K, 200)))
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, inputs)
     print(json.dumps(res), flush=True)

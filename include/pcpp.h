@@ -220,7 +220,7 @@ size_t pcpp_transformer_block_workspace_size(const pcpp_geom_t* g,
  *                next step (Sec. 3.2); either may be NULL
  *   workspace    device scratch, ws_bytes >= the workspace size
  * Requires dtype PCPP_DTYPE_BF16 and head_dim 64 (PCPP_ENOTSUP otherwise),
- * C <= 2048 (PCPP_ENOTSUP), text_dim >= 32 with text_dim % 32 == 0,
+ * C <= 2048 and gn_groups <= 256 (PCPP_ENOTSUP), text_dim >= 32 with text_dim % 32 == 0,
  * n_text >= 1, ff_inner % 64 == 0, C % gn_groups == 0 (PCPP_EINVAL).  All
  * pointers, weights included, must be 16-byte aligned (PCPP_EINVAL).
  * The workspace follows the contract above (zero-filled before first use).

@@ -68,7 +68,7 @@ constexpr int TILE_BYTES = KT * D * 2;      // 8 KB of K or of V
 constexpr int SLOTS = 4;                    // LDS slots for K tiles, and for V tiles
 constexpr int V_REGION = SLOTS * TILE_BYTES;
 constexpr float P_LIMIT = 1048576.0f;       // 2^20: bound on a lane's probability sum per half-tile
-constexpr int MIN_TILES_PER_PIECE = 2;
+constexpr int MIN_TILES_PER_PIECE = 3;
 constexpr int CUS_PER_XCD = 32;             // gfx950
 
 constexpr int PIECES = TILE_BYTES / 1024 / NW;  // 1 KB pieces of a tile each wavefront stages

@@ -47,7 +47,7 @@ int validate_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, int32_t 
     if (n_text < 1 || text_dim < 32 || text_dim % 32 != 0) return PCPP_EINVAL;
     if (w->ff_inner < 64 || w->ff_inner % 64 != 0) return PCPP_EINVAL;
     if (w->gn_groups < 1 || r->C % w->gn_groups != 0) return PCPP_EINVAL;
-    if (r->C > 2048) return PCPP_ENOTSUP;  // LayerNorm keeps a row in registers
+    if (!norm_shapes_ok(r->C, w->gn_groups)) return PCPP_ENOTSUP;  // LayerNorm keeps a row in registers
     if (g->heads > 65535 || g->batch > 65535) return PCPP_EINVAL;
     return PCPP_OK;
 }
@@ -97,7 +97,7 @@ BlockLayout layout(const pcpp_geom_t* g, const Geo& r, const pcpp_block_weights_
     L.v2 = take((size_t)g->batch * n_text * C * 2);
     L.u16 = take(rows * (size_t)w->ff_inner * 2);
     L.attn_ws = take(L.attn_ws_bytes);
-    L.gn = take(group_norm_ws_bytes(g->batch, w->gn_groups));
+    L.gn = take(group_norm_ws_bytes(g->batch, w->gn_groups, r.nq));
     L.total = off;
     return L;
 }
@@ -198,7 +198,6 @@ PCPP_EXPORT int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_we
     gp.N = N;
     gp.C = C;
     gp.G = w->gn_groups;
-    gp.chunks = 8;
     gp.eps = 1e-6f;
     PCPP_CHECK(launch_group_norm(gp, s));
     PCPP_CHECK(launch_gemm(gemm(t16, C, false, w->proj_in_w, w->proj_in_b, rows, C, C, hid, C, true), s));

@@ -37,11 +37,13 @@ struct GroupNormParams {
     __bf16* y;            // [B, N, C]
     const __bf16* gamma;
     const __bf16* beta;
-    float* stats;         // workspace [B, G, chunks, 3]
-    int32_t B, N, C, G, chunks;
+    float* stats;         // workspace of group_norm_ws_bytes(B, G, N)
+    int32_t B, N, C, G, chunks;  // chunks: set by launch_group_norm
     float eps;
 };
-size_t group_norm_ws_bytes(int B, int G);
+size_t group_norm_ws_bytes(int B, int G, int N);
+// C % 8 == 0, C <= 2048, 1 <= G <= 256 divides C.
+bool norm_shapes_ok(int C, int G);
 hipError_t launch_group_norm(GroupNormParams p, hipStream_t s);
 
 // LayerNorm over the channel axis of fp32 rows, bf16 output.

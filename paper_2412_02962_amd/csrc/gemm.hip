@@ -23,7 +23,23 @@ namespace {
 constexpr int BK = 32;
 constexpr int LSTR = 40;  // LDS row stride in elements
 
-__device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
+// erf by Abramowitz and Stegun, Handbook of Mathematical Functions, formula
+// 7.1.26: erf(x) = 1 - (a1 t + ... + a5 t^5) exp(-x^2), t = 1 / (1 + p x) for
+// x >= 0, odd extension; absolute error at most 1.5e-7, far below the bf16
+// rounding of the products it feeds.
+__device__ __forceinline__ float erf_as(float x) {
+    const float a = fabsf(x);
+    const float t = __builtin_amdgcn_rcpf(__builtin_fmaf(0.3275911f, a, 1.0f));
+    float y = __builtin_fmaf(1.061405429f, t, -1.453152027f);
+    y = __builtin_fmaf(y, t, 1.421413741f);
+    y = __builtin_fmaf(y, t, -0.284496736f);
+    y = __builtin_fmaf(y, t, 0.254829592f);
+    y *= t;
+    const float e = __builtin_amdgcn_exp2f(-a * a * 1.4426950408889634f);
+    return copysignf(__builtin_fmaf(-y, e, 1.0f), x);
+}
+
+__device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erf_as(x * 0.70710678118654752f)); }
 
 typedef const __attribute__((address_space(1))) u32x4* gchunk;
 
@@ -373,49 +389,67 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
     }
 
     // Epilogue: lane holds token (m-block base + col) and W rows
-    // (n-block base + 8c + 4*half + 0..3) in registers 4c..4c+3.
+    // (n-block base + 8c + 4*half + 0..3) in registers 4c..4c+3.  All bias
+    // and residual loads are issued before the first store: the output may
+    // be the residual buffer itself (an in-place update, each element read
+    // and written by the same lane), so the compiler could not move a load
+    // above an earlier store.
     constexpr int NBO = GEGLU ? 1 : WNB;
+    auto n_of = [&](int i, int c) {
+        return n0 + (GEGLU ? 32 * wn + 8 * c + 4 * half : (BN / 2) * wn + 32 * i + 8 * c + 4 * half);
+    };
+    auto m_of = [&](int j) { return m0 + (BM / 2) * wm + 32 * j + col; };
+    float bias_v[NBO][4][4], bias_g[4][4];
+    f32x4 res_v[NBO][WMB][4];
+#pragma unroll
+    for (int i = 0; i < NBO; ++i)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int n = n_of(i, c);
+            bf16x4 bv = {}, bg = {};
+            if (p.bias != nullptr) {
+                bv = *(const bf16x4*)(p.bias + n);
+                if constexpr (GEGLU) bg = *(const bf16x4*)(p.bias + p.F + n);
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                bias_v[i][c][e] = bf16_to_f32(bv[e]);
+                if constexpr (GEGLU) bias_g[c][e] = bf16_to_f32(bg[e]);
+            }
+#pragma unroll
+            for (int j = 0; j < WMB; ++j) {
+                const int m = min(m_of(j), p.M - 1);
+                f32x4 rv = {0.f, 0.f, 0.f, 0.f};
+                if (p.resid != nullptr) {
+                    if (p.resid_f32) {
+                        rv = *(const f32x4*)((const float*)p.resid + (int64_t)m * p.ldr + n);
+                    } else {
+                        const bf16x4 rb = *(const bf16x4*)((const bf16*)p.resid + (int64_t)m * p.ldr + n);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) rv[e] = bf16_to_f32(rb[e]);
+                    }
+                }
+                res_v[i][j][c] = rv;
+            }
+        }
 #pragma unroll
     for (int i = 0; i < NBO; ++i) {
 #pragma unroll
         for (int j = 0; j < WMB; ++j) {
-            const int m = m0 + (BM / 2) * wm + 32 * j + col;
+            const int m = m_of(j);
             if (m >= p.M) continue;
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
-                const int nloc = GEGLU ? 32 * wn + 8 * c + 4 * half : (BN / 2) * wn + 32 * i + 8 * c + 4 * half;
-                const int n = n0 + nloc;
+                const int n = n_of(i, c);
                 float v[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * c + e];
-                if (p.bias != nullptr) {
-                    bf16x4 bv = *(const bf16x4*)(p.bias + n);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) v[e] += bf16_to_f32(bv[e]);
-                }
+                for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * c + e] + bias_v[i][c][e];
                 if constexpr (GEGLU) {
-                    float g[4];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) g[e] = acc[1][j][4 * c + e];
-                    if (p.bias != nullptr) {
-                        bf16x4 bg = *(const bf16x4*)(p.bias + p.F + n);
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) g[e] += bf16_to_f32(bg[e]);
-                    }
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) v[e] *= gelu_erf(g[e]);
+                    for (int e = 0; e < 4; ++e) v[e] *= gelu_erf(acc[1][j][4 * c + e] + bias_g[c][e]);
                 }
-                if (p.resid != nullptr) {
-                    if (p.resid_f32) {
-                        f32x4 rv = *(const f32x4*)((const float*)p.resid + (int64_t)m * p.ldr + n);
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) v[e] += rv[e];
-                    } else {
-                        bf16x4 rv = *(const bf16x4*)((const bf16*)p.resid + (int64_t)m * p.ldr + n);
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) v[e] += bf16_to_f32(rv[e]);
-                    }
-                }
+                for (int e = 0; e < 4; ++e) v[e] += res_v[i][j][c][e];
                 const int seg = n / p.seg;
                 const int ns = n - seg * p.seg;
                 void* dst = p.out[seg];
@@ -468,7 +502,7 @@ hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
     // that still gives about a workgroup per compute unit.
     if (!p.a_f32 && p.K % DBK == 0 && p.seg % 4 == 0) {
         if (p.geglu) {
-            if (p.N % 64 == 0) return launch_dma<128, 128, 3, true>(p, s);
+            if (p.N % 64 == 0) return launch_dma<128, 128, 2, true>(p, s);
         } else {
             const int64_t mt128 = (p.M + 127) / 128, mt64 = (p.M + 63) / 64;
             if (p.N % 128 == 0 && mt128 * (p.N / 128) >= 200) return launch_dma<128, 128, 3, false>(p, s);
