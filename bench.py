@@ -161,6 +161,23 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
     out["gather_GBps"] = round(gbytes / us / 1e3, 1)
     out["gather_frac_hbm"] = round(gbytes / us / 1e3 / PEAK_HBM_GBS, 4)
 
+    # p-aware boundary messages of the same band: both messages packed from
+    # the fresh K/V (sender side) and both placed into the stale buffers
+    # (receiver side); bytes = read + write of every message.
+    nb = pcpp.pcpp_boundary_bytes(g)
+    s_up = torch.empty(nb // 2, dtype=torch.bfloat16, device=dev)
+    s_dn = torch.empty(nb // 2, dtype=torch.bfloat16, device=dev)
+    ku, vu, kd, vd = (torch.empty_like(d["k_fresh"]) for _ in range(4))
+    us = graph_time_us(torch, lambda: pcpp.pcpp_pack_boundary(g, d["k_fresh"], d["v_fresh"], s_up, s_dn), reps,
+                       use_graph)
+    out["pack_us"] = round(us, 3)
+    out["pack_GBps"] = round(2 * 2 * nb / us / 1e3, 1)
+    out["pack_frac_hbm"] = round(2 * 2 * nb / us / 1e3 / PEAK_HBM_GBS, 4)
+    out["message_bytes"] = nb
+    us = graph_time_us(torch, lambda: pcpp.pcpp_unpack_boundary(g, s_dn, s_up, ku, vu, kd, vd), reps, use_graph)
+    out["unpack_us"] = round(us, 3)
+    out["unpack_GBps"] = round(2 * 2 * nb / us / 1e3, 1)
+
     c50 = synth.ATTN_CONFIGS["sdxl2048_l1_p50"]
     d50 = {k: to_dev(v) for k, v in synth.attention_inputs(c50).items()}
     g50 = pcpp.make_geom(c50.H, c50.W, c50.n, c50.i, c50.p, c50.heads, c50.d, 1, 0, pcpp.PCPP_DTYPE_BF16)

@@ -233,6 +233,49 @@ int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w,
                            void* y, void* k_fresh_out, void* v_fresh_out,
                            void* workspace, size_t ws_bytes, void* stream);
 
+/*
+ * p-aware boundary messages of the neighbour exchange (Sec. 3.2 with Eq. 1).
+ * At the next step band i-1 reads the first r rows of band i's fresh keys
+ * and values (its context below) and band i+1 reads the last r rows (its
+ * context above), r = min(h, floor(p*h + 1e-9)).  Sending only those rows
+ * instead of the whole band is the p-aware form of the exchange; these
+ * calls build and place the messages on one device (the transfer between
+ * devices is the caller's).
+ *
+ * Message layout: [B][2][r*W][C] - per image, the r key rows, then the r
+ * value rows, each row W tokens of C elements, dtype of g.
+ */
+
+/* Bytes of one message for geometry g: B * 2 * r * W * C * element size
+ * (0 for an invalid geometry, and when r = 0 or n = 1). */
+size_t pcpp_boundary_bytes(const pcpp_geom_t* g);
+
+/*
+ * Builds band i's messages from its fresh keys/values [B, h*W, C]:
+ *   send_up  for band i-1: rows 0 .. r-1 of this band (needed when i > 0
+ *            and r > 0, else ignored and may be NULL)
+ *   send_dn  for band i+1: rows h-r .. h-1 (needed when i < n-1 and r > 0)
+ * Messages must not overlap the inputs or each other (PCPP_EINVAL).  No
+ * alignment is required.  Asynchronous on `stream`.
+ */
+int pcpp_pack_boundary(const pcpp_geom_t* g, const void* k_fresh,
+                       const void* v_fresh, void* send_up, void* send_dn,
+                       void* stream);
+
+/*
+ * Places the messages band i received into its stale buffers [B, h*W, C],
+ * at the rows pcpp_partial_attention reads from them:
+ *   recv_up (built by band i-1 as its send_dn) -> the last r rows of k_up
+ *            and v_up (needed when i > 0 and r > 0)
+ *   recv_dn (built by band i+1 as its send_up) -> the first r rows of k_dn
+ *            and v_dn (needed when i < n-1 and r > 0)
+ * The other rows of the stale buffers are left untouched; the attention
+ * never reads them.  Buffers must not overlap (PCPP_EINVAL).  Asynchronous.
+ */
+int pcpp_unpack_boundary(const pcpp_geom_t* g, const void* recv_up,
+                         const void* recv_dn, void* k_up, void* v_up,
+                         void* k_dn, void* v_dn, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -8,6 +8,7 @@ from .pcpp_oracle import (  # noqa: F401
     CTX_EPS,
     as_f64,
     assemble_context,
+    boundary_messages,
     context_rows,
     context_token_ids,
     from_bf16_bits,
@@ -18,5 +19,6 @@ from .pcpp_oracle import (  # noqa: F401
     linear,
     mha,
     partial_attention,
+    place_boundary_messages,
     transformer_block,
 )

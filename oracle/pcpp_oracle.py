@@ -128,6 +128,63 @@ def assemble_context(H: int, W: int, n: int, i: int, p: float,
 
 
 # ---------------------------------------------------------------------------
+# Sec. 3.2 with Eq. 1: the rows a patch's neighbours read from it
+# ---------------------------------------------------------------------------
+
+def boundary_messages(H: int, W: int, n: int, i: int, p: float,
+                      k_fresh: np.ndarray, v_fresh: np.ndarray):
+    """What patch i sends its two neighbours for their next step.
+
+    Sec. 3.2: a patch exchanges its activations only with the neighbouring
+    patches, which use them one step later as stale context.  Eq. 1 (seen
+    from the neighbours): patch i-1 is conditioned on the upper rows of
+    patch i, as many as patch i-1's own geometry takes from below; patch
+    i+1 on the lower rows of patch i, as many as it takes from above.  Only
+    those rows need to travel (the p-aware form of the exchange; the paper
+    sends whole patches).
+
+    k_fresh, v_fresh: [B, h*W, C].  Returns (to_up, to_dn), each
+    [B, 2, rows*W, C] (keys, then values), or None when that neighbour does
+    not exist or takes no rows.
+    """
+    h = H // n
+    to_up = to_dn = None
+    if i > 0:
+        rows = context_rows(H, n, i - 1, p)[2]  # what patch i-1 takes from below
+        if rows > 0:
+            to_up = np.stack([k_fresh[:, :rows * W, :], v_fresh[:, :rows * W, :]], axis=1)
+    if i < n - 1:
+        rows = context_rows(H, n, i + 1, p)[1]  # what patch i+1 takes from above
+        if rows > 0:
+            to_dn = np.stack([k_fresh[:, (h - rows) * W:h * W, :], v_fresh[:, (h - rows) * W:h * W, :]],
+                             axis=1)
+    return to_up, to_dn
+
+
+def place_boundary_messages(H: int, W: int, n: int, i: int, p: float,
+                            from_up: Optional[np.ndarray], from_dn: Optional[np.ndarray],
+                            k_up: np.ndarray, v_up: np.ndarray,
+                            k_dn: np.ndarray, v_dn: np.ndarray):
+    """Receiver side of boundary_messages for patch i.
+
+    from_up was built by patch i-1 (its lower rows), from_dn by patch i+1
+    (its upper rows).  They are written where Eq. 1 reads them: the last
+    `up` rows of the stale buffer of the patch above, the first `dn` rows of
+    that of the patch below.  Returns new (k_up, v_up, k_dn, v_dn); the
+    inputs are not modified and their other rows are kept.
+    """
+    h, up, dn, _ = context_rows(H, n, i, p)
+    k_up, v_up, k_dn, v_dn = (None if a is None else np.array(a, copy=True) for a in (k_up, v_up, k_dn, v_dn))
+    if up > 0:
+        k_up[:, (h - up) * W:h * W, :] = from_up[:, 0]
+        v_up[:, (h - up) * W:h * W, :] = from_up[:, 1]
+    if dn > 0:
+        k_dn[:, :dn * W, :] = from_dn[:, 0]
+        v_dn[:, :dn * W, :] = from_dn[:, 1]
+    return k_up, v_up, k_dn, v_dn
+
+
+# ---------------------------------------------------------------------------
 # Sec. 3.3: multi-head scaled dot-product attention over the context
 # ---------------------------------------------------------------------------
 

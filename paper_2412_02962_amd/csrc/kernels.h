@@ -53,4 +53,21 @@ struct GatherParams {
 };
 hipError_t launch_gather(const GatherParams& p, hipStream_t stream);
 
+// Up to four contiguous runs of `bytes` per image, image b's run starting at
+// src + b * src_bstride and going to dst + b * dst_bstride (bytes).  Runs
+// must not overlap each other's destinations or any source.
+struct CopySeg {
+    const char* src;
+    char* dst;
+    int64_t src_bstride;
+    int64_t dst_bstride;
+    int64_t bytes;
+};
+struct CopyParams {
+    CopySeg seg[4];
+    int32_t n_seg;
+    int32_t batch;
+};
+hipError_t launch_seg_copy(const CopyParams& p, int esize, hipStream_t stream);
+
 }  // namespace pcpp

@@ -182,3 +182,117 @@ PCPP_EXPORT int pcpp_partial_attention(const pcpp_geom_t* g, const void* q, cons
     }
     return e == hipSuccess ? PCPP_OK : PCPP_EHIP;
 }
+
+// ---------------------------------------------------------------------------
+// p-aware boundary messages (Sec. 3.2 with Eq. 1)
+// ---------------------------------------------------------------------------
+
+namespace {
+
+// Rows a neighbour of band i reads from it: ctx rows of the neighbour's own
+// geometry (the same r for every band of one layer).
+int32_t neighbour_rows(const Geo& r) { return r.up > r.dn ? r.up : r.dn; }
+
+bool ranges_overlap(const void* a, int64_t na, const void* b, int64_t nb) {
+    if (!a || !b || na <= 0 || nb <= 0) return false;
+    const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    return x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
+}
+
+}  // namespace
+
+PCPP_EXPORT size_t pcpp_boundary_bytes(const pcpp_geom_t* g) {
+    Geo r;
+    if (validate_geom(g, &r) != PCPP_OK) return 0;
+    if (g->dtype != PCPP_DTYPE_BF16 && g->dtype != PCPP_DTYPE_F32) return 0;
+    return (size_t)g->batch * 2 * (size_t)neighbour_rows(r) * g->W * r.C * r.esize;
+}
+
+PCPP_EXPORT int pcpp_pack_boundary(const pcpp_geom_t* g, const void* k_fresh, const void* v_fresh,
+                                   void* send_up, void* send_dn, void* stream) {
+    Geo r;
+    int st = validate_geom(g, &r);
+    if (st != PCPP_OK) return st;
+    if (g->dtype != PCPP_DTYPE_BF16 && g->dtype != PCPP_DTYPE_F32) return PCPP_ENOTSUP;
+    if (g->batch > 65535) return PCPP_EINVAL;
+    const bool to_up = r.up > 0, to_dn = r.dn > 0;  // band i-1 / i+1 exists and reads rows
+    if (!to_up && !to_dn) return PCPP_OK;
+    if (!k_fresh || !v_fresh) return PCPP_EINVAL;
+    if ((to_up && !send_up) || (to_dn && !send_dn)) return PCPP_EINVAL;
+    const int64_t row = (int64_t)g->W * r.C * r.esize;  // bytes of one token row
+    const int64_t band = row * r.h;
+    const int64_t run = row * neighbour_rows(r);
+    const int64_t msg = 2 * run * g->batch;
+    const int64_t fresh_all = band * g->batch;
+    for (const void* out : {(const void*)(to_up ? send_up : nullptr), (const void*)(to_dn ? send_dn : nullptr)})
+        if (ranges_overlap(out, msg, k_fresh, fresh_all) || ranges_overlap(out, msg, v_fresh, fresh_all))
+            return PCPP_EINVAL;
+    if (to_up && to_dn && ranges_overlap(send_up, msg, send_dn, msg)) return PCPP_EINVAL;
+    CopyParams p;
+    p.n_seg = 0;
+    p.batch = g->batch;
+    auto add = [&](const void* src, int64_t src_off, void* dst, int64_t dst_off) {
+        CopySeg& s = p.seg[p.n_seg++];
+        s.src = (const char*)src + src_off;
+        s.dst = (char*)dst + dst_off;
+        s.src_bstride = band;
+        s.dst_bstride = 2 * run;
+        s.bytes = run;
+    };
+    if (to_up) {  // the band above reads this band's first r rows
+        add(k_fresh, 0, send_up, 0);
+        add(v_fresh, 0, send_up, run);
+    }
+    if (to_dn) {  // the band below reads this band's last r rows
+        add(k_fresh, band - run, send_dn, 0);
+        add(v_fresh, band - run, send_dn, run);
+    }
+    return launch_seg_copy(p, r.esize, (hipStream_t)stream) == hipSuccess ? PCPP_OK : PCPP_EHIP;
+}
+
+PCPP_EXPORT int pcpp_unpack_boundary(const pcpp_geom_t* g, const void* recv_up, const void* recv_dn,
+                                     void* k_up, void* v_up, void* k_dn, void* v_dn, void* stream) {
+    Geo r;
+    int st = validate_geom(g, &r);
+    if (st != PCPP_OK) return st;
+    if (g->dtype != PCPP_DTYPE_BF16 && g->dtype != PCPP_DTYPE_F32) return PCPP_ENOTSUP;
+    if (g->batch > 65535) return PCPP_EINVAL;
+    const bool from_up = r.up > 0, from_dn = r.dn > 0;
+    if ((from_up && (!recv_up || !k_up || !v_up)) || (from_dn && (!recv_dn || !k_dn || !v_dn)))
+        return PCPP_EINVAL;
+    if (!from_up && !from_dn) return PCPP_OK;
+    const int64_t row = (int64_t)g->W * r.C * r.esize;
+    const int64_t band = row * r.h;
+    const int64_t run = row * neighbour_rows(r);
+    const int64_t msg = 2 * run * g->batch;
+    const int64_t stale_all = band * g->batch;
+    const void* recvs[2] = {from_up ? recv_up : nullptr, from_dn ? recv_dn : nullptr};
+    void* outs[4] = {from_up ? k_up : nullptr, from_up ? v_up : nullptr, from_dn ? k_dn : nullptr,
+                     from_dn ? v_dn : nullptr};
+    for (int a = 0; a < 4; ++a) {
+        for (const void* in : recvs)
+            if (ranges_overlap(outs[a], stale_all, in, msg)) return PCPP_EINVAL;
+        for (int c = a + 1; c < 4; ++c)
+            if (ranges_overlap(outs[a], stale_all, outs[c], stale_all)) return PCPP_EINVAL;
+    }
+    CopyParams p;
+    p.n_seg = 0;
+    p.batch = g->batch;
+    auto add = [&](const void* src, int64_t src_off, void* dst, int64_t dst_off) {
+        CopySeg& s = p.seg[p.n_seg++];
+        s.src = (const char*)src + src_off;
+        s.dst = (char*)dst + dst_off;
+        s.src_bstride = 2 * run;
+        s.dst_bstride = band;
+        s.bytes = run;
+    };
+    if (from_up) {  // the band above sent its last r rows: they close the stale buffer
+        add(recv_up, 0, k_up, band - run);
+        add(recv_up, run, v_up, band - run);
+    }
+    if (from_dn) {  // the band below sent its first r rows: they open the stale buffer
+        add(recv_dn, 0, k_dn, 0);
+        add(recv_dn, run, v_dn, 0);
+    }
+    return launch_seg_copy(p, r.esize, (hipStream_t)stream) == hipSuccess ? PCPP_OK : PCPP_EHIP;
+}

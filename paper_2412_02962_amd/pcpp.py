@@ -72,6 +72,9 @@ def _load():
         "pcpp_transformer_block_workspace_size": (sz, [gp, wp, i32, i32]),
         "pcpp_transformer_block": (ctypes.c_int, [gp, wp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp,
                                                   vp, sz, vp]),
+        "pcpp_boundary_bytes": (sz, [gp]),
+        "pcpp_pack_boundary": (ctypes.c_int, [gp, vp, vp, vp, vp, vp]),
+        "pcpp_unpack_boundary": (ctypes.c_int, [gp, vp, vp, vp, vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -85,6 +88,7 @@ EXPORTED = (
     "pcpp_version", "pcpp_strerror", "pcpp_context_rows", "pcpp_gather_context",
     "pcpp_partial_attention_workspace_size", "pcpp_partial_attention",
     "pcpp_transformer_block_workspace_size", "pcpp_transformer_block",
+    "pcpp_boundary_bytes", "pcpp_pack_boundary", "pcpp_unpack_boundary",
 )
 
 
@@ -170,4 +174,19 @@ def pcpp_transformer_block(g, w, x, text, n_text, text_dim, k_up, v_up, k_dn, v_
     _check("pcpp_transformer_block", _lib.pcpp_transformer_block(
         ctypes.byref(g), ctypes.byref(w), _ptr(x), _ptr(text), n_text, text_dim, _ptr(k_up), _ptr(v_up),
         _ptr(k_dn), _ptr(v_dn), _ptr(y), _ptr(k_fresh_out), _ptr(v_fresh_out), _ptr(workspace), ws_bytes,
+        _stream(stream)))
+
+
+def pcpp_boundary_bytes(g) -> int:
+    return _lib.pcpp_boundary_bytes(ctypes.byref(g))
+
+
+def pcpp_pack_boundary(g, k_fresh, v_fresh, send_up, send_dn, stream=None):
+    _check("pcpp_pack_boundary", _lib.pcpp_pack_boundary(
+        ctypes.byref(g), _ptr(k_fresh), _ptr(v_fresh), _ptr(send_up), _ptr(send_dn), _stream(stream)))
+
+
+def pcpp_unpack_boundary(g, recv_up, recv_dn, k_up, v_up, k_dn, v_dn, stream=None):
+    _check("pcpp_unpack_boundary", _lib.pcpp_unpack_boundary(
+        ctypes.byref(g), _ptr(recv_up), _ptr(recv_dn), _ptr(k_up), _ptr(v_up), _ptr(k_dn), _ptr(v_dn),
         _stream(stream)))

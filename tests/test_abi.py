@@ -185,3 +185,38 @@ def test_block_workspace_size_scales_with_batch_and_rejects_invalid():
                                                      2048)
     assert 0 < one < two <= 2 * one + 4096
     assert pcpp.pcpp_transformer_block_workspace_size(pcpp.make_geom(10, 128, 8, 3, 0.25, 10), w, 77, 2048) == 0
+
+
+def test_boundary_bytes_follow_eq1_rows():
+    from paper_2412_02962_amd import pcpp
+    for (H, W, n, i, p, heads, B, dt, esize) in [(128, 128, 8, 3, 0.25, 10, 1, pcpp.PCPP_DTYPE_BF16, 2),
+                                                 (128, 128, 8, 0, 0.25, 10, 2, pcpp.PCPP_DTYPE_BF16, 2),
+                                                 (32, 48, 2, 1, 0.3, 3, 1, pcpp.PCPP_DTYPE_F32, 4),
+                                                 (64, 64, 4, 2, 0.0, 1, 1, pcpp.PCPP_DTYPE_BF16, 2)]:
+        g = pcpp.make_geom(H, W, n, i, p, heads, 64, B, 0, dt)
+        h, up, dn, _ = oracle.context_rows(H, n, i, p)
+        r = max(up, dn)
+        assert pcpp.pcpp_boundary_bytes(g) == B * 2 * r * W * heads * 64 * esize
+    assert pcpp.pcpp_boundary_bytes(pcpp.make_geom(10, 8, 4, 0, 0.5, 2)) == 0        # H % n != 0
+    assert pcpp.pcpp_boundary_bytes(pcpp.make_geom(16, 8, 1, 0, 0.5, 2)) == 0        # one band: no neighbour
+
+
+def test_boundary_validation_errors_before_launch():
+    from paper_2412_02962_amd import pcpp
+    lib = pcpp.lib()
+    g = pcpp.make_geom(16, 16, 4, 1, 0.25, 2)   # interior band, r = 1
+    pack = lambda *a: lib.pcpp_pack_boundary(ctypes.byref(g), *a, None)
+    unpack = lambda *a: lib.pcpp_unpack_boundary(ctypes.byref(g), *a, None)
+    A, Bp = FAKE, FAKE + (1 << 30)
+    assert pack(None, Bp, A + (1 << 31), A + (1 << 32)) == pcpp.PCPP_EINVAL      # keys missing
+    assert pack(A, Bp, None, A + (1 << 32)) == pcpp.PCPP_EINVAL                  # message for band i-1 missing
+    assert pack(A, Bp, A + 64, A + (1 << 32)) == pcpp.PCPP_EINVAL                # message overlaps the keys
+    assert pack(A, Bp, A + (1 << 31), A + (1 << 31) + 64) == pcpp.PCPP_EINVAL    # messages overlap
+    assert unpack(A, None, Bp, Bp + (1 << 26), Bp + (2 << 26), Bp + (3 << 26)) == pcpp.PCPP_EINVAL
+    assert unpack(A, A + (1 << 26), Bp, Bp + 64, Bp + (2 << 26), Bp + (3 << 26)) == pcpp.PCPP_EINVAL
+    # nothing to send or receive: a valid no-op without pointers
+    none = pcpp.make_geom(16, 16, 4, 1, 0.0, 2)
+    assert lib.pcpp_pack_boundary(ctypes.byref(none), None, None, None, None, None) == pcpp.PCPP_OK
+    assert lib.pcpp_unpack_boundary(ctypes.byref(none), None, None, None, None, None, None, None) == pcpp.PCPP_OK
+    bad = pcpp.make_geom(16, 16, 4, 4, 0.25, 2)
+    assert lib.pcpp_pack_boundary(ctypes.byref(bad), A, Bp, FAKE, FAKE, None) == pcpp.PCPP_EINVAL
