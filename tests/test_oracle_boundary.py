@@ -92,3 +92,70 @@ def test_placing_keeps_the_other_rows():
     assert np.array_equal(vd[:, 2 * W:], bufs[3][:, 2 * W:]) and np.array_equal(vd[:, :2 * W], dn_msg[:, 1])
     for a, b in zip(bufs, (ku, vu, kd, vd)):
         assert a is not b
+
+
+# ---------------------------------------------------------------------------
+# Planted mistakes: each must fail the checks above (CPU, monkeypatched)
+# ---------------------------------------------------------------------------
+
+def _battery():
+    try:
+        for n, h, W in ((3, 4, 2), (4, 3, 3), (2, 5, 1)):
+            test_messages_carry_the_rows_the_neighbours_read(n, h, W)
+        test_placed_messages_reproduce_the_whole_band_context(dict(H=16, W=4, n=4, p=0.5))
+        test_placed_messages_reproduce_the_whole_band_context(dict(H=20, W=3, n=2, p=0.3))
+    except AssertionError:
+        return False
+    return True
+
+
+def test_unmodified_oracle_passes_the_boundary_battery():
+    assert _battery()
+
+
+def _msgs_shifted(H, W, n, i, p, k, v):        # rows one further into the band
+    h = H // n
+    up, dn = _ORIG_MSGS(H, W, n, i, p, k, v)
+    r = None if up is None else up.shape[2] // W
+    if up is not None and r < h:
+        up = np.stack([k[:, W:(r + 1) * W], v[:, W:(r + 1) * W]], axis=1)
+    return up, dn
+
+
+def _msgs_swapped(H, W, n, i, p, k, v):        # directions exchanged
+    up, dn = _ORIG_MSGS(H, W, n, i, p, k, v)
+    if up is not None and dn is not None:
+        return dn, up
+    return up, dn
+
+
+def _msgs_keys_twice(H, W, n, i, p, k, v):     # keys sent in place of values
+    up, dn = _ORIG_MSGS(H, W, n, i, p, k, v)
+    fix = lambda m: None if m is None else np.stack([m[:, 0], m[:, 0]], axis=1)
+    return fix(up), fix(dn)
+
+
+def _place_at_band_start(H, W, n, i, p, fu, fd, ku, vu, kd, vd):   # stale-above rows at the wrong end
+    h, up, dn, _ = oracle.context_rows(H, n, i, p)
+    ku, vu, kd, vd = (None if a is None else np.array(a, copy=True) for a in (ku, vu, kd, vd))
+    if up > 0:
+        ku[:, :up * W] = fu[:, 0]
+        vu[:, :up * W] = fu[:, 1]
+    if dn > 0:
+        kd[:, :dn * W] = fd[:, 0]
+        vd[:, :dn * W] = fd[:, 1]
+    return ku, vu, kd, vd
+
+
+_ORIG_MSGS = oracle.boundary_messages
+
+
+@pytest.mark.parametrize("name,mutant", [
+    ("boundary_messages", _msgs_shifted),
+    ("boundary_messages", _msgs_swapped),
+    ("boundary_messages", _msgs_keys_twice),
+    ("place_boundary_messages", _place_at_band_start),
+])
+def test_planted_boundary_mistakes_are_caught(monkeypatch, name, mutant):
+    monkeypatch.setattr(oracle, name, mutant)
+    assert not _battery()
