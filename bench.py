@@ -217,6 +217,33 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
         out[f"l2_{name}_TFLOPs"] = round(attn_flops(c2, nkv2) / us / 1e6, 1)
     out["derived_unet_selfattn_ms_per_band_step"] = round((10 * out_l1_us + 60 * l2["interior"]) / 1e3, 4)
 
+    # The paper's own band splits (two bands at p = 0.3, four at p = 0.8) on
+    # both SDXL self-attention grids at 1024, 2048 and 3840 px; repetitions
+    # scaled to about 20 ms of GPU time per shape.  Derived per split and
+    # resolution: 10 level-1 + 60 level-2 layers of one band.
+    geo = {}
+    for name, c in synth.PAPER_GEOMETRIES.items():
+        dg = {k: to_dev(v) for k, v in synth.attention_inputs(c).items()}
+        gg = pcpp.make_geom(c.H, c.W, c.n, c.i, c.p, c.heads, c.d, 1, 0, pcpp.PCPP_DTYPE_BF16)
+        _, _, _, nkvg = pcpp.pcpp_context_rows(gg)
+        og = torch.empty_like(dg["q"])
+        wg = pcpp.pcpp_partial_attention_workspace_size(gg)
+        wsg = torch.zeros(max(wg, 1), dtype=torch.uint8, device=dev)
+        fl = attn_flops(c, nkvg)
+        k_reps = int(max(5, min(reps, 2e10 / fl)))
+        us = graph_time_us(torch, lambda: pcpp.pcpp_partial_attention(gg, dg["q"], dg["k_fresh"], dg["v_fresh"],
+                                                                      dg["k_up"], dg["v_up"], dg["k_dn"],
+                                                                      dg["v_dn"], og, wsg, wg), k_reps, use_graph)
+        geo[name] = {"us": round(us, 3), "keys": nkvg, "queries": c.n_q, "TFLOPs": round(fl / us / 1e6, 1)}
+        del dg, og, wsg
+    out["paper_geometries"] = geo
+    der = {}
+    for res in (1024, 2048, 3840):
+        for n, pp in ((2, 0.3), (4, 0.8)):
+            l1, l2 = geo[f"paper_{res}_l1_n{n}_p{pp}"]["us"], geo[f"paper_{res}_l2_n{n}_p{pp}"]["us"]
+            der[f"{res}px_n{n}_p{pp}"] = round((10 * l1 + 60 * l2) / 1e3, 4)
+    out["derived_unet_selfattn_ms_per_band_step_paper"] = der
+
     bc = synth.BLOCK_CONFIG
     bcfg = bc.attn
     bi = {k: to_dev(v) for k, v in synth.block_inputs(bc).items()}

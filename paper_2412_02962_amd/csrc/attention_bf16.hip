@@ -8,9 +8,12 @@
 // straddles two sources (or the end) picks the source row by row.
 //
 // Work decomposition.  A block is 256 queries of one (image, head); its key
-// tiles are cut into k equal pieces (k = compute units / blocks, so that
-// every compute unit holds one workgroup) and a workgroup computes one piece
-// of one block.  The blocks are dealt out to the XCDs in contiguous ranges
+// tiles are cut into k equal pieces and a workgroup computes one piece of one
+// block.  One workgroup fits a compute unit, so a launch runs in waves of as
+// many workgroups as there are compute units; k is chosen by a cost estimate
+// (waves x (tiles per piece + a fixed cost per piece)): at the 2048 px
+// level-1 shape k = 3 fills one wave, larger shapes take several waves of
+// smaller pieces instead of a ragged last wave of whole blocks.  The blocks are dealt out to the XCDs in contiguous ranges
 // and all pieces of a block run on one XCD: workgroup w runs on XCD w % n_xcd
 // (the hardware deals workgroups out round-robin), so the pieces of a block
 // are merged through that XCD's L2 with ordinary stores and one counter per
@@ -106,8 +109,7 @@ struct Sched {
     int32_t n_tiles;    // key tiles per block
     int32_t nqb;        // blocks per (image, head)
     int32_t n_blocks;   // blocks in total
-    int* xcc_of;        // [grid]: XCC id + 1 each workgroup ran on (diagnostic)
-    int* counters;      // [n_blocks]: zero at launch, left zero
+    int* counters;      // [n_blocks]: zero at launch, left zero (split launches only)
     float* part_o;      // [grid][QB * D] partial outputs of pieces
     float* part_ml;     // [grid][QB][2] their row statistics
 };
@@ -179,7 +181,6 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
     const int piece = j - bl * sc.k;
     const int blk = x * sc.bpx + bl;
     if (bl >= sc.bpx || blk >= sc.n_blocks) return;  // idle slot of the last XCD (uniform)
-    if (tid == 0) sc.xcc_of[blockIdx.x] = (__builtin_amdgcn_s_getreg(0xf814) & 15) + 1;  // HW_REG_XCC_ID
     const int t0 = (int)((int64_t)n_tiles * piece / sc.k);
     const int t1 = (int)((int64_t)n_tiles * (piece + 1) / sc.k);
 
@@ -550,7 +551,7 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
 
 struct Plan {
     int32_t n_xcd, bpx, k, grid, max_grid, n_tiles, nqb, n_blocks;
-    size_t off_xcc, off_counters, off_o, off_ml, ws_bytes;
+    size_t off_counters, off_o, off_ml, ws_bytes;
     bool fits;
 };
 
@@ -564,10 +565,33 @@ int device_cus() {
     return cus;
 }
 
-// Two workgroups per compute unit.  The workspace layout depends only on the
-// compute unit count: [XCC record: max_grid ints][counters: max_grid ints]
-// [partial outputs: max_grid pieces][partial row statistics: same].  Pieces
-// are only used when k > 1, which keeps the grid within max_grid.
+// Pieces per block.  A launch runs in waves of max_grid workgroups (one per
+// compute unit); with k pieces per block it takes ceil(blocks * k / max_grid)
+// waves of ceil(tiles / k) tiles each, plus a fixed cost per piece (first
+// loads, partial store and merge) of about PIECE_COST_TILES tile periods.
+// The k with the smallest estimate wins (the smallest such k on ties).
+constexpr int64_t PIECE_COST_TILES = 4;
+constexpr int64_t MAX_SPLIT_BLOCKS = 65536;  // work counters kept at a fixed place
+
+int64_t pick_k(int64_t slots, int64_t max_grid, int64_t n_tiles) {
+    const int64_t k_max = n_tiles / MIN_TILES_PER_PIECE;
+    int64_t best_k = 1, best = -1;
+    for (int64_t k = 1; k <= k_max && k <= 64; ++k) {
+        const int64_t waves = (slots * k + max_grid - 1) / max_grid;
+        const int64_t cost = waves * ((n_tiles + k - 1) / k + PIECE_COST_TILES);
+        if (best < 0 || cost < best) {
+            best = cost;
+            best_k = k;
+        }
+    }
+    return best_k;
+}
+
+// Workspace layout, independent of the geometry where it matters: [work
+// counters: MAX_SPLIT_BLOCKS ints, always at offset 0, left zero by every
+// call][partial outputs: one per workgroup][partial row statistics: same].
+// The partial regions grow with the grid of a split launch; their contents
+// need no clearing.
 Plan make_plan(const AttnParams& p) {
     Plan pl;
     const int cus = device_cus();
@@ -581,24 +605,21 @@ Plan make_plan(const AttnParams& p) {
     const bool xcd_known = cus % CUS_PER_XCD == 0;
     pl.n_xcd = xcd_known ? cus / CUS_PER_XCD : 1;
     const int64_t bpx = (n_blocks + pl.n_xcd - 1) / pl.n_xcd;
-    int64_t k = xcd_known ? pl.max_grid / (pl.n_xcd * bpx) : 1;
-    const int64_t k_tiles = pl.n_tiles / MIN_TILES_PER_PIECE;
-    if (k > k_tiles) k = k_tiles;
-    if (k < 1) k = 1;
+    int64_t k = 1;
+    if (xcd_known && n_blocks <= MAX_SPLIT_BLOCKS) k = pick_k(pl.n_xcd * bpx, pl.max_grid, pl.n_tiles);
     pl.k = (int32_t)k;
     pl.bpx = (int32_t)(bpx < INT32_MAX ? bpx : INT32_MAX);
     const int64_t grid = (int64_t)pl.n_xcd * bpx * k;
     pl.grid = (int32_t)(grid < INT32_MAX ? grid : INT32_MAX);
     pl.fits = grid < INT32_MAX && n_blocks < INT32_MAX / 2;
+    const size_t pieces = k > 1 ? (size_t)grid : 0;
     size_t off = 0;
-    pl.off_xcc = off;
-    off += align256((size_t)pl.max_grid * sizeof(int));
     pl.off_counters = off;
-    off += align256((size_t)pl.max_grid * sizeof(int));
+    off += align256((size_t)MAX_SPLIT_BLOCKS * sizeof(int));
     pl.off_o = off;
-    off += align256((size_t)pl.max_grid * QB * D * sizeof(float));
+    off += align256(pieces * QB * D * sizeof(float));
     pl.off_ml = off;
-    off += align256((size_t)pl.max_grid * QB * 2 * sizeof(float));
+    off += align256(pieces * QB * 2 * sizeof(float));
     pl.ws_bytes = off;
     return pl;
 }
@@ -618,7 +639,6 @@ hipError_t launch_attention_bf16(const AttnParams& p, void* ws, size_t ws_bytes,
     sc.n_tiles = pl.n_tiles;
     sc.nqb = pl.nqb;
     sc.n_blocks = pl.n_blocks;
-    sc.xcc_of = (int*)((char*)ws + pl.off_xcc);
     sc.counters = (int*)((char*)ws + pl.off_counters);
     sc.part_o = (float*)((char*)ws + pl.off_o);
     sc.part_ml = (float*)((char*)ws + pl.off_ml);

@@ -94,6 +94,18 @@ ATTN_CONFIGS: Dict[str, AttnConfig] = {
     ]
 }
 
+# The paper's own band splits (Sec. 5.1: two devices at p = 0.3, four at
+# p = 0.8) on SDXL's two self-attention grids (level 1: R/16 square, 640
+# channels; level 2: R/32 square, 1280 channels) at 1024, 2048 and 3840 px.
+# Two bands: band 0 (each band is an edge band); four bands: interior band 1.
+PAPER_GEOMETRIES: Dict[str, AttnConfig] = {}
+for _res in (1024, 2048, 3840):
+    for _lvl, _div, _heads in ((1, 16, 10), (2, 32, 20)):
+        for _n, _p, _i in ((2, 0.3, 0), (4, 0.8, 1)):
+            _name = f"paper_{_res}_l{_lvl}_n{_n}_p{_p}"
+            PAPER_GEOMETRIES[_name] = _cfg(_name, _res // _div, _res // _div, _n, _i, _p, _heads, 64, DTYPE_BF16,
+                                           60 + _res // 1024 * 4 + _lvl * 2 + _n // 2)
+
 BLOCK_CONFIG = BlockConfig(
     name="sdxl2048_block",
     attn=_cfg("sdxl2048_block_attn", 128, 128, 8, 3, 0.25, 10, 64, DTYPE_BF16, 5),

@@ -225,3 +225,52 @@ def test_gather_index_only_and_unaligned_width():
     assert np.array_equal(idx.cpu().numpy(), oracle.context_token_ids(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p))
     want = oracle.assemble_context(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, inp["v_fresh"], inp["v_up"], inp["v_dn"])
     assert np.array_equal(vc.cpu().view(torch.int16).numpy().view(np.uint16), want)
+
+
+@pytest.mark.parametrize("name", list(synth.PAPER_GEOMETRIES))
+def test_paper_geometries(name):
+    # the paper's band splits (n = 2 at p = 0.3, n = 4 at p = 0.8) on both SDXL
+    # self-attention grids at 1024, 2048 and 3840 px; fractional p*h throughout.
+    # Large shapes are checked on a sample of query rows.
+    cfg = synth.PAPER_GEOMETRIES[name]
+    _say("paper geometry", name)
+    inp = synth.attention_inputs(cfg)
+    got = gu.to_f64(gu.run_attention(cfg, inp))
+    f = {k: oracle.as_f64(v, cfg.dtype) for k, v in inp.items()}
+    if cfg.n_q <= 1024:
+        rows = np.arange(cfg.n_q)
+    else:
+        rows = np.sort(np.random.default_rng(6).choice(cfg.n_q, 128, replace=False))
+        rows[0], rows[-1] = 0, cfg.n_q - 1
+    want = oracle.partial_attention(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, f["q"][:, rows],
+                                    f["k_fresh"], f["v_fresh"], f["k_up"], f["v_up"], f["k_dn"], f["v_dn"])
+    gu.assert_close(cfg, got[:, rows], want, name)
+
+
+def test_workspace_reuse_with_multi_wave_launches():
+    # shapes whose pieces run in several waves of workgroups share one
+    # workspace with one-wave shapes; the counters must come back to zero
+    import torch
+    from paper_2412_02962_amd import pcpp
+    names = ["paper_2048_l1_n2_p0.3", "sdxl2048_l1_p25", "paper_2048_l1_n4_p0.8", "sdxl1024_l1",
+             "paper_2048_l2_n2_p0.3", "sdxl2048_l1_p25"]
+    allc = dict(synth.ATTN_CONFIGS)
+    allc.update(synth.PAPER_GEOMETRIES)
+    cfgs = [allc[n] for n in names]
+    need = max(pcpp.pcpp_partial_attention_workspace_size(gu.geom(c)) for c in cfgs)
+    ws = torch.zeros(need, dtype=torch.uint8, device=gu.DEV)
+    rows_rng = np.random.default_rng(8)
+    for n, cfg in zip(names, cfgs):
+        _say("reuse (waves)", n)
+        inp = synth.attention_inputs(cfg)
+        d = {k: gu.to_dev(v, cfg.dtype) for k, v in inp.items()}
+        out = torch.empty_like(d["q"])
+        pcpp.pcpp_partial_attention(gu.geom(cfg), d["q"], d["k_fresh"], d["v_fresh"], d["k_up"], d["v_up"],
+                                    d["k_dn"], d["v_dn"], out, ws, need)
+        torch.cuda.synchronize()
+        rows = np.sort(rows_rng.choice(cfg.n_q, min(cfg.n_q, 96), replace=False))
+        f = {k: oracle.as_f64(v, cfg.dtype) for k, v in inp.items()}
+        want = oracle.partial_attention(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, f["q"][:, rows],
+                                        f["k_fresh"], f["v_fresh"], f["k_up"], f["v_up"], f["k_dn"], f["v_dn"])
+        gu.assert_close(cfg, gu.to_f64(out)[:, rows], want, f"reuse {n}")
+    assert int(ws[:65536 * 4].view(torch.int32).abs().sum().item()) == 0   # counters left zero
