@@ -130,9 +130,10 @@ int pcpp_gather_context(const pcpp_geom_t* g,
  *
  * Workspace contract: the buffer must be zero-filled before its first use
  * (e.g. hipMemset once after allocation).  Every call leaves its counters
- * zero again and the layout does not depend on the geometry, so the same
- * buffer (of the largest size needed) serves any number of later calls of
- * any geometry on that device, graph replays included, without clearing.
+ * zero again, and the counters sit at the same offset for every geometry
+ * (the float32 partials after them need no clearing), so the same buffer (of
+ * the largest size needed) serves any number of later calls of any geometry
+ * on that device, graph replays included, without clearing.
  * Calls that share one workspace must be ordered on one stream.
  */
 size_t pcpp_partial_attention_workspace_size(const pcpp_geom_t* g);
