@@ -339,6 +339,32 @@ def pmc_summarize(fetch_dir, write_dir):
     print(text)
 
 
+def pmc_report(dirs):
+    """Per-dispatch averages of every counter rocprofv3 --pmc recorded for the
+    attention kernel in the given output folders (one folder per pass), with
+    the dispatch durations, for the counter summary under profiles/."""
+    import csv
+    import glob
+    lines = ["# Hardware counters of attn_bf16_kernel, 2048 px level-1 workload, per dispatch "
+             "(rocprofv3 --pmc; averages over the dispatches of each pass)"]
+    for d in dirs:
+        f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+        vals, durs = {}, {}
+        for r in csv.DictReader(open(f)):
+            if "attn_bf16_kernel" not in r["Kernel_Name"]:
+                continue
+            vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+            durs[r["Dispatch_Id"]] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        dd = sorted(durs.values())
+        lines.append(f"## pass {os.path.basename(os.path.normpath(d))}: {len(dd)} dispatches, "
+                     f"median duration {dd[len(dd) // 2]:.2f} us")
+        for k in sorted(vals):
+            v = vals[k]
+            lines.append(f"{k}: {sum(v) / len(v):.1f}")
+    lines.append(f"kernel_source_sha256_16: {kernel_source_hash()}")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -352,9 +378,14 @@ def main():
                     help="counter-collection workload: a calibration copy, then --steps attention calls")
     ap.add_argument("--pmc-summarize", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the traffic summary from two rocprofv3 --pmc output folders")
+    ap.add_argument("--pmc-report", nargs="+", metavar="DIR",
+                    help="print per-dispatch counter averages of the attention kernel from rocprofv3 --pmc folders")
     args = ap.parse_args()
     if args.pmc_summarize:
         pmc_summarize(*args.pmc_summarize)
+        return
+    if args.pmc_report:
+        pmc_report(args.pmc_report)
         return
     if args.pmc_run:
         pmc_run(args)
