@@ -161,6 +161,21 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
     out["gather_GBps"] = round(gbytes / us / 1e3, 1)
     out["gather_frac_hbm"] = round(gbytes / us / 1e3 / PEAK_HBM_GBS, 4)
 
+    # The same copy with the caches flushed before each call (a 512 MiB
+    # write between calls).
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+
+    def flushed_us(fn, n=20):
+        # graph of n x (flush, call) minus a graph of n x flush
+        t_both = graph_time_us(torch, lambda: (flush.fill_(1), fn()), n, use_graph)
+        t_flush = graph_time_us(torch, lambda: flush.fill_(1), n, use_graph)
+        return max(t_both - t_flush, 1e-3)
+
+    us = flushed_us(lambda: pcpp.pcpp_gather_context(g, d["k_fresh"], d["v_fresh"], d["k_up"], d["v_up"],
+                                                     d["k_dn"], d["v_dn"], idx, kc, vc))
+    out["gather_flushed_us"] = round(us, 3)
+    out["gather_flushed_GBps"] = round(gbytes / us / 1e3, 1)
+
     # p-aware boundary messages of the same band: both messages packed from
     # the fresh K/V (sender side) and both placed into the stale buffers
     # (receiver side); bytes = read + write of every message.
@@ -177,6 +192,10 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
     us = graph_time_us(torch, lambda: pcpp.pcpp_unpack_boundary(g, s_dn, s_up, ku, vu, kd, vd), reps, use_graph)
     out["unpack_us"] = round(us, 3)
     out["unpack_GBps"] = round(2 * 2 * nb / us / 1e3, 1)
+    us = flushed_us(lambda: pcpp.pcpp_pack_boundary(g, d["k_fresh"], d["v_fresh"], s_up, s_dn))
+    out["pack_flushed_us"] = round(us, 3)
+    out["pack_flushed_GBps"] = round(2 * 2 * nb / us / 1e3, 1)
+    del flush
 
     c50 = synth.ATTN_CONFIGS["sdxl2048_l1_p50"]
     d50 = {k: to_dev(v) for k, v in synth.attention_inputs(c50).items()}
@@ -339,6 +358,31 @@ def pmc_summarize(fetch_dir, write_dir):
     print(text)
 
 
+def block_run(args):
+    """Workload for a kernel-trace profile of the transformer block: --steps
+    calls of pcpp_transformer_block on the 2048 px level-1 band, nothing else."""
+    import numpy as np
+    import torch
+
+    from paper_2412_02962_amd import pcpp, synth
+    dev = "cuda:0"
+    to_dev = lambda x: None if x is None else torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(
+        torch.bfloat16).to(dev)
+    bc = synth.BLOCK_CONFIG
+    c = bc.attn
+    bi = {k: to_dev(v) for k, v in synth.block_inputs(bc).items()}
+    g = pcpp.make_geom(c.H, c.W, c.n, c.i, c.p, c.heads, c.d, 1, 0, pcpp.PCPP_DTYPE_BF16)
+    w = pcpp.make_block_weights(bi, bc.ff_inner, bc.gn_groups)
+    y, ko, vo = (torch.empty_like(bi["x"]) for _ in range(3))
+    wsb = pcpp.pcpp_transformer_block_workspace_size(g, w, bc.n_text, bc.text_dim)
+    ws = torch.zeros(wsb, dtype=torch.uint8, device=dev)
+    for _ in range(args.steps):
+        pcpp.pcpp_transformer_block(g, w, bi["x"], bi["text"], bc.n_text, bc.text_dim, bi["k_up"], bi["v_up"],
+                                    bi["k_dn"], bi["v_dn"], y, ko, vo, ws, wsb)
+    torch.cuda.synchronize()
+    print(f"block run: {args.steps} calls", flush=True)
+
+
 def pmc_report(dirs):
     """Per-dispatch averages of every counter rocprofv3 --pmc recorded for the
     attention kernel in the given output folders (one folder per pass), with
@@ -378,6 +422,8 @@ def main():
                     help="counter-collection workload: a calibration copy, then --steps attention calls")
     ap.add_argument("--pmc-summarize", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the traffic summary from two rocprofv3 --pmc output folders")
+    ap.add_argument("--block-run", action="store_true",
+                    help="profiling workload: --steps transformer-block calls, nothing else")
     ap.add_argument("--pmc-report", nargs="+", metavar="DIR",
                     help="print per-dispatch counter averages of the attention kernel from rocprofv3 --pmc folders")
     args = ap.parse_args()
@@ -386,6 +432,9 @@ def main():
         return
     if args.pmc_report:
         pmc_report(args.pmc_report)
+        return
+    if args.block_run:
+        block_run(args)
         return
     if args.pmc_run:
         pmc_run(args)
