@@ -235,6 +235,32 @@ int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w,
                            void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * pcpp_transformer_block with synchronized GroupNorm (Sec. 3.3 keeps the
+ * GroupNorm of DistriFusion, whose statistics cover the whole image and are
+ * exchanged among all devices).  Arguments as pcpp_transformer_block, plus:
+ *   gn_bands  [n_patches][B][gn_groups][3] float32: (count, mean, M2) of
+ *             every band's GroupNorm input (M2 = sum of squared deviations
+ *             from that band's mean), as all-gathered from the previous
+ *             step; entry patch_idx is not read (this band's own statistics
+ *             of this step take its place).  The bands are merged in band
+ *             order.  NULL: band-local statistics (pcpp_transformer_block).
+ *   gn_own    [B][gn_groups][3] float32 output: this band's own statistics
+ *             of this step, what the other bands read at the next one; may
+ *             be NULL.
+ * Both need 4-byte alignment (PCPP_EINVAL otherwise).
+ */
+int pcpp_transformer_block_sync_gn(const pcpp_geom_t* g,
+                                   const pcpp_block_weights_t* w,
+                                   const void* x, const void* text,
+                                   int32_t n_text, int32_t text_dim,
+                                   const void* k_up, const void* v_up,
+                                   const void* k_dn, const void* v_dn,
+                                   const float* gn_bands, float* gn_own,
+                                   void* y, void* k_fresh_out,
+                                   void* v_fresh_out, void* workspace,
+                                   size_t ws_bytes, void* stream);
+
+/*
  * p-aware boundary messages of the neighbour exchange (Sec. 3.2 with Eq. 1).
  * At the next step band i-1 reads the first r rows of band i's fresh keys
  * and values (its context below) and band i+1 reads the last r rows (its

@@ -15,6 +15,8 @@ from .pcpp_oracle import (  # noqa: F401
     gelu,
     geglu,
     group_norm,
+    group_norm_synchronized,
+    group_stats,
     layer_norm,
     linear,
     mha,

@@ -255,6 +255,49 @@ def group_norm(x: np.ndarray, groups: int, gamma: np.ndarray, beta: np.ndarray,
     return y * gamma + beta
 
 
+def group_stats(x: np.ndarray, groups: int) -> np.ndarray:
+    """Per image and group of a patch's tokens x [B, N, C]: (count, mean,
+    M2) with M2 the sum of squared deviations from the mean; [B, groups, 3]."""
+    B, N, C = x.shape
+    cg = C // groups
+    st = np.empty((B, groups, 3))
+    for b in range(B):
+        for g in range(groups):
+            blk = x[b, :, g * cg:(g + 1) * cg]
+            mean = blk.mean()
+            st[b, g] = (blk.size, mean, ((blk - mean) ** 2).sum())
+    return st
+
+
+def group_norm_synchronized(x: np.ndarray, groups: int, gamma: np.ndarray, beta: np.ndarray,
+                            band_stats: np.ndarray, i: int, eps: float = 1e-6) -> np.ndarray:
+    """GroupNorm of patch i with statistics over the whole image.
+
+    Sec. 3.3 keeps DistriFusion's synchronized GroupNorm: the statistics
+    come from every patch, exchanged among all devices.  band_stats
+    [n, B, groups, 3] holds each patch's (count, mean, M2) (the other
+    patches' from the previous step, as exchanged); entry i is replaced by
+    this patch's own statistics of x.  The whole-image mean is the
+    count-weighted mean of the patch means, and the whole-image M2 is the sum
+    of the patch M2 plus count * (patch mean - whole mean)^2 (law of total
+    variance); variance = M2 / count (biased).
+    """
+    st = np.array(band_stats, dtype=np.float64, copy=True)
+    st[i] = group_stats(x, groups)
+    n_all = st[..., 0].sum(axis=0)                          # [B, G]
+    mean = (st[..., 0] * st[..., 1]).sum(axis=0) / n_all
+    m2 = (st[..., 2] + st[..., 0] * (st[..., 1] - mean[None]) ** 2).sum(axis=0)
+    var = m2 / n_all
+    B, N, C = x.shape
+    cg = C // groups
+    y = np.empty_like(x)
+    for b in range(B):
+        for g in range(groups):
+            blk = x[b, :, g * cg:(g + 1) * cg]
+            y[b, :, g * cg:(g + 1) * cg] = (blk - mean[b, g]) / math.sqrt(var[b, g] + eps)
+    return y * gamma + beta
+
+
 def layer_norm(x: np.ndarray, gamma: np.ndarray, beta: np.ndarray,
                eps: float = 1e-5) -> np.ndarray:
     """LayerNorm over the channel axis (last), biased variance."""
@@ -285,7 +328,7 @@ def transformer_block(H: int, W: int, n: int, i: int, p: float, heads: int,
                       wts: Dict[str, np.ndarray], x: np.ndarray, text: np.ndarray,
                       k_up: Optional[np.ndarray], v_up: Optional[np.ndarray],
                       k_dn: Optional[np.ndarray], v_dn: Optional[np.ndarray],
-                      gn_groups: int = 32):
+                      gn_groups: int = 32, gn_band_stats: Optional[np.ndarray] = None):
     """One SDXL-shaped transformer block on patch i, float64.
 
     x [B, h*W, C] (the patch's tokens), text [B, n_text, text_dim].
@@ -296,9 +339,14 @@ def transformer_block(H: int, W: int, n: int, i: int, p: float, heads: int,
     GEGLU feed-forward + residual -> proj_out + the block input.
     Returns (y, k_fresh, v_fresh): the output and the patch's own K and V,
     which the neighbours read as stale context at the next step (Sec. 3.2).
+    With gn_band_stats [n, B, groups, 3] the GroupNorm is the synchronized
+    one (group_norm_synchronized) instead of the patch-local one.
     """
     C = x.shape[-1]
-    t = group_norm(x, gn_groups, wts["gn_gamma"], wts["gn_beta"])
+    if gn_band_stats is None:
+        t = group_norm(x, gn_groups, wts["gn_gamma"], wts["gn_beta"])
+    else:
+        t = group_norm_synchronized(x, gn_groups, wts["gn_gamma"], wts["gn_beta"], gn_band_stats, i)
     hid = linear(t, wts["proj_in_w"], wts["proj_in_b"])
 
     n1 = layer_norm(hid, wts["ln1_gamma"], wts["ln1_beta"])

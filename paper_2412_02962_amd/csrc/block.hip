@@ -142,11 +142,12 @@ PCPP_EXPORT size_t pcpp_transformer_block_workspace_size(const pcpp_geom_t* g, c
     return layout(g, r, w, n_text).total;
 }
 
-PCPP_EXPORT int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, const void* x,
-                                       const void* text, int32_t n_text, int32_t text_dim, const void* k_up,
-                                       const void* v_up, const void* k_dn, const void* v_dn, void* y,
-                                       void* k_fresh_out, void* v_fresh_out, void* workspace, size_t ws_bytes,
-                                       void* stream) {
+namespace {
+
+int run_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, const void* x, const void* text,
+              int32_t n_text, int32_t text_dim, const void* k_up, const void* v_up, const void* k_dn,
+              const void* v_dn, const float* gn_bands, float* gn_own, void* y, void* k_fresh_out,
+              void* v_fresh_out, void* workspace, size_t ws_bytes, void* stream) {
     Geo r;
     int st = validate_block(g, w, n_text, text_dim, &r);
     if (st != PCPP_OK) return st;
@@ -199,6 +200,10 @@ PCPP_EXPORT int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_we
     gp.C = C;
     gp.G = w->gn_groups;
     gp.eps = 1e-6f;
+    gp.bands = gn_bands;
+    gp.n_bands = g->n_patches;
+    gp.band = g->patch_idx;
+    gp.own_out = gn_own;
     PCPP_CHECK(launch_group_norm(gp, s));
     PCPP_CHECK(launch_gemm(gemm(t16, C, false, w->proj_in_w, w->proj_in_b, rows, C, C, hid, C, true), s));
 
@@ -288,4 +293,27 @@ PCPP_EXPORT int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_we
     }
 #undef PCPP_CHECK
     return PCPP_OK;
+}
+
+}  // namespace
+
+PCPP_EXPORT int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, const void* x,
+                                       const void* text, int32_t n_text, int32_t text_dim, const void* k_up,
+                                       const void* v_up, const void* k_dn, const void* v_dn, void* y,
+                                       void* k_fresh_out, void* v_fresh_out, void* workspace, size_t ws_bytes,
+                                       void* stream) {
+    return run_block(g, w, x, text, n_text, text_dim, k_up, v_up, k_dn, v_dn, nullptr, nullptr, y, k_fresh_out,
+                     v_fresh_out, workspace, ws_bytes, stream);
+}
+
+PCPP_EXPORT int pcpp_transformer_block_sync_gn(const pcpp_geom_t* g, const pcpp_block_weights_t* w, const void* x,
+                                               const void* text, int32_t n_text, int32_t text_dim,
+                                               const void* k_up, const void* v_up, const void* k_dn,
+                                               const void* v_dn, const float* gn_bands, float* gn_own, void* y,
+                                               void* k_fresh_out, void* v_fresh_out, void* workspace,
+                                               size_t ws_bytes, void* stream) {
+    if (gn_bands != nullptr && ((uintptr_t)gn_bands & 3u) != 0) return PCPP_EINVAL;
+    if (gn_own != nullptr && ((uintptr_t)gn_own & 3u) != 0) return PCPP_EINVAL;
+    return run_block(g, w, x, text, n_text, text_dim, k_up, v_up, k_dn, v_dn, gn_bands, gn_own, y, k_fresh_out,
+                     v_fresh_out, workspace, ws_bytes, stream);
 }

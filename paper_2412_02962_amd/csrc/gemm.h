@@ -40,6 +40,11 @@ struct GroupNormParams {
     float* stats;         // workspace of group_norm_ws_bytes(B, G, N)
     int32_t B, N, C, G, chunks;  // chunks: set by launch_group_norm
     float eps;
+    // Synchronized statistics: [n_bands][B][G] x (count, mean, M2) of every
+    // band, entry `band` replaced by this band's own; null = this band's only.
+    const float* bands;
+    int32_t n_bands, band;
+    float* own_out;       // [B][G] x (count, mean, M2) of this band, or null
 };
 size_t group_norm_ws_bytes(int B, int G, int N);
 // C % 8 == 0, C <= 2048, 1 <= G <= 256 divides C.

@@ -7,7 +7,9 @@
 // then squared deviations from the chunk mean).  gn_finalize (one workgroup
 // per image) merges the chunk statistics of every group with Chan et al.'s
 // pairwise update in a fixed order and stores mean and 1/sqrt(var + eps)
-// (biased variance).  gn_apply: per-channel scale and shift in LDS, 16-byte
+// (biased variance).  Synchronized GroupNorm (the whole image's statistics,
+// Sec. 3.3 of arXiv 2412.02962) merges every band's (count, mean, M2) in
+// band order, this band's own in its place, before that.  gn_apply: per-channel scale and shift in LDS, 16-byte
 // vectors.
 // LayerNorm: one wavefront per fp32 row, 16-byte loads, two passes over
 // registers, 8-byte bf16 stores.
@@ -173,6 +175,28 @@ __global__ __launch_bounds__(GN_THREADS) void gn_finalize(GroupNormParams p) {
         if (tid < ng) {
             for (int k = 1; k < S; ++k)
                 chan_merge(n, mean, m2, mrg[tid + k * ng][0], mrg[tid + k * ng][1], mrg[tid + k * ng][2]);
+            if (p.own_out != nullptr) {
+                float* o = p.own_out + ((int64_t)b * p.G + g) * 3;
+                o[0] = n;
+                o[1] = mean;
+                o[2] = m2;
+            }
+            if (p.bands != nullptr) {
+                // whole-image statistics: every band's, in band order, this
+                // band's own in its place
+                float tn = 0.f, tm = 0.f, tq = 0.f;
+                for (int j = 0; j < p.n_bands; ++j) {
+                    if (j == p.band) {
+                        chan_merge(tn, tm, tq, n, mean, m2);
+                    } else {
+                        const float* o = p.bands + (((int64_t)j * p.B + b) * p.G + g) * 3;
+                        chan_merge(tn, tm, tq, o[0], o[1], o[2]);
+                    }
+                }
+                n = tn;
+                mean = tm;
+                m2 = tq;
+            }
             fin[((int64_t)b * p.G + g) * 2] = mean;
             fin[((int64_t)b * p.G + g) * 2 + 1] = n > 0.f ? rsqrtf(m2 / n + p.eps) : 0.f;
         }

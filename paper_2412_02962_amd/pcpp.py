@@ -72,6 +72,8 @@ def _load():
         "pcpp_transformer_block_workspace_size": (sz, [gp, wp, i32, i32]),
         "pcpp_transformer_block": (ctypes.c_int, [gp, wp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp,
                                                   vp, sz, vp]),
+        "pcpp_transformer_block_sync_gn": (ctypes.c_int, [gp, wp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp,
+                                                          vp, vp, vp, vp, sz, vp]),
         "pcpp_boundary_bytes": (sz, [gp]),
         "pcpp_pack_boundary": (ctypes.c_int, [gp, vp, vp, vp, vp, vp]),
         "pcpp_unpack_boundary": (ctypes.c_int, [gp, vp, vp, vp, vp, vp, vp, vp]),
@@ -88,7 +90,7 @@ EXPORTED = (
     "pcpp_version", "pcpp_strerror", "pcpp_context_rows", "pcpp_gather_context",
     "pcpp_partial_attention_workspace_size", "pcpp_partial_attention",
     "pcpp_transformer_block_workspace_size", "pcpp_transformer_block",
-    "pcpp_boundary_bytes", "pcpp_pack_boundary", "pcpp_unpack_boundary",
+    "pcpp_boundary_bytes", "pcpp_pack_boundary", "pcpp_unpack_boundary", "pcpp_transformer_block_sync_gn",
 )
 
 
@@ -190,3 +192,11 @@ def pcpp_unpack_boundary(g, recv_up, recv_dn, k_up, v_up, k_dn, v_dn, stream=Non
     _check("pcpp_unpack_boundary", _lib.pcpp_unpack_boundary(
         ctypes.byref(g), _ptr(recv_up), _ptr(recv_dn), _ptr(k_up), _ptr(v_up), _ptr(k_dn), _ptr(v_dn),
         _stream(stream)))
+
+
+def pcpp_transformer_block_sync_gn(g, w, x, text, n_text, text_dim, k_up, v_up, k_dn, v_dn, gn_bands, gn_own, y,
+                                   k_fresh_out, v_fresh_out, workspace, ws_bytes, stream=None):
+    _check("pcpp_transformer_block_sync_gn", _lib.pcpp_transformer_block_sync_gn(
+        ctypes.byref(g), ctypes.byref(w), _ptr(x), _ptr(text), n_text, text_dim, _ptr(k_up), _ptr(v_up),
+        _ptr(k_dn), _ptr(v_dn), _ptr(gn_bands), _ptr(gn_own), _ptr(y), _ptr(k_fresh_out), _ptr(v_fresh_out),
+        _ptr(workspace), ws_bytes, _stream(stream)))

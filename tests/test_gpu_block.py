@@ -114,3 +114,58 @@ def test_block_without_kv_export_gives_same_output():
     y1, _, _ = _run_block(bc, inp, 1, want_kv=True)
     y2, _, _ = _run_block(bc, inp, 1, want_kv=False)
     assert torch.equal(y1, y2)
+
+
+def _other_band_stats(cfg, G, B, seed):
+    """(count, mean, M2) of synthetic GroupNorm inputs of every other band
+    (each band with its own offset and scale), float32-rounded as passed to
+    the library; entry cfg.i is NaN: it must not be read."""
+    rng = np.random.default_rng(seed)
+    st = np.full((cfg.n, B, G, 3), np.nan)
+    for j in range(cfg.n):
+        if j != cfg.i:
+            xj = 0.3 * j + (1.0 + 0.1 * j) * rng.standard_normal((B, cfg.n_q, cfg.C))
+            st[j] = oracle.group_stats(xj, G)
+    return st.astype(np.float32)
+
+
+@pytest.mark.parametrize("which", ["2048", "small_b2"])
+def test_block_synchronized_group_norm(which):
+    import torch
+    from paper_2412_02962_amd import pcpp
+    if which == "2048":
+        bc, B = synth.BLOCK_CONFIG, 1
+    else:
+        attn = synth.AttnConfig(name="blk", H=16, W=16, n=4, i=2, p=0.5, heads=2, d=64, dtype="bf16", seed_id=54)
+        bc, B = synth.BlockConfig(name="blk", attn=attn, n_text=5, text_dim=64, ff_inner=128, gn_groups=8,
+                                  seed_id=55), 2
+    cfg = bc.attn
+    _say("block synchronized GroupNorm", which)
+    inp = synth.block_inputs(bc, batch=B)
+    st = _other_band_stats(cfg, bc.gn_groups, B, 12)
+    d = {k: gu.to_dev(v, "bf16") for k, v in inp.items()}
+    g = pcpp.make_geom(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, cfg.d, B, 0, pcpp.PCPP_DTYPE_BF16)
+    w = pcpp.make_block_weights(d, bc.ff_inner, bc.gn_groups)
+    y, k_out, v_out = (torch.empty_like(d["x"]) for _ in range(3))
+    own = torch.empty((B, bc.gn_groups, 3), dtype=torch.float32, device=gu.DEV)
+    bands = torch.from_numpy(st).to(gu.DEV)
+    wsb = pcpp.pcpp_transformer_block_workspace_size(g, w, bc.n_text, bc.text_dim)
+    ws = torch.zeros(wsb, dtype=torch.uint8, device=gu.DEV)
+    pcpp.pcpp_transformer_block_sync_gn(g, w, d["x"], d["text"], bc.n_text, bc.text_dim, d["k_up"], d["v_up"],
+                                        d["k_dn"], d["v_dn"], bands, own, y, k_out, v_out, ws, wsb)
+    torch.cuda.synchronize()
+    f = {k: (None if v is None else oracle.from_bf16_bits(v)) for k, v in inp.items()}
+    wts = {k: f[k] for k in synth.block_weight_shapes(bc)}
+    want_y, want_k, want_v = oracle.transformer_block(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, wts, f["x"],
+                                                      f["text"], f["k_up"], f["v_up"], f["k_dn"], f["v_dn"],
+                                                      gn_groups=bc.gn_groups, gn_band_stats=st.astype(np.float64))
+    _check(gu.to_f64(y), want_y, tag="sync-GN block")
+    _check_kv(gu.to_f64(k_out), want_k, "sync-GN k export")
+    want_own = oracle.group_stats(f["x"], bc.gn_groups)
+    got_own = own.cpu().numpy().astype(np.float64)
+    assert np.array_equal(got_own[..., 0], want_own[..., 0])
+    assert np.allclose(got_own[..., 1], want_own[..., 1], rtol=0, atol=1e-5)
+    assert np.allclose(got_own[..., 2], want_own[..., 2], rtol=1e-4, atol=0)
+    # the band-local block differs (the statistics are not this band's alone)
+    y_local, _, _ = _run_block(bc, inp, B)
+    assert not torch.equal(y_local, y)

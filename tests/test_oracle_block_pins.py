@@ -146,3 +146,35 @@ def test_whole_block_matches_torch_composition(i):
     np.testing.assert_allclose(y, yt, rtol=0, atol=1e-11)
     np.testing.assert_allclose(k, kt, rtol=0, atol=1e-12)
     np.testing.assert_allclose(v, vt, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("n,i,B", [(4, 1, 1), (8, 7, 2), (2, 0, 1), (1, 0, 1)])
+def test_synchronized_group_norm_is_whole_image_group_norm(n, i, B):
+    # with every band's fresh statistics, the synchronized GroupNorm of band i
+    # is torch's GroupNorm over the whole image restricted to band i's rows
+    import torch
+    import torch.nn.functional as F
+    rng = np.random.default_rng(20 + n)
+    h, W, C, G = 3, 5, 32, 8
+    x = rng.standard_normal((B, n * h * W, C)) * 2.0 + 0.5
+    gm, bt = 1 + 0.1 * rng.standard_normal(C), 0.1 * rng.standard_normal(C)
+    bands = [x[:, j * h * W:(j + 1) * h * W] for j in range(n)]
+    st = np.stack([oracle.group_stats(bj, G) for bj in bands])
+    st_other = st.copy()
+    st_other[i] = np.nan   # entry i is never read
+    got = oracle.group_norm_synchronized(bands[i], G, gm, bt, st_other, i)
+    full = F.group_norm(torch.from_numpy(x).permute(0, 2, 1), G, torch.from_numpy(gm), torch.from_numpy(bt),
+                        eps=1e-6).permute(0, 2, 1).numpy()
+    assert np.allclose(got, full[:, i * h * W:(i + 1) * h * W], rtol=0, atol=1e-12)
+
+
+def test_group_stats_against_numpy():
+    rng = np.random.default_rng(31)
+    x = rng.standard_normal((2, 7, 12))
+    st = oracle.group_stats(x, 3)
+    for b in range(2):
+        for g in range(3):
+            blk = x[b, :, 4 * g:4 * g + 4].ravel()
+            assert st[b, g, 0] == blk.size
+            assert math.isclose(st[b, g, 1], float(np.mean(blk)), rel_tol=0, abs_tol=1e-14)
+            assert math.isclose(st[b, g, 2], float(np.var(blk)) * blk.size, rel_tol=1e-12)
