@@ -236,6 +236,32 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
         out[f"l2_{name}_TFLOPs"] = round(attn_flops(c2, nkv2) / us / 1e6, 1)
     out["derived_unet_selfattn_ms_per_band_step"] = round((10 * out_l1_us + 60 * l2["interior"]) / 1e3, 4)
 
+    # Multi-hop context (p > 1): 8 bands at 2048 px level 1, p = 1.5 (24 rows
+    # on each side, from two bands), the stale rows given compactly.
+    import dataclasses
+    cm = dataclasses.replace(synth.ATTN_CONFIGS[WORKLOAD], p=1.5)
+    h_, upm, dnm = cm.h, 24, 24
+    qm = to_dev(synth.store(synth.patch_tensor(cm, cm.i, "q", False), "bf16"))
+    mh = {}
+    for kind in ("k", "v"):
+        grid = np.concatenate([synth.patch_tensor(cm, j, kind, stale=(j != cm.i)) for j in range(cm.n)], axis=1)
+        W_ = cm.W
+        mh[kind + "_fresh"] = to_dev(synth.store(grid[:, cm.i * h_ * W_:(cm.i + 1) * h_ * W_], "bf16"))
+        mh[kind + "_above"] = to_dev(synth.store(grid[:, (cm.i * h_ - upm) * W_:cm.i * h_ * W_], "bf16"))
+        mh[kind + "_below"] = to_dev(synth.store(grid[:, (cm.i + 1) * h_ * W_:((cm.i + 1) * h_ + dnm) * W_], "bf16"))
+        del grid
+    gm = pcpp.make_geom(cm.H, cm.W, cm.n, cm.i, cm.p, cm.heads, cm.d, 1, 0, pcpp.PCPP_DTYPE_BF16)
+    om = torch.empty_like(qm)
+    wm = pcpp.pcpp_partial_attention_multihop_workspace_size(gm)
+    wsm = torch.zeros(max(wm, 1), dtype=torch.uint8, device=dev)
+    us = graph_time_us(torch, lambda: pcpp.pcpp_partial_attention_multihop(
+        gm, qm, mh["k_fresh"], mh["v_fresh"], mh["k_above"], mh["v_above"], mh["k_below"], mh["v_below"], om, wsm,
+        wm), reps, use_graph)
+    nkm = (upm + h_ + dnm) * cm.W
+    out["multihop_p1.5_us"] = round(us, 3)
+    out["multihop_p1.5_keys"] = nkm
+    out["multihop_p1.5_TFLOPs"] = round(attn_flops(cm, nkm) / us / 1e6, 1)
+
     # The paper's own band splits (two bands at p = 0.3, four at p = 0.8) on
     # both SDXL self-attention grids at 1024, 2048 and 3840 px; repetitions
     # scaled to about 20 ms of GPU time per shape.  Derived per split and

@@ -162,6 +162,29 @@ int pcpp_partial_attention(const pcpp_geom_t* g, const void* q,
                            void* stream);
 
 /*
+ * Multi-hop partially conditioned attention: p may exceed 1, the context
+ * reaching past the immediate neighbours (Sec. 6 hypothesises that many
+ * bands need it), up to the whole image at p = n - 1.  The band attends to
+ * the up = min(r, i*h) rows directly above it and the dn = min(r, (n-1-i)*h)
+ * rows directly below it, r = floor(p*h + 1e-9), stale, plus its own fresh
+ * rows; for p <= 1 this is pcpp_partial_attention's context.  The stale rows
+ * come compact instead of as whole neighbour bands:
+ *   k_above, v_above  [B, up*W, C]: image rows i*h-up .. i*h-1, in order
+ *                     (from bands i-1, i-2, ...; NULL when up = 0)
+ *   k_below, v_below  [B, dn*W, C]: image rows (i+1)*h .. (i+1)*h+dn-1
+ * p must lie in [0, max(1, n-1)] (PCPP_EINVAL otherwise).  Other arguments,
+ * the workspace contract and the numerics as pcpp_partial_attention; the
+ * workspace size comes from the function below.
+ */
+size_t pcpp_partial_attention_multihop_workspace_size(const pcpp_geom_t* g);
+int pcpp_partial_attention_multihop(const pcpp_geom_t* g, const void* q,
+                                    const void* k_fresh, const void* v_fresh,
+                                    const void* k_above, const void* v_above,
+                                    const void* k_below, const void* v_below,
+                                    void* out, void* workspace, size_t ws_bytes,
+                                    void* stream);
+
+/*
  * Weights of one SDXL-shaped transformer block (device pointers, bf16,
  * nn.Linear layout [out, in]).  C = heads * head_dim, F = ff_inner,
  * T = text_dim.

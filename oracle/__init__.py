@@ -10,6 +10,7 @@ from .pcpp_oracle import (  # noqa: F401
     assemble_context,
     boundary_messages,
     context_rows,
+    context_rows_multihop,
     context_token_ids,
     from_bf16_bits,
     gelu,
@@ -21,6 +22,7 @@ from .pcpp_oracle import (  # noqa: F401
     linear,
     mha,
     partial_attention,
+    partial_attention_multihop,
     place_boundary_messages,
     transformer_block,
 )

@@ -127,6 +127,38 @@ def assemble_context(H: int, W: int, n: int, i: int, p: float,
     return np.concatenate(parts, axis=1)
 
 
+def context_rows_multihop(H: int, n: int, i: int, p: float) -> Tuple[int, int, int, int]:
+    """Row counts when p may exceed 1 (Sec. 6: context beyond the immediate
+    neighbours).  Eq. 1 read with the patch boundaries dropped: the r =
+    floor(p*h) image rows directly above the patch and directly below it,
+    clipped to the image (reading R2 for the floor).  Returns (h, up, dn,
+    rows); equals context_rows for p <= 1."""
+    if n <= 0 or H % n != 0:
+        raise ValueError("H must be a positive multiple of n")
+    if not (0 <= i < n):
+        raise ValueError("patch index out of range")
+    if not (0.0 <= p <= max(1, n - 1)):
+        raise ValueError("p must lie in [0, max(1, n - 1)]")
+    h = H // n
+    r = int(math.floor(p * h + CTX_EPS))
+    up = min(r, i * h)
+    dn = min(r, (n - 1 - i) * h)
+    return h, up, dn, up + h + dn
+
+
+def partial_attention_multihop(H: int, W: int, n: int, i: int, p: float, heads: int,
+                               q: np.ndarray, k_fresh: np.ndarray, v_fresh: np.ndarray,
+                               k_above: Optional[np.ndarray], v_above: Optional[np.ndarray],
+                               k_below: Optional[np.ndarray], v_below: Optional[np.ndarray]):
+    """Partially conditioned attention with the stale rows given compactly:
+    k_above [B, up*W, C] = image rows i*h-up .. i*h-1, k_below [B, dn*W, C]
+    = rows (i+1)*h .. (i+1)*h+dn-1 (context_rows_multihop)."""
+    h, up, dn, _ = context_rows_multihop(H, n, i, p)
+    kc = np.concatenate(([k_above] if up else []) + [k_fresh] + ([k_below] if dn else []), axis=1)
+    vc = np.concatenate(([v_above] if up else []) + [v_fresh] + ([v_below] if dn else []), axis=1)
+    return mha(q, kc, vc, heads)
+
+
 # ---------------------------------------------------------------------------
 # Sec. 3.2 with Eq. 1: the rows a patch's neighbours read from it
 # ---------------------------------------------------------------------------

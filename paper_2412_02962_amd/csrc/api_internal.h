@@ -20,6 +20,7 @@ struct Geo {
 };
 
 int validate_geom(const pcpp_geom_t* g, Geo* out);
+int validate_geom_hops(const pcpp_geom_t* g, bool multi_hop, Geo* out);
 KvSource make_kv_source(const pcpp_geom_t* g, const Geo& r, const void* k_fresh, const void* v_fresh,
                         const void* k_up, const void* v_up, const void* k_dn, const void* v_dn);
 AttnParams make_attn_params(const pcpp_geom_t* g, const Geo& r, const void* q, void* out,

@@ -19,22 +19,36 @@ namespace pcpp {
 // Sec. 3.1: h = H/n.  Eq. 1: r = p*h rows from each existing neighbour; a
 // fractional p*h is floored (the small epsilon keeps decimal fractions such
 // as p = 0.29, h = 100 at their exact value).
-int validate_geom(const pcpp_geom_t* g, Geo* out) {
+int validate_geom(const pcpp_geom_t* g, Geo* out) { return validate_geom_hops(g, false, out); }
+
+// With multi_hop, p may exceed 1: context reaching past the neighbours (the
+// extension Sec. 6 hypothesises for many bands), up to the whole image at
+// p = n - 1.  r = floor(p*h + 1e-9) rows above and below the band, clipped
+// to the image.
+int validate_geom_hops(const pcpp_geom_t* g, bool multi_hop, Geo* out) {
     if (g == nullptr) return PCPP_EINVAL;
     if (g->reserved != 0) return PCPP_EINVAL;
     if (g->n_patches < 1 || g->H < 1 || g->W < 1) return PCPP_EINVAL;
     if (g->H % g->n_patches != 0) return PCPP_EINVAL;
     if (g->patch_idx < 0 || g->patch_idx >= g->n_patches) return PCPP_EINVAL;
-    if (!(g->partial >= 0.0 && g->partial <= 1.0)) return PCPP_EINVAL;  // NaN fails too
+    const double p_max = multi_hop ? (double)(g->n_patches - 1 > 1 ? g->n_patches - 1 : 1) : 1.0;
+    if (!(g->partial >= 0.0 && g->partial <= p_max)) return PCPP_EINVAL;  // NaN fails too
     if (g->heads < 1 || g->head_dim < 1 || g->batch < 1 || g->step < 0) return PCPP_EINVAL;
     if ((int64_t)g->H * g->W > INT32_MAX / 2) return PCPP_EINVAL;
     if ((int64_t)g->heads * g->head_dim > (1 << 20)) return PCPP_EINVAL;
     Geo r;
     r.h = g->H / g->n_patches;
-    double rows = floor(g->partial * (double)r.h + 1e-9);
-    int32_t ctx = rows >= (double)r.h ? r.h : (int32_t)rows;
-    r.up = g->patch_idx > 0 ? ctx : 0;
-    r.dn = g->patch_idx < g->n_patches - 1 ? ctx : 0;
+    const double rows = floor(g->partial * (double)r.h + 1e-9);
+    if (multi_hop) {
+        const int64_t ctx = (int64_t)rows;
+        const int64_t above = (int64_t)g->patch_idx * r.h, below = (int64_t)(g->n_patches - 1 - g->patch_idx) * r.h;
+        r.up = (int32_t)(ctx < above ? ctx : above);
+        r.dn = (int32_t)(ctx < below ? ctx : below);
+    } else {
+        const int32_t ctx = rows >= (double)r.h ? r.h : (int32_t)rows;
+        r.up = g->patch_idx > 0 ? ctx : 0;
+        r.dn = g->patch_idx < g->n_patches - 1 ? ctx : 0;
+    }
     r.nq = r.h * g->W;
     r.n_kv = (r.up + r.h + r.dn) * g->W;
     r.C = g->heads * g->head_dim;
@@ -55,6 +69,27 @@ KvSource make_kv_source(const pcpp_geom_t* g, const Geo& r, const void* k_fresh,
     s.k[2] = r.dn > 0 ? k_dn : nullptr;
     s.v[2] = r.dn > 0 ? v_dn : nullptr;
     s.bstride[0] = s.bstride[1] = s.bstride[2] = band;
+    s.end0 = r.up * g->W;
+    s.end1 = (r.up + r.h) * g->W;
+    s.n_kv = r.n_kv;
+    return s;
+}
+
+// Key/value sources from compact stale rows: the up rows directly above the
+// band and the dn rows directly below it, each [B, rows*W, C].
+KvSource make_kv_source_compact(const pcpp_geom_t* g, const Geo& r, const void* k_fresh, const void* v_fresh,
+                                const void* k_above, const void* v_above, const void* k_below,
+                                const void* v_below) {
+    KvSource s;
+    s.k[0] = r.up > 0 ? k_above : nullptr;
+    s.v[0] = r.up > 0 ? v_above : nullptr;
+    s.k[1] = k_fresh;
+    s.v[1] = v_fresh;
+    s.k[2] = r.dn > 0 ? k_below : nullptr;
+    s.v[2] = r.dn > 0 ? v_below : nullptr;
+    s.bstride[0] = (int64_t)r.up * g->W * r.C;
+    s.bstride[1] = (int64_t)r.nq * r.C;
+    s.bstride[2] = (int64_t)r.dn * g->W * r.C;
     s.end0 = r.up * g->W;
     s.end1 = (r.up + r.h) * g->W;
     s.n_kv = r.n_kv;
@@ -160,6 +195,44 @@ PCPP_EXPORT size_t pcpp_partial_attention_workspace_size(const pcpp_geom_t* g) {
     if (g->dtype != PCPP_DTYPE_BF16 || g->head_dim != 64) return 0;
     KvSource kv = make_kv_source(g, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
     return attention_bf16_ws_bytes(make_attn_params(g, r, nullptr, nullptr, kv));
+}
+
+PCPP_EXPORT size_t pcpp_partial_attention_multihop_workspace_size(const pcpp_geom_t* g) {
+    Geo r;
+    if (validate_geom_hops(g, true, &r) != PCPP_OK) return 0;
+    if (g->dtype != PCPP_DTYPE_BF16 || g->head_dim != 64) return 0;
+    KvSource kv = make_kv_source_compact(g, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
+    return attention_bf16_ws_bytes(make_attn_params(g, r, nullptr, nullptr, kv));
+}
+
+PCPP_EXPORT int pcpp_partial_attention_multihop(const pcpp_geom_t* g, const void* q, const void* k_fresh,
+                                                const void* v_fresh, const void* k_above, const void* v_above,
+                                                const void* k_below, const void* v_below, void* out,
+                                                void* workspace, size_t ws_bytes, void* stream) {
+    Geo r;
+    int st = validate_geom_hops(g, true, &r);
+    if (st != PCPP_OK) return st;
+    if (g->dtype != PCPP_DTYPE_BF16 && g->dtype != PCPP_DTYPE_F32) return PCPP_ENOTSUP;
+    if (g->head_dim != 64) return PCPP_ENOTSUP;
+    if (!q || !k_fresh || !v_fresh || !out) return PCPP_EINVAL;
+    if (r.up > 0 && (!k_above || !v_above)) return PCPP_EINVAL;
+    if (r.dn > 0 && (!k_below || !v_below)) return PCPP_EINVAL;
+    if (g->heads > 65535 || g->batch > 65535) return PCPP_EINVAL;
+    const void* ptrs[8] = {q, k_fresh, v_fresh, k_above, v_above, k_below, v_below, out};
+    for (const void* p : ptrs)
+        if (p && !aligned16(p)) return PCPP_EINVAL;
+    KvSource kv = make_kv_source_compact(g, r, k_fresh, v_fresh, k_above, v_above, k_below, v_below);
+    AttnParams p = make_attn_params(g, r, q, out, kv);
+    hipError_t e;
+    if (g->dtype == PCPP_DTYPE_BF16) {
+        const size_t need = attention_bf16_ws_bytes(p);
+        if (workspace == nullptr || ws_bytes < need) return PCPP_EWORKSPACE;
+        if (!aligned16(workspace)) return PCPP_EINVAL;
+        e = launch_attention_bf16(p, workspace, ws_bytes, (hipStream_t)stream);
+    } else {
+        e = launch_attention_f32(p, (hipStream_t)stream);
+    }
+    return e == hipSuccess ? PCPP_OK : PCPP_EHIP;
 }
 
 PCPP_EXPORT int pcpp_partial_attention(const pcpp_geom_t* g, const void* q, const void* k_fresh,

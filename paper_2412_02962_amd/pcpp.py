@@ -74,6 +74,8 @@ def _load():
                                                   vp, sz, vp]),
         "pcpp_transformer_block_sync_gn": (ctypes.c_int, [gp, wp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp,
                                                           vp, vp, vp, vp, sz, vp]),
+        "pcpp_partial_attention_multihop_workspace_size": (sz, [gp]),
+        "pcpp_partial_attention_multihop": (ctypes.c_int, [gp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "pcpp_boundary_bytes": (sz, [gp]),
         "pcpp_pack_boundary": (ctypes.c_int, [gp, vp, vp, vp, vp, vp]),
         "pcpp_unpack_boundary": (ctypes.c_int, [gp, vp, vp, vp, vp, vp, vp, vp]),
@@ -91,6 +93,7 @@ EXPORTED = (
     "pcpp_partial_attention_workspace_size", "pcpp_partial_attention",
     "pcpp_transformer_block_workspace_size", "pcpp_transformer_block",
     "pcpp_boundary_bytes", "pcpp_pack_boundary", "pcpp_unpack_boundary", "pcpp_transformer_block_sync_gn",
+    "pcpp_partial_attention_multihop_workspace_size", "pcpp_partial_attention_multihop",
 )
 
 
@@ -200,3 +203,14 @@ def pcpp_transformer_block_sync_gn(g, w, x, text, n_text, text_dim, k_up, v_up, 
         ctypes.byref(g), ctypes.byref(w), _ptr(x), _ptr(text), n_text, text_dim, _ptr(k_up), _ptr(v_up),
         _ptr(k_dn), _ptr(v_dn), _ptr(gn_bands), _ptr(gn_own), _ptr(y), _ptr(k_fresh_out), _ptr(v_fresh_out),
         _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def pcpp_partial_attention_multihop_workspace_size(g) -> int:
+    return _lib.pcpp_partial_attention_multihop_workspace_size(ctypes.byref(g))
+
+
+def pcpp_partial_attention_multihop(g, q, k_fresh, v_fresh, k_above, v_above, k_below, v_below, out,
+                                    workspace=None, ws_bytes=0, stream=None):
+    _check("pcpp_partial_attention_multihop", _lib.pcpp_partial_attention_multihop(
+        ctypes.byref(g), _ptr(q), _ptr(k_fresh), _ptr(v_fresh), _ptr(k_above), _ptr(v_above), _ptr(k_below),
+        _ptr(v_below), _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)))

@@ -220,3 +220,20 @@ def test_boundary_validation_errors_before_launch():
     assert lib.pcpp_unpack_boundary(ctypes.byref(none), None, None, None, None, None, None, None) == pcpp.PCPP_OK
     bad = pcpp.make_geom(16, 16, 4, 4, 0.25, 2)
     assert lib.pcpp_pack_boundary(ctypes.byref(bad), A, Bp, FAKE, FAKE, None) == pcpp.PCPP_EINVAL
+
+
+def test_multihop_geometry_and_validation():
+    from paper_2412_02962_amd import pcpp
+    lib = pcpp.lib()
+    # p > 1 is rejected by the neighbour form and accepted (up to n - 1) by the multi-hop form
+    g = pcpp.make_geom(64, 64, 8, 3, 1.5, 10)
+    assert pcpp.pcpp_partial_attention_workspace_size(g) == 0
+    assert pcpp.pcpp_partial_attention_multihop_workspace_size(g) > 0
+    assert pcpp.pcpp_partial_attention_multihop_workspace_size(pcpp.make_geom(64, 64, 8, 3, 7.5, 10)) == 0
+    call = lambda gg, *a: lib.pcpp_partial_attention_multihop(ctypes.byref(gg), *a, None)
+    # rows above needed but missing
+    assert call(g, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30) == pcpp.PCPP_EINVAL
+    # misaligned output
+    assert call(g, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE + 2, FAKE, 1 << 30) == pcpp.PCPP_EINVAL
+    # workspace too small
+    assert call(g, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 16) == pcpp.PCPP_EWORKSPACE

@@ -274,3 +274,67 @@ def test_workspace_reuse_with_multi_wave_launches():
                                         f["k_fresh"], f["v_fresh"], f["k_up"], f["v_up"], f["k_dn"], f["v_dn"])
         gu.assert_close(cfg, gu.to_f64(out)[:, rows], want, f"reuse {n}")
     assert int(ws[:65536 * 4].view(torch.int32).abs().sum().item()) == 0   # counters left zero
+
+
+def _multihop_inputs(cfg):
+    """Stored-dtype inputs of a multi-hop call: q, fresh K/V of band i and
+    the compact stale rows above and below it, cut from the stale copies of
+    the other bands."""
+    _, up, dn, _ = oracle.context_rows_multihop(cfg.H, cfg.n, cfg.i, cfg.p)
+    W, h, i = cfg.W, cfg.h, cfg.i
+    out = {"q": synth.store(synth.patch_tensor(cfg, i, "q", False), cfg.dtype)}
+    for kind in ("k", "v"):
+        grid = np.concatenate([synth.patch_tensor(cfg, j, kind, stale=(j != i)) for j in range(cfg.n)], axis=1)
+        out[kind + "_fresh"] = synth.store(grid[:, i * h * W:(i + 1) * h * W], cfg.dtype)
+        out[kind + "_above"] = synth.store(grid[:, (i * h - up) * W:i * h * W], cfg.dtype) if up else None
+        out[kind + "_below"] = synth.store(grid[:, (i + 1) * h * W:((i + 1) * h + dn) * W], cfg.dtype) if dn else None
+    return out
+
+
+@pytest.mark.parametrize("geo", [
+    dict(H=64, W=64, n=8, i=3, p=1.5, heads=10),     # 24 rows each side: bands i-1 and i-2
+    dict(H=64, W=64, n=8, i=1, p=2.5, heads=10),     # clipped above (8 rows), 20 rows below
+    dict(H=32, W=24, n=4, i=2, p=3.0, heads=3),      # p = n - 1: the whole image
+    dict(H=40, W=20, n=5, i=0, p=1.3, heads=2),      # top band, fractional p*h
+])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_multihop_attention_matches_oracle(geo, dtype):
+    import torch
+    from paper_2412_02962_amd import pcpp
+    cfg = synth.AttnConfig(name="mh", d=64, dtype=dtype, seed_id=45, **geo)
+    _say("multi-hop", geo, dtype)
+    inp = _multihop_inputs(cfg)
+    d = {k: gu.to_dev(v, cfg.dtype) for k, v in inp.items()}
+    g = gu.geom(cfg)
+    wsb = pcpp.pcpp_partial_attention_multihop_workspace_size(g)
+    ws = torch.zeros(max(wsb, 1), dtype=torch.uint8, device=gu.DEV)
+    out = torch.empty_like(d["q"])
+    pcpp.pcpp_partial_attention_multihop(g, d["q"], d["k_fresh"], d["v_fresh"], d["k_above"], d["v_above"],
+                                         d["k_below"], d["v_below"], out, ws, wsb)
+    torch.cuda.synchronize()
+    f = {k: (None if v is None else oracle.as_f64(v, cfg.dtype)) for k, v in inp.items()}
+    want = oracle.partial_attention_multihop(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, f["q"], f["k_fresh"],
+                                             f["v_fresh"], f["k_above"], f["v_above"], f["k_below"], f["v_below"])
+    gu.assert_close(cfg, gu.to_f64(out), want, f"multi-hop {geo}")
+
+
+def test_multihop_equals_neighbour_form_for_p_up_to_one():
+    # same kernel, same rows: bit-identical to pcpp_partial_attention
+    import torch
+    from paper_2412_02962_amd import pcpp
+    cfg = synth.ATTN_CONFIGS["sdxl2048_l1_p25"]
+    _say("multi-hop p <= 1")
+    inp = synth.attention_inputs(cfg)
+    ref = gu.run_attention(cfg, inp)
+    h, up, dn, _ = oracle.context_rows(cfg.H, cfg.n, cfg.i, cfg.p)
+    d = {k: gu.to_dev(v, cfg.dtype) for k, v in inp.items()}
+    W = cfg.W
+    g = gu.geom(cfg)
+    wsb = pcpp.pcpp_partial_attention_multihop_workspace_size(g)
+    ws = torch.zeros(wsb, dtype=torch.uint8, device=gu.DEV)
+    out = torch.empty_like(d["q"])
+    pcpp.pcpp_partial_attention_multihop(g, d["q"], d["k_fresh"], d["v_fresh"],
+                                         d["k_up"][:, (h - up) * W:].contiguous(), d["v_up"][:, (h - up) * W:].contiguous(),
+                                         d["k_dn"][:, :dn * W].contiguous(), d["v_dn"][:, :dn * W].contiguous(), out, ws, wsb)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)

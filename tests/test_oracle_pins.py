@@ -304,3 +304,55 @@ def test_bf16_widening_is_exact():
     x = np.random.default_rng(1).standard_normal(10000) * 10
     tb = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
     assert np.array_equal(synth.bf16_bits(x), tb)
+
+
+# ---------------------------------------------------------------------------
+# Multi-hop context (p > 1, Sec. 6): the rows within r = floor(p h) of the
+# patch, clipped to the image
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("n", [2, 3, 5, 8])
+def test_multihop_rows_by_brute_force(n):
+    from fractions import Fraction
+    for h in (1, 3, 4):
+        H = n * h
+        for p in (0.0, 0.5, 1.0, 1.5, 2.0, 2.7, float(n - 1)):
+            if p > max(1, n - 1):
+                continue
+            r = int(Fraction(str(p)) * h // 1)
+            for i in range(n):
+                rows = [row for row in range(H) if i * h - r <= row < (i + 1) * h + r]
+                _, up, dn, total = oracle.context_rows_multihop(H, n, i, p)
+                assert total == len(rows)
+                assert rows[0] == i * h - up and rows[-1] == (i + 1) * h + dn - 1
+                if p <= 1.0:
+                    assert oracle.context_rows_multihop(H, n, i, p) == oracle.context_rows(H, n, i, p)
+    with pytest.raises(ValueError):
+        oracle.context_rows_multihop(8, 4, 1, 3.5)
+
+
+def test_multihop_whole_image_and_neighbour_equivalence():
+    # p = n - 1 with stale == fresh: full-image attention restricted to the
+    # patch (torch SDPA, a library routine); p <= 1: the neighbour form
+    n, h, W, heads, d = 4, 2, 3, 2, 8
+    H = n * h
+    cfg = synth.AttnConfig(name="mh", H=H, W=W, n=n, i=1, p=0.5, heads=heads, d=d, dtype="f32", seed_id=33)
+    grid = {k: full_grid(cfg, k, cfg.i, "stale_eq_fresh", synth) for k in ("q", "k", "v")}
+    band = lambda x, a, b: x[:, a * W:b * W]
+    for i in range(n):
+        q = band(grid["q"], i * h, (i + 1) * h)
+        _, up, dn, _ = oracle.context_rows_multihop(H, n, i, n - 1)
+        got = oracle.partial_attention_multihop(
+            H, W, n, i, n - 1, heads, q, band(grid["k"], i * h, (i + 1) * h), band(grid["v"], i * h, (i + 1) * h),
+            band(grid["k"], i * h - up, i * h) if up else None, band(grid["v"], i * h - up, i * h) if up else None,
+            band(grid["k"], (i + 1) * h, (i + 1) * h + dn) if dn else None,
+            band(grid["v"], (i + 1) * h, (i + 1) * h + dn) if dn else None)
+        assert np.allclose(got, _sdpa_torch(q, grid["k"], grid["v"], heads), rtol=0, atol=1e-12)
+    g = _inputs64(cfg)
+    _, up, dn, _ = oracle.context_rows(H, n, 1, 0.5)
+    want = oracle.partial_attention(H, W, n, 1, 0.5, heads, g["q"], g["k_fresh"], g["v_fresh"], g["k_up"],
+                                    g["v_up"], g["k_dn"], g["v_dn"])
+    got = oracle.partial_attention_multihop(H, W, n, 1, 0.5, heads, g["q"], g["k_fresh"], g["v_fresh"],
+                                            g["k_up"][:, (h - up) * W:], g["v_up"][:, (h - up) * W:],
+                                            g["k_dn"][:, :dn * W], g["v_dn"][:, :dn * W])
+    assert np.array_equal(got, want)
