@@ -326,6 +326,50 @@ int pcpp_unpack_boundary(const pcpp_geom_t* g, const void* recv_up,
                          const void* recv_dn, void* k_up, void* v_up,
                          void* k_dn, void* v_dn, void* stream);
 
+/*
+ * Messages of the exchange with multi-hop context (p > 1, the context
+ * beyond the immediate neighbours that Sec. 6 suggests for many bands; the
+ * stale blocks are the compact ones pcpp_partial_attention_multihop reads).
+ * With r = floor(p*h + 1e-9), bands i and j exchange
+ *   rows(i, j) = clamp(r - (|i - j| - 1) * h, 0, h)
+ * rows in each direction: band j above band i reads band i's first rows,
+ * band j below reads its last rows.  For |i - j| = 1 and p <= 1 these are
+ * the messages of pcpp_pack_boundary.  Same message layout as above:
+ * [B][2][rows*W][C].  The geometry g is band i's; p may go up to
+ * max(1, n - 1).  `peer` is j, any band index; j = i and bands out of reach
+ * give rows = 0.
+ */
+
+/* Bytes of the message between bands g.patch_idx and peer, either
+ * direction (0 when none, or for invalid arguments). */
+size_t pcpp_multihop_message_bytes(const pcpp_geom_t* g, int32_t peer);
+
+/*
+ * Builds band i's message for band `peer` from its fresh keys/values
+ * [B, h*W, C].  Nothing to do (PCPP_OK, pointers may be NULL) when rows =
+ * 0.  The message must not overlap the inputs (PCPP_EINVAL); peer out of
+ * range is PCPP_EINVAL.  Asynchronous on `stream`.
+ */
+int pcpp_pack_multihop(const pcpp_geom_t* g, int32_t peer,
+                       const void* k_fresh, const void* v_fresh, void* send,
+                       void* stream);
+
+/*
+ * Places the message band i received from band `peer` (built there by
+ * pcpp_pack_multihop with peer = i) into band i's compact stale blocks, at
+ * the image rows it holds:
+ *   peer < i: k_above/v_above [B, up*W, C] (image rows i*h-up .. i*h-1)
+ *             receive band peer's last rows; the below pair may be NULL
+ *   peer > i: k_below/v_below [B, dn*W, C] (rows (i+1)*h .. (i+1)*h+dn-1)
+ *             receive band peer's first rows; the above pair may be NULL
+ * Other rows are left untouched.  Calling it for every other band fills
+ * both blocks completely.  Buffers must not overlap (PCPP_EINVAL).
+ * Asynchronous on `stream`.
+ */
+int pcpp_unpack_multihop(const pcpp_geom_t* g, int32_t peer,
+                         const void* recv, void* k_above, void* v_above,
+                         void* k_below, void* v_below, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

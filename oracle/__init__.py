@@ -21,8 +21,11 @@ from .pcpp_oracle import (  # noqa: F401
     layer_norm,
     linear,
     mha,
+    multihop_message,
+    multihop_message_rows,
     partial_attention,
     partial_attention_multihop,
     place_boundary_messages,
+    place_multihop_message,
     transformer_block,
 )

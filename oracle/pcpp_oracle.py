@@ -216,6 +216,56 @@ def place_boundary_messages(H: int, W: int, n: int, i: int, p: float,
     return k_up, v_up, k_dn, v_dn
 
 
+def multihop_message_rows(H: int, n: int, i: int, p: float, j: int) -> Tuple[int, bool]:
+    """How many rows of patch i patch j reads with multi-hop context
+    (context_rows_multihop), and whether they are patch i's first rows
+    (j above i) or its last rows (j below i)."""
+    h = H // n
+    if j == i or not (0 <= j < n):
+        return 0, j < i
+    _, up_j, dn_j, _ = context_rows_multihop(H, n, j, p)
+    if j < i:   # patch j's context below reaches into patch i from its top
+        return max(0, min(h, (j + 1) * h + dn_j - i * h)), True
+    # patch j's context above reaches into patch i from its bottom
+    return max(0, (i + 1) * h - max(i * h, j * h - up_j)), False
+
+
+def multihop_message(H: int, W: int, n: int, i: int, p: float, j: int,
+                     k_fresh: np.ndarray, v_fresh: np.ndarray) -> Optional[np.ndarray]:
+    """What patch i sends patch j with multi-hop context: the rows of patch
+    i that patch j's context holds, [B, 2, rows*W, C] (keys, then values), or
+    None.  For |i - j| = 1 and p <= 1 these are boundary_messages."""
+    rows, first = multihop_message_rows(H, n, i, p, j)
+    if rows == 0:
+        return None
+    h = H // n
+    sl = slice(0, rows * W) if first else slice((h - rows) * W, h * W)
+    return np.stack([k_fresh[:, sl], v_fresh[:, sl]], axis=1)
+
+
+def place_multihop_message(H: int, W: int, n: int, i: int, p: float, j: int, msg: np.ndarray,
+                           k_above: np.ndarray, v_above: np.ndarray,
+                           k_below: np.ndarray, v_below: np.ndarray):
+    """Receiver side for patch i: writes patch j's message into copies of
+    the compact stale blocks (rows i*h-up .. i*h-1 above, (i+1)*h ..
+    (i+1)*h+dn-1 below) at the image rows it holds.  Returns the new
+    (k_above, v_above, k_below, v_below)."""
+    h, up, dn, _ = context_rows_multihop(H, n, i, p)
+    rows, _ = multihop_message_rows(H, n, j, p, i)
+    ka, va, kb, vb = (None if a is None else np.array(a, copy=True) for a in (k_above, v_above, k_below, v_below))
+    if rows == 0:
+        return ka, va, kb, vb
+    if j < i:   # patch j's last rows: image rows (j+1)*h - rows .. (j+1)*h - 1
+        off = (j + 1) * h - rows - (i * h - up)
+        ka[:, off * W:(off + rows) * W] = msg[:, 0]
+        va[:, off * W:(off + rows) * W] = msg[:, 1]
+    else:       # patch j's first rows: image rows j*h .. j*h + rows - 1
+        off = j * h - (i + 1) * h
+        kb[:, off * W:(off + rows) * W] = msg[:, 0]
+        vb[:, off * W:(off + rows) * W] = msg[:, 1]
+    return ka, va, kb, vb
+
+
 # ---------------------------------------------------------------------------
 # Sec. 3.3: multi-head scaled dot-product attention over the context
 # ---------------------------------------------------------------------------

@@ -369,3 +369,103 @@ PCPP_EXPORT int pcpp_unpack_boundary(const pcpp_geom_t* g, const void* recv_up, 
     }
     return launch_seg_copy(p, r.esize, (hipStream_t)stream) == hipSuccess ? PCPP_OK : PCPP_EHIP;
 }
+
+// ---------------------------------------------------------------------------
+// Multi-hop messages (p > 1, the context beyond the neighbours of Sec. 6)
+// ---------------------------------------------------------------------------
+
+namespace {
+
+// Rows bands i and j exchange, the same in both directions: band j's
+// context (r rows past its edge) reaches r - (|i-j|-1)*h rows into band i,
+// at most the whole band.  The clip of the context to the image never cuts
+// these rows, they lie inside it.
+int64_t hop_rows(const pcpp_geom_t* g, const Geo& r, int32_t peer) {
+    const int64_t d = peer > g->patch_idx ? peer - g->patch_idx : g->patch_idx - peer;
+    if (d == 0) return 0;
+    const int64_t ctx = (int64_t)floor(g->partial * (double)r.h + 1e-9);
+    const int64_t rows = ctx - (d - 1) * r.h;
+    return rows < 0 ? 0 : (rows > r.h ? r.h : rows);
+}
+
+int validate_peer(const pcpp_geom_t* g, int32_t peer, Geo* r) {
+    int st = validate_geom_hops(g, true, r);
+    if (st != PCPP_OK) return st;
+    if (peer < 0 || peer >= g->n_patches) return PCPP_EINVAL;
+    if (g->dtype != PCPP_DTYPE_BF16 && g->dtype != PCPP_DTYPE_F32) return PCPP_ENOTSUP;
+    if (g->batch > 65535) return PCPP_EINVAL;
+    return PCPP_OK;
+}
+
+}  // namespace
+
+PCPP_EXPORT size_t pcpp_multihop_message_bytes(const pcpp_geom_t* g, int32_t peer) {
+    Geo r;
+    if (validate_peer(g, peer, &r) != PCPP_OK) return 0;
+    return (size_t)g->batch * 2 * (size_t)hop_rows(g, r, peer) * g->W * r.C * r.esize;
+}
+
+PCPP_EXPORT int pcpp_pack_multihop(const pcpp_geom_t* g, int32_t peer, const void* k_fresh,
+                                   const void* v_fresh, void* send, void* stream) {
+    Geo r;
+    int st = validate_peer(g, peer, &r);
+    if (st != PCPP_OK) return st;
+    const int64_t rows = hop_rows(g, r, peer);
+    if (rows == 0) return PCPP_OK;
+    if (!k_fresh || !v_fresh || !send) return PCPP_EINVAL;
+    const int64_t row = (int64_t)g->W * r.C * r.esize;
+    const int64_t band = row * r.h;
+    const int64_t run = row * rows;
+    const int64_t msg = 2 * run * g->batch;
+    if (ranges_overlap(send, msg, k_fresh, band * g->batch) || ranges_overlap(send, msg, v_fresh, band * g->batch))
+        return PCPP_EINVAL;
+    // a band above reads this band's first rows, a band below its last rows
+    const int64_t src_off = peer < g->patch_idx ? 0 : band - run;
+    CopyParams p;
+    p.n_seg = 2;
+    p.batch = g->batch;
+    for (int s = 0; s < 2; ++s) {
+        p.seg[s].src = (const char*)(s == 0 ? k_fresh : v_fresh) + src_off;
+        p.seg[s].dst = (char*)send + s * run;
+        p.seg[s].src_bstride = band;
+        p.seg[s].dst_bstride = 2 * run;
+        p.seg[s].bytes = run;
+    }
+    return launch_seg_copy(p, r.esize, (hipStream_t)stream) == hipSuccess ? PCPP_OK : PCPP_EHIP;
+}
+
+PCPP_EXPORT int pcpp_unpack_multihop(const pcpp_geom_t* g, int32_t peer, const void* recv, void* k_above,
+                                     void* v_above, void* k_below, void* v_below, void* stream) {
+    Geo r;
+    int st = validate_peer(g, peer, &r);
+    if (st != PCPP_OK) return st;
+    const int64_t rows = hop_rows(g, r, peer);
+    if (rows == 0) return PCPP_OK;
+    const bool above = peer < g->patch_idx;
+    void* kd = above ? k_above : k_below;
+    void* vd = above ? v_above : v_below;
+    if (!recv || !kd || !vd) return PCPP_EINVAL;
+    const int64_t row = (int64_t)g->W * r.C * r.esize;
+    const int64_t run = row * rows;
+    const int64_t block = row * (above ? r.up : r.dn);  // one image of the compact stale block
+    const int64_t msg = 2 * run * g->batch;
+    if (ranges_overlap(kd, block * g->batch, vd, block * g->batch) ||
+        ranges_overlap(recv, msg, kd, block * g->batch) || ranges_overlap(recv, msg, vd, block * g->batch))
+        return PCPP_EINVAL;
+    // The block above holds image rows i*h-up .. i*h-1 and receives the last
+    // rows of band j; the block below holds (i+1)*h .. (i+1)*h+dn-1 and
+    // receives the first rows of band j.
+    const int64_t i = g->patch_idx, j = peer, h = r.h;
+    const int64_t dst_row = above ? (j + 1) * h - rows - (i * h - r.up) : (j - i - 1) * h;
+    CopyParams p;
+    p.n_seg = 2;
+    p.batch = g->batch;
+    for (int s = 0; s < 2; ++s) {
+        p.seg[s].src = (const char*)recv + s * run;
+        p.seg[s].dst = (char*)(s == 0 ? kd : vd) + dst_row * row;
+        p.seg[s].src_bstride = 2 * run;
+        p.seg[s].dst_bstride = block;
+        p.seg[s].bytes = run;
+    }
+    return launch_seg_copy(p, r.esize, (hipStream_t)stream) == hipSuccess ? PCPP_OK : PCPP_EHIP;
+}

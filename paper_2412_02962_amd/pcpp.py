@@ -79,6 +79,9 @@ def _load():
         "pcpp_boundary_bytes": (sz, [gp]),
         "pcpp_pack_boundary": (ctypes.c_int, [gp, vp, vp, vp, vp, vp]),
         "pcpp_unpack_boundary": (ctypes.c_int, [gp, vp, vp, vp, vp, vp, vp, vp]),
+        "pcpp_multihop_message_bytes": (sz, [gp, i32]),
+        "pcpp_pack_multihop": (ctypes.c_int, [gp, i32, vp, vp, vp, vp]),
+        "pcpp_unpack_multihop": (ctypes.c_int, [gp, i32, vp, vp, vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -94,6 +97,7 @@ EXPORTED = (
     "pcpp_transformer_block_workspace_size", "pcpp_transformer_block",
     "pcpp_boundary_bytes", "pcpp_pack_boundary", "pcpp_unpack_boundary", "pcpp_transformer_block_sync_gn",
     "pcpp_partial_attention_multihop_workspace_size", "pcpp_partial_attention_multihop",
+    "pcpp_multihop_message_bytes", "pcpp_pack_multihop", "pcpp_unpack_multihop",
 )
 
 
@@ -214,3 +218,18 @@ def pcpp_partial_attention_multihop(g, q, k_fresh, v_fresh, k_above, v_above, k_
     _check("pcpp_partial_attention_multihop", _lib.pcpp_partial_attention_multihop(
         ctypes.byref(g), _ptr(q), _ptr(k_fresh), _ptr(v_fresh), _ptr(k_above), _ptr(v_above), _ptr(k_below),
         _ptr(v_below), _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def pcpp_multihop_message_bytes(g, peer) -> int:
+    return _lib.pcpp_multihop_message_bytes(ctypes.byref(g), peer)
+
+
+def pcpp_pack_multihop(g, peer, k_fresh, v_fresh, send, stream=None):
+    _check("pcpp_pack_multihop", _lib.pcpp_pack_multihop(
+        ctypes.byref(g), peer, _ptr(k_fresh), _ptr(v_fresh), _ptr(send), _stream(stream)))
+
+
+def pcpp_unpack_multihop(g, peer, recv, k_above, v_above, k_below, v_below, stream=None):
+    _check("pcpp_unpack_multihop", _lib.pcpp_unpack_multihop(
+        ctypes.byref(g), peer, _ptr(recv), _ptr(k_above), _ptr(v_above), _ptr(k_below), _ptr(v_below),
+        _stream(stream)))

@@ -72,3 +72,19 @@ def assert_close(cfg, got, want, tag=""):
         assert mx <= TOL_BF16_MAX, f"{tag} bf16 max-abs {mx:.3e} > {TOL_BF16_MAX}"
         assert mean <= TOL_BF16_MEAN, f"{tag} bf16 mean-abs {mean:.3e} > {TOL_BF16_MEAN}"
     return mx, mean
+
+
+def multihop_inputs(cfg):
+    """Stored-dtype inputs of a multi-hop call: q, fresh K/V of band i and
+    the compact stale rows above and below it, cut from the stale copies of
+    the other bands."""
+    import oracle
+    _, up, dn, _ = oracle.context_rows_multihop(cfg.H, cfg.n, cfg.i, cfg.p)
+    W, h, i = cfg.W, cfg.h, cfg.i
+    out = {"q": synth.store(synth.patch_tensor(cfg, i, "q", False), cfg.dtype)}
+    for kind in ("k", "v"):
+        grid = np.concatenate([synth.patch_tensor(cfg, j, kind, stale=(j != i)) for j in range(cfg.n)], axis=1)
+        out[kind + "_fresh"] = synth.store(grid[:, i * h * W:(i + 1) * h * W], cfg.dtype)
+        out[kind + "_above"] = synth.store(grid[:, (i * h - up) * W:i * h * W], cfg.dtype) if up else None
+        out[kind + "_below"] = synth.store(grid[:, (i + 1) * h * W:((i + 1) * h + dn) * W], cfg.dtype) if dn else None
+    return out

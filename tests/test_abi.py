@@ -237,3 +237,43 @@ def test_multihop_geometry_and_validation():
     assert call(g, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE + 2, FAKE, 1 << 30) == pcpp.PCPP_EINVAL
     # workspace too small
     assert call(g, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 16) == pcpp.PCPP_EWORKSPACE
+
+
+def test_multihop_message_bytes_match_the_oracle_rows():
+    from paper_2412_02962_amd import pcpp
+    for (H, W, n, p, heads, B) in [(64, 64, 8, 1.5, 2, 1), (48, 8, 6, 2.5, 1, 2), (32, 16, 4, 3.0, 1, 1),
+                                   (64, 64, 8, 0.25, 2, 1), (16, 4, 2, 1.0, 1, 3)]:
+        for i in range(n):
+            g = pcpp.make_geom(H, W, n, i, p, heads, 64, B)
+            for j in range(n):
+                rows, _ = oracle.multihop_message_rows(H, n, i, p, j)
+                rows_back, _ = oracle.multihop_message_rows(H, n, j, p, i)
+                assert rows == rows_back                      # the same count in both directions
+                assert pcpp.pcpp_multihop_message_bytes(g, j) == B * 2 * rows * W * heads * 64 * 2, (H, n, p, i, j)
+            # p <= 1: the neighbour messages are the boundary messages
+            if p <= 1.0 and 0 < i:
+                assert pcpp.pcpp_multihop_message_bytes(g, i - 1) == pcpp.pcpp_boundary_bytes(g)
+    g = pcpp.make_geom(64, 64, 8, 3, 1.5, 2)
+    assert pcpp.pcpp_multihop_message_bytes(g, 8) == 0 and pcpp.pcpp_multihop_message_bytes(g, -1) == 0
+
+
+def test_multihop_message_validation_errors_before_launch():
+    from paper_2412_02962_amd import pcpp
+    lib = pcpp.lib()
+    g = pcpp.make_geom(64, 64, 8, 3, 1.5, 2)    # h = 8, r = 12: bands 1, 2, 4, 5 in reach
+    pack = lambda peer, *a: lib.pcpp_pack_multihop(ctypes.byref(g), peer, *a, None)
+    unpack = lambda peer, *a: lib.pcpp_unpack_multihop(ctypes.byref(g), peer, *a, None)
+    A, Bp = FAKE, FAKE + (1 << 30)
+    assert pack(8, A, Bp, A + (1 << 31)) == pcpp.PCPP_EINVAL              # no band 8
+    assert pack(2, None, Bp, A + (1 << 31)) == pcpp.PCPP_EINVAL           # keys missing
+    assert pack(2, A, Bp, None) == pcpp.PCPP_EINVAL                       # message missing
+    assert pack(2, A, Bp, Bp + 64) == pcpp.PCPP_EINVAL                    # message overlaps the values
+    assert pack(0, None, None, None) == pcpp.PCPP_OK                      # band 0 is out of reach
+    assert pack(3, None, None, None) == pcpp.PCPP_OK                      # itself
+    assert unpack(1, A, None, None, Bp, Bp + (1 << 26)) == pcpp.PCPP_EINVAL   # block above missing
+    assert unpack(5, A, Bp, Bp + (1 << 26), None, None) == pcpp.PCPP_EINVAL   # block below missing
+    assert unpack(1, A, Bp, Bp + 64, None, None) == pcpp.PCPP_EINVAL          # keys and values overlap
+    assert unpack(1, Bp + 64, Bp, Bp + (1 << 26), None, None) == pcpp.PCPP_EINVAL  # message overlaps keys
+    assert unpack(7, None, None, None, None, None) == pcpp.PCPP_OK
+    f64 = pcpp.make_geom(64, 64, 8, 3, 1.5, 2, 64, 1, 0, 7)
+    assert lib.pcpp_pack_multihop(ctypes.byref(f64), 2, A, Bp, A + (1 << 31), None) != pcpp.PCPP_OK

@@ -276,21 +276,6 @@ def test_workspace_reuse_with_multi_wave_launches():
     assert int(ws[:65536 * 4].view(torch.int32).abs().sum().item()) == 0   # counters left zero
 
 
-def _multihop_inputs(cfg):
-    """Stored-dtype inputs of a multi-hop call: q, fresh K/V of band i and
-    the compact stale rows above and below it, cut from the stale copies of
-    the other bands."""
-    _, up, dn, _ = oracle.context_rows_multihop(cfg.H, cfg.n, cfg.i, cfg.p)
-    W, h, i = cfg.W, cfg.h, cfg.i
-    out = {"q": synth.store(synth.patch_tensor(cfg, i, "q", False), cfg.dtype)}
-    for kind in ("k", "v"):
-        grid = np.concatenate([synth.patch_tensor(cfg, j, kind, stale=(j != i)) for j in range(cfg.n)], axis=1)
-        out[kind + "_fresh"] = synth.store(grid[:, i * h * W:(i + 1) * h * W], cfg.dtype)
-        out[kind + "_above"] = synth.store(grid[:, (i * h - up) * W:i * h * W], cfg.dtype) if up else None
-        out[kind + "_below"] = synth.store(grid[:, (i + 1) * h * W:((i + 1) * h + dn) * W], cfg.dtype) if dn else None
-    return out
-
-
 @pytest.mark.parametrize("geo", [
     dict(H=64, W=64, n=8, i=3, p=1.5, heads=10),     # 24 rows each side: bands i-1 and i-2
     dict(H=64, W=64, n=8, i=1, p=2.5, heads=10),     # clipped above (8 rows), 20 rows below
@@ -303,7 +288,7 @@ def test_multihop_attention_matches_oracle(geo, dtype):
     from paper_2412_02962_amd import pcpp
     cfg = synth.AttnConfig(name="mh", d=64, dtype=dtype, seed_id=45, **geo)
     _say("multi-hop", geo, dtype)
-    inp = _multihop_inputs(cfg)
+    inp = gu.multihop_inputs(cfg)
     d = {k: gu.to_dev(v, cfg.dtype) for k, v in inp.items()}
     g = gu.geom(cfg)
     wsb = pcpp.pcpp_partial_attention_multihop_workspace_size(g)

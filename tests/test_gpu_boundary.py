@@ -131,3 +131,103 @@ def test_attention_over_exchanged_rows_only(geo):
     torch.cuda.synchronize()
     assert not torch.isnan(out).any()
     assert torch.equal(out, ref)
+
+
+# ---------------------------------------------------------------------------
+# Multi-hop messages (p > 1): band i sends each band within reach its rows
+# ---------------------------------------------------------------------------
+
+MH_GEOS = [
+    dict(H=64, W=64, n=8, i=3, p=1.5, heads=10, batch=1),    # two bands each way, 4 of 8 rows from the far ones
+    dict(H=64, W=64, n=8, i=1, p=2.5, heads=4, batch=2),     # clipped above, three bands below
+    dict(H=32, W=24, n=4, i=2, p=3.0, heads=3, batch=1),     # p = n - 1: every band whole
+    dict(H=40, W=20, n=5, i=0, p=1.3, heads=2, batch=3),     # top band, fractional p*h
+    dict(H=48, W=16, n=6, i=4, p=0.5, heads=2, batch=1),     # p <= 1: the neighbour messages
+]
+
+
+def _mh_cfg(geo, dtype, seed_id=46):
+    return synth.AttnConfig(name="mhx", d=64, dtype=dtype, seed_id=seed_id, **geo)
+
+
+@pytest.mark.parametrize("geo", MH_GEOS)
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_pack_multihop_is_bit_exact(geo, dtype):
+    import torch
+    from paper_2412_02962_amd import pcpp
+    cfg = _mh_cfg(geo, dtype)
+    _say("pack multi-hop", geo, dtype)
+    k, v = _stored(cfg, cfg.i, "k", False), _stored(cfg, cfg.i, "v", False)
+    g = gu.geom(cfg)
+    kd, vd = gu.to_dev(k, dtype), gu.to_dev(v, dtype)
+    tdt = torch.bfloat16 if dtype == synth.DTYPE_BF16 else torch.float32
+    esize = 2 if dtype == synth.DTYPE_BF16 else 4
+    for j in range(cfg.n):
+        want = oracle.multihop_message(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, j, k, v)
+        nbytes = pcpp.pcpp_multihop_message_bytes(g, j)
+        if want is None:
+            assert nbytes == 0
+            pcpp.pcpp_pack_multihop(g, j, None, None, None)       # nothing to send: no pointers needed
+            continue
+        assert want.size * esize == nbytes
+        send = torch.full((nbytes // esize,), 7, dtype=tdt, device=gu.DEV)
+        pcpp.pcpp_pack_multihop(g, j, kd, vd, send)
+        torch.cuda.synchronize()
+        assert np.array_equal(_raw(send, dtype), want.reshape(-1)), (geo, j)
+        if cfg.p <= 1.0 and abs(j - cfg.i) == 1:                   # same bytes as the neighbour form
+            both = [torch.zeros_like(send) for _ in range(2)]
+            pcpp.pcpp_pack_boundary(g, kd, vd, both[0], both[1])
+            torch.cuda.synchronize()
+            assert np.array_equal(_raw(send, dtype), _raw(both[0] if j < cfg.i else both[1], dtype))
+
+
+@pytest.mark.parametrize("geo", MH_GEOS[:4])
+def test_multihop_exchange_then_attention(geo):
+    """Every other band packs its previous-step K/V for band i on the GPU;
+    band i unpacks all of them into NaN-filled compact blocks, which then
+    equal the blocks cut from the whole stale image, and the multi-hop
+    attention over them equals the one over the cut blocks, bit for bit."""
+    import torch
+    from paper_2412_02962_amd import pcpp
+    cfg = _mh_cfg(geo, "bf16")
+    _say("multi-hop exchange + attention", geo)
+    i, n = cfg.i, cfg.n
+    inp = gu.multihop_inputs(cfg)
+    d = {k: gu.to_dev(v, cfg.dtype) for k, v in inp.items()}
+    blocks = {key: None if d[key] is None else torch.full_like(d[key], float("nan"))
+              for key in ("k_above", "v_above", "k_below", "v_below")}
+    g = gu.geom(cfg)
+    sent = 0
+    for j in range(n):
+        if j == i:
+            continue
+        gj = gu.geom(dataclasses.replace(cfg, i=j))
+        nb = pcpp.pcpp_multihop_message_bytes(gj, i)
+        assert nb == pcpp.pcpp_multihop_message_bytes(g, j)
+        if nb == 0:
+            continue
+        kj = gu.to_dev(_stored(cfg, j, "k", True), cfg.dtype)
+        vj = gu.to_dev(_stored(cfg, j, "v", True), cfg.dtype)
+        msg = torch.empty(nb // 2, dtype=torch.bfloat16, device=gu.DEV)
+        pcpp.pcpp_pack_multihop(gj, i, kj, vj, msg)
+        pcpp.pcpp_unpack_multihop(g, j, msg, blocks["k_above"], blocks["v_above"], blocks["k_below"],
+                                  blocks["v_below"])
+        sent += 1
+    torch.cuda.synchronize()
+    assert sent > 0
+    for key, blk in blocks.items():
+        if blk is None:
+            assert d[key] is None
+            continue
+        assert torch.equal(blk.view(torch.int16), d[key].view(torch.int16)), key
+    wsb = pcpp.pcpp_partial_attention_multihop_workspace_size(g)
+    ws = torch.zeros(wsb, dtype=torch.uint8, device=gu.DEV)
+    outs = []
+    for src in (blocks, d):
+        out = torch.empty_like(d["q"])
+        pcpp.pcpp_partial_attention_multihop(g, d["q"], d["k_fresh"], d["v_fresh"], src["k_above"], src["v_above"],
+                                             src["k_below"], src["v_below"], out, ws, wsb)
+        outs.append(out)
+    torch.cuda.synchronize()
+    assert not torch.isnan(outs[0]).any()
+    assert torch.equal(outs[0], outs[1])

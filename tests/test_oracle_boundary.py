@@ -159,3 +159,115 @@ _ORIG_MSGS = oracle.boundary_messages
 def test_planted_boundary_mistakes_are_caught(monkeypatch, name, mutant):
     monkeypatch.setattr(oracle, name, mutant)
     assert not _battery()
+
+
+# ---------------------------------------------------------------------------
+# Multi-hop messages (p > 1): every patch within reach gets the rows it reads
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("n,h,W", [(4, 3, 2), (6, 2, 3), (8, 4, 1), (3, 5, 2)])
+def test_multihop_messages_carry_the_rows_each_patch_reads(n, h, W):
+    from fractions import Fraction
+    H = n * h
+    for p in [q for q in (0.5, 1.0, 1.5, 2.3, float(n - 1)) if q <= max(1, n - 1)]:
+        r = int(Fraction(str(p)) * h // 1)
+        for i in range(n):
+            k, v = _id_tensors(H, W, n, i)
+            band = set(range(i * h * W, (i + 1) * h * W))
+            for j in range(n):
+                if j == i:
+                    continue
+                # brute force: image rows within r of patch j, every column
+                ctx = {row * W + c for row in range(H) if j * h - r <= row < (j + 1) * h + r for c in range(W)}
+                want = sorted(ctx & band)
+                msg = oracle.multihop_message(H, W, n, i, p, j, k, v)
+                if not want:
+                    assert msg is None, (n, h, p, i, j)
+                    continue
+                assert msg is not None and msg.shape[2] == len(want), (n, h, p, i, j)
+                assert (msg[0, 0, :, 0]).tolist() == [float(x) for x in want], (n, h, p, i, j)
+                assert np.array_equal(msg[:, 1], -msg[:, 0])
+                if abs(i - j) == 1 and p <= 1.0:
+                    up_msg, dn_msg = oracle.boundary_messages(H, W, n, i, p, k, v)
+                    assert np.array_equal(msg, up_msg if j < i else dn_msg)
+
+
+@pytest.mark.parametrize("n,h,W,p", [(6, 3, 2, 1.5), (8, 2, 3, 2.5), (4, 4, 2, 3.0), (5, 3, 1, 0.7)])
+def test_placed_multihop_messages_rebuild_the_stale_rows(n, h, W, p):
+    H, B, C = n * h, 2, 3
+    rng = np.random.default_rng(7)
+    prev = [(rng.standard_normal((B, h * W, C)), rng.standard_normal((B, h * W, C))) for _ in range(n)]
+    grid_k = np.concatenate([x[0] for x in prev], axis=1)
+    grid_v = np.concatenate([x[1] for x in prev], axis=1)
+    for i in range(n):
+        _, up, dn, _ = oracle.context_rows_multihop(H, n, i, p)
+        bufs = [np.full((B, up * W, C), np.nan), np.full((B, up * W, C), np.nan),
+                np.full((B, dn * W, C), np.nan), np.full((B, dn * W, C), np.nan)]
+        for j in range(n):
+            if j == i:
+                continue
+            msg = oracle.multihop_message(H, W, n, j, p, i, *prev[j])
+            assert (msg is None) == (oracle.multihop_message_rows(H, n, j, p, i)[0] == 0)
+            if msg is not None:
+                bufs = list(oracle.place_multihop_message(H, W, n, i, p, j, msg, *bufs))
+        assert np.array_equal(bufs[0], grid_k[:, (i * h - up) * W:i * h * W])
+        assert np.array_equal(bufs[1], grid_v[:, (i * h - up) * W:i * h * W])
+        assert np.array_equal(bufs[2], grid_k[:, (i + 1) * h * W:((i + 1) * h + dn) * W])
+        assert np.array_equal(bufs[3], grid_v[:, (i + 1) * h * W:((i + 1) * h + dn) * W])
+
+
+def _multihop_battery():
+    try:
+        for n, h, W in ((4, 3, 2), (6, 2, 3)):
+            test_multihop_messages_carry_the_rows_each_patch_reads(n, h, W)
+        for n, h, W, p in ((6, 3, 2, 1.5), (8, 2, 3, 2.5)):
+            test_placed_multihop_messages_rebuild_the_stale_rows(n, h, W, p)
+    except AssertionError:
+        return False
+    return True
+
+
+def test_unmodified_oracle_passes_the_multihop_battery():
+    assert _multihop_battery()
+
+
+_ORIG_HOP_ROWS = oracle.multihop_message_rows
+_ORIG_HOP_MSG = oracle.multihop_message
+_ORIG_HOP_PLACE = oracle.place_multihop_message
+
+
+def _hop_rows_one_hop_short(H, n, i, p, j):       # (|i-j|) h subtracted instead of (|i-j|-1) h
+    rows, first = _ORIG_HOP_ROWS(H, n, i, p, j)
+    h = H // n
+    return (max(0, rows - h) if abs(i - j) > 1 else rows), first
+
+
+def _hop_msg_wrong_end(H, W, n, i, p, j, k, v):    # first rows where the last are read
+    rows, first = oracle.multihop_message_rows(H, n, i, p, j)
+    if rows == 0:
+        return None
+    h = H // n
+    sl = slice((h - rows) * W, h * W) if first else slice(0, rows * W)
+    return np.stack([k[:, sl], v[:, sl]], axis=1)
+
+
+def _hop_place_unshifted(H, W, n, i, p, j, msg, ka, va, kb, vb):   # every message at the block's start
+    rows, _ = oracle.multihop_message_rows(H, n, j, p, i)
+    ka, va, kb, vb = (None if a is None else np.array(a, copy=True) for a in (ka, va, kb, vb))
+    if rows:
+        tk, tv = (ka, va) if j < i else (kb, vb)
+        tk[:, :rows * W] = msg[:, 0]
+        tv[:, :rows * W] = msg[:, 1]
+    return ka, va, kb, vb
+
+
+@pytest.mark.parametrize("name,mutant", [
+    ("multihop_message_rows", _hop_rows_one_hop_short),
+    ("multihop_message", _hop_msg_wrong_end),
+    ("place_multihop_message", _hop_place_unshifted),
+])
+def test_planted_multihop_mistakes_are_caught(monkeypatch, name, mutant):
+    import oracle.pcpp_oracle as mod
+    monkeypatch.setattr(oracle, name, mutant)
+    monkeypatch.setattr(mod, name, mutant)      # the oracle's own calls go through the module
+    assert not _multihop_battery()
