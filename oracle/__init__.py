@@ -29,3 +29,16 @@ from .pcpp_oracle import (  # noqa: F401
     place_multihop_message,
     transformer_block,
 )
+from .unet_oracle import (  # noqa: F401
+    RESNET_GN_EPS,
+    conv3x3_band,
+    edge_rows,
+    guided_noise,
+    pad_band,
+    resnet_block,
+    resnet_weight_shapes,
+    reverse_step_ddim,
+    reverse_step_ddpm,
+    scaled_linear_alphabar,
+    silu,
+)

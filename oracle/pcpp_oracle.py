@@ -19,7 +19,9 @@ notes):
       the paper's patch i is index i-1 here.
   R2  the number of context rows taken from a neighbour is
       r = min(h, floor(p*h + 1e-9)) when p*h is not a whole number.
-  R3  p must lie in [0, 1] (p > 1, multi-hop context, is not handled).
+  R3  p lies in [0, 1] for the neighbour form; the multi-hop form
+      (context_rows_multihop) takes p up to max(1, n - 1), r image rows past
+      each band edge, clipped to the image.
   R4  the exchanged tensors are the neighbours' key and value projections
       (Sec. 3.3: K and V are extended with stale keys and values), never Q.
   R6  the local patch's rows are always fresh; its own stale copy is unused.

@@ -1,0 +1,187 @@
+"""CPU float64 oracle for the rest of one per-band U-Net step: the 3x3
+convolution with its halo rows, the SDXL-shaped ResNet block around two of
+them, and the guided reverse-diffusion update.
+
+TEST INFRASTRUCTURE ONLY, like the rest of this package: only the test
+suite, the smoke check and the benchmark's CPU-baseline leg may use it, and
+it shares no code with the GPU library.
+
+Citations are to arXiv 2412.02962: Sec. 3.1 (classifier-free guidance,
+Eq. 2; the reverse step, Eq. 3 and Eq. 4), Sec. 3.3 (the U-Net's layers are
+attention, convolution and GroupNorm; convolutions keep DistriFusion's
+exchange of boundary pixels), Sec. 4 (SDXL with a 50-step DDIM sampler and
+guidance scale 5).
+
+Readings (also in the design notes):
+  R19 a 3x3 convolution of band i reads one row above and one row below the
+      band: the neighbours' boundary rows of the convolution input as they
+      were exchanged at the previous step (stale), zeros at the image's top
+      and bottom and at its left and right edges.
+  R20 ResNet block (SDXL's): GroupNorm (32 groups, eps 1e-5) -> SiLU ->
+      conv 3x3 -> + linear(SiLU(time embedding)) per channel -> GroupNorm ->
+      SiLU -> conv 3x3 -> + shortcut (the input, or a 1x1 convolution of it
+      when the channel count changes).
+  R21 the reverse step is Eq. 3 and Eq. 4 with beta_t = 1 - alpha_t; the
+      DDIM sampler the experiments use is Song et al.'s deterministic update
+      (eta = 0).
+"""
+
+from __future__ import annotations
+
+import math
+from typing import Dict, Optional, Tuple
+
+import numpy as np
+
+from .pcpp_oracle import group_norm, group_norm_synchronized, linear
+
+
+def silu(x: np.ndarray) -> np.ndarray:
+    """SiLU(x) = x * sigmoid(x)."""
+    return x / (1.0 + np.exp(-x))
+
+
+# ---------------------------------------------------------------------------
+# 3x3 convolution of one row band (Sec. 3.3: boundary pixels from neighbours)
+# ---------------------------------------------------------------------------
+
+def pad_band(x: np.ndarray, W: int, halo_up: Optional[np.ndarray],
+             halo_dn: Optional[np.ndarray]) -> np.ndarray:
+    """The band's input x [B, h*W, C] framed for a 3x3 convolution:
+    [B, h+2, W+2, C] with the row above (halo_up [B, W, C], or zeros) on
+    top, the row below (halo_dn, or zeros) at the bottom and zero columns at
+    both sides (R19)."""
+    B, N, C = x.shape
+    h = N // W
+    out = np.zeros((B, h + 2, W + 2, C))
+    out[:, 1:h + 1, 1:W + 1] = x.reshape(B, h, W, C)
+    if halo_up is not None:
+        out[:, 0, 1:W + 1] = halo_up
+    if halo_dn is not None:
+        out[:, h + 1, 1:W + 1] = halo_dn
+    return out
+
+
+def conv3x3_band(x: np.ndarray, W: int, w: np.ndarray, b: Optional[np.ndarray],
+                 halo_up: Optional[np.ndarray], halo_dn: Optional[np.ndarray]) -> np.ndarray:
+    """out[b, y, x, o] = bias[o] + sum over taps (ky, kx) and channels c of
+    w[o, ky, kx, c] * in[b, y + ky - 1, x + kx - 1, c], `in` being the framed
+    band (pad_band).  w is [C_out, 3, 3, C_in] (tap-major, channel-minor).
+    Returns [B, h*W, C_out]."""
+    B, N, C = x.shape
+    h = N // W
+    xp = pad_band(x, W, halo_up, halo_dn)
+    out = np.zeros((B, h, W, w.shape[0]))
+    for ky in range(3):
+        for kx in range(3):
+            out += xp[:, ky:ky + h, kx:kx + W, :] @ w[:, ky, kx, :].T
+    if b is not None:
+        out += b
+    return out.reshape(B, N, w.shape[0])
+
+
+def edge_rows(a: np.ndarray, W: int) -> np.ndarray:
+    """What a band exports for its neighbours' next 3x3 convolution: its
+    first and last rows of the convolution input a [B, h*W, C], as
+    [B, 2, W, C] (row 0, then row h-1)."""
+    B, N, C = a.shape
+    h = N // W
+    g = a.reshape(B, h, W, C)
+    return np.stack([g[:, 0], g[:, h - 1]], axis=1)
+
+
+# ---------------------------------------------------------------------------
+# ResNet block (R20)
+# ---------------------------------------------------------------------------
+
+RESNET_GN_EPS = 1e-5
+
+
+def resnet_block(W: int, wts: Dict[str, np.ndarray], x: np.ndarray, temb: np.ndarray,
+                 edges1_up: Optional[np.ndarray], edges1_dn: Optional[np.ndarray],
+                 edges2_up: Optional[np.ndarray], edges2_dn: Optional[np.ndarray],
+                 groups: int = 32, i: int = 0,
+                 gn1_band_stats: Optional[np.ndarray] = None,
+                 gn2_band_stats: Optional[np.ndarray] = None):
+    """One SDXL-shaped ResNet block on a row band, float64.
+
+    x [B, h*W, C_in]; temb [B, T] (the step's time embedding).  edges*_up is
+    the band above's export of the convolution input (edge_rows, [B, 2, W, C],
+    its row 1 = its last row is read), edges*_dn the band below's (its row 0
+    is read); None at the image's edge.  With gn*_band_stats [n, B, G, 3] the
+    GroupNorm is the synchronized one (every band's statistics, this band's
+    own, index i, in its place).
+    Returns (y [B, h*W, C_out], edges1, edges2): the output and this band's
+    own exports of the two convolution inputs.
+    """
+    def gn(t, gamma, beta, stats):
+        if stats is None:
+            return group_norm(t, groups, gamma, beta, eps=RESNET_GN_EPS)
+        return group_norm_synchronized(t, groups, gamma, beta, stats, i, eps=RESNET_GN_EPS)
+
+    a1 = silu(gn(x, wts["gn1_gamma"], wts["gn1_beta"], gn1_band_stats))
+    hid = conv3x3_band(a1, W, wts["conv1_w"], wts["conv1_b"],
+                       None if edges1_up is None else edges1_up[:, 1],
+                       None if edges1_dn is None else edges1_dn[:, 0])
+    hid = hid + linear(silu(temb), wts["temb_w"], wts["temb_b"])[:, None, :]
+    a2 = silu(gn(hid, wts["gn2_gamma"], wts["gn2_beta"], gn2_band_stats))
+    hid = conv3x3_band(a2, W, wts["conv2_w"], wts["conv2_b"],
+                       None if edges2_up is None else edges2_up[:, 1],
+                       None if edges2_dn is None else edges2_dn[:, 0])
+    skip = x if "skip_w" not in wts else linear(x, wts["skip_w"], wts["skip_b"])
+    return skip + hid, edge_rows(a1, W), edge_rows(a2, W)
+
+
+# ---------------------------------------------------------------------------
+# Guided reverse step (Eq. 2, Eq. 3, Eq. 4; R21)
+# ---------------------------------------------------------------------------
+
+def guided_noise(eps_uncond: np.ndarray, eps_cond: np.ndarray, s: float) -> np.ndarray:
+    """Eq. 2: the unconditional prediction plus s times the difference of the
+    conditional and the unconditional one."""
+    return eps_uncond + s * (eps_cond - eps_uncond)
+
+
+def reverse_step_ddpm(x_t: np.ndarray, eps_uncond: np.ndarray, eps_cond: np.ndarray, s: float,
+                      alpha_t: float, alphabar_t: float, sigma_t: float,
+                      z: Optional[np.ndarray]) -> np.ndarray:
+    """Eq. 3 then Eq. 4: mu = (x_t - beta_t / sqrt(1 - alphabar_t) * eps) /
+    sqrt(alpha_t) with beta_t = 1 - alpha_t, then x_{t-1} = mu + sigma_t z."""
+    e = guided_noise(eps_uncond, eps_cond, s)
+    mu = (x_t - (1.0 - alpha_t) / math.sqrt(1.0 - alphabar_t) * e) / math.sqrt(alpha_t)
+    return mu if z is None else mu + sigma_t * z
+
+
+def reverse_step_ddim(x_t: np.ndarray, eps_uncond: np.ndarray, eps_cond: np.ndarray, s: float,
+                      alphabar_t: float, alphabar_prev: float) -> np.ndarray:
+    """Deterministic DDIM (Song et al., eta = 0) with the guided noise of
+    Eq. 2: the predicted clean sample x0 = (x_t - sqrt(1 - alphabar_t) eps) /
+    sqrt(alphabar_t), re-noised to the previous level: sqrt(alphabar_prev) x0
+    + sqrt(1 - alphabar_prev) eps."""
+    e = guided_noise(eps_uncond, eps_cond, s)
+    x0 = (x_t - math.sqrt(1.0 - alphabar_t) * e) / math.sqrt(alphabar_t)
+    return math.sqrt(alphabar_prev) * x0 + math.sqrt(1.0 - alphabar_prev) * e
+
+
+def scaled_linear_alphabar(n_train: int = 1000, beta_start: float = 0.00085,
+                           beta_end: float = 0.012) -> np.ndarray:
+    """SDXL's training noise schedule: betas on a line in sqrt space from
+    beta_start to beta_end, alphabar_t = prod_{s <= t} (1 - beta_s)."""
+    betas = np.linspace(math.sqrt(beta_start), math.sqrt(beta_end), n_train) ** 2
+    return np.cumprod(1.0 - betas)
+
+
+def resnet_weight_shapes(c_in: int, c_out: int, temb_dim: int) -> Dict[str, Tuple[int, ...]]:
+    """Shapes of the ResNet block's weights, in the layout the oracle and the
+    library use: linears [out, in], 3x3 kernels [C_out, 3, 3, C_in]."""
+    s = {
+        "gn1_gamma": (c_in,), "gn1_beta": (c_in,),
+        "conv1_w": (c_out, 3, 3, c_in), "conv1_b": (c_out,),
+        "temb_w": (c_out, temb_dim), "temb_b": (c_out,),
+        "gn2_gamma": (c_out,), "gn2_beta": (c_out,),
+        "conv2_w": (c_out, 3, 3, c_out), "conv2_b": (c_out,),
+    }
+    if c_in != c_out:
+        s["skip_w"] = (c_out, c_in)
+        s["skip_b"] = (c_out,)
+    return s

@@ -1,0 +1,250 @@
+"""Pins of the oracle's per-band U-Net step pieces (unet_oracle), CPU only.
+
+  U1  conv3x3_band of every band, given the true neighbour rows as its halo,
+      reproduces torch's conv2d (padding 1, NCHW) of the whole image
+  U2  with n = 1 the ResNet block equals a composition of torch's
+      group_norm, silu, conv2d and linear on the whole image (NCHW)
+  U3  every band's ResNet block, given the true neighbour edge rows and the
+      true per-band statistics (synchronized GroupNorm), reproduces the
+      whole image's block, and its edge exports are the whole image's rows
+  U4  Eq. 3 with the true noise equals the DDPM posterior mean written from
+      x0 and x_t (a different closed form); DDIM with the true noise moves
+      x_t exactly to the previous noise level; Eq. 2 at s = 0 / 1 gives the
+      unconditional / conditional prediction
+  U5  planted mistakes (tap order, halo sides, temb SiLU, shortcut, Eq. 3
+      coefficient, DDIM re-noising) fail the pins
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+import oracle.unet_oracle as uo
+
+
+def _torch_conv(img, w, b):
+    """img [B, H, W, C] -> [B, H, W, C_out] by torch conv2d (padding 1); w [Co, 3, 3, Ci]."""
+    x = torch.from_numpy(img).permute(0, 3, 1, 2)
+    k = torch.from_numpy(np.ascontiguousarray(w.transpose(0, 3, 1, 2)))
+    y = F.conv2d(x, k, None if b is None else torch.from_numpy(b), padding=1)
+    return y.permute(0, 2, 3, 1).numpy()
+
+
+def _bands(img, n):
+    B, H, W, C = img.shape
+    h = H // n
+    return [img[:, j * h:(j + 1) * h].reshape(B, h * W, C) for j in range(n)]
+
+
+@pytest.mark.parametrize("B,H,W,ci,co,n", [(1, 12, 7, 3, 5, 3), (2, 8, 5, 4, 4, 4), (1, 6, 9, 2, 3, 1),
+                                           (1, 10, 4, 5, 2, 5)])
+def test_u1_band_conv_with_true_halos_is_the_whole_image_conv(B, H, W, ci, co, n):
+    rng = np.random.default_rng(1)
+    img = rng.standard_normal((B, H, W, ci))
+    w = rng.standard_normal((co, 3, 3, ci))
+    b = rng.standard_normal(co)
+    want = _torch_conv(img, w, b)
+    h = H // n
+    for i, xb in enumerate(_bands(img, n)):
+        up = img[:, i * h - 1] if i > 0 else None
+        dn = img[:, (i + 1) * h] if i < n - 1 else None
+        got = uo.conv3x3_band(xb, W, w, b, up, dn)
+        assert np.allclose(got.reshape(B, h, W, co), want[:, i * h:(i + 1) * h], rtol=1e-12, atol=1e-12), i
+
+
+def _wts(ci, co, T, seed=2):
+    rng = np.random.default_rng(seed)
+    out = {}
+    for k, shp in uo.resnet_weight_shapes(ci, co, T).items():
+        if k.endswith("gamma"):
+            out[k] = 1.0 + 0.1 * rng.standard_normal(shp)
+        elif k.endswith("_w"):
+            out[k] = rng.standard_normal(shp) / math.sqrt(np.prod(shp[1:]))
+        else:
+            out[k] = 0.1 * rng.standard_normal(shp)
+    return out
+
+
+def _torch_resnet(img, temb, wts, groups):
+    """Whole image [B, H, W, Ci] -> [B, H, W, Co] by torch ops in NCHW."""
+    x = torch.from_numpy(img).permute(0, 3, 1, 2)
+    t = {k: torch.from_numpy(np.ascontiguousarray(v)) for k, v in wts.items()}
+    k1 = t["conv1_w"].permute(0, 3, 1, 2)
+    k2 = t["conv2_w"].permute(0, 3, 1, 2)
+    a1 = F.silu(F.group_norm(x, groups, t["gn1_gamma"], t["gn1_beta"], eps=1e-5))
+    hid = F.conv2d(a1, k1, t["conv1_b"], padding=1)
+    hid = hid + F.linear(F.silu(torch.from_numpy(temb)), t["temb_w"], t["temb_b"])[:, :, None, None]
+    a2 = F.silu(F.group_norm(hid, groups, t["gn2_gamma"], t["gn2_beta"], eps=1e-5))
+    hid = F.conv2d(a2, k2, t["conv2_b"], padding=1)
+    skip = x if "skip_w" not in t else F.conv2d(x, t["skip_w"][:, :, None, None], t["skip_b"])
+    return (skip + hid).permute(0, 2, 3, 1).numpy(), a1.permute(0, 2, 3, 1).numpy(), a2.permute(0, 2, 3, 1).numpy()
+
+
+@pytest.mark.parametrize("ci,co", [(8, 8), (8, 12)])
+def test_u2_whole_image_resnet_is_torchs(ci, co):
+    B, H, W, T, G = 2, 6, 5, 7, 4
+    rng = np.random.default_rng(3)
+    img = rng.standard_normal((B, H, W, ci))
+    temb = rng.standard_normal((B, T))
+    wts = _wts(ci, co, T)
+    want, _, _ = _torch_resnet(img, temb, wts, G)
+    got, e1, e2 = uo.resnet_block(W, wts, img.reshape(B, H * W, ci), temb, None, None, None, None, groups=G)
+    assert np.allclose(got.reshape(B, H, W, co), want, rtol=1e-11, atol=1e-11)
+    assert e1.shape == (B, 2, W, ci) and e2.shape == (B, 2, W, co)
+
+
+@pytest.mark.parametrize("n,ci,co", [(4, 8, 8), (3, 8, 12), (2, 4, 4)])
+def test_u3_bands_with_true_edges_and_statistics_rebuild_the_whole_block(n, ci, co):
+    B, h, W, T, G = 2, 3, 5, 6, 4
+    H = n * h
+    rng = np.random.default_rng(4)
+    img = rng.standard_normal((B, H, W, ci))
+    temb = rng.standard_normal((B, T))
+    wts = _wts(ci, co, T)
+    want, a1, a2 = _torch_resnet(img, temb, wts, G)
+    # true per-band statistics of both GroupNorm inputs (x, and conv1's output)
+    xs = _bands(img, n)
+    st1 = np.stack([oracle.group_stats(xb, G) for xb in xs])
+    hid_img = uo.conv3x3_band(a1.reshape(B, H * W, ci), W, wts["conv1_w"], wts["conv1_b"], None, None)
+    hid_img = hid_img + oracle.linear(uo.silu(temb), wts["temb_w"], wts["temb_b"])[:, None, :]
+    st2 = np.stack([oracle.group_stats(hb, G) for hb in _bands(hid_img.reshape(B, H, W, co), n)])
+    edges1 = [uo.edge_rows(b_, W) for b_ in _bands(a1, n)]
+    edges2 = [uo.edge_rows(b_, W) for b_ in _bands(a2, n)]
+    for i in range(n):
+        y, e1, e2 = uo.resnet_block(W, wts, xs[i], temb,
+                                    edges1[i - 1] if i > 0 else None, edges1[i + 1] if i < n - 1 else None,
+                                    edges2[i - 1] if i > 0 else None, edges2[i + 1] if i < n - 1 else None,
+                                    groups=G, i=i, gn1_band_stats=st1, gn2_band_stats=st2)
+        assert np.allclose(y.reshape(B, h, W, co), want[:, i * h:(i + 1) * h], rtol=1e-10, atol=1e-10), i
+        assert np.allclose(e1[:, 0], a1[:, i * h]) and np.allclose(e1[:, 1], a1[:, (i + 1) * h - 1])
+        assert np.allclose(e2[:, 0], a2[:, i * h]) and np.allclose(e2[:, 1], a2[:, (i + 1) * h - 1])
+
+
+def test_u4_reverse_steps_against_closed_forms():
+    rng = np.random.default_rng(5)
+    x0 = rng.standard_normal((2, 24, 4))
+    eps = rng.standard_normal((2, 24, 4))
+    other = rng.standard_normal((2, 24, 4))
+    abar = oracle.scaled_linear_alphabar()
+    for t in (999, 500, 20, 1):
+        a_t = abar[t] / abar[t - 1]
+        x_t = math.sqrt(abar[t]) * x0 + math.sqrt(1 - abar[t]) * eps
+        # Eq. 2 at s = 1 is the conditional prediction: here the true noise
+        mu = uo.reverse_step_ddpm(x_t, other, eps, 1.0, a_t, abar[t], 0.0, None)
+        beta = 1 - a_t
+        post = (math.sqrt(abar[t - 1]) * beta / (1 - abar[t])) * x0 + \
+               (math.sqrt(a_t) * (1 - abar[t - 1]) / (1 - abar[t])) * x_t
+        assert np.allclose(mu, post, rtol=1e-9, atol=1e-9), t
+        z = rng.standard_normal(x0.shape)
+        assert np.allclose(uo.reverse_step_ddpm(x_t, other, eps, 1.0, a_t, abar[t], 0.3, z), post + 0.3 * z,
+                           rtol=1e-9, atol=1e-9)
+        # s = 0: the unconditional prediction decides
+        assert np.allclose(uo.reverse_step_ddpm(x_t, eps, other, 0.0, a_t, abar[t], 0.0, None), post,
+                           rtol=1e-9, atol=1e-9)
+        for prev in (t - 1, max(t - 20, 0)):
+            got = uo.reverse_step_ddim(x_t, other, eps, 1.0, abar[t], abar[prev])
+            want = math.sqrt(abar[prev]) * x0 + math.sqrt(1 - abar[prev]) * eps
+            assert np.allclose(got, want, rtol=1e-9, atol=1e-9), (t, prev)
+        assert np.allclose(uo.reverse_step_ddim(x_t, eps, other, 0.0, abar[t], abar[t]), x_t, rtol=1e-12, atol=1e-12)
+    # guidance at s = 5 (the scale the paper uses) is an affine combination
+    e = uo.guided_noise(other, eps, 5.0)
+    assert np.allclose(e, -4.0 * other + 5.0 * eps)
+
+
+def test_u4_scaled_linear_schedule_endpoints():
+    abar = oracle.scaled_linear_alphabar(1000, 0.00085, 0.012)
+    betas = 1 - abar / np.concatenate([[1.0], abar[:-1]])
+    assert abs(betas[0] - 0.00085) < 1e-15 and abs(betas[-1] - 0.012) < 1e-12
+    d = np.diff(np.sqrt(betas))
+    assert np.allclose(d, d[0], rtol=1e-9) and (np.diff(abar) < 0).all()
+
+
+# ---------------------------------------------------------------------------
+# U5 planted mistakes
+# ---------------------------------------------------------------------------
+
+def _battery():
+    try:
+        test_u1_band_conv_with_true_halos_is_the_whole_image_conv(1, 12, 7, 3, 5, 3)
+        test_u2_whole_image_resnet_is_torchs(8, 12)
+        test_u2_whole_image_resnet_is_torchs(8, 8)
+        test_u3_bands_with_true_edges_and_statistics_rebuild_the_whole_block(3, 8, 12)
+        test_u4_reverse_steps_against_closed_forms()
+    except AssertionError:
+        return False
+    return True
+
+
+def test_u5_unmodified_oracle_passes():
+    assert _battery()
+
+
+_ORIG = {k: getattr(uo, k) for k in ("conv3x3_band", "pad_band", "silu", "linear", "reverse_step_ddpm",
+                                      "reverse_step_ddim", "edge_rows")}
+
+
+def _conv_taps_transposed(x, W, w, b, up, dn):
+    return _ORIG["conv3x3_band"](x, W, np.ascontiguousarray(w.transpose(0, 2, 1, 3)), b, up, dn)
+
+
+def _pad_sides_swapped(x, W, up, dn):
+    return _ORIG["pad_band"](x, W, dn, up)
+
+
+def _edges_reversed(a, W):
+    return _ORIG["edge_rows"](a, W)[:, ::-1]
+
+
+def _ddpm_beta_over_alphabar(x_t, eu, ec, s, a_t, abar_t, sig, z):
+    e = uo.guided_noise(eu, ec, s)
+    mu = (x_t - (1.0 - a_t) / (1.0 - abar_t) * e) / math.sqrt(a_t)   # sqrt dropped
+    return mu if z is None else mu + sig * z
+
+
+def _ddim_no_renoise(x_t, eu, ec, s, abar_t, abar_prev):
+    e = uo.guided_noise(eu, ec, s)
+    return math.sqrt(abar_prev) * (x_t - math.sqrt(1.0 - abar_t) * e) / math.sqrt(abar_t)
+
+
+def _resnet_shortcut_of_normed(W, wts, x, temb, *a, **k):
+    y, e1, e2 = _ORIG_RESNET(W, wts, x, temb, *a, **k)
+    if "skip_w" in wts:
+        return y, e1, e2
+    xn = oracle.group_norm(x, k.get("groups", 32), wts["gn1_gamma"], wts["gn1_beta"], eps=1e-5)
+    return y - x + xn, e1, e2
+
+
+_ORIG_RESNET = uo.resnet_block
+
+
+def _resnet_temb_without_silu(W, wts, x, temb, *a, **k):
+    # silu(temb) replaced by temb: enter through the module's silu only for the temb call
+    calls = {"n": 0}
+    real = _ORIG["silu"]
+
+    def silu_skip_second(v):
+        calls["n"] += 1
+        return v if calls["n"] == 2 else real(v)
+    uo.silu = silu_skip_second
+    try:
+        return _ORIG_RESNET(W, wts, x, temb, *a, **k)
+    finally:
+        uo.silu = real
+
+
+@pytest.mark.parametrize("name,mutant", [
+    ("conv3x3_band", _conv_taps_transposed),
+    ("pad_band", _pad_sides_swapped),
+    ("edge_rows", _edges_reversed),
+    ("reverse_step_ddpm", _ddpm_beta_over_alphabar),
+    ("reverse_step_ddim", _ddim_no_renoise),
+    ("resnet_block", _resnet_shortcut_of_normed),
+    ("resnet_block", _resnet_temb_without_silu),
+])
+def test_u5_planted_mistakes_are_caught(monkeypatch, name, mutant):
+    monkeypatch.setattr(uo, name, mutant)
+    assert not _battery()
