@@ -370,6 +370,117 @@ int pcpp_unpack_multihop(const pcpp_geom_t* g, int32_t peer,
                          const void* recv, void* k_above, void* v_above,
                          void* k_below, void* v_below, void* stream);
 
+/*
+ * SDXL-shaped ResNet block on one row band: the U-Net's convolution layers
+ * (Sec. 3.3 keeps their exchange of boundary pixels: a band's 3x3
+ * convolution reads its neighbours' edge rows of the convolution input as
+ * exchanged at the previous step).
+ *   a1 = SiLU(GroupNorm(x));           h1 = conv3x3(a1) + conv1_b + tb
+ *   tb = SiLU(temb) temb_w^T + temb_b  (per image, added to every token)
+ *   a2 = SiLU(GroupNorm(h1));          y  = conv3x3(a2) + conv2_b + s
+ *   s  = x (c_in == c_out), else x skip_w^T + skip_b (a 1x1 convolution)
+ * The convolutions pad with zeros at the image's edges (left, right, and
+ * above band 0 / below band n-1) and read the neighbours' edge rows
+ * elsewhere.  bf16 storage, float32 accumulation; a1, h1 and a2 are stored
+ * in bf16, s in float32.
+ */
+typedef struct {
+    int32_t H, W;          /* the layer's token grid                         */
+    int32_t n_patches;     /* n, H % n == 0                                  */
+    int32_t patch_idx;     /* band i, 0-based                                */
+    int32_t c_in, c_out;   /* channels, multiples of 64, <= 2048             */
+    int32_t temb_dim;      /* time-embedding width T, multiple of 8          */
+    int32_t groups;        /* GroupNorm groups, dividing c_in and c_out, <= 256 */
+    int32_t batch;         /* images B (the guidance branches), <= 65535     */
+    float eps;             /* GroupNorm epsilon (SDXL: 1e-5)                 */
+    int32_t reserved;      /* must be 0                                      */
+} pcpp_resnet_geom_t;
+
+/* Device pointers, bf16, 16-byte aligned.  3x3 kernels are
+ * [c_out][3][3][c_in_of_that_conv] (tap-major, channel-minor: element
+ * (o, ky, kx, c) at ((o * 3 + ky) * 3 + kx) * C + c), linears [out][in]. */
+typedef struct {
+    const void* gn1_gamma; const void* gn1_beta;   /* [c_in]                 */
+    const void* conv1_w;   const void* conv1_b;    /* [c_out][3][3][c_in], [c_out] */
+    const void* temb_w;    const void* temb_b;     /* [c_out][T], [c_out]    */
+    const void* gn2_gamma; const void* gn2_beta;   /* [c_out]                */
+    const void* conv2_w;   const void* conv2_b;    /* [c_out][3][3][c_out], [c_out] */
+    const void* skip_w;    const void* skip_b;     /* [c_out][c_in], [c_out]; used (and
+                                                      required) only when c_in != c_out */
+} pcpp_resnet_weights_t;
+
+/* Bytes of device workspace pcpp_resnet_block needs (0 if g is invalid).
+ * The workspace needs no clearing; nothing in it survives a call. */
+size_t pcpp_resnet_block_workspace_size(const pcpp_resnet_geom_t* g);
+
+/*
+ *   x            [B, h*W, c_in] bf16 band tokens (h = H / n)
+ *   temb         [B, T] bf16 time embedding of the step
+ *   edges1_up    the band above's edges1_out of the previous step
+ *                [B, 2, W, c_in] (its row 1, the band's last row, is read);
+ *                needed when i > 0, else ignored
+ *   edges1_dn    the band below's edges1_out (its row 0 is read); needed
+ *                when i < n-1
+ *   edges2_up/dn the same for the second convolution's input, [B, 2, W, c_out]
+ *   gn1_bands,   NULL: GroupNorm statistics over the band's own tokens.
+ *   gn2_bands    Else the synchronized GroupNorm (Sec. 3.3) as in
+ *                pcpp_transformer_block_sync_gn: [n][B][groups] x (count,
+ *                mean, M2) float32 of every band, entry i replaced by this
+ *                band's own; 4-byte aligned
+ *   gn1_own,     NULL, or [B][groups] x (count, mean, M2) float32 of this
+ *   gn2_own      band's two GroupNorm inputs, for the others' next step
+ *   y            [B, h*W, c_out] bf16 output
+ *   edges1_out,  NULL, or this band's first and last rows of a1 / a2,
+ *   edges2_out   [B, 2, W, c] bf16: what its neighbours read at the next step
+ * Errors: PCPP_EINVAL (geometry, NULL or misaligned pointers, 16-byte
+ * alignment for the bf16 tensors), PCPP_ENOTSUP (channels not multiples of
+ * 64 or above 2048, groups above 256), PCPP_EWORKSPACE.  Asynchronous.
+ */
+int pcpp_resnet_block(const pcpp_resnet_geom_t* g, const pcpp_resnet_weights_t* w,
+                      const void* x, const void* temb,
+                      const void* edges1_up, const void* edges1_dn,
+                      const void* edges2_up, const void* edges2_dn,
+                      const float* gn1_bands, float* gn1_own,
+                      const float* gn2_bands, float* gn2_own,
+                      void* y, void* edges1_out, void* edges2_out,
+                      void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * The update of a band's latent at the end of a step (Sec. 3.1): the two
+ * guidance branches' noise predictions are combined by classifier-free
+ * guidance (Eq. 2), e = eps_u + s (eps_c - eps_u), and then
+ *   PCPP_STEP_DDPM: Eq. 3 and Eq. 4,
+ *     x_{t-1} = (x_t - (1 - alpha_t) / sqrt(1 - alphabar_t) e) / sqrt(alpha_t)
+ *               + sigma_t z          (z may be NULL: no noise term)
+ *   PCPP_STEP_DDIM: the deterministic DDIM update (the paper's sampler,
+ *     Sec. 4): x_{t-1} = sqrt(alphabar_prev) x0 + sqrt(1 - alphabar_prev) e
+ *     with x0 = (x_t - sqrt(1 - alphabar_t) e) / sqrt(alphabar_t); z must be NULL.
+ * The two coefficients of x_t and e are computed on the host in double
+ * precision, the update in float32 on the device.
+ */
+#define PCPP_STEP_DDPM 0
+#define PCPP_STEP_DDIM 1
+
+typedef struct {
+    float guidance;       /* s (the paper uses 5), finite                  */
+    float alpha_t;        /* DDPM: (0, 1]                                   */
+    float alphabar_t;     /* DDPM: (0, 1); DDIM: (0, 1]                     */
+    float sigma_t;        /* DDPM: scale of z                               */
+    float alphabar_prev;  /* DDIM: (0, 1], the level stepped to             */
+    int32_t mode;         /* PCPP_STEP_DDPM or PCPP_STEP_DDIM               */
+    int32_t reserved;     /* must be 0                                      */
+} pcpp_step_params_t;
+
+/*
+ * x_t, eps_uncond, eps_cond, z, x_prev: n float32 values each (any layout,
+ * the same for all), device pointers; x_prev may be x_t (in place), no
+ * other overlap.  No alignment is required.  PCPP_EINVAL for invalid
+ * parameters or NULL pointers (n > 0).  Asynchronous on `stream`.
+ */
+int pcpp_guided_step(const pcpp_step_params_t* sp, int64_t n, const float* x_t,
+                     const float* eps_uncond, const float* eps_cond,
+                     const float* z, float* x_prev, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

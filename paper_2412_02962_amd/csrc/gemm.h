@@ -25,6 +25,15 @@ struct GemmParams {
     int64_t ldo;          // row stride of each output segment
     int32_t out_f32;
     void* out_bf16;       // optional bf16 copy of the output [M, N] (row stride ldo), or null
+    // Implicit 3x3 convolution when conv_W > 0 (bf16 a, pipelined kernel
+    // only): a is the framed band [B][conv_rows + 2][conv_W + 2][K / 9] (lda
+    // unused), token m is (b, y, x) of [B][conv_rows][conv_W], and
+    // K = 9 * C_in with k = (3 ky + kx) * C_in + c; C_in % 64 == 0.
+    int32_t conv_W = 0, conv_rows = 0;
+    // Optional per-image float bias added to output n of token m:
+    // bias2[(m / bias2_rows) * N + n] (16-byte aligned), or null.
+    const float* bias2 = nullptr;
+    int32_t bias2_rows = 1;
 };
 
 bool gemm_shape_ok(const GemmParams& p);
@@ -45,6 +54,11 @@ struct GroupNormParams {
     const float* bands;
     int32_t n_bands, band;
     float* own_out;       // [B][G] x (count, mean, M2) of this band, or null
+    int32_t silu = 0;     // 1: y = SiLU(normalized value)
+    // pad_W > 0: y is the framed band [B][N / pad_W + 2][pad_W + 2][C] of a
+    // 3x3 convolution and token t = (row, col) of image b is written at
+    // (row + 1, col + 1); the frame itself is not written.
+    int32_t pad_W = 0;
 };
 size_t group_norm_ws_bytes(int B, int G, int N);
 // C % 8 == 0, C <= 2048, 1 <= G <= 256 divides C.

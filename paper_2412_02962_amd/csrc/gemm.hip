@@ -256,7 +256,7 @@ __device__ __forceinline__ u32x4 lds_b128(uint32_t a) {
     return r;
 }
 
-template <int BM, int BN, int NS, bool GEGLU>
+template <int BM, int BN, int NS, bool GEGLU, bool CONV>
 __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
     constexpr int WMB = BM / 64;                      // 32-token blocks per wavefront
     constexpr int WNB = BN / 64;                      // 32-row W blocks per wavefront
@@ -284,13 +284,26 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
     // chunk (lane & 7) ^ swizzle), k offset added per k-tile.
     const char* xsrc[XP];
     const char* wsrc[WP];
+    const int cin = CONV ? p.K / 9 : 0;
 #pragma unroll
     for (int i = 0; i < XP; ++i) {
         const int r = 8 * (wave + 4 * i) + (lane >> 3);
         const int m = min(m0 + r, p.M - 1);
         const int c = (lane & 7) ^ ((r >> 1) & 7);
-        xsrc[i] = (const char*)p.a + ((int64_t)m * p.lda + 8 * c) * 2;
+        int64_t row = (int64_t)m * p.lda;
+        if constexpr (CONV) {  // the tap (0, 0) of token (b, y, x) sits at framed (y, x)
+            const int per = p.conv_rows * p.conv_W;
+            const int b = m / per, rem = m - b * per;
+            const int y = rem / p.conv_W, x = rem - y * p.conv_W;
+            row = ((int64_t)(b * (p.conv_rows + 2) + y) * (p.conv_W + 2) + x) * cin;
+        }
+        xsrc[i] = (const char*)p.a + (row + 8 * c) * 2;
     }
+    // Convolution: the k-tiles are issued in order, so the X offset of the
+    // next one advances by 64 channels, then to the next tap (one token
+    // right, or to the next framed row's first tap column).
+    int iss_cb = 0, iss_kx = 0;
+    int64_t iss_xoff = 0;
 #pragma unroll
     for (int i = 0; i < WP; ++i) {
         const int r = 8 * (wave + 4 * i) + (lane >> 3);
@@ -301,9 +314,23 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
     auto issue = [&](int kt, int stage) {
         char* st = lds + stage * STAGE;
         const int koff = kt * DBK * 2;
+        const int64_t xoff = CONV ? iss_xoff : koff;
+        if constexpr (CONV) {
+            if (++iss_cb * DBK == cin) {
+                iss_cb = 0;
+                if (++iss_kx == 3) {
+                    iss_kx = 0;
+                    iss_xoff += ((int64_t)(p.conv_W + 2) * cin - 2 * cin - (cin - DBK)) * 2;
+                } else {
+                    iss_xoff += DBK * 2;
+                }
+            } else {
+                iss_xoff += DBK * 2;
+            }
+        }
 #pragma unroll
         for (int i = 0; i < XP; ++i)
-            __builtin_amdgcn_global_load_lds((gvoid)(xsrc[i] + koff), (lvoid)(st + (wave + 4 * i) * 1024), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds((gvoid)(xsrc[i] + xoff), (lvoid)(st + (wave + 4 * i) * 1024), 16, 0, 0);
 #pragma unroll
         for (int i = 0; i < WP; ++i)
             __builtin_amdgcn_global_load_lds((gvoid)(wsrc[i] + koff), (lvoid)(st + BM * 128 + (wave + 4 * i) * 1024),
@@ -429,6 +456,11 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
                         for (int e = 0; e < 4; ++e) rv[e] = bf16_to_f32(rb[e]);
                     }
                 }
+                if (p.bias2 != nullptr) {
+                    const f32x4 b2 = *(const f32x4*)(p.bias2 + (int64_t)(m / p.bias2_rows) * p.N + n);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) rv[e] += b2[e];
+                }
                 res_v[i][j][c] = rv;
             }
         }
@@ -473,7 +505,10 @@ template <int BM, int BN, int NS, bool GEGLU>
 hipError_t launch_dma(const GemmParams& p, hipStream_t s) {
     const int bn_out = GEGLU ? BN / 2 : BN;
     dim3 grid((p.M + BM - 1) / BM, p.N / bn_out);
-    gemm_dma_kernel<BM, BN, NS, GEGLU><<<grid, 256, 0, s>>>(p);
+    if (!GEGLU && p.conv_W > 0)
+        gemm_dma_kernel<BM, BN, NS, GEGLU, true><<<grid, 256, 0, s>>>(p);
+    else
+        gemm_dma_kernel<BM, BN, NS, GEGLU, false><<<grid, 256, 0, s>>>(p);
     return hipGetLastError();
 }
 
@@ -493,11 +528,16 @@ hipError_t launch_shape(const GemmParams& p, hipStream_t s) {
 
 bool gemm_shape_ok(const GemmParams& p) {
     if (p.K % BK != 0 || p.M < 1 || p.N < 1) return false;
+    if (p.bias2 != nullptr && (p.bias2_rows < 1 || p.N % 4 != 0)) return false;
+    if (p.conv_W > 0)
+        return !p.a_f32 && !p.geglu && p.conv_rows > 0 && p.K % (9 * DBK) == 0 && p.N % 64 == 0 &&
+               p.seg % 4 == 0 && p.M % (p.conv_rows * p.conv_W) == 0;
     if (p.geglu) return p.N % 64 == 0;  // two n-blocks of 32 per workgroup pair
     return p.N % 64 == 0 && p.seg % 4 == 0;
 }
 
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
+    if (p.conv_W > 0 && !gemm_shape_ok(p)) return hipErrorInvalidValue;
     // bf16 X with K % 64 == 0: the pipelined kernel, with the largest tile
     // that still gives about a workgroup per compute unit.
     if (!p.a_f32 && p.K % DBK == 0 && p.seg % 4 == 0) {
@@ -510,7 +550,8 @@ hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
             if (p.N % 64 == 0) return launch_dma<64, 64, 4, false>(p, s);
         }
     }
-    if (p.out_bf16 != nullptr) return hipErrorInvalidValue;  // only the pipelined kernel writes a bf16 copy
+    // only the pipelined kernel writes a bf16 copy, adds bias2 or convolves
+    if (p.out_bf16 != nullptr || p.bias2 != nullptr || p.conv_W > 0) return hipErrorInvalidValue;
     // 128x128 tiles when they still give about a workgroup per compute unit,
     // else 64x128 / 64x64.
     if (p.geglu) return launch_shape<2, 2>(p, s);

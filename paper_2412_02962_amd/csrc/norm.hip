@@ -234,6 +234,7 @@ __global__ __launch_bounds__(GN_THREADS) void gn_apply(GroupNormParams p) {
         sh[c] = bf16_to_f32(p.beta[c]) - fin[2 * g] * a;
     }
     __syncthreads();
+    const int pad_rows = p.pad_W > 0 ? p.N / p.pad_W : 0;
 #pragma unroll
     for (int k = 0; k < VPT; ++k) {
         const int i = tid + GN_THREADS * k;
@@ -241,8 +242,17 @@ __global__ __launch_bounds__(GN_THREADS) void gn_apply(GroupNormParams p) {
             const int t = i / vpr, c = (i - t * vpr) * 8;
             bf16x8 y;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) y[e] = f32_to_bf16(__builtin_fmaf((float)xv[k][e], sc[c + e], sh[c + e]));
-            *(bf16x8*)(p.y + base + (int64_t)t * C + c) = y;
+            for (int e = 0; e < 8; ++e) {
+                float v = __builtin_fmaf((float)xv[k][e], sc[c + e], sh[c + e]);
+                if (p.silu) v = v * __builtin_amdgcn_rcpf(1.f + __expf(-v));
+                y[e] = f32_to_bf16(v);
+            }
+            int64_t dst = base + (int64_t)t * C;
+            if (p.pad_W > 0) {  // token (row, col) of image b at framed (row + 1, col + 1)
+                const int tok = tok0 + t, row = tok / p.pad_W, col = tok - row * p.pad_W;
+                dst = ((int64_t)(b * (pad_rows + 2) + row + 1) * (p.pad_W + 2) + col + 1) * C;
+            }
+            *(bf16x8*)(p.y + dst + c) = y;
         }
     }
 }
@@ -315,6 +325,7 @@ bool norm_shapes_ok(int C, int G) {
 
 hipError_t launch_group_norm(GroupNormParams p, hipStream_t s) {
     if (!norm_shapes_ok(p.C, p.G)) return hipErrorInvalidValue;
+    if (p.pad_W < 0 || (p.pad_W > 0 && p.N % p.pad_W != 0)) return hipErrorInvalidValue;
     p.chunks = gn_chunks(p.N);
     gn_stats<<<dim3(p.chunks, p.B), GN_THREADS, 0, s>>>(p);
     hipError_t e = hipGetLastError();

@@ -53,6 +53,38 @@ class pcpp_block_weights_t(ctypes.Structure):
         ("ff_inner", ctypes.c_int32), ("gn_groups", ctypes.c_int32)]
 
 
+class pcpp_resnet_geom_t(ctypes.Structure):
+    _fields_ = [
+        ("H", ctypes.c_int32), ("W", ctypes.c_int32),
+        ("n_patches", ctypes.c_int32), ("patch_idx", ctypes.c_int32),
+        ("c_in", ctypes.c_int32), ("c_out", ctypes.c_int32),
+        ("temb_dim", ctypes.c_int32), ("groups", ctypes.c_int32),
+        ("batch", ctypes.c_int32), ("eps", ctypes.c_float), ("reserved", ctypes.c_int32),
+    ]
+
+
+RESNET_PTR_FIELDS = (
+    "gn1_gamma", "gn1_beta", "conv1_w", "conv1_b", "temb_w", "temb_b",
+    "gn2_gamma", "gn2_beta", "conv2_w", "conv2_b", "skip_w", "skip_b",
+)
+
+
+class pcpp_resnet_weights_t(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in RESNET_PTR_FIELDS]
+
+
+PCPP_STEP_DDPM = 0
+PCPP_STEP_DDIM = 1
+
+
+class pcpp_step_params_t(ctypes.Structure):
+    _fields_ = [
+        ("guidance", ctypes.c_float), ("alpha_t", ctypes.c_float), ("alphabar_t", ctypes.c_float),
+        ("sigma_t", ctypes.c_float), ("alphabar_prev", ctypes.c_float),
+        ("mode", ctypes.c_int32), ("reserved", ctypes.c_int32),
+    ]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built: run __graft_entry__.build() "
@@ -82,6 +114,11 @@ def _load():
         "pcpp_multihop_message_bytes": (sz, [gp, i32]),
         "pcpp_pack_multihop": (ctypes.c_int, [gp, i32, vp, vp, vp, vp]),
         "pcpp_unpack_multihop": (ctypes.c_int, [gp, i32, vp, vp, vp, vp, vp, vp]),
+        "pcpp_resnet_block_workspace_size": (sz, [ctypes.POINTER(pcpp_resnet_geom_t)]),
+        "pcpp_resnet_block": (ctypes.c_int, [ctypes.POINTER(pcpp_resnet_geom_t),
+                                             ctypes.POINTER(pcpp_resnet_weights_t)] + [vp] * 14 + [sz, vp]),
+        "pcpp_guided_step": (ctypes.c_int, [ctypes.POINTER(pcpp_step_params_t), ctypes.c_int64,
+                                            vp, vp, vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -98,6 +135,7 @@ EXPORTED = (
     "pcpp_boundary_bytes", "pcpp_pack_boundary", "pcpp_unpack_boundary", "pcpp_transformer_block_sync_gn",
     "pcpp_partial_attention_multihop_workspace_size", "pcpp_partial_attention_multihop",
     "pcpp_multihop_message_bytes", "pcpp_pack_multihop", "pcpp_unpack_multihop",
+    "pcpp_resnet_block_workspace_size", "pcpp_resnet_block", "pcpp_guided_step",
 )
 
 
@@ -233,3 +271,39 @@ def pcpp_unpack_multihop(g, peer, recv, k_above, v_above, k_below, v_below, stre
     _check("pcpp_unpack_multihop", _lib.pcpp_unpack_multihop(
         ctypes.byref(g), peer, _ptr(recv), _ptr(k_above), _ptr(v_above), _ptr(k_below), _ptr(v_below),
         _stream(stream)))
+
+
+def make_resnet_geom(H, W, n_patches, patch_idx, c_in, c_out, temb_dim=1280, groups=32, batch=1, eps=1e-5,
+                     reserved=0) -> pcpp_resnet_geom_t:
+    return pcpp_resnet_geom_t(H, W, n_patches, patch_idx, c_in, c_out, temb_dim, groups, batch, float(eps),
+                              reserved)
+
+
+def make_resnet_weights(tensors: dict) -> pcpp_resnet_weights_t:
+    w = pcpp_resnet_weights_t()
+    for name in RESNET_PTR_FIELDS:
+        setattr(w, name, _ptr(tensors.get(name)))
+    return w
+
+
+def pcpp_resnet_block_workspace_size(g) -> int:
+    return _lib.pcpp_resnet_block_workspace_size(ctypes.byref(g))
+
+
+def pcpp_resnet_block(g, w, x, temb, edges1_up, edges1_dn, edges2_up, edges2_dn, gn1_bands, gn1_own, gn2_bands,
+                      gn2_own, y, edges1_out, edges2_out, workspace, ws_bytes, stream=None):
+    _check("pcpp_resnet_block", _lib.pcpp_resnet_block(
+        ctypes.byref(g), ctypes.byref(w), _ptr(x), _ptr(temb), _ptr(edges1_up), _ptr(edges1_dn), _ptr(edges2_up),
+        _ptr(edges2_dn), _ptr(gn1_bands), _ptr(gn1_own), _ptr(gn2_bands), _ptr(gn2_own), _ptr(y), _ptr(edges1_out),
+        _ptr(edges2_out), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def make_step_params(mode, guidance, alpha_t=1.0, alphabar_t=0.5, sigma_t=0.0, alphabar_prev=1.0,
+                     reserved=0) -> pcpp_step_params_t:
+    return pcpp_step_params_t(float(guidance), float(alpha_t), float(alphabar_t), float(sigma_t),
+                              float(alphabar_prev), mode, reserved)
+
+
+def pcpp_guided_step(sp, n, x_t, eps_uncond, eps_cond, z, x_prev, stream=None):
+    _check("pcpp_guided_step", _lib.pcpp_guided_step(
+        ctypes.byref(sp), n, _ptr(x_t), _ptr(eps_uncond), _ptr(eps_cond), _ptr(z), _ptr(x_prev), _stream(stream)))

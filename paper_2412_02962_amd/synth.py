@@ -264,3 +264,96 @@ def block_inputs(bc: BlockConfig = BLOCK_CONFIG, seed: Optional[int] = None,
             out["k_" + tag] = None
             out["v_" + tag] = None
     return out
+
+
+# ---------------------------------------------------------------------------
+# ResNet block and the latent update of a step
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class ResnetConfig:
+    """One band of an SDXL ResNet block: token grid H x W split in n bands,
+    band i, c_in -> c_out channels, a T-wide time embedding."""
+    name: str
+    H: int
+    W: int
+    n: int
+    i: int
+    c_in: int
+    c_out: int
+    temb_dim: int = 1280
+    groups: int = 32
+    batch: int = 1
+    seed_id: int = 80
+
+    @property
+    def h(self) -> int:
+        return self.H // self.n
+
+
+# SDXL's ResNets at the 2048 px image's first transformer level (128 x 128
+# tokens of 640 channels, 8 bands): the plain one, and the first one of the
+# level, which widens 320 channels to 640.
+RESNET_CONFIGS = {
+    "sdxl2048_l1_res640": ResnetConfig("sdxl2048_l1_res640", 128, 128, 8, 3, 640, 640, seed_id=80),
+    "sdxl2048_l1_res320_640": ResnetConfig("sdxl2048_l1_res320_640", 128, 128, 8, 3, 320, 640, seed_id=81),
+}
+
+
+def resnet_weight_shapes(rc: ResnetConfig) -> Dict[str, tuple]:
+    s = {
+        "gn1_gamma": (rc.c_in,), "gn1_beta": (rc.c_in,),
+        "conv1_w": (rc.c_out, 3, 3, rc.c_in), "conv1_b": (rc.c_out,),
+        "temb_w": (rc.c_out, rc.temb_dim), "temb_b": (rc.c_out,),
+        "gn2_gamma": (rc.c_out,), "gn2_beta": (rc.c_out,),
+        "conv2_w": (rc.c_out, 3, 3, rc.c_out), "conv2_b": (rc.c_out,),
+    }
+    if rc.c_in != rc.c_out:
+        s["skip_w"] = (rc.c_out, rc.c_in)
+        s["skip_b"] = (rc.c_out,)
+    return s
+
+
+def resnet_inputs(rc: ResnetConfig, seed: Optional[int] = None) -> Dict[str, Optional[np.ndarray]]:
+    """bf16 inputs of one ResNet-block call on band rc.i.
+
+    x [B, h*W, c_in] ~ N(0, 1); temb [B, T] ~ N(0, 1); weights ~ N(0,
+    1/fan_in) (fan_in = 9 c for a 3x3 kernel); biases ~ 0.02 N(0, 1); norm
+    scales ~ 1 + 0.1 N(0, 1), shifts ~ 0.1 N(0, 1).  The neighbours' edge
+    rows of the two convolution inputs ([B, 2, W, c], None at the image's
+    edges) are N(0, 1) clipped below at -0.28, the range of SiLU's outputs.
+    """
+    s = BASE_SEED + rc.seed_id if seed is None else seed
+    B, W = rc.batch, rc.W
+    out: Dict[str, Optional[np.ndarray]] = {}
+    out["x"] = bf16_bits(_stream(s, 400).standard_normal((B, rc.h * W, rc.c_in)))
+    out["temb"] = bf16_bits(_stream(s, 401).standard_normal((B, rc.temb_dim)))
+    for idx, (name, shape) in enumerate(resnet_weight_shapes(rc).items()):
+        g = _stream(s, 500 + idx)
+        if name.endswith("_w"):
+            w = g.standard_normal(shape) / np.sqrt(np.prod(shape[1:]))
+        elif name.endswith("_b") or name.endswith("_beta"):
+            w = (0.02 if name.endswith("_b") else 0.1) * g.standard_normal(shape)
+        else:
+            w = 1.0 + 0.1 * g.standard_normal(shape)
+        out[name] = bf16_bits(w)
+    for k, (tag, c) in enumerate((("edges1", rc.c_in), ("edges2", rc.c_out))):
+        for side, j in (("up", rc.i - 1), ("dn", rc.i + 1)):
+            key = f"{tag}_{side}"
+            if 0 <= j < rc.n:
+                e = _stream(s, 600 + 2 * k + (side == "dn")).standard_normal((B, 2, W, c))
+                out[key] = bf16_bits(np.maximum(e, -0.28))
+            else:
+                out[key] = None
+    return out
+
+
+def step_inputs(n: int, seed: int, with_noise: bool = True) -> Dict[str, Optional[np.ndarray]]:
+    """float32 latent-update inputs: x_t, the two guidance branches' noise
+    predictions and (optionally) the DDPM noise z, each n values ~ N(0, 1)."""
+    out: Dict[str, Optional[np.ndarray]] = {}
+    for k, name in enumerate(("x_t", "eps_uncond", "eps_cond", "z")):
+        out[name] = _stream(seed, 700 + k).standard_normal(n).astype(np.float32)
+    if not with_noise:
+        out["z"] = None
+    return out

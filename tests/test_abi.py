@@ -277,3 +277,59 @@ def test_multihop_message_validation_errors_before_launch():
     assert unpack(7, None, None, None, None, None) == pcpp.PCPP_OK
     f64 = pcpp.make_geom(64, 64, 8, 3, 1.5, 2, 64, 1, 0, 7)
     assert lib.pcpp_pack_multihop(ctypes.byref(f64), 2, A, Bp, A + (1 << 31), None) != pcpp.PCPP_OK
+
+
+def test_resnet_geometry_and_validation():
+    from paper_2412_02962_amd import pcpp
+    lib = pcpp.lib()
+    g = pcpp.make_resnet_geom(128, 128, 8, 3, 640, 640, 1280, 32, 1)
+    ws = pcpp.pcpp_resnet_block_workspace_size(g)
+    framed = 1 * 18 * 130 * 640 * 2
+    assert ws >= 2 * framed + 16 * 128 * 640 * 2 + 640 * 4
+    g2 = pcpp.make_resnet_geom(128, 128, 8, 3, 320, 640, 1280, 32, 1)
+    assert pcpp.pcpp_resnet_block_workspace_size(g2) >= 16 * 128 * 640 * 4       # float32 shortcut
+    bad = [pcpp.make_resnet_geom(100, 128, 8, 3, 640, 640),         # H % n
+           pcpp.make_resnet_geom(128, 128, 8, 8, 640, 640),         # band index
+           pcpp.make_resnet_geom(128, 128, 8, 3, 640, 640, 1284),   # T % 8
+           pcpp.make_resnet_geom(128, 128, 8, 3, 640, 640, 1280, 48),   # groups do not divide
+           pcpp.make_resnet_geom(128, 128, 8, 3, 640, 640, eps=0.0),
+           pcpp.make_resnet_geom(128, 128, 8, 3, 640, 640, reserved=1)]
+    for b in bad:
+        assert pcpp.pcpp_resnet_block_workspace_size(b) == 0
+    for c_in, c_out in ((96, 96), (640, 2560)):
+        gg = pcpp.make_resnet_geom(64, 64, 4, 1, c_in, c_out, groups=32)
+        assert pcpp.pcpp_resnet_block_workspace_size(gg) == 0
+        assert lib.pcpp_resnet_block(ctypes.byref(gg), ctypes.byref(pcpp.pcpp_resnet_weights_t()), *([None] * 14),
+                                     0, None) == pcpp.PCPP_ENOTSUP
+    w = pcpp.make_resnet_weights({k: FAKE for k in pcpp.RESNET_PTR_FIELDS if not k.startswith("skip")})
+    call = lambda gg, ww, *a: lib.pcpp_resnet_block(ctypes.byref(gg), ctypes.byref(ww), *a, None)
+    big = 1 << 30
+    ok_args = [FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None, None, FAKE, None, None, FAKE, big]
+    assert call(g, w, *ok_args[:-2], None, big) == pcpp.PCPP_EWORKSPACE
+    assert call(g, w, *ok_args[:-2], FAKE, 16) == pcpp.PCPP_EWORKSPACE
+    a = list(ok_args); a[2] = None                                   # band 3 needs the rows above
+    assert call(g, w, *a) == pcpp.PCPP_EINVAL
+    a = list(ok_args); a[0] = FAKE + 2                               # misaligned x
+    assert call(g, w, *a) == pcpp.PCPP_EINVAL
+    a = list(ok_args); a[6] = FAKE + 2                               # misaligned statistics
+    assert call(g, w, *a) == pcpp.PCPP_EINVAL
+    assert call(g2, w, *ok_args) == pcpp.PCPP_EINVAL                 # 320 -> 640 needs the shortcut weights
+
+
+def test_guided_step_validation():
+    from paper_2412_02962_amd import pcpp
+    lib = pcpp.lib()
+    call = lambda sp, n, *a: lib.pcpp_guided_step(ctypes.byref(sp), n, *a, None)
+    ddpm = pcpp.make_step_params(pcpp.PCPP_STEP_DDPM, 5.0, alpha_t=0.99, alphabar_t=0.5, sigma_t=0.1)
+    ddim = pcpp.make_step_params(pcpp.PCPP_STEP_DDIM, 5.0, alphabar_t=0.5, alphabar_prev=0.6)
+    assert call(ddpm, 0, None, None, None, None, None) == pcpp.PCPP_OK          # nothing to do
+    assert call(ddpm, 16, FAKE, None, FAKE, None, FAKE) == pcpp.PCPP_EINVAL
+    assert call(ddim, 16, FAKE, FAKE, FAKE, FAKE, FAKE) == pcpp.PCPP_EINVAL       # DDIM takes no noise
+    for bad in (pcpp.make_step_params(pcpp.PCPP_STEP_DDPM, 5.0, alpha_t=0.0, alphabar_t=0.5),
+                pcpp.make_step_params(pcpp.PCPP_STEP_DDPM, 5.0, alpha_t=0.9, alphabar_t=1.0),
+                pcpp.make_step_params(pcpp.PCPP_STEP_DDIM, 5.0, alphabar_t=0.5, alphabar_prev=0.0),
+                pcpp.make_step_params(pcpp.PCPP_STEP_DDIM, float("nan"), alphabar_t=0.5, alphabar_prev=0.6),
+                pcpp.make_step_params(2, 5.0),
+                pcpp.make_step_params(pcpp.PCPP_STEP_DDIM, 5.0, alphabar_t=0.5, alphabar_prev=0.6, reserved=3)):
+        assert call(bad, 16, FAKE, FAKE, FAKE, None, FAKE) == pcpp.PCPP_EINVAL
+    assert call(ddpm, -1, FAKE, FAKE, FAKE, None, FAKE) == pcpp.PCPP_EINVAL
