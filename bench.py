@@ -106,6 +106,36 @@ def block_flops(bc, n_kv):
     return gemm + attn
 
 
+def resnet_flops(rc):
+    """Algorithmic FLOPs of one ResNet-block call: the two 3x3 convolutions,
+    the 1x1 shortcut when the width changes, the time-embedding projection."""
+    M = rc.batch * rc.h * rc.W
+    f = 2.0 * M * 9 * rc.c_in * rc.c_out + 2.0 * M * 9 * rc.c_out * rc.c_out
+    if rc.c_in != rc.c_out:
+        f += 2.0 * M * rc.c_in * rc.c_out
+    return f + 2.0 * rc.batch * rc.temb_dim * rc.c_out
+
+
+def resnet_call(torch, pcpp, synth, rc, dev):
+    """(fn, tensors): one pcpp_resnet_block call on band rc.i with its inputs on dev."""
+    import numpy as np
+    to_dev = lambda x: None if x is None else torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(
+        torch.bfloat16).to(dev)
+    d = {k: to_dev(v) for k, v in synth.resnet_inputs(rc).items()}
+    g = pcpp.make_resnet_geom(rc.H, rc.W, rc.n, rc.i, rc.c_in, rc.c_out, rc.temb_dim, rc.groups, rc.batch, 1e-5)
+    w = pcpp.make_resnet_weights(d)
+    y = torch.empty((rc.batch, rc.h * rc.W, rc.c_out), dtype=torch.bfloat16, device=dev)
+    e1 = torch.empty((rc.batch, 2, rc.W, rc.c_in), dtype=torch.bfloat16, device=dev)
+    e2 = torch.empty((rc.batch, 2, rc.W, rc.c_out), dtype=torch.bfloat16, device=dev)
+    wsb = pcpp.pcpp_resnet_block_workspace_size(g)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+
+    def fn():
+        pcpp.pcpp_resnet_block(g, w, d["x"], d["temb"], d["edges1_up"], d["edges1_dn"], d["edges2_up"],
+                               d["edges2_dn"], None, None, None, None, y, e1, e2, ws, wsb)
+    return fn, (d, y, e1, e2, ws)
+
+
 def graph_time_us(torch, fn, K, use_graph=True):
     """Average microseconds per call of fn: K calls captured in one HIP graph
     and replayed (or K eager calls)."""
@@ -307,6 +337,23 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
     out["block_us"] = round(us, 3)
     out["block_TFLOPs"] = round(block_flops(bc, nkvb) / us / 1e6, 1)
     out["block_gflop"] = round(block_flops(bc, nkvb) / 1e9, 2)
+
+    # ResNet blocks of the same level (bf16, batch 1: one guidance branch per device)
+    for name, rc in synth.RESNET_CONFIGS.items():
+        fn, keep = resnet_call(torch, pcpp, synth, rc, dev)
+        us = graph_time_us(torch, fn, max(reps // 4, 1), use_graph)
+        out[f"resnet_{name}_us"] = round(us, 3)
+        out[f"resnet_{name}_TFLOPs"] = round(resnet_flops(rc) / us / 1e6, 1)
+        del keep
+
+    # the latent update of one band of the 2048 px image (latent 256 x 256 x 4, 8 bands)
+    n = 256 // 8 * 256 * 4
+    lat = [torch.randn(n, dtype=torch.float32, device=dev) for _ in range(4)]
+    abar = 0.5
+    sp = pcpp.make_step_params(pcpp.PCPP_STEP_DDIM, 5.0, alphabar_t=abar, alphabar_prev=0.55)
+    us = graph_time_us(torch, lambda: pcpp.pcpp_guided_step(sp, n, lat[0], lat[1], lat[2], None, lat[3]), reps,
+                       use_graph)
+    out["guided_step_2048px_band_us"] = round(us, 3)
     return out
 
 
@@ -409,6 +456,21 @@ def block_run(args):
     print(f"block run: {args.steps} calls", flush=True)
 
 
+def resnet_run(args):
+    """Workload for a kernel-trace profile of the ResNet blocks: --steps calls
+    of each 2048 px level-1 ResNet block, nothing else."""
+    import torch
+
+    from paper_2412_02962_amd import pcpp, synth
+    for name, rc in synth.RESNET_CONFIGS.items():
+        fn, keep = resnet_call(torch, pcpp, synth, rc, "cuda:0")
+        for _ in range(args.steps):
+            fn()
+        torch.cuda.synchronize()
+        print(f"resnet run {name}: {args.steps} calls", flush=True)
+        del keep
+
+
 def pmc_report(dirs):
     """Per-dispatch averages of every counter rocprofv3 --pmc recorded for the
     attention kernel in the given output folders (one folder per pass), with
@@ -450,6 +512,8 @@ def main():
                     help="write the traffic summary from two rocprofv3 --pmc output folders")
     ap.add_argument("--block-run", action="store_true",
                     help="profiling workload: --steps transformer-block calls, nothing else")
+    ap.add_argument("--resnet-run", action="store_true",
+                    help="profiling workload: --steps calls of each ResNet block, nothing else")
     ap.add_argument("--pmc-report", nargs="+", metavar="DIR",
                     help="print per-dispatch counter averages of the attention kernel from rocprofv3 --pmc folders")
     args = ap.parse_args()
@@ -461,6 +525,9 @@ def main():
         return
     if args.block_run:
         block_run(args)
+        return
+    if args.resnet_run:
+        resnet_run(args)
         return
     if args.pmc_run:
         pmc_run(args)

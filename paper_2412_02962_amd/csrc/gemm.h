@@ -34,7 +34,19 @@ struct GemmParams {
     // bias2[(m / bias2_rows) * N + n] (16-byte aligned), or null.
     const float* bias2 = nullptr;
     int32_t bias2_rows = 1;
+    // Workspace that lets a convolution split K over several workgroups
+    // (gemm_split_ws_bytes; its first bytes are counters that must be zero
+    // before the first use and are left zero), or null.
+    void* split_ws = nullptr;
+    size_t split_ws_bytes = 0;
+    // Set by launch_gemm for a split launch.
+    int32_t splitk = 1, n_xcd = 1, tpx = 0, n_tiles = 0;
 };
+
+// Bytes of split-K workspace a convolution GEMM of this shape can use (0:
+// it runs unsplit); counters come first, at most GEMM_SPLIT_COUNTERS ints.
+constexpr int GEMM_SPLIT_COUNTERS = 4096;
+size_t gemm_split_ws_bytes(int M, int N, int K);
 
 bool gemm_shape_ok(const GemmParams& p);
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s);

@@ -275,10 +275,27 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
     const int wn = wave >> 1;
     const int col = lane & 31;
     const int half = lane >> 5;
-    const int m0 = blockIdx.x * BM;
     const int bn_out = GEGLU ? BN / 2 : BN;
-    const int n0 = blockIdx.y * bn_out;
-    const int nk = p.K / DBK;
+    // Split K: workgroup w runs on XCD w % n_xcd; the tiles of an XCD are a
+    // contiguous range of tpx tiles, and the splitk pieces of a tile follow
+    // each other within it, so all pieces of a tile share one L2.
+    int m_tile = blockIdx.x, n_tile = blockIdx.y, piece = 0, tile = 0, xcd = 0, tl = 0;
+    if (p.splitk > 1) {
+        xcd = blockIdx.x % p.n_xcd;
+        const int j = blockIdx.x / p.n_xcd;
+        tl = j / p.splitk;
+        piece = j - tl * p.splitk;
+        tile = xcd * p.tpx + tl;
+        if (tl >= p.tpx || tile >= p.n_tiles) return;  // idle slot of the last XCD (uniform)
+        const int mt = (p.M + BM - 1) / BM;
+        n_tile = tile / mt;
+        m_tile = tile - n_tile * mt;
+    }
+    const int m0 = m_tile * BM;
+    const int n0 = n_tile * bn_out;
+    const int nk_all = p.K / DBK;
+    const int kt0 = (int)((int64_t)nk_all * piece / p.splitk);
+    const int kt1 = (int)((int64_t)nk_all * (piece + 1) / p.splitk);
 
     // Per-lane global source of each staged piece (row 8q + (lane >> 3),
     // chunk (lane & 7) ^ swizzle), k offset added per k-tile.
@@ -304,6 +321,13 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
     // right, or to the next framed row's first tap column).
     int iss_cb = 0, iss_kx = 0;
     int64_t iss_xoff = 0;
+    if (CONV && kt0 > 0) {
+        const int cbn = cin / DBK;
+        const int t = kt0 / cbn, ky = t / 3;
+        iss_cb = kt0 - t * cbn;
+        iss_kx = t - 3 * ky;
+        iss_xoff = ((int64_t)(ky * (p.conv_W + 2) + iss_kx) * cin + iss_cb * DBK) * 2;
+    }
 #pragma unroll
     for (int i = 0; i < WP; ++i) {
         const int r = 8 * (wave + 4 * i) + (lane >> 3);
@@ -382,10 +406,10 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
 
 #pragma unroll
     for (int s = 0; s < NS - 1; ++s)
-        if (s < nk) issue(s, s);
-    for (int kt = 0; kt < nk; ++kt) {
-        // k-tiles issued after kt so far: min(nk - 1 - kt, NS - 2), PT loads each
-        const int later = min(nk - 1 - kt, NS - 2);
+        if (kt0 + s < kt1) issue(kt0 + s, s);
+    for (int kt = kt0; kt < kt1; ++kt) {
+        // k-tiles issued after kt so far: min(kt1 - 1 - kt, NS - 2), PT loads each
+        const int later = min(kt1 - 1 - kt, NS - 2);
         if (NS >= 4 && later >= 2)
             __builtin_amdgcn_s_waitcnt(0xF70 | (2 * PT));
         else if (later >= 1)
@@ -393,8 +417,8 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
         else
             __builtin_amdgcn_s_waitcnt(0xF70);
         __builtin_amdgcn_s_barrier();  // everyone's pieces of tile kt landed; the stage of tile kt-1 is free
-        if (kt + NS - 1 < nk) issue(kt + NS - 1, (kt + NS - 1) % NS);
-        const uint32_t sbase = lds0 + (kt % NS) * STAGE;
+        if (kt + NS - 1 < kt1) issue(kt + NS - 1, (kt - kt0 + NS - 1) % NS);
+        const uint32_t sbase = lds0 + ((kt - kt0) % NS) * STAGE;
         Ops o[2];
         read_ops(sbase, 0, o[0]);
 #pragma unroll
@@ -412,6 +436,63 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
                 for (int j = 0; j < WMB; ++j)
                     acc[i][j] = mfma32x32x16(__builtin_bit_cast(bf16x8, cur.w[i]), __builtin_bit_cast(bf16x8, cur.x[j]),
                                              acc[i][j]);
+        }
+    }
+
+    // Split K: every piece stores its partial tile (fp32, 1 KB per wavefront
+    // store); the last piece of a tile to arrive adds all of them in piece
+    // order (its own from registers: the same values) and runs the epilogue.
+    if (p.splitk > 1) {
+        __shared__ int last_flag;
+        constexpr int NQ = WNB * WMB * 4;  // f32x4 chunks per lane
+        auto part_of = [&](int wg) { return (float*)p.split_ws + GEMM_SPLIT_COUNTERS + (int64_t)wg * BM * BN; };
+        {
+            float* dst = part_of(blockIdx.x) + (wave * 64 + lane) * 4;
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) {
+                const f32x16& a = acc[q / (4 * WMB)][(q / 4) % WMB];
+                const f32x4 v = {a[4 * (q & 3)], a[4 * (q & 3) + 1], a[4 * (q & 3) + 2], a[4 * (q & 3) + 3]};
+                *(f32x4*)(dst + q * 1024) = v;
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): this thread's stores reached the L2
+        __syncthreads();
+        if (tid == 0) {
+            int* counter = (int*)p.split_ws + tile;
+            const int prev = __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            const int last = prev == p.splitk - 1;
+            if (last) __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            last_flag = last;
+        }
+        __syncthreads();
+        if (!last_flag) return;
+        f32x16 own[WNB][WMB];
+#pragma unroll
+        for (int i = 0; i < WNB; ++i)
+#pragma unroll
+            for (int j = 0; j < WMB; ++j) {
+                own[i][j] = acc[i][j];
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+            }
+        for (int pc = 0; pc < p.splitk; ++pc) {
+            if (pc == piece) {
+#pragma unroll
+                for (int i = 0; i < WNB; ++i)
+#pragma unroll
+                    for (int j = 0; j < WMB; ++j)
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) acc[i][j][r] += own[i][j][r];
+                continue;
+            }
+            const float* src = part_of((tl * p.splitk + pc) * p.n_xcd + xcd) + (wave * 64 + lane) * 4;
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) {
+                const f32x4 v = *(const f32x4*)(src + q * 1024);
+                f32x16& a = acc[q / (4 * WMB)][(q / 4) % WMB];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) a[4 * (q & 3) + e] += v[e];
+            }
         }
     }
 
@@ -505,6 +586,7 @@ template <int BM, int BN, int NS, bool GEGLU>
 hipError_t launch_dma(const GemmParams& p, hipStream_t s) {
     const int bn_out = GEGLU ? BN / 2 : BN;
     dim3 grid((p.M + BM - 1) / BM, p.N / bn_out);
+    if (p.splitk > 1) grid = dim3((unsigned)(p.n_xcd * p.tpx * p.splitk), 1);
     if (!GEGLU && p.conv_W > 0)
         gemm_dma_kernel<BM, BN, NS, GEGLU, true><<<grid, 256, 0, s>>>(p);
     else
@@ -536,8 +618,67 @@ bool gemm_shape_ok(const GemmParams& p) {
     return p.N % 64 == 0 && p.seg % 4 == 0;
 }
 
-hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
+namespace {
+
+constexpr int CUS_PER_XCD = 32;  // gfx950
+
+int cu_count() {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 256;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        return 256;
+    return cus;
+}
+
+// Split of a convolution GEMM over 128 x 128 tiles: as many pieces per tile
+// as still fit one workgroup per compute unit, each at least 16 k-tiles
+// long, used only when the split launch fills at least 90% of the compute
+// units (else the unsplit 64 x 64 tiles, two workgroups per compute unit,
+// are faster).
+struct SplitPlan {
+    int splitk, n_xcd, tpx, n_tiles;
+    size_t bytes;
+};
+
+SplitPlan split_plan(int M, int N, int K) {
+    SplitPlan sp{1, 1, 0, 0, 0};
+    const int cus = cu_count();
+    if (cus % CUS_PER_XCD != 0 || N % 128 != 0 || K % DBK != 0) return sp;
+    const int64_t tiles = (int64_t)((M + 127) / 128) * (N / 128);
+    if (tiles < 1 || tiles > GEMM_SPLIT_COUNTERS) return sp;
+    const int n_xcd = cus / CUS_PER_XCD;
+    const int64_t tpx = (tiles + n_xcd - 1) / n_xcd;
+    int64_t k = cus / (n_xcd * tpx);
+    const int64_t k_max = (K / DBK) / 16;
+    if (k > k_max) k = k_max;
+    if (k > 8) k = 8;
+    if (k < 2 || 10 * n_xcd * tpx * k < 9 * (int64_t)cus) return sp;
+    sp.splitk = (int)k;
+    sp.n_xcd = n_xcd;
+    sp.tpx = (int)tpx;
+    sp.n_tiles = (int)tiles;
+    sp.bytes = (size_t)GEMM_SPLIT_COUNTERS * 4 + (size_t)n_xcd * tpx * k * 128 * 128 * 4;
+    return sp;
+}
+
+}  // namespace
+
+size_t gemm_split_ws_bytes(int M, int N, int K) { return split_plan(M, N, K).bytes; }
+
+hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
+    GemmParams p = p_in;
     if (p.conv_W > 0 && !gemm_shape_ok(p)) return hipErrorInvalidValue;
+    p.splitk = 1;
+    if (p.conv_W > 0 && p.split_ws != nullptr) {
+        const SplitPlan sp = split_plan(p.M, p.N, p.K);
+        if (sp.splitk > 1 && p.split_ws_bytes >= sp.bytes && ((uintptr_t)p.split_ws & 15u) == 0) {
+            p.splitk = sp.splitk;
+            p.n_xcd = sp.n_xcd;
+            p.tpx = sp.tpx;
+            p.n_tiles = sp.n_tiles;
+            return launch_dma<128, 128, 3, false>(p, s);
+        }
+    }
     // bf16 X with K % 64 == 0: the pipelined kernel, with the largest tile
     // that still gives about a workgroup per compute unit.
     if (!p.a_f32 && p.K % DBK == 0 && p.seg % 4 == 0) {

@@ -67,8 +67,12 @@ __global__ __launch_bounds__(kThreads) void frame_band(bf16* f, const bf16* edge
 
 // tb[b][n] = bt[n] + sum_k SiLU(temb[b][k]) Wt[n][k]: one wavefront per
 // output, 16-byte chunks of k per lane.
+// Block 0 also clears the convolutions' split counters (n_zero ints), so the
+// workspace needs no clearing by the caller.
 __global__ __launch_bounds__(kThreads) void temb_proj(float* tb, const bf16* temb, const bf16* wt, const bf16* bt,
-                                                      int B, int N, int T) {
+                                                      int B, int N, int T, int* zero, int n_zero) {
+    if (blockIdx.x == 0 && zero != nullptr)
+        for (int i = threadIdx.x; i < n_zero; i += kThreads) zero[i] = 0;
     const int o = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (o >= B * N) return;
@@ -89,7 +93,7 @@ __global__ __launch_bounds__(kThreads) void temb_proj(float* tb, const bf16* tem
 }
 
 struct ResLayout {
-    size_t f1, h1, f2, skip, tb, gn, total;
+    size_t f1, h1, f2, skip, tb, gn, split, split_bytes, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -110,6 +114,10 @@ ResLayout res_layout(const pcpp_resnet_geom_t* g) {
     L.skip = g->c_in != g->c_out ? take(B * h * W * g->c_out * 4) : 0;
     L.tb = take(B * g->c_out * 4);
     L.gn = take(group_norm_ws_bytes(g->batch, g->groups, (int)(h * W)));
+    const int M = (int)(B * h * W);
+    const size_t s1 = gemm_split_ws_bytes(M, g->c_out, 9 * g->c_in), s2 = gemm_split_ws_bytes(M, g->c_out, 9 * g->c_out);
+    L.split_bytes = s1 > s2 ? s1 : s2;
+    L.split = L.split_bytes ? take(L.split_bytes) : 0;
     L.total = off;
     return L;
 }
@@ -247,12 +255,16 @@ PCPP_EXPORT int pcpp_resnet_block(const pcpp_resnet_geom_t* g, const pcpp_resnet
 
     PCPP_CHECK(norm(x, Ci, w->gn1_gamma, w->gn1_beta, gn1_bands, gn1_own, f1));
     PCPP_CHECK(frame(f1, edges1_up, edges1_dn, Ci));
+    void* split_ws = L.split_bytes ? ws + L.split : nullptr;
     temb_proj<<<(B * Co + 3) / 4, kThreads, 0, s>>>(tb, (const bf16*)temb, (const bf16*)w->temb_w,
-                                                   (const bf16*)w->temb_b, B, Co, g->temb_dim);
+                                                   (const bf16*)w->temb_b, B, Co, g->temb_dim, (int*)split_ws,
+                                                   split_ws ? GEMM_SPLIT_COUNTERS : 0);
     PCPP_CHECK(hipGetLastError());
     GemmParams c1 = conv_params(f1, w->conv1_w, w->conv1_b, rows, Co, 9 * Ci, h, W, h1);
     c1.bias2 = tb;
     c1.bias2_rows = N;
+    c1.split_ws = split_ws;
+    c1.split_ws_bytes = L.split_bytes;
     PCPP_CHECK(launch_gemm(c1, s));
     PCPP_CHECK(norm(h1, Co, w->gn2_gamma, w->gn2_beta, gn2_bands, gn2_own, f2));
     PCPP_CHECK(frame(f2, edges2_up, edges2_dn, Co));
@@ -266,6 +278,8 @@ PCPP_EXPORT int pcpp_resnet_block(const pcpp_resnet_geom_t* g, const pcpp_resnet
     c2.resid = proj_skip ? (const void*)skip : x;
     c2.ldr = Co;
     c2.resid_f32 = proj_skip ? 1 : 0;
+    c2.split_ws = split_ws;
+    c2.split_ws_bytes = L.split_bytes;
     PCPP_CHECK(launch_gemm(c2, s));
     // This band's edge rows of both convolution inputs, for its neighbours.
     if (edges1_out || edges2_out) {

@@ -41,6 +41,8 @@ SMALL = [
     synth.ResnetConfig("r_bot", 12, 20, 3, 2, 128, 128, temb_dim=64, groups=8, batch=1, seed_id=84),
     synth.ResnetConfig("r_one", 8, 24, 1, 0, 128, 64, temb_dim=128, groups=32, batch=1, seed_id=85),
     synth.ResnetConfig("r_tiny", 4, 3, 2, 1, 64, 64, temb_dim=8, groups=32, batch=3, seed_id=86),
+    # conv1 (K = 9 * 1024) splits K eight ways over 32 tiles: the whole device
+    synth.ResnetConfig("r_split", 32, 128, 2, 1, 1024, 256, temb_dim=64, groups=32, batch=1, seed_id=88),
 ]
 FULL = [synth.RESNET_CONFIGS["sdxl2048_l1_res640"], synth.RESNET_CONFIGS["sdxl2048_l1_res320_640"]]
 
@@ -204,6 +206,19 @@ def test_bands_exchanging_edges_and_statistics_rebuild_the_whole_image(n):
         st2 = torch.stack(own2s)
     got = torch.cat(outs, dim=1)                  # bands in order = the whole image's tokens
     _check(gu.to_f64(got), want, 4, f"exchange chain n={n}")
+
+
+@pytest.mark.parametrize("rc", [SMALL[5], FULL[0]], ids=lambda r: r.name)
+def test_resnet_is_deterministic(rc):
+    """The split convolutions add their pieces in a fixed order: repeated
+    calls give the same bits."""
+    import torch
+    _say("resnet determinism", rc.name)
+    inp = synth.resnet_inputs(rc)
+    d = {k: gu.to_dev(v, "bf16") for k, v in inp.items()}
+    ref = _run(rc, d)[0]
+    for _ in range(3):
+        assert torch.equal(_run(rc, d)[0], ref)
 
 
 def test_resnet_workspace_needs_no_clearing():
