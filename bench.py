@@ -471,6 +471,26 @@ def resnet_run(args):
         del keep
 
 
+def gemm_calibration():
+    """hipBLASLt (through torch.matmul, bf16, HIP graph of 20 calls) on the
+    GEMM shapes of the 2048 px level-1 block and ResNets: a yardstick for the
+    library's own GEMM kernels at these small-M shapes."""
+    import torch
+    dev = "cuda:0"
+    shapes = [("3x3 convolution 640 -> 640 as a plain GEMM", 2048, 640, 5760),
+              ("3x3 convolution 320 -> 640 as a plain GEMM", 2048, 640, 2880),
+              ("640 x 640 projection", 2048, 640, 640), ("Q/K/V", 2048, 1920, 640),
+              ("GEGLU product (no GELU)", 2048, 5120, 640), ("FF-out", 2048, 640, 2560),
+              ("large square", 8192, 8192, 8192)]
+    for name, M, N, K in shapes:
+        a = torch.randn(M, K, device=dev, dtype=torch.bfloat16)
+        w = torch.randn(N, K, device=dev, dtype=torch.bfloat16)
+        out = torch.empty(M, N, device=dev, dtype=torch.bfloat16)
+        us = graph_time_us(torch, lambda: torch.matmul(a, w.t(), out=out), 20 if M < 8192 else 5)
+        print(f"{name:45s} M={M:5d} N={N:5d} K={K:5d}: {us:8.2f} us {2.0 * M * N * K / us / 1e6:7.1f} TFLOP/s",
+              flush=True)
+
+
 def pmc_report(dirs):
     """Per-dispatch averages of every counter rocprofv3 --pmc recorded for the
     attention kernel in the given output folders (one folder per pass), with
@@ -514,6 +534,8 @@ def main():
                     help="profiling workload: --steps transformer-block calls, nothing else")
     ap.add_argument("--resnet-run", action="store_true",
                     help="profiling workload: --steps calls of each ResNet block, nothing else")
+    ap.add_argument("--gemm-calibration", action="store_true",
+                    help="time hipBLASLt (torch.matmul) on the block's and ResNets' GEMM shapes")
     ap.add_argument("--pmc-report", nargs="+", metavar="DIR",
                     help="print per-dispatch counter averages of the attention kernel from rocprofv3 --pmc folders")
     args = ap.parse_args()
@@ -528,6 +550,9 @@ def main():
         return
     if args.resnet_run:
         resnet_run(args)
+        return
+    if args.gemm_calibration:
+        gemm_calibration()
         return
     if args.pmc_run:
         pmc_run(args)

@@ -431,7 +431,8 @@ size_t pcpp_resnet_block_workspace_size(const pcpp_resnet_geom_t* g);
  *   gn2_own      band's two GroupNorm inputs, for the others' next step
  *   y            [B, h*W, c_out] bf16 output
  *   edges1_out,  NULL, or this band's first and last rows of a1 / a2,
- *   edges2_out   [B, 2, W, c] bf16: what its neighbours read at the next step
+ *   edges2_out   [B, 2, W, c] bf16: what its neighbours read at the next step;
+ *                they must not overlap each other or the edges inputs
  * Errors: PCPP_EINVAL (geometry, NULL or misaligned pointers, 16-byte
  * alignment for the bf16 tensors), PCPP_ENOTSUP (channels not multiples of
  * 64 or above 2048, groups above 256), PCPP_EWORKSPACE.  Asynchronous.

@@ -67,10 +67,16 @@ struct GroupNormParams {
     int32_t n_bands, band;
     float* own_out;       // [B][G] x (count, mean, M2) of this band, or null
     int32_t silu = 0;     // 1: y = SiLU(normalized value)
-    // pad_W > 0: y is the framed band [B][N / pad_W + 2][pad_W + 2][C] of a
-    // 3x3 convolution and token t = (row, col) of image b is written at
-    // (row + 1, col + 1); the frame itself is not written.
+    // pad_W > 0: y is the framed band [B][rows + 2][pad_W + 2][C] of a 3x3
+    // convolution (rows = N / pad_W): token (row, col) of image b is written
+    // at (row + 1, col + 1); framed row 0 takes row 1 of frame_up
+    // [B][2][pad_W][C] (zeros if null), framed row rows + 1 row 0 of
+    // frame_dn, the side columns zeros; edges_out [B][2][pad_W][C], if not
+    // null, receives the band's rows 0 and rows - 1 (all 16-byte aligned).
     int32_t pad_W = 0;
+    const __bf16* frame_up = nullptr;
+    const __bf16* frame_dn = nullptr;
+    __bf16* edges_out = nullptr;
 };
 size_t group_norm_ws_bytes(int B, int G, int N);
 // C % 8 == 0, C <= 2048, 1 <= G <= 256 divides C.

@@ -1,16 +1,23 @@
-// GroupNorm and LayerNorm of the transformer block (bandwidth-bound).
+// GroupNorm and LayerNorm (bandwidth-bound).
 //
 // GroupNorm uses the statistics of the band's own tokens (each image, each
-// group of C/G consecutive channels).  gn_stats: a workgroup holds a chunk of
-// 16 whole token rows in registers (coalesced channel pairs) and reduces them
-// to per-group (count, mean, M2) with two passes over the registers (sum,
-// then squared deviations from the chunk mean).  gn_finalize (one workgroup
-// per image) merges the chunk statistics of every group with Chan et al.'s
-// pairwise update in a fixed order and stores mean and 1/sqrt(var + eps)
-// (biased variance).  Synchronized GroupNorm (the whole image's statistics,
-// Sec. 3.3 of arXiv 2412.02962) merges every band's (count, mean, M2) in
-// band order, this band's own in its place, before that.  gn_apply: per-channel scale and shift in LDS, 16-byte
-// vectors.
+// group of C/G consecutive channels), or with `bands` the whole image's
+// (synchronized GroupNorm, Sec. 3.3 of arXiv 2412.02962: every band's
+// (count, mean, M2) merged in band order, this band's own in its place).
+// Two kernels:
+//   gn_stats  one workgroup per chunk of 32 tokens, held in registers
+//             (coalesced channel pairs), reduced to per-group (count, mean,
+//             M2) with two passes over the registers (sum, then squared
+//             deviations from the chunk mean).
+//   gn_apply  every workgroup first merges its image's chunk records with
+//             Chan et al.'s pairwise update in a fixed order (so all of them
+//             get the same statistics), then the bands, then applies the
+//             per-channel scale and shift to 8 tokens with 16-byte vectors
+//             (optionally SiLU).  Workgroup 0 of an image writes the band's
+//             own statistics.  In framed mode (the input of a 3x3
+//             convolution) it writes into [B][rows+2][W+2][C], and the
+//             workgroups also fill the frame (neighbour edge rows or zeros)
+//             and export the band's own first and last rows.
 // LayerNorm: one wavefront per fp32 row, 16-byte loads, two passes over
 // registers, 8-byte bf16 stores.
 
@@ -24,25 +31,15 @@ namespace pcpp {
 namespace {
 
 constexpr int GN_THREADS = 256;
-constexpr int GN_MAX_C = 2048;     // channels (registers of gn_stats, LDS tables of gn_apply)
+constexpr int GN_MAX_C = 2048;     // channels (LDS tables of gn_apply)
 constexpr int GN_MAX_G = 256;
 constexpr int GN_TOKENS_PER_APPLY = 8;
-constexpr int GN_CHUNK_TOKENS = 16;  // tokens per statistics workgroup
+constexpr int GN_CHUNK_TOKENS = 32;  // tokens per statistics workgroup
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-// Workspace of GroupNorm, per image: [chunks][G] x (count, mean, M2), then
-// [G] x (mean, rstd).
-struct GnLayout {
-    size_t part, fin, total;
-};
-__host__ __device__ inline GnLayout gn_layout(int B, int G, int chunks) {
-    GnLayout l;
-    l.part = 0;
-    l.fin = l.part + (size_t)B * G * chunks * 3 * sizeof(float);
-    l.total = l.fin + (size_t)B * G * 2 * sizeof(float);
-    return l;
-}
+// Workspace of GroupNorm: [B][chunks][G] x (count, mean, M2).
+size_t gn_part_bytes(int B, int G, int chunks) { return (size_t)B * G * chunks * 3 * sizeof(float); }
 
 // Chan et al.'s pairwise update of (n, mean, M2) with (nb, mb, m2b).
 __device__ __forceinline__ void chan_merge(float& n, float& mean, float& m2, float nb, float mb, float m2b) {
@@ -61,16 +58,13 @@ __global__ __launch_bounds__(GN_THREADS) void gn_stats(GroupNormParams p) {
     const int ch = blockIdx.x, b = blockIdx.y;
     const int tid = threadIdx.x;
     const int C = p.C, G = p.G, cg = C / G, np = C / 2;
-    const int t0 = (int)((int64_t)p.N * ch / p.chunks);
-    const int t1 = (int)((int64_t)p.N * (ch + 1) / p.chunks);
-    const bf16* xb = p.x + (int64_t)b * p.N * C;
-    const GnLayout L = gn_layout(p.B, G, p.chunks);
-    char* ws = (char*)p.stats;
-    float* part = (float*)(ws + L.part);
+    const int t0 = ch * GN_CHUNK_TOKENS;
+    const int nt = min(GN_CHUNK_TOKENS, p.N - t0);
+    const bf16* xb = p.x + ((int64_t)b * p.N + t0) * C;
 
     // The chunk's rows, channel pairs per lane, held in registers for both
-    // passes (at most GN_CHUNK_TOKENS tokens and GN_MAX_C / 2 / GN_THREADS
-    // pairs per thread).
+    // passes (GN_CHUNK_TOKENS tokens, at most GN_MAX_C / 2 / GN_THREADS
+    // pairs per thread): all loads of a thread in flight together.
     constexpr int PP = GN_MAX_C / 2 / GN_THREADS;
     bf16x2 xv[PP][GN_CHUNK_TOKENS];
 #pragma unroll
@@ -79,7 +73,7 @@ __global__ __launch_bounds__(GN_THREADS) void gn_stats(GroupNormParams p) {
 #pragma unroll
         for (int t = 0; t < GN_CHUNK_TOKENS; ++t) {
             bf16x2 v = {};
-            if (cp < np && t0 + t < t1) v = *(const bf16x2*)(xb + (int64_t)(t0 + t) * C + 2 * cp);
+            if (cp < np && t < nt) v = *(const bf16x2*)(xb + (int64_t)t * C + 2 * cp);
             xv[k][t] = v;
         }
     }
@@ -98,12 +92,11 @@ __global__ __launch_bounds__(GN_THREADS) void gn_stats(GroupNormParams p) {
         chan_acc[2 * cp + 1] = s1;
     }
     __syncthreads();
-    const int nt = t1 - t0;
     const float n_chunk = (float)nt * (float)cg;
     for (int g = tid; g < G; g += GN_THREADS) {
         float s = 0.f;
         for (int c = g * cg; c < (g + 1) * cg; ++c) s += chan_acc[c];
-        g_mean[g] = n_chunk > 0.f ? s / n_chunk : 0.f;
+        g_mean[g] = s / n_chunk;
     }
     __syncthreads();
     // Pass 2: squared deviations from the chunk mean of the channel's group.
@@ -128,93 +121,26 @@ __global__ __launch_bounds__(GN_THREADS) void gn_stats(GroupNormParams p) {
     for (int g = tid; g < G; g += GN_THREADS) {
         float q = 0.f;
         for (int c = g * cg; c < (g + 1) * cg; ++c) q += chan_acc[c];
-        float* st = part + (((int64_t)b * p.chunks + ch) * G + g) * 3;
+        float* st = p.stats + (((int64_t)b * p.chunks + ch) * G + g) * 3;
         st[0] = n_chunk;
         st[1] = g_mean[g];
         st[2] = q;
     }
 }
 
-__global__ __launch_bounds__(GN_THREADS) void gn_finalize(GroupNormParams p) {
-    __shared__ float mrg[GN_THREADS][3];
-    const int b = blockIdx.x;
-    const int tid = threadIdx.x;
-    float* fin = (float*)((char*)p.stats + gn_layout(p.B, p.G, p.chunks).fin);
-    // Group statistics of the image from the chunk statistics, in a fixed
-    // order: thread (g, j) of S = GN_THREADS / G per group (consecutive
-    // threads take consecutive groups: coalesced loads) merges chunks j,
-    // j + S, ... (sixteen loads in flight), then thread (g, 0) merges the S
-    // results in order j = 0, 1, ...
-    const float* part = (const float*)((const char*)p.stats + gn_layout(p.B, p.G, p.chunks).part);
-    for (int g0 = 0; g0 < p.G; g0 += GN_THREADS) {
-        const int ng = min(p.G - g0, GN_THREADS);
-        const int S = GN_THREADS / ng;
-        const int g = g0 + tid % ng, j = tid / ng;
-        float n = 0.f, mean = 0.f, m2 = 0.f;
-        if (tid < ng * S) {
-            const float* st = part + ((int64_t)b * p.chunks * p.G + g) * 3;
-            for (int k0 = j; k0 < p.chunks; k0 += 16 * S) {
-                float cn[16], cm[16], cq[16];
-#pragma unroll
-                for (int u = 0; u < 16; ++u) {
-                    const int k = k0 + u * S;
-                    const bool ok = k < p.chunks;
-                    const float* r = st + (int64_t)k * p.G * 3;
-                    cn[u] = ok ? r[0] : 0.f;
-                    cm[u] = ok ? r[1] : 0.f;
-                    cq[u] = ok ? r[2] : 0.f;
-                }
-#pragma unroll
-                for (int u = 0; u < 16; ++u) chan_merge(n, mean, m2, cn[u], cm[u], cq[u]);
-            }
-        }
-        mrg[tid][0] = n;
-        mrg[tid][1] = mean;
-        mrg[tid][2] = m2;
-        __syncthreads();
-        if (tid < ng) {
-            for (int k = 1; k < S; ++k)
-                chan_merge(n, mean, m2, mrg[tid + k * ng][0], mrg[tid + k * ng][1], mrg[tid + k * ng][2]);
-            if (p.own_out != nullptr) {
-                float* o = p.own_out + ((int64_t)b * p.G + g) * 3;
-                o[0] = n;
-                o[1] = mean;
-                o[2] = m2;
-            }
-            if (p.bands != nullptr) {
-                // whole-image statistics: every band's, in band order, this
-                // band's own in its place
-                float tn = 0.f, tm = 0.f, tq = 0.f;
-                for (int j = 0; j < p.n_bands; ++j) {
-                    if (j == p.band) {
-                        chan_merge(tn, tm, tq, n, mean, m2);
-                    } else {
-                        const float* o = p.bands + (((int64_t)j * p.B + b) * p.G + g) * 3;
-                        chan_merge(tn, tm, tq, o[0], o[1], o[2]);
-                    }
-                }
-                n = tn;
-                mean = tm;
-                m2 = tq;
-            }
-            fin[((int64_t)b * p.G + g) * 2] = mean;
-            fin[((int64_t)b * p.G + g) * 2 + 1] = n > 0.f ? rsqrtf(m2 / n + p.eps) : 0.f;
-        }
-        __syncthreads();
-    }
-}
-
 __global__ __launch_bounds__(GN_THREADS) void gn_apply(GroupNormParams p) {
     __shared__ float sc[GN_MAX_C];
     __shared__ float sh[GN_MAX_C];
+    __shared__ float mrg[GN_THREADS][3];
+    __shared__ float g_mean[GN_MAX_G], g_rstd[GN_MAX_G];
     const int b = blockIdx.y;
     const int tid = threadIdx.x;
-    const int C = p.C, cg = C / p.G;
+    const int C = p.C, G = p.G, cg = C / G;
     const int tok0 = blockIdx.x * GN_TOKENS_PER_APPLY;
     const int ntok = min(GN_TOKENS_PER_APPLY, p.N - tok0);
     const int vpr = C / 8;  // 16-byte vectors per token row
     const int64_t base = ((int64_t)b * p.N + tok0) * C;
-    // The tile's vectors are loaded first, the scale/shift tables meanwhile.
+    // The tile's vectors are loaded first, the statistics merged meanwhile.
     constexpr int VPT = GN_TOKENS_PER_APPLY * GN_MAX_C / 8 / GN_THREADS;
     bf16x8 xv[VPT];
 #pragma unroll
@@ -225,13 +151,66 @@ __global__ __launch_bounds__(GN_THREADS) void gn_apply(GroupNormParams p) {
             xv[k] = *(const bf16x8*)(p.x + base + (int64_t)t * C + c);
         }
     }
-    const GnLayout L = gn_layout(p.B, p.G, p.chunks);
-    const float* fin = (const float*)((const char*)p.stats + L.fin) + (int64_t)b * p.G * 2;
+    // Thread (g, j) of S = GN_THREADS / G per group merges chunks j, j + S, ...
+    // (records of one chunk are consecutive in g: coalesced), then thread g
+    // merges the S results in order j = 0, 1, ...
+    {
+        const int S = GN_THREADS / G;
+        const int g = tid % G, j = tid / G;
+        float n = 0.f, mean = 0.f, m2 = 0.f;
+        if (j < S) {
+            const float* st = p.stats + ((int64_t)b * p.chunks * G + g) * 3;
+            for (int k0 = j; k0 < p.chunks; k0 += 8 * S) {
+                float cn[8], cm[8], cq[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int k = k0 + u * S;
+                    const bool ok = k < p.chunks;
+                    const float* r = st + (int64_t)k * G * 3;
+                    cn[u] = ok ? r[0] : 0.f;
+                    cm[u] = ok ? r[1] : 0.f;
+                    cq[u] = ok ? r[2] : 0.f;
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) chan_merge(n, mean, m2, cn[u], cm[u], cq[u]);
+            }
+        }
+        mrg[tid][0] = n;
+        mrg[tid][1] = mean;
+        mrg[tid][2] = m2;
+        __syncthreads();
+        if (tid < G) {
+            for (int k = 1; k < S; ++k) chan_merge(n, mean, m2, mrg[tid + k * G][0], mrg[tid + k * G][1], mrg[tid + k * G][2]);
+            if (p.own_out != nullptr && blockIdx.x == 0) {
+                float* o = p.own_out + ((int64_t)b * G + tid) * 3;
+                o[0] = n;
+                o[1] = mean;
+                o[2] = m2;
+            }
+            if (p.bands != nullptr) {
+                float tn = 0.f, tm = 0.f, tq = 0.f;
+                for (int jb = 0; jb < p.n_bands; ++jb) {
+                    if (jb == p.band) {
+                        chan_merge(tn, tm, tq, n, mean, m2);
+                    } else {
+                        const float* o = p.bands + (((int64_t)jb * p.B + b) * G + tid) * 3;
+                        chan_merge(tn, tm, tq, o[0], o[1], o[2]);
+                    }
+                }
+                n = tn;
+                mean = tm;
+                m2 = tq;
+            }
+            g_mean[tid] = mean;
+            g_rstd[tid] = n > 0.f ? rsqrtf(m2 / n + p.eps) : 0.f;
+        }
+        __syncthreads();
+    }
     for (int c = tid; c < C; c += GN_THREADS) {
         const int g = c / cg;
-        const float a = fin[2 * g + 1] * bf16_to_f32(p.gamma[c]);
+        const float a = g_rstd[g] * bf16_to_f32(p.gamma[c]);
         sc[c] = a;
-        sh[c] = bf16_to_f32(p.beta[c]) - fin[2 * g] * a;
+        sh[c] = bf16_to_f32(p.beta[c]) - g_mean[g] * a;
     }
     __syncthreads();
     const int pad_rows = p.pad_W > 0 ? p.N / p.pad_W : 0;
@@ -247,12 +226,48 @@ __global__ __launch_bounds__(GN_THREADS) void gn_apply(GroupNormParams p) {
                 if (p.silu) v = v * __builtin_amdgcn_rcpf(1.f + __expf(-v));
                 y[e] = f32_to_bf16(v);
             }
-            int64_t dst = base + (int64_t)t * C;
             if (p.pad_W > 0) {  // token (row, col) of image b at framed (row + 1, col + 1)
                 const int tok = tok0 + t, row = tok / p.pad_W, col = tok - row * p.pad_W;
-                dst = ((int64_t)(b * (pad_rows + 2) + row + 1) * (p.pad_W + 2) + col + 1) * C;
+                const int64_t dst = ((int64_t)(b * (pad_rows + 2) + row + 1) * (p.pad_W + 2) + col + 1) * C;
+                *(bf16x8*)(p.y + dst + c) = y;
+                if (p.edges_out != nullptr) {  // the band's first and last rows, for its neighbours
+                    if (row == 0) *(bf16x8*)(p.edges_out + ((int64_t)(2 * b) * p.pad_W + col) * C + c) = y;
+                    if (row == pad_rows - 1)
+                        *(bf16x8*)(p.edges_out + ((int64_t)(2 * b + 1) * p.pad_W + col) * C + c) = y;
+                }
+            } else {
+                *(bf16x8*)(p.y + base + (int64_t)t * C + c) = y;
             }
-            *(bf16x8*)(p.y + dst + c) = y;
+        }
+    }
+    // Framed mode: the frame of image b, spread over the image's workgroups:
+    // framed row 0 (columns 1..W) from row 1 of frame_up [B][2][W][C] or
+    // zeros, framed row rows+1 from row 0 of frame_dn or zeros, and zero
+    // columns 0 and W+1 of every framed row.
+    if (p.pad_W > 0) {
+        const int W = p.pad_W;
+        const int64_t halo = 2LL * W * vpr;
+        const int64_t total = halo + 2LL * (pad_rows + 2) * vpr;
+        bf16* fb = p.y + (int64_t)b * (pad_rows + 2) * (W + 2) * C;
+        for (int64_t u = (int64_t)blockIdx.x * GN_THREADS + tid; u < total; u += (int64_t)gridDim.x * GN_THREADS) {
+            u32x4 v = {0u, 0u, 0u, 0u};
+            int64_t dst;
+            if (u < halo) {
+                const int side = (int)(u / ((int64_t)W * vpr));
+                const int64_t jj = u - (int64_t)side * W * vpr;
+                const int x = (int)(jj / vpr), c = (int)(jj - (int64_t)x * vpr) * 8;
+                const bf16* src = side == 0 ? p.frame_up : p.frame_dn;
+                if (src != nullptr) v = *(const u32x4*)(src + ((int64_t)(2 * b + (side == 0 ? 1 : 0)) * W + x) * C + c);
+                dst = ((int64_t)(side == 0 ? 0 : pad_rows + 1) * (W + 2) + x + 1) * C + c;
+            } else {
+                const int64_t jj = u - halo;
+                const int row = (int)(jj / (2 * vpr));
+                const int rem = (int)(jj - (int64_t)row * 2 * vpr);
+                const int col = rem < vpr ? 0 : W + 1;
+                const int c = (rem < vpr ? rem : rem - vpr) * 8;
+                dst = ((int64_t)row * (W + 2) + col) * C + c;
+            }
+            *(u32x4*)(fb + dst) = v;
         }
     }
 }
@@ -317,7 +332,7 @@ int gn_chunks(int N) { return N > 0 ? (N + GN_CHUNK_TOKENS - 1) / GN_CHUNK_TOKEN
 
 }  // namespace
 
-size_t group_norm_ws_bytes(int B, int G, int N) { return gn_layout(B, G, gn_chunks(N)).total; }
+size_t group_norm_ws_bytes(int B, int G, int N) { return gn_part_bytes(B, G, gn_chunks(N)); }
 
 bool norm_shapes_ok(int C, int G) {
     return C > 0 && C % 8 == 0 && C <= GN_MAX_C && C <= 4 * 64 * LN_MAX_VEC && G > 0 && G <= GN_MAX_G && C % G == 0;
@@ -329,9 +344,6 @@ hipError_t launch_group_norm(GroupNormParams p, hipStream_t s) {
     p.chunks = gn_chunks(p.N);
     gn_stats<<<dim3(p.chunks, p.B), GN_THREADS, 0, s>>>(p);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    gn_finalize<<<p.B, GN_THREADS, 0, s>>>(p);
-    e = hipGetLastError();
     if (e != hipSuccess) return e;
     gn_apply<<<dim3((p.N + GN_TOKENS_PER_APPLY - 1) / GN_TOKENS_PER_APPLY, p.B), GN_THREADS, 0, s>>>(p);
     return hipGetLastError();

@@ -11,10 +11,12 @@
 //   F2 = frame(SiLU(GroupNorm(h1)))       bf16
 //   s  = x Ws^T + bs  (C_in != C_out)     fp32, else s = x
 //   y  = conv3x3(F2) + b2 + s             bf16  (epilogue residual)
-// frame(): GroupNorm's apply writes the band inside a zero frame one token
-// wide; the top frame row takes the band above's last edge row, the bottom
-// one the band below's first (zeros at the image's edges), so every tap of
-// the convolution is one constant offset from a token's framed position.
+// frame(): GroupNorm's apply writes the band inside a frame one token wide:
+// the top frame row takes the band above's last edge row, the bottom one the
+// band below's first (zeros at the image's edges), the side columns zeros, so
+// every tap of the convolution is one constant offset from a token's framed
+// position.  The same kernel exports the band's own first and last rows of
+// each convolution input for its neighbours.
 
 #include <math.h>
 #include <stdint.h>
@@ -31,39 +33,6 @@ namespace pcpp {
 namespace {
 
 constexpr int kThreads = 256;
-
-// Writes the frame of [B][h+2][W+2][C]: framed row 0 (columns 1..W) from
-// row 1 of edges_up [B][2][W][C] or zeros, framed row h+1 from row 0 of
-// edges_dn or zeros, and zero columns 0 and W+1 of every framed row.
-__global__ __launch_bounds__(kThreads) void frame_band(bf16* f, const bf16* edges_up, const bf16* edges_dn,
-                                                       int h, int W, int C) {
-    const int b = blockIdx.y;
-    const int vpt = C / 8;
-    const int64_t halo = 2LL * W * vpt;
-    const int64_t total = halo + 2LL * (h + 2) * vpt;
-    bf16* fb = f + (int64_t)b * (h + 2) * (W + 2) * C;
-    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < total; i += (int64_t)gridDim.x * kThreads) {
-        u32x4 v = {0u, 0u, 0u, 0u};
-        int64_t dst;
-        if (i < halo) {
-            const int side = (int)(i / ((int64_t)W * vpt));
-            const int64_t j = i - (int64_t)side * W * vpt;
-            const int x = (int)(j / vpt), c = (int)(j - (int64_t)x * vpt) * 8;
-            const bf16* src = side == 0 ? edges_up : edges_dn;
-            if (src != nullptr)
-                v = *(const u32x4*)(src + ((int64_t)(2 * b + (side == 0 ? 1 : 0)) * W + x) * C + c);
-            dst = ((int64_t)(side == 0 ? 0 : h + 1) * (W + 2) + x + 1) * C + c;
-        } else {
-            const int64_t j = i - halo;
-            const int row = (int)(j / (2 * vpt));
-            const int rem = (int)(j - (int64_t)row * 2 * vpt);
-            const int col = rem < vpt ? 0 : W + 1;
-            const int c = (rem < vpt ? rem : rem - vpt) * 8;
-            dst = ((int64_t)row * (W + 2) + col) * C + c;
-        }
-        *(u32x4*)(fb + dst) = v;
-    }
-}
 
 // tb[b][n] = bt[n] + sum_k SiLU(temb[b][k]) Wt[n][k]: one wavefront per
 // output, 16-byte chunks of k per lane.
@@ -205,6 +174,16 @@ PCPP_EXPORT int pcpp_resnet_block(const pcpp_resnet_geom_t* g, const pcpp_resnet
     const void* fptrs[] = {gn1_bands, gn1_own, gn2_bands, gn2_own};
     for (const void* p : fptrs)
         if (p && ((uintptr_t)p & 3u) != 0) return PCPP_EINVAL;
+    // the exports are written while the neighbours' rows are read: no overlap
+    auto overlap = [](const void* a, const void* b, int64_t n) {
+        return a && b && (uintptr_t)a < (uintptr_t)b + (uintptr_t)n && (uintptr_t)b < (uintptr_t)a + (uintptr_t)n;
+    };
+    const int64_t e1 = 4LL * g->batch * g->W * g->c_in, e2 = 4LL * g->batch * g->W * g->c_out;
+    if (overlap(edges1_out, edges1_up, e1) || overlap(edges1_out, edges1_dn, e1) ||
+        overlap(edges2_out, edges2_up, e2) || overlap(edges2_out, edges2_dn, e2) ||
+        (edges1_out && edges2_out && (uintptr_t)edges1_out < (uintptr_t)edges2_out + (uintptr_t)e2 &&
+         (uintptr_t)edges2_out < (uintptr_t)edges1_out + (uintptr_t)e1))
+        return PCPP_EINVAL;
     const ResLayout L = res_layout(g);
     if (workspace == nullptr || ws_bytes < L.total) return PCPP_EWORKSPACE;
     if (!aligned16(workspace)) return PCPP_EINVAL;
@@ -224,7 +203,7 @@ PCPP_EXPORT int pcpp_resnet_block(const pcpp_resnet_geom_t* g, const pcpp_resnet
     } while (0)
 
     auto norm = [&](const void* in, int C, const void* gamma, const void* beta, const float* bands, float* own,
-                    bf16* framed) {
+                    bf16* framed, const void* up, const void* dn, void* edges_out) {
         GroupNormParams gp;
         gp.x = (const __bf16*)in;
         gp.y = framed;
@@ -242,19 +221,13 @@ PCPP_EXPORT int pcpp_resnet_block(const pcpp_resnet_geom_t* g, const pcpp_resnet
         gp.own_out = own;
         gp.silu = 1;
         gp.pad_W = W;
+        gp.frame_up = has_up ? (const bf16*)up : nullptr;
+        gp.frame_dn = has_dn ? (const bf16*)dn : nullptr;
+        gp.edges_out = (bf16*)edges_out;
         return launch_group_norm(gp, s);
     };
-    auto frame = [&](bf16* framed, const void* up, const void* dn, int C) {
-        const int64_t units = (2LL * W + 2LL * (h + 2)) * (C / 8);
-        int blocks = (int)((units + kThreads - 1) / kThreads);
-        blocks = blocks > 1024 ? 1024 : blocks;
-        frame_band<<<dim3(blocks, B), kThreads, 0, s>>>(framed, has_up ? (const bf16*)up : nullptr,
-                                                         has_dn ? (const bf16*)dn : nullptr, h, W, C);
-        return hipGetLastError();
-    };
 
-    PCPP_CHECK(norm(x, Ci, w->gn1_gamma, w->gn1_beta, gn1_bands, gn1_own, f1));
-    PCPP_CHECK(frame(f1, edges1_up, edges1_dn, Ci));
+    PCPP_CHECK(norm(x, Ci, w->gn1_gamma, w->gn1_beta, gn1_bands, gn1_own, f1, edges1_up, edges1_dn, edges1_out));
     void* split_ws = L.split_bytes ? ws + L.split : nullptr;
     temb_proj<<<(B * Co + 3) / 4, kThreads, 0, s>>>(tb, (const bf16*)temb, (const bf16*)w->temb_w,
                                                    (const bf16*)w->temb_b, B, Co, g->temb_dim, (int*)split_ws,
@@ -266,8 +239,7 @@ PCPP_EXPORT int pcpp_resnet_block(const pcpp_resnet_geom_t* g, const pcpp_resnet
     c1.split_ws = split_ws;
     c1.split_ws_bytes = L.split_bytes;
     PCPP_CHECK(launch_gemm(c1, s));
-    PCPP_CHECK(norm(h1, Co, w->gn2_gamma, w->gn2_beta, gn2_bands, gn2_own, f2));
-    PCPP_CHECK(frame(f2, edges2_up, edges2_dn, Co));
+    PCPP_CHECK(norm(h1, Co, w->gn2_gamma, w->gn2_beta, gn2_bands, gn2_own, f2, edges2_up, edges2_dn, edges2_out));
     if (proj_skip) {
         GemmParams sp = conv_params(x, w->skip_w, w->skip_b, rows, Co, Ci, 0, 0, skip);
         sp.lda = Ci;
@@ -281,26 +253,6 @@ PCPP_EXPORT int pcpp_resnet_block(const pcpp_resnet_geom_t* g, const pcpp_resnet
     c2.split_ws = split_ws;
     c2.split_ws_bytes = L.split_bytes;
     PCPP_CHECK(launch_gemm(c2, s));
-    // This band's edge rows of both convolution inputs, for its neighbours.
-    if (edges1_out || edges2_out) {
-        CopyParams cp;
-        cp.n_seg = 0;
-        cp.batch = B;
-        auto add = [&](const bf16* framed, int C, void* out) {
-            const int64_t fstride = (int64_t)(h + 2) * (W + 2) * C * 2, row = (int64_t)W * C * 2;
-            for (int side = 0; side < 2; ++side) {
-                CopySeg& sg = cp.seg[cp.n_seg++];
-                sg.src = (const char*)framed + ((int64_t)(side == 0 ? 1 : h) * (W + 2) + 1) * C * 2;
-                sg.dst = (char*)out + side * row;
-                sg.src_bstride = fstride;
-                sg.dst_bstride = 2 * row;
-                sg.bytes = row;
-            }
-        };
-        if (edges1_out) add(f1, Ci, edges1_out);
-        if (edges2_out) add(f2, Co, edges2_out);
-        PCPP_CHECK(launch_seg_copy(cp, 2, s));
-    }
 #undef PCPP_CHECK
     return PCPP_OK;
 }

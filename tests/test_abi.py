@@ -314,6 +314,8 @@ def test_resnet_geometry_and_validation():
     a = list(ok_args); a[6] = FAKE + 2                               # misaligned statistics
     assert call(g, w, *a) == pcpp.PCPP_EINVAL
     assert call(g2, w, *ok_args) == pcpp.PCPP_EINVAL                 # 320 -> 640 needs the shortcut weights
+    a = list(ok_args); a[2] = FAKE + (1 << 28); a[11] = FAKE + (1 << 28) + 4096   # export over the rows above
+    assert call(g, w, *a) == pcpp.PCPP_EINVAL
 
 
 def test_guided_step_validation():
