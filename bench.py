@@ -338,7 +338,25 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
     out["block_TFLOPs"] = round(block_flops(bc, nkvb) / us / 1e6, 1)
     out["block_gflop"] = round(block_flops(bc, nkvb) / 1e9, 2)
 
-    # ResNet blocks of the same level (bf16, batch 1: one guidance branch per device)
+    # the block at the second transformer level (1280 channels, 20 heads)
+    bc2 = synth.BLOCK_CONFIG_L2
+    c2 = bc2.attn
+    b2 = {k: to_dev(v) for k, v in synth.block_inputs(bc2).items()}
+    g2 = pcpp.make_geom(c2.H, c2.W, c2.n, c2.i, c2.p, c2.heads, c2.d, 1, 0, pcpp.PCPP_DTYPE_BF16)
+    _, _, _, nkv2 = pcpp.pcpp_context_rows(g2)
+    w2 = pcpp.make_block_weights(b2, bc2.ff_inner, bc2.gn_groups)
+    y2, k2o, v2o = (torch.empty_like(b2["x"]) for _ in range(3))
+    ws2b = pcpp.pcpp_transformer_block_workspace_size(g2, w2, bc2.n_text, bc2.text_dim)
+    ws2 = torch.zeros(ws2b, dtype=torch.uint8, device=dev)
+    us = graph_time_us(torch, lambda: pcpp.pcpp_transformer_block(g2, w2, b2["x"], b2["text"], bc2.n_text,
+                                                                  bc2.text_dim, b2["k_up"], b2["v_up"], b2["k_dn"],
+                                                                  b2["v_dn"], y2, k2o, v2o, ws2, ws2b),
+                       max(reps // 4, 1), use_graph)
+    out["block_l2_us"] = round(us, 3)
+    out["block_l2_TFLOPs"] = round(block_flops(bc2, nkv2) / us / 1e6, 1)
+    out["block_l2_gflop"] = round(block_flops(bc2, nkv2) / 1e9, 2)
+
+    # ResNet blocks of the three levels (bf16, batch 1: one guidance branch per device)
     for name, rc in synth.RESNET_CONFIGS.items():
         fn, keep = resnet_call(torch, pcpp, synth, rc, dev)
         us = graph_time_us(torch, fn, max(reps // 4, 1), use_graph)
@@ -433,7 +451,8 @@ def pmc_summarize(fetch_dir, write_dir):
 
 def block_run(args):
     """Workload for a kernel-trace profile of the transformer block: --steps
-    calls of pcpp_transformer_block on the 2048 px level-1 band, nothing else."""
+    calls of pcpp_transformer_block on the 2048 px level-1 band (--level 2:
+    the level-2 band), nothing else."""
     import numpy as np
     import torch
 
@@ -441,7 +460,7 @@ def block_run(args):
     dev = "cuda:0"
     to_dev = lambda x: None if x is None else torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(
         torch.bfloat16).to(dev)
-    bc = synth.BLOCK_CONFIG
+    bc = synth.BLOCK_CONFIG_L2 if args.level == 2 else synth.BLOCK_CONFIG
     c = bc.attn
     bi = {k: to_dev(v) for k, v in synth.block_inputs(bc).items()}
     g = pcpp.make_geom(c.H, c.W, c.n, c.i, c.p, c.heads, c.d, 1, 0, pcpp.PCPP_DTYPE_BF16)
@@ -532,6 +551,7 @@ def main():
                     help="write the traffic summary from two rocprofv3 --pmc output folders")
     ap.add_argument("--block-run", action="store_true",
                     help="profiling workload: --steps transformer-block calls, nothing else")
+    ap.add_argument("--level", type=int, default=1, choices=(1, 2), help="transformer level of --block-run")
     ap.add_argument("--resnet-run", action="store_true",
                     help="profiling workload: --steps calls of each ResNet block, nothing else")
     ap.add_argument("--gemm-calibration", action="store_true",

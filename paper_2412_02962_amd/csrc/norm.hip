@@ -5,7 +5,8 @@
 // (synchronized GroupNorm, Sec. 3.3 of arXiv 2412.02962: every band's
 // (count, mean, M2) merged in band order, this band's own in its place).
 // Two kernels:
-//   gn_stats  one workgroup per chunk of 32 tokens, held in registers
+//   gn_stats  one workgroup per chunk of 32 tokens (8 for bands under 2048
+//             tokens), held in registers
 //             (coalesced channel pairs), reduced to per-group (count, mean,
 //             M2) with two passes over the registers (sum, then squared
 //             deviations from the chunk mean).
@@ -34,7 +35,12 @@ constexpr int GN_THREADS = 256;
 constexpr int GN_MAX_C = 2048;     // channels (LDS tables of gn_apply)
 constexpr int GN_MAX_G = 256;
 constexpr int GN_TOKENS_PER_APPLY = 8;
-constexpr int GN_CHUNK_TOKENS = 32;  // tokens per statistics workgroup
+// Tokens per statistics workgroup: 32, or 8 when a band has fewer than
+// 2048 tokens (so that it still gives about 64 or more workgroups per image
+// while the apply merges few chunk records).
+constexpr int GN_CHUNK_LONG = 32;
+constexpr int GN_CHUNK_SHORT = 8;
+__host__ __device__ inline int gn_chunk_tokens(int N) { return N >= 64 * GN_CHUNK_LONG ? GN_CHUNK_LONG : GN_CHUNK_SHORT; }
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
@@ -52,6 +58,7 @@ __device__ __forceinline__ void chan_merge(float& n, float& mean, float& m2, flo
     n = nn;
 }
 
+template <int GN_CHUNK_TOKENS>
 __global__ __launch_bounds__(GN_THREADS) void gn_stats(GroupNormParams p) {
     __shared__ float chan_acc[GN_MAX_C];
     __shared__ float g_mean[GN_MAX_G];
@@ -328,7 +335,10 @@ __global__ __launch_bounds__(256) void ln_kernel(LayerNormParams p) {
     }
 }
 
-int gn_chunks(int N) { return N > 0 ? (N + GN_CHUNK_TOKENS - 1) / GN_CHUNK_TOKENS : 1; }
+int gn_chunks(int N) {
+    const int ct = gn_chunk_tokens(N);
+    return N > 0 ? (N + ct - 1) / ct : 1;
+}
 
 }  // namespace
 
@@ -342,7 +352,10 @@ hipError_t launch_group_norm(GroupNormParams p, hipStream_t s) {
     if (!norm_shapes_ok(p.C, p.G)) return hipErrorInvalidValue;
     if (p.pad_W < 0 || (p.pad_W > 0 && p.N % p.pad_W != 0)) return hipErrorInvalidValue;
     p.chunks = gn_chunks(p.N);
-    gn_stats<<<dim3(p.chunks, p.B), GN_THREADS, 0, s>>>(p);
+    if (gn_chunk_tokens(p.N) == GN_CHUNK_LONG)
+        gn_stats<GN_CHUNK_LONG><<<dim3(p.chunks, p.B), GN_THREADS, 0, s>>>(p);
+    else
+        gn_stats<GN_CHUNK_SHORT><<<dim3(p.chunks, p.B), GN_THREADS, 0, s>>>(p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     gn_apply<<<dim3((p.N + GN_TOKENS_PER_APPLY - 1) / GN_TOKENS_PER_APPLY, p.B), GN_THREADS, 0, s>>>(p);

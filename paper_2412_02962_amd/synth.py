@@ -111,6 +111,15 @@ BLOCK_CONFIG = BlockConfig(
     attn=_cfg("sdxl2048_block_attn", 128, 128, 8, 3, 0.25, 10, 64, DTYPE_BF16, 5),
 )
 
+# The same block at the second transformer level (64 x 64 tokens of 1280
+# channels, 20 heads, feed-forward 4 x 1280), interior band 3 of 8.
+BLOCK_CONFIG_L2 = BlockConfig(
+    name="sdxl2048_l2_block",
+    attn=_cfg("sdxl2048_l2_block_attn", 64, 64, 8, 3, 0.25, 20, 64, DTYPE_BF16, 6),
+    ff_inner=5120,
+    seed_id=6,
+)
+
 # Input variants.
 #   "unit"      : Q, K, V ~ N(0,1); the kernel's 1/sqrt(d) makes logits unit-std
 #   "prescaled" : Q, K, V ~ N(0,1)/sqrt(d) as well (near-uniform softmax)
@@ -297,6 +306,12 @@ class ResnetConfig:
 RESNET_CONFIGS = {
     "sdxl2048_l1_res640": ResnetConfig("sdxl2048_l1_res640", 128, 128, 8, 3, 640, 640, seed_id=80),
     "sdxl2048_l1_res320_640": ResnetConfig("sdxl2048_l1_res320_640", 128, 128, 8, 3, 320, 640, seed_id=81),
+    # the other levels of the 2048 px image: 256 x 256 tokens of 320 channels
+    # (no attention there), 64 x 64 tokens of 1280 channels (and the ResNet
+    # entering it from 640 channels)
+    "sdxl2048_l0_res320": ResnetConfig("sdxl2048_l0_res320", 256, 256, 8, 3, 320, 320, seed_id=89),
+    "sdxl2048_l2_res1280": ResnetConfig("sdxl2048_l2_res1280", 64, 64, 8, 3, 1280, 1280, seed_id=90),
+    "sdxl2048_l2_res640_1280": ResnetConfig("sdxl2048_l2_res640_1280", 64, 64, 8, 3, 640, 1280, seed_id=91),
 }
 
 

@@ -75,8 +75,8 @@ def _check_kv(got, want, tag):
     _check(got, want, stages=3, tag=tag)
 
 
-def test_block_matches_oracle_at_2048px():
-    bc = synth.BLOCK_CONFIG
+@pytest.mark.parametrize("bc", [synth.BLOCK_CONFIG, synth.BLOCK_CONFIG_L2], ids=lambda b: b.name)
+def test_block_matches_oracle_at_2048px(bc):
     _say("block", bc.name)
     inp = synth.block_inputs(bc)
     y, k, v = _run_block(bc, inp, 1)

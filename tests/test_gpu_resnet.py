@@ -44,7 +44,9 @@ SMALL = [
     # conv1 (K = 9 * 1024) splits K eight ways over 32 tiles: the whole device
     synth.ResnetConfig("r_split", 32, 128, 2, 1, 1024, 256, temb_dim=64, groups=32, batch=1, seed_id=88),
 ]
-FULL = [synth.RESNET_CONFIGS["sdxl2048_l1_res640"], synth.RESNET_CONFIGS["sdxl2048_l1_res320_640"]]
+FULL = [synth.RESNET_CONFIGS["sdxl2048_l1_res640"], synth.RESNET_CONFIGS["sdxl2048_l1_res320_640"],
+        synth.RESNET_CONFIGS["sdxl2048_l0_res320"], synth.RESNET_CONFIGS["sdxl2048_l2_res1280"],
+        synth.RESNET_CONFIGS["sdxl2048_l2_res640_1280"]]
 
 
 def _say(*a):
