@@ -32,6 +32,7 @@ from .pcpp_oracle import (  # noqa: F401
 from .unet_oracle import (  # noqa: F401
     RESNET_GN_EPS,
     conv3x3_band,
+    conv3x3_band_mode,
     edge_rows,
     guided_noise,
     pad_band,

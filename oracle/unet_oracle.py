@@ -80,6 +80,38 @@ def conv3x3_band(x: np.ndarray, W: int, w: np.ndarray, b: Optional[np.ndarray],
     return out.reshape(B, N, w.shape[0])
 
 
+def conv3x3_band_mode(x: np.ndarray, W: int, w: np.ndarray, b: Optional[np.ndarray],
+                      row_up: Optional[np.ndarray], row_dn: Optional[np.ndarray], mode: str) -> np.ndarray:
+    """The U-Net's three 3x3 convolutions on a band x [B, h*W, C_in] (R19):
+    'same'  stride 1 (ResNets, conv_in, conv_out): rows row_up / row_dn
+            [B, W, C_in] (the neighbours' adjacent rows, or zeros) frame the band;
+    'down'  stride 2, padding 1 (SDXL's downsampler): output (y, x) reads
+            input rows 2y-1 .. 2y+1 and columns 2x-1 .. 2x+1, so only the row
+            above is read; h and W even; output [B, (h/2)*(W/2), C_out];
+    'up'    nearest 2x upsampling, then stride 1 (SDXL's upsampler): every
+            input token becomes a 2 x 2 block, the neighbours' rows are
+            upsampled the same way; output [B, (2h)*(2W), C_out]."""
+    B, N, C = x.shape
+    h = N // W
+    if mode == "same":
+        return conv3x3_band(x, W, w, b, row_up, row_dn)
+    if mode == "down":
+        xp = pad_band(x, W, row_up, None)           # [B, h+2, W+2, C]
+        ho, wo = h // 2, W // 2
+        out = np.zeros((B, ho, wo, w.shape[0]))
+        for ky in range(3):
+            for kx in range(3):
+                out += xp[:, ky:ky + 2 * ho:2, kx:kx + 2 * wo:2, :] @ w[:, ky, kx, :].T
+        if b is not None:
+            out += b
+        return out.reshape(B, ho * wo, w.shape[0])
+    if mode == "up":
+        g = np.repeat(np.repeat(x.reshape(B, h, W, C), 2, axis=1), 2, axis=2).reshape(B, 4 * N, C)
+        up2 = lambda r: None if r is None else np.repeat(r, 2, axis=1)
+        return conv3x3_band(g, 2 * W, w, b, up2(row_up), up2(row_dn))
+    raise ValueError(mode)
+
+
 def edge_rows(a: np.ndarray, W: int) -> np.ndarray:
     """What a band exports for its neighbours' next 3x3 convolution: its
     first and last rows of the convolution input a [B, h*W, C], as

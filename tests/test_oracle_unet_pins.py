@@ -12,7 +12,11 @@
       x_t exactly to the previous noise level; Eq. 2 at s = 0 / 1 gives the
       unconditional / conditional prediction
   U5  planted mistakes (tap order, halo sides, temb SiLU, shortcut, Eq. 3
-      coefficient, DDIM re-noising) fail the pins
+      coefficient, DDIM re-noising, stride-2 grid, upsampled grid) fail the pins
+  U6  the stride-2 (downsampling) and nearest-2x-then-conv (upsampling)
+      convolutions of every band, given the true neighbour rows, reproduce
+      torch's whole-image conv2d (stride 2) and interpolate + conv2d; the
+      stride-2 band never reads the row below
 """
 
 import math
@@ -174,6 +178,8 @@ def _battery():
         test_u2_whole_image_resnet_is_torchs(8, 8)
         test_u3_bands_with_true_edges_and_statistics_rebuild_the_whole_block(3, 8, 12)
         test_u4_reverse_steps_against_closed_forms()
+        test_u6_band_downsample_is_the_whole_image_stride2_conv(1, 12, 8, 3, 5, 3)
+        test_u6_band_upsample_is_the_whole_image_nearest_then_conv(1, 6, 4, 3, 5, 3)
     except AssertionError:
         return False
     return True
@@ -184,7 +190,34 @@ def test_u5_unmodified_oracle_passes():
 
 
 _ORIG = {k: getattr(uo, k) for k in ("conv3x3_band", "pad_band", "silu", "linear", "reverse_step_ddpm",
-                                      "reverse_step_ddim", "edge_rows")}
+                                      "reverse_step_ddim", "edge_rows", "conv3x3_band_mode")}
+
+
+def _down_grid_shifted(x, W, w, b, up, dn, mode):      # stride-2 grid one input row lower
+    if mode != "down":
+        return _ORIG["conv3x3_band_mode"](x, W, w, b, up, dn, mode)
+    B, N, C = x.shape
+    h = N // W
+    xp = np.zeros((B, h + 2, W + 2, C))
+    xp[:, 1:h + 1, 1:W + 1] = x.reshape(B, h, W, C)
+    if up is not None:
+        xp[:, 0, 1:W + 1] = up
+    ho, wo = h // 2, W // 2
+    out = np.zeros((B, ho, wo, w.shape[0]))
+    for ky in range(3):
+        for kx in range(3):
+            out += xp[:, ky + 1:ky + 1 + 2 * ho:2, kx:kx + 2 * wo:2, :] @ w[:, ky, kx, :].T
+    return (out + b).reshape(B, ho * wo, w.shape[0])
+
+
+def _up_shifted_columns(x, W, w, b, up, dn, mode):     # upsampled grid shifted by one column
+    if mode != "up":
+        return _ORIG["conv3x3_band_mode"](x, W, w, b, up, dn, mode)
+    B, N, C = x.shape
+    h = N // W
+    g = np.roll(np.repeat(np.repeat(x.reshape(B, h, W, C), 2, axis=1), 2, axis=2), 1, axis=2).reshape(B, 4 * N, C)
+    up2 = lambda r: None if r is None else np.repeat(r, 2, axis=1)
+    return uo.conv3x3_band(g, 2 * W, w, b, up2(up), up2(dn))
 
 
 def _conv_taps_transposed(x, W, w, b, up, dn):
@@ -244,7 +277,53 @@ def _resnet_temb_without_silu(W, wts, x, temb, *a, **k):
     ("reverse_step_ddim", _ddim_no_renoise),
     ("resnet_block", _resnet_shortcut_of_normed),
     ("resnet_block", _resnet_temb_without_silu),
+    ("conv3x3_band_mode", _down_grid_shifted),
+    ("conv3x3_band_mode", _up_shifted_columns),
 ])
 def test_u5_planted_mistakes_are_caught(monkeypatch, name, mutant):
     monkeypatch.setattr(uo, name, mutant)
     assert not _battery()
+
+
+# ---------------------------------------------------------------------------
+# U6: the downsampling and upsampling convolutions of the U-Net, per band
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("B,H,W,ci,co,n", [(1, 12, 8, 3, 5, 3), (2, 8, 6, 4, 4, 4), (1, 6, 10, 2, 3, 1),
+                                           (1, 16, 4, 3, 2, 2)])
+def test_u6_band_downsample_is_the_whole_image_stride2_conv(B, H, W, ci, co, n):
+    rng = np.random.default_rng(11)
+    img = rng.standard_normal((B, H, W, ci))
+    w = rng.standard_normal((co, 3, 3, ci))
+    b = rng.standard_normal(co)
+    x = torch.from_numpy(img).permute(0, 3, 1, 2)
+    k = torch.from_numpy(np.ascontiguousarray(w.transpose(0, 3, 1, 2)))
+    want = F.conv2d(x, k, torch.from_numpy(b), stride=2, padding=1).permute(0, 2, 3, 1).numpy()
+    h = H // n
+    for i, xb in enumerate(_bands(img, n)):
+        up = img[:, i * h - 1] if i > 0 else None
+        got = uo.conv3x3_band_mode(xb, W, w, b, up, None, "down")
+        assert np.allclose(got.reshape(B, h // 2, W // 2, co), want[:, i * h // 2:(i + 1) * h // 2],
+                           rtol=1e-12, atol=1e-12), i
+        # the row below never matters
+        dn = rng.standard_normal((B, W, ci))
+        assert np.array_equal(uo.conv3x3_band_mode(xb, W, w, b, up, dn, "down"), got)
+
+
+@pytest.mark.parametrize("B,H,W,ci,co,n", [(1, 6, 4, 3, 5, 3), (2, 4, 3, 4, 4, 4), (1, 3, 5, 2, 3, 1)])
+def test_u6_band_upsample_is_the_whole_image_nearest_then_conv(B, H, W, ci, co, n):
+    rng = np.random.default_rng(12)
+    img = rng.standard_normal((B, H, W, ci))
+    w = rng.standard_normal((co, 3, 3, ci))
+    b = rng.standard_normal(co)
+    x = torch.from_numpy(img).permute(0, 3, 1, 2)
+    k = torch.from_numpy(np.ascontiguousarray(w.transpose(0, 3, 1, 2)))
+    want = F.conv2d(F.interpolate(x, scale_factor=2.0, mode="nearest"), k, torch.from_numpy(b), padding=1)
+    want = want.permute(0, 2, 3, 1).numpy()
+    h = H // n
+    for i, xb in enumerate(_bands(img, n)):
+        up = img[:, i * h - 1] if i > 0 else None
+        dn = img[:, (i + 1) * h] if i < n - 1 else None
+        got = uo.conv3x3_band_mode(xb, W, w, b, up, dn, "up")
+        assert np.allclose(got.reshape(B, 2 * h, 2 * W, co), want[:, 2 * i * h:2 * (i + 1) * h],
+                           rtol=1e-12, atol=1e-12), i
