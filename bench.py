@@ -364,6 +364,20 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
         out[f"resnet_{name}_TFLOPs"] = round(resnet_flops(rc) / us / 1e6, 1)
         del keep
 
+    # the U-Net's resolution-changing convolutions (2048 px, 8 bands, band 3)
+    for name, (H, W, n, i, ci, co, mode) in synth.CONV_CONFIGS.items():
+        d = {k: to_dev(v) for k, v in synth.conv_inputs(H, W, n, i, ci, co, 1, 60).items()}
+        g = pcpp.make_conv_geom(H, W, n, i, ci, co, 1, mode)
+        h = H // n
+        tokens = {0: h * W, 1: (h // 2) * (W // 2), 2: 4 * h * W}[mode]
+        y = torch.empty((1, tokens, co), dtype=torch.bfloat16, device=dev)
+        wsb = pcpp.pcpp_conv3x3_workspace_size(g)
+        ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+        us = graph_time_us(torch, lambda: pcpp.pcpp_conv3x3(g, d["x"], d["row_up"], d["row_dn"], d["w"], d["b"], y,
+                                                            ws, wsb), max(reps // 4, 1), use_graph)
+        out[f"conv_{name}_us"] = round(us, 3)
+        out[f"conv_{name}_TFLOPs"] = round(2.0 * tokens * 9 * ci * co / us / 1e6, 1)
+
     # the latent update of one band of the 2048 px image (latent 256 x 256 x 4, 8 bands)
     n = 256 // 8 * 256 * 4
     lat = [torch.randn(n, dtype=torch.float32, device=dev) for _ in range(4)]

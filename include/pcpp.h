@@ -447,6 +447,55 @@ int pcpp_resnet_block(const pcpp_resnet_geom_t* g, const pcpp_resnet_weights_t* 
                       void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * The U-Net's 3x3 convolutions on one row band (Sec. 3.3 keeps the exchange
+ * of boundary pixels for convolutions): the row directly above the band and
+ * the row directly below it come from the neighbours (their last / first
+ * row of the convolution input, as exchanged), zeros at the image's edges
+ * and at the left and right.  Weights [c_out][3][3][c_in] bf16 (element
+ * (o, ky, kx, c) at ((o * 3 + ky) * 3 + kx) * c_in + c), bias [c_out] or
+ * NULL; bf16 storage, float32 accumulation.
+ *   PCPP_CONV_SAME  stride 1: y [B, h*W, c_out]
+ *   PCPP_CONV_DOWN  stride 2, padding 1 (SDXL's downsampler): output (y, x)
+ *                   reads input rows 2y-1 .. 2y+1 of the band, so only the
+ *                   row above is needed; h and W even; y [B, (h/2)*(W/2), c_out]
+ *   PCPP_CONV_UP    nearest 2x upsampling, then stride 1 (SDXL's upsampler):
+ *                   the neighbour rows are upsampled the same way;
+ *                   y [B, (2h)*(2W), c_out]
+ */
+#define PCPP_CONV_SAME 0
+#define PCPP_CONV_DOWN 1
+#define PCPP_CONV_UP   2
+
+typedef struct {
+    int32_t H, W;          /* the input's token grid                         */
+    int32_t n_patches;     /* n, H % n == 0                                  */
+    int32_t patch_idx;     /* band i, 0-based                                */
+    int32_t c_in, c_out;   /* multiples of 64                                */
+    int32_t batch;         /* images B, <= 65535                             */
+    int32_t mode;          /* PCPP_CONV_SAME, PCPP_CONV_DOWN or PCPP_CONV_UP */
+    int32_t reserved;      /* must be 0                                      */
+} pcpp_conv_geom_t;
+
+/* Bytes of device workspace pcpp_conv3x3 needs (0 if g is invalid).  The
+ * workspace needs no clearing; nothing in it survives a call. */
+size_t pcpp_conv3x3_workspace_size(const pcpp_conv_geom_t* g);
+
+/*
+ *   x       [B, h*W, c_in] bf16 band tokens (h = H / n)
+ *   row_up  [B, W, c_in] the row above the band (the band above's last row);
+ *           needed when i > 0, else ignored
+ *   row_dn  [B, W, c_in] the row below (the band below's first row); needed
+ *           when i < n-1 for SAME and UP, ignored for DOWN
+ *   w, bias, y as above; all pointers 16-byte aligned, y must not overlap
+ *           the inputs.
+ * Errors: PCPP_EINVAL (geometry, NULL or misaligned pointers), PCPP_ENOTSUP
+ * (channels not multiples of 64), PCPP_EWORKSPACE.  Asynchronous on `stream`.
+ */
+int pcpp_conv3x3(const pcpp_conv_geom_t* g, const void* x, const void* row_up,
+                 const void* row_dn, const void* w, const void* bias, void* y,
+                 void* workspace, size_t ws_bytes, void* stream);
+
+/*
  * The update of a band's latent at the end of a step (Sec. 3.1): the two
  * guidance branches' noise predictions are combined by classifier-free
  * guidance (Eq. 2), e = eps_u + s (eps_c - eps_u), and then

@@ -30,6 +30,9 @@ struct GemmParams {
     // unused), token m is (b, y, x) of [B][conv_rows][conv_W], and
     // K = 9 * C_in with k = (3 ky + kx) * C_in + c; C_in % 64 == 0.
     int32_t conv_W = 0, conv_rows = 0;
+    // 2: stride 2 (conv_rows and conv_W even): output token (b, y, x) of
+    // [B][conv_rows / 2][conv_W / 2] has its tap (0, 0) at framed (2y, 2x).
+    int32_t conv_stride = 1;
     // Optional per-image float bias added to output n of token m:
     // bias2[(m / bias2_rows) * N + n] (16-byte aligned), or null.
     const float* bias2 = nullptr;

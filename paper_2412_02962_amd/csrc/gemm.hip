@@ -308,11 +308,13 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
         const int m = min(m0 + r, p.M - 1);
         const int c = (lane & 7) ^ ((r >> 1) & 7);
         int64_t row = (int64_t)m * p.lda;
-        if constexpr (CONV) {  // the tap (0, 0) of token (b, y, x) sits at framed (y, x)
-            const int per = p.conv_rows * p.conv_W;
+        if constexpr (CONV) {  // the tap (0, 0) of output token (b, y, x) sits at framed (s y, s x)
+            const int st = p.conv_stride;
+            const int wo = p.conv_W / st;
+            const int per = (p.conv_rows / st) * wo;
             const int b = m / per, rem = m - b * per;
-            const int y = rem / p.conv_W, x = rem - y * p.conv_W;
-            row = ((int64_t)(b * (p.conv_rows + 2) + y) * (p.conv_W + 2) + x) * cin;
+            const int y = rem / wo, x = rem - y * wo;
+            row = ((int64_t)(b * (p.conv_rows + 2) + st * y) * (p.conv_W + 2) + st * x) * cin;
         }
         xsrc[i] = (const char*)p.a + (row + 8 * c) * 2;
     }
@@ -611,9 +613,12 @@ hipError_t launch_shape(const GemmParams& p, hipStream_t s) {
 bool gemm_shape_ok(const GemmParams& p) {
     if (p.K % BK != 0 || p.M < 1 || p.N < 1) return false;
     if (p.bias2 != nullptr && (p.bias2_rows < 1 || p.N % 4 != 0)) return false;
-    if (p.conv_W > 0)
+    if (p.conv_W > 0) {
+        const int st = p.conv_stride;
+        if ((st != 1 && st != 2) || (st == 2 && (p.conv_rows % 2 != 0 || p.conv_W % 2 != 0))) return false;
         return !p.a_f32 && !p.geglu && p.conv_rows > 0 && p.K % (9 * DBK) == 0 && p.N % 64 == 0 &&
-               p.seg % 4 == 0 && p.M % (p.conv_rows * p.conv_W) == 0;
+               p.seg % 4 == 0 && p.M % ((p.conv_rows / st) * (p.conv_W / st)) == 0;
+    }
     if (p.geglu) return p.N % 64 == 0;  // two n-blocks of 32 per workgroup pair
     return p.N % 64 == 0 && p.seg % 4 == 0;
 }

@@ -73,6 +73,20 @@ class pcpp_resnet_weights_t(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in RESNET_PTR_FIELDS]
 
 
+PCPP_CONV_SAME = 0
+PCPP_CONV_DOWN = 1
+PCPP_CONV_UP = 2
+
+
+class pcpp_conv_geom_t(ctypes.Structure):
+    _fields_ = [
+        ("H", ctypes.c_int32), ("W", ctypes.c_int32),
+        ("n_patches", ctypes.c_int32), ("patch_idx", ctypes.c_int32),
+        ("c_in", ctypes.c_int32), ("c_out", ctypes.c_int32),
+        ("batch", ctypes.c_int32), ("mode", ctypes.c_int32), ("reserved", ctypes.c_int32),
+    ]
+
+
 PCPP_STEP_DDPM = 0
 PCPP_STEP_DDIM = 1
 
@@ -119,6 +133,8 @@ def _load():
                                              ctypes.POINTER(pcpp_resnet_weights_t)] + [vp] * 14 + [sz, vp]),
         "pcpp_guided_step": (ctypes.c_int, [ctypes.POINTER(pcpp_step_params_t), ctypes.c_int64,
                                             vp, vp, vp, vp, vp, vp]),
+        "pcpp_conv3x3_workspace_size": (sz, [ctypes.POINTER(pcpp_conv_geom_t)]),
+        "pcpp_conv3x3": (ctypes.c_int, [ctypes.POINTER(pcpp_conv_geom_t)] + [vp] * 7 + [sz, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -136,6 +152,7 @@ EXPORTED = (
     "pcpp_partial_attention_multihop_workspace_size", "pcpp_partial_attention_multihop",
     "pcpp_multihop_message_bytes", "pcpp_pack_multihop", "pcpp_unpack_multihop",
     "pcpp_resnet_block_workspace_size", "pcpp_resnet_block", "pcpp_guided_step",
+    "pcpp_conv3x3_workspace_size", "pcpp_conv3x3",
 )
 
 
@@ -307,3 +324,18 @@ def make_step_params(mode, guidance, alpha_t=1.0, alphabar_t=0.5, sigma_t=0.0, a
 def pcpp_guided_step(sp, n, x_t, eps_uncond, eps_cond, z, x_prev, stream=None):
     _check("pcpp_guided_step", _lib.pcpp_guided_step(
         ctypes.byref(sp), n, _ptr(x_t), _ptr(eps_uncond), _ptr(eps_cond), _ptr(z), _ptr(x_prev), _stream(stream)))
+
+
+def make_conv_geom(H, W, n_patches, patch_idx, c_in, c_out, batch=1, mode=PCPP_CONV_SAME,
+                   reserved=0) -> pcpp_conv_geom_t:
+    return pcpp_conv_geom_t(H, W, n_patches, patch_idx, c_in, c_out, batch, mode, reserved)
+
+
+def pcpp_conv3x3_workspace_size(g) -> int:
+    return _lib.pcpp_conv3x3_workspace_size(ctypes.byref(g))
+
+
+def pcpp_conv3x3(g, x, row_up, row_dn, w, bias, y, workspace, ws_bytes, stream=None):
+    _check("pcpp_conv3x3", _lib.pcpp_conv3x3(
+        ctypes.byref(g), _ptr(x), _ptr(row_up), _ptr(row_dn), _ptr(w), _ptr(bias), _ptr(y), _ptr(workspace),
+        ws_bytes, _stream(stream)))

@@ -372,3 +372,31 @@ def step_inputs(n: int, seed: int, with_noise: bool = True) -> Dict[str, Optiona
     if not with_noise:
         out["z"] = None
     return out
+
+
+def conv_inputs(H: int, W: int, n: int, i: int, c_in: int, c_out: int, batch: int, seed: int
+                ) -> Dict[str, Optional[np.ndarray]]:
+    """bf16 inputs of one 3x3 band convolution: x [B, h*W, c_in] ~ N(0, 1),
+    the rows above / below the band [B, W, c_in] ~ N(0, 1) (None at the
+    image's edges), weights [c_out, 3, 3, c_in] ~ N(0, 1/(9 c_in)), bias
+    ~ 0.02 N(0, 1)."""
+    s = BASE_SEED + seed
+    h = H // n
+    out: Dict[str, Optional[np.ndarray]] = {
+        "x": bf16_bits(_stream(s, 800).standard_normal((batch, h * W, c_in))),
+        "row_up": bf16_bits(_stream(s, 801).standard_normal((batch, W, c_in))) if i > 0 else None,
+        "row_dn": bf16_bits(_stream(s, 802).standard_normal((batch, W, c_in))) if i < n - 1 else None,
+        "w": bf16_bits(_stream(s, 803).standard_normal((c_out, 3, 3, c_in)) / np.sqrt(9 * c_in)),
+        "b": bf16_bits(0.02 * _stream(s, 804).standard_normal(c_out)),
+    }
+    return out
+
+
+# SDXL's resolution changes at 2048 px, 8 bands, band 3: the downsampler from
+# level 0 (256 x 256 tokens, 320 channels) and the upsamplers into level 1
+# and level 0, as (H, W, n, i, c_in, c_out, mode: 0 same, 1 down, 2 up).
+CONV_CONFIGS = {
+    "sdxl2048_down_l0": (256, 256, 8, 3, 320, 320, 1),
+    "sdxl2048_up_l2": (64, 64, 8, 3, 1280, 1280, 2),
+    "sdxl2048_up_l1": (128, 128, 8, 3, 640, 640, 2),
+}

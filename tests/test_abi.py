@@ -19,7 +19,7 @@ HEADER = os.path.join(ROOT, "include", "pcpp.h")
 def _declared():
     txt = open(HEADER).read()
     txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
-    return sorted(set(re.findall(r"\b(pcpp_[a-z_]+)\s*\(", txt)))
+    return sorted(set(re.findall(r"\b(pcpp_[a-z0-9_]+)\s*\(", txt)))
 
 
 def test_library_exports_every_declared_function():
@@ -335,3 +335,29 @@ def test_guided_step_validation():
                 pcpp.make_step_params(pcpp.PCPP_STEP_DDIM, 5.0, alphabar_t=0.5, alphabar_prev=0.6, reserved=3)):
         assert call(bad, 16, FAKE, FAKE, FAKE, None, FAKE) == pcpp.PCPP_EINVAL
     assert call(ddpm, -1, FAKE, FAKE, FAKE, None, FAKE) == pcpp.PCPP_EINVAL
+
+
+def test_conv3x3_geometry_and_validation():
+    from paper_2412_02962_amd import pcpp
+    lib = pcpp.lib()
+    ok = pcpp.make_conv_geom(256, 256, 8, 3, 320, 320, 1, pcpp.PCPP_CONV_DOWN)
+    assert pcpp.pcpp_conv3x3_workspace_size(ok) >= 1 * 34 * 258 * 320 * 2
+    up = pcpp.make_conv_geom(64, 64, 8, 3, 1280, 1280, 1, pcpp.PCPP_CONV_UP)
+    assert pcpp.pcpp_conv3x3_workspace_size(up) >= 1 * 18 * 130 * 1280 * 2
+    for bad in (pcpp.make_conv_geom(24, 20, 8, 3, 64, 64, 1, pcpp.PCPP_CONV_DOWN),   # odd band height
+                pcpp.make_conv_geom(16, 21, 4, 1, 64, 64, 1, pcpp.PCPP_CONV_DOWN),   # odd width
+                pcpp.make_conv_geom(16, 20, 4, 4, 64, 64, 1, 0),                       # band index
+                pcpp.make_conv_geom(16, 20, 4, 1, 64, 64, 1, 3),                       # mode
+                pcpp.make_conv_geom(16, 20, 4, 1, 64, 64, 1, 0, 1)):                   # reserved
+        assert pcpp.pcpp_conv3x3_workspace_size(bad) == 0
+    ns = pcpp.make_conv_geom(16, 20, 4, 1, 4, 64, 1, 0)
+    assert lib.pcpp_conv3x3(ctypes.byref(ns), FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, 1 << 30, None) == \
+        pcpp.PCPP_ENOTSUP
+    g = pcpp.make_conv_geom(16, 20, 4, 1, 64, 64, 1, pcpp.PCPP_CONV_SAME)
+    call = lambda *a: lib.pcpp_conv3x3(ctypes.byref(g), *a, None)
+    assert call(FAKE, FAKE, None, FAKE, None, FAKE, FAKE, 1 << 30) == pcpp.PCPP_EINVAL      # row below missing
+    assert call(FAKE, FAKE + 2, FAKE, FAKE, None, FAKE, FAKE, 1 << 30) == pcpp.PCPP_EINVAL  # misaligned
+    assert call(FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, 16) == pcpp.PCPP_EWORKSPACE
+    d = pcpp.make_conv_geom(16, 20, 4, 1, 64, 64, 1, pcpp.PCPP_CONV_DOWN)
+    assert lib.pcpp_conv3x3(ctypes.byref(d), FAKE, FAKE, None, FAKE, None, FAKE, FAKE, 16, None) == \
+        pcpp.PCPP_EWORKSPACE                                                                  # no row below needed
