@@ -388,7 +388,7 @@ typedef struct {
     int32_t H, W;          /* the layer's token grid                         */
     int32_t n_patches;     /* n, H % n == 0                                  */
     int32_t patch_idx;     /* band i, 0-based                                */
-    int32_t c_in, c_out;   /* channels, multiples of 64, <= 2048             */
+    int32_t c_in, c_out;   /* channels, multiples of 64, <= 2560             */
     int32_t temb_dim;      /* time-embedding width T, multiple of 8          */
     int32_t groups;        /* GroupNorm groups, dividing c_in and c_out, <= 256 */
     int32_t batch;         /* images B (the guidance branches), <= 65535     */
@@ -435,7 +435,7 @@ size_t pcpp_resnet_block_workspace_size(const pcpp_resnet_geom_t* g);
  *                they must not overlap each other or the edges inputs
  * Errors: PCPP_EINVAL (geometry, NULL or misaligned pointers, 16-byte
  * alignment for the bf16 tensors), PCPP_ENOTSUP (channels not multiples of
- * 64 or above 2048, groups above 256), PCPP_EWORKSPACE.  Asynchronous.
+ * 64 or above 2560, groups above 256), PCPP_EWORKSPACE.  Asynchronous.
  */
 int pcpp_resnet_block(const pcpp_resnet_geom_t* g, const pcpp_resnet_weights_t* w,
                       const void* x, const void* temb,

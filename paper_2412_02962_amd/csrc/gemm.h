@@ -83,7 +83,8 @@ struct GroupNormParams {
 };
 size_t group_norm_ws_bytes(int B, int G, int N);
 // C % 8 == 0, C <= 2048, 1 <= G <= 256 divides C.
-bool norm_shapes_ok(int C, int G);
+bool norm_shapes_ok(int C, int G);  // GroupNorm and LayerNorm: C <= 2048
+bool gn_shapes_ok(int C, int G);    // GroupNorm alone: C <= 2560
 hipError_t launch_group_norm(GroupNormParams p, hipStream_t s);
 
 // LayerNorm over the channel axis of fp32 rows, bf16 output.

@@ -32,7 +32,7 @@ namespace pcpp {
 namespace {
 
 constexpr int GN_THREADS = 256;
-constexpr int GN_MAX_C = 2048;     // channels (LDS tables of gn_apply)
+constexpr int GN_MAX_C = 2560;     // channels (LDS tables of gn_apply; the U-Net's widest concatenation)
 constexpr int GN_MAX_G = 256;
 constexpr int GN_TOKENS_PER_APPLY = 8;
 // Tokens per statistics workgroup: 32, or 8 when a band has fewer than
@@ -58,7 +58,7 @@ __device__ __forceinline__ void chan_merge(float& n, float& mean, float& m2, flo
     n = nn;
 }
 
-template <int GN_CHUNK_TOKENS>
+template <int GN_CHUNK_TOKENS, int PP>  // PP: channel pairs per thread, ceil(C / 2 / GN_THREADS)
 __global__ __launch_bounds__(GN_THREADS) void gn_stats(GroupNormParams p) {
     __shared__ float chan_acc[GN_MAX_C];
     __shared__ float g_mean[GN_MAX_G];
@@ -70,9 +70,8 @@ __global__ __launch_bounds__(GN_THREADS) void gn_stats(GroupNormParams p) {
     const bf16* xb = p.x + ((int64_t)b * p.N + t0) * C;
 
     // The chunk's rows, channel pairs per lane, held in registers for both
-    // passes (GN_CHUNK_TOKENS tokens, at most GN_MAX_C / 2 / GN_THREADS
-    // pairs per thread): all loads of a thread in flight together.
-    constexpr int PP = GN_MAX_C / 2 / GN_THREADS;
+    // passes (GN_CHUNK_TOKENS tokens, PP pairs per thread): all loads of a
+    // thread in flight together.
     bf16x2 xv[PP][GN_CHUNK_TOKENS];
 #pragma unroll
     for (int k = 0; k < PP; ++k) {
@@ -344,18 +343,35 @@ int gn_chunks(int N) {
 
 size_t group_norm_ws_bytes(int B, int G, int N) { return gn_part_bytes(B, G, gn_chunks(N)); }
 
-bool norm_shapes_ok(int C, int G) {
-    return C > 0 && C % 8 == 0 && C <= GN_MAX_C && C <= 4 * 64 * LN_MAX_VEC && G > 0 && G <= GN_MAX_G && C % G == 0;
+bool gn_shapes_ok(int C, int G) {
+    return C > 0 && C % 8 == 0 && C <= GN_MAX_C && G > 0 && G <= GN_MAX_G && C % G == 0;
 }
 
+bool norm_shapes_ok(int C, int G) { return gn_shapes_ok(C, G) && C <= 4 * 64 * LN_MAX_VEC; }
+
 hipError_t launch_group_norm(GroupNormParams p, hipStream_t s) {
-    if (!norm_shapes_ok(p.C, p.G)) return hipErrorInvalidValue;
+    if (!gn_shapes_ok(p.C, p.G)) return hipErrorInvalidValue;
     if (p.pad_W < 0 || (p.pad_W > 0 && p.N % p.pad_W != 0)) return hipErrorInvalidValue;
     p.chunks = gn_chunks(p.N);
-    if (gn_chunk_tokens(p.N) == GN_CHUNK_LONG)
-        gn_stats<GN_CHUNK_LONG><<<dim3(p.chunks, p.B), GN_THREADS, 0, s>>>(p);
-    else
-        gn_stats<GN_CHUNK_SHORT><<<dim3(p.chunks, p.B), GN_THREADS, 0, s>>>(p);
+    const dim3 grid(p.chunks, p.B);
+    const bool lng = gn_chunk_tokens(p.N) == GN_CHUNK_LONG;
+    switch ((p.C / 2 + GN_THREADS - 1) / GN_THREADS) {
+#define PCPP_GN_STATS(PP)                                                                      \
+    case PP:                                                                                   \
+        if (lng)                                                                               \
+            gn_stats<GN_CHUNK_LONG, PP><<<grid, GN_THREADS, 0, s>>>(p);                         \
+        else                                                                                   \
+            gn_stats<GN_CHUNK_SHORT, PP><<<grid, GN_THREADS, 0, s>>>(p);                        \
+        break;
+        PCPP_GN_STATS(1)
+        PCPP_GN_STATS(2)
+        PCPP_GN_STATS(3)
+        PCPP_GN_STATS(4)
+        PCPP_GN_STATS(5)
+#undef PCPP_GN_STATS
+        default:
+            return hipErrorInvalidValue;
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     gn_apply<<<dim3((p.N + GN_TOKENS_PER_APPLY - 1) / GN_TOKENS_PER_APPLY, p.B), GN_THREADS, 0, s>>>(p);

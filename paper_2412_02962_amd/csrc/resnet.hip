@@ -104,7 +104,7 @@ int validate_resnet(const pcpp_resnet_geom_t* g) {
     if ((int64_t)g->batch * (g->H / g->n_patches) * g->W > INT32_MAX / 4) return PCPP_EINVAL;
     // the convolution's k-tiles hold 64 channels of one tap
     if (g->c_in % 64 != 0 || g->c_out % 64 != 0) return PCPP_ENOTSUP;
-    if (!norm_shapes_ok(g->c_in, g->groups) || !norm_shapes_ok(g->c_out, g->groups)) return PCPP_ENOTSUP;
+    if (!gn_shapes_ok(g->c_in, g->groups) || !gn_shapes_ok(g->c_out, g->groups)) return PCPP_ENOTSUP;
     return PCPP_OK;
 }
 

@@ -312,6 +312,10 @@ RESNET_CONFIGS = {
     "sdxl2048_l0_res320": ResnetConfig("sdxl2048_l0_res320", 256, 256, 8, 3, 320, 320, seed_id=89),
     "sdxl2048_l2_res1280": ResnetConfig("sdxl2048_l2_res1280", 64, 64, 8, 3, 1280, 1280, seed_id=90),
     "sdxl2048_l2_res640_1280": ResnetConfig("sdxl2048_l2_res640_1280", 64, 64, 8, 3, 640, 1280, seed_id=91),
+    # the up path's first ResNet of each level, on the concatenation with the skip
+    "sdxl2048_l2_res2560_1280": ResnetConfig("sdxl2048_l2_res2560_1280", 64, 64, 8, 3, 2560, 1280, seed_id=92),
+    "sdxl2048_l1_res1920_640": ResnetConfig("sdxl2048_l1_res1920_640", 128, 128, 8, 3, 1920, 640, seed_id=93),
+    "sdxl2048_l0_res960_320": ResnetConfig("sdxl2048_l0_res960_320", 256, 256, 8, 3, 960, 320, seed_id=94),
 }
 
 

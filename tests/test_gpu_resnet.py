@@ -46,7 +46,8 @@ SMALL = [
 ]
 FULL = [synth.RESNET_CONFIGS["sdxl2048_l1_res640"], synth.RESNET_CONFIGS["sdxl2048_l1_res320_640"],
         synth.RESNET_CONFIGS["sdxl2048_l0_res320"], synth.RESNET_CONFIGS["sdxl2048_l2_res1280"],
-        synth.RESNET_CONFIGS["sdxl2048_l2_res640_1280"]]
+        synth.RESNET_CONFIGS["sdxl2048_l2_res640_1280"], synth.RESNET_CONFIGS["sdxl2048_l2_res2560_1280"],
+        synth.RESNET_CONFIGS["sdxl2048_l1_res1920_640"], synth.RESNET_CONFIGS["sdxl2048_l0_res960_320"]]
 
 
 def _say(*a):
