@@ -28,6 +28,8 @@ from .pcpp_oracle import (  # noqa: F401
     place_boundary_messages,
     place_multihop_message,
     transformer_block,
+    transformer_module,
+    MODULE_BLOCK_KEYS,
 )
 from .unet_oracle import (  # noqa: F401
     RESNET_GN_EPS,

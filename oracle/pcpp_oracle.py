@@ -454,3 +454,46 @@ def transformer_block(H: int, W: int, n: int, i: int, p: float, heads: int,
 
     y = linear(hid, wts["proj_out_w"], wts["proj_out_b"]) + x
     return y, k, v
+
+
+MODULE_BLOCK_KEYS = ("ln1_gamma", "ln1_beta", "attn1_qkv_w", "attn1_out_w", "attn1_out_b",
+                     "ln2_gamma", "ln2_beta", "attn2_q_w", "attn2_kv_w", "attn2_out_w", "attn2_out_b",
+                     "ln3_gamma", "ln3_beta", "ff1_w", "ff1_b", "ff2_w", "ff2_b")
+
+
+def transformer_module(H: int, W: int, n: int, i: int, p: float, heads: int,
+                       module_wts: Dict[str, np.ndarray], block_wts, x: np.ndarray, text: np.ndarray,
+                       stale, gn_groups: int = 32, gn_band_stats: Optional[np.ndarray] = None):
+    """SDXL's transformer module of depth d = len(block_wts) on patch i,
+    float64: GroupNorm -> proj_in -> d basic blocks -> proj_out + the module
+    input.  Basic block j: LayerNorm -> Q, K, V of the local patch -> partial
+    self-attention with the neighbours' stale K/V of that block (stale[j] =
+    (k_up, v_up, k_dn, v_dn), Sec. 3.3) -> out-proj + residual -> LayerNorm ->
+    cross-attention to the text -> out-proj + residual -> LayerNorm -> GEGLU
+    feed-forward + residual.  module_wts holds gn_gamma, gn_beta, proj_in_w,
+    proj_in_b, proj_out_w, proj_out_b; block_wts[j] the MODULE_BLOCK_KEYS.
+    Returns (y, [K_j], [V_j]): every block's own K and V, what the neighbours
+    read at the next step."""
+    C = x.shape[-1]
+    if gn_band_stats is None:
+        t = group_norm(x, gn_groups, module_wts["gn_gamma"], module_wts["gn_beta"])
+    else:
+        t = group_norm_synchronized(x, gn_groups, module_wts["gn_gamma"], module_wts["gn_beta"], gn_band_stats, i)
+    hid = linear(t, module_wts["proj_in_w"], module_wts["proj_in_b"])
+    ks, vs = [], []
+    for bw, (k_up, v_up, k_dn, v_dn) in zip(block_wts, stale):
+        n1 = layer_norm(hid, bw["ln1_gamma"], bw["ln1_beta"])
+        q = linear(n1, bw["attn1_qkv_w"][0:C])
+        k = linear(n1, bw["attn1_qkv_w"][C:2 * C])
+        v = linear(n1, bw["attn1_qkv_w"][2 * C:3 * C])
+        hid = hid + linear(partial_attention(H, W, n, i, p, heads, q, k, v, k_up, v_up, k_dn, v_dn),
+                           bw["attn1_out_w"], bw["attn1_out_b"])
+        n2 = layer_norm(hid, bw["ln2_gamma"], bw["ln2_beta"])
+        k2 = linear(text, bw["attn2_kv_w"][0:C])
+        v2 = linear(text, bw["attn2_kv_w"][C:2 * C])
+        hid = hid + linear(mha(linear(n2, bw["attn2_q_w"]), k2, v2, heads), bw["attn2_out_w"], bw["attn2_out_b"])
+        n3 = layer_norm(hid, bw["ln3_gamma"], bw["ln3_beta"])
+        hid = hid + linear(geglu(n3, bw["ff1_w"], bw["ff1_b"]), bw["ff2_w"], bw["ff2_b"])
+        ks.append(k)
+        vs.append(v)
+    return linear(hid, module_wts["proj_out_w"], module_wts["proj_out_b"]) + x, ks, vs

@@ -178,3 +178,79 @@ def test_group_stats_against_numpy():
             assert st[b, g, 0] == blk.size
             assert math.isclose(st[b, g, 1], float(np.mean(blk)), rel_tol=0, abs_tol=1e-14)
             assert math.isclose(st[b, g, 2], float(np.var(blk)) * blk.size, rel_tol=1e-12)
+
+
+def _torch_module(H, W, n, i, p, heads, mw, bws, x, text, stale_full, groups):
+    """A depth-d module as torch.nn.functional calls; block j's self-attention
+    context gathered by brute force from Eq. 1 out of its own stale image."""
+    T = {k: _t(v) for k, v in mw.items()}
+    xt = _t(x)
+    B, N, C = x.shape
+    d = C // heads
+    h = H // n
+    ids = torch.from_numpy(eq1_token_ids_brute(H, W, n, i, p).astype(np.int64))
+
+    def attn(q, k, v):
+        def sp(z):
+            return z.reshape(B, z.shape[1], heads, d).permute(0, 2, 1, 3)
+        o = F.scaled_dot_product_attention(sp(q), sp(k), sp(v))
+        return o.permute(0, 2, 1, 3).reshape(B, q.shape[1], C)
+
+    t = F.group_norm(xt.permute(0, 2, 1), groups, T["gn_gamma"], T["gn_beta"], eps=1e-6).permute(0, 2, 1)
+    hid = F.linear(t, T["proj_in_w"], T["proj_in_b"])
+    for bw, (sk, sv) in zip(bws, stale_full):
+        Tb = {k: _t(v) for k, v in bw.items()}
+        n1 = F.layer_norm(hid, (C,), Tb["ln1_gamma"], Tb["ln1_beta"], eps=1e-5)
+        q, k, v = F.linear(n1, Tb["attn1_qkv_w"]).chunk(3, dim=-1)
+        kf, vf = _t(sk).clone(), _t(sv).clone()
+        kf[:, i * h * W:(i + 1) * h * W] = k
+        vf[:, i * h * W:(i + 1) * h * W] = v
+        hid = hid + F.linear(attn(q, kf[:, ids], vf[:, ids]), Tb["attn1_out_w"], Tb["attn1_out_b"])
+        n2 = F.layer_norm(hid, (C,), Tb["ln2_gamma"], Tb["ln2_beta"], eps=1e-5)
+        k2, v2 = F.linear(_t(text), Tb["attn2_kv_w"]).chunk(2, dim=-1)
+        hid = hid + F.linear(attn(F.linear(n2, Tb["attn2_q_w"]), k2, v2), Tb["attn2_out_w"], Tb["attn2_out_b"])
+        n3 = F.layer_norm(hid, (C,), Tb["ln3_gamma"], Tb["ln3_beta"], eps=1e-5)
+        val, gate = F.linear(n3, Tb["ff1_w"], Tb["ff1_b"]).chunk(2, dim=-1)
+        hid = hid + F.linear(val * F.gelu(gate), Tb["ff2_w"], Tb["ff2_b"])
+    return (F.linear(hid, T["proj_out_w"], T["proj_out_b"]) + xt).numpy()
+
+
+@pytest.mark.parametrize("depth,i", [(1, 1), (2, 0), (3, 2)])
+def test_transformer_module_matches_torch_composition(depth, i):
+    H, W, n, p, heads, d, groups = 12, 4, 3, 0.5, 2, 8, 4
+    C, Tn, Td, Fi = heads * d, 5, 12, 24
+    h = H // n
+    rng = np.random.default_rng(31 + depth)
+
+    def draw(shp, name):
+        if name.endswith("_w"):
+            return rng.standard_normal(shp) / math.sqrt(shp[1])
+        return (1 + 0.1 * rng.standard_normal(shp)) if name.endswith("gamma") else 0.1 * rng.standard_normal(shp)
+    mw = {k: draw(s, k) for k, s in {"gn_gamma": (C,), "gn_beta": (C,), "proj_in_w": (C, C), "proj_in_b": (C,),
+                                     "proj_out_w": (C, C), "proj_out_b": (C,)}.items()}
+    bshapes = {"ln1_gamma": (C,), "ln1_beta": (C,), "attn1_qkv_w": (3 * C, C), "attn1_out_w": (C, C),
+               "attn1_out_b": (C,), "ln2_gamma": (C,), "ln2_beta": (C,), "attn2_q_w": (C, C),
+               "attn2_kv_w": (2 * C, Td), "attn2_out_w": (C, C), "attn2_out_b": (C,), "ln3_gamma": (C,),
+               "ln3_beta": (C,), "ff1_w": (2 * Fi, C), "ff1_b": (2 * Fi,), "ff2_w": (C, Fi), "ff2_b": (C,)}
+    assert tuple(bshapes) == oracle.MODULE_BLOCK_KEYS
+    bws = [{k: draw(s, k) for k, s in bshapes.items()} for _ in range(depth)]
+    x = rng.standard_normal((1, h * W, C))
+    text = rng.standard_normal((1, Tn, Td))
+    stale_full = [(rng.standard_normal((1, H * W, C)), rng.standard_normal((1, H * W, C))) for _ in range(depth)]
+
+    def band(z, j):
+        return z[:, j * h * W:(j + 1) * h * W] if 0 <= j < n else None
+    stale = [(band(k, i - 1), band(v, i - 1), band(k, i + 1), band(v, i + 1)) for k, v in stale_full]
+    y, ks, vs = oracle.transformer_module(H, W, n, i, p, heads, mw, bws, x, text, stale, gn_groups=groups)
+    yt = _torch_module(H, W, n, i, p, heads, mw, bws, x, text, stale_full, groups)
+    np.testing.assert_allclose(y, yt, rtol=0, atol=1e-10)
+    assert len(ks) == depth and len(vs) == depth
+    if depth == 1:   # the depth-1 module is the block
+        wb = dict(mw)
+        wb.update(bws[0])
+        yb, kb, vb = oracle.transformer_block(H, W, n, i, p, heads, wb, x, text, *stale[0], gn_groups=groups)
+        np.testing.assert_array_equal(y, yb)
+        np.testing.assert_array_equal(ks[0], kb)
+    else:            # each block reads its own stale K/V: swapping two blocks' changes the result
+        y2, _, _ = oracle.transformer_module(H, W, n, i, p, heads, mw, bws, x, text, stale[::-1], gn_groups=groups)
+        assert not np.allclose(y2, y) or i == 0 and n == 1
