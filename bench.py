@@ -356,6 +356,32 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
     out["block_l2_TFLOPs"] = round(block_flops(bc2, nkv2) / us / 1e6, 1)
     out["block_l2_gflop"] = round(block_flops(bc2, nkv2) / 1e9, 2)
 
+    # SDXL's transformer modules: depth 2 at level 1, depth 10 at level 2
+    for tag, bcm, depth in (("l1_depth2", synth.BLOCK_CONFIG, 2), ("l2_depth10", synth.BLOCK_CONFIG_L2, 10)):
+        cm = bcm.attn
+        x, text, module, blocks, stale = synth.module_inputs(bcm, depth)
+        md = {k: to_dev(v) for k, v in module.items()}
+        bd = [{k: to_dev(v) for k, v in blk.items()} for blk in blocks]
+        wm, keep = pcpp.make_module_weights(md, bd, bcm.ff_inner, bcm.gn_groups)
+        gm = pcpp.make_geom(cm.H, cm.W, cm.n, cm.i, cm.p, cm.heads, cm.d, 1, 0, pcpp.PCPP_DTYPE_BF16)
+        _, _, _, nkvm = pcpp.pcpp_context_rows(gm)
+        xd, td = to_dev(x), to_dev(text)
+        cols = [[to_dev(a) for a in c] for c in zip(*stale)]
+        ym = torch.empty_like(xd)
+        kom = [torch.empty_like(xd) for _ in range(depth)]
+        vom = [torch.empty_like(xd) for _ in range(depth)]
+        wsm = pcpp.pcpp_transformer_module_workspace_size(gm, wm, bcm.n_text, bcm.text_dim)
+        wsmt = torch.zeros(wsm, dtype=torch.uint8, device=dev)
+        us = graph_time_us(torch, lambda: pcpp.pcpp_transformer_module(gm, wm, xd, td, bcm.n_text, bcm.text_dim,
+                                                                       *cols, None, None, ym, kom, vom, wsmt, wsm),
+                           max(reps // 20, 1), use_graph)
+        cmf = block_flops(bcm, nkvm)
+        proj = 2.0 * cm.n_q * cm.C * cm.C * 2          # proj_in and proj_out, once per module
+        flops = depth * (cmf - proj) + proj
+        out[f"module_{tag}_us"] = round(us, 3)
+        out[f"module_{tag}_TFLOPs"] = round(flops / us / 1e6, 1)
+        del keep, cols, bd, md
+
     # ResNet blocks of the three levels (bf16, batch 1: one guidance branch per device)
     for name, rc in synth.RESNET_CONFIGS.items():
         fn, keep = resnet_call(torch, pcpp, synth, rc, dev)

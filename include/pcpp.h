@@ -284,6 +284,65 @@ int pcpp_transformer_block_sync_gn(const pcpp_geom_t* g,
                                    size_t ws_bytes, void* stream);
 
 /*
+ * SDXL's transformer module of depth d (2 at the first transformer level, 10
+ * at the second) on band i: GroupNorm -> proj_in -> d basic blocks ->
+ * proj_out + the module input.  Each basic block is pcpp_transformer_block's
+ * body (LayerNorm, Q/K/V, partially conditioned self-attention over the
+ * band and the stale neighbour rows, out-proj + residual, LayerNorm,
+ * cross-attention to the text, out-proj + residual, LayerNorm, GEGLU
+ * feed-forward + residual) with its own weights and its own stale K/V: every
+ * self-attention layer exchanges its own K and V (Sec. 3.2, 3.3).  Depth 1
+ * is exactly pcpp_transformer_block.
+ */
+typedef struct {
+    const void* ln1_gamma;   const void* ln1_beta;      /* [C]                 */
+    const void* attn1_qkv_w;                            /* [3C, C] W_q, W_k, W_v */
+    const void* attn1_out_w; const void* attn1_out_b;   /* [C, C], [C]         */
+    const void* ln2_gamma;   const void* ln2_beta;      /* [C]                 */
+    const void* attn2_q_w;                              /* [C, C]              */
+    const void* attn2_kv_w;                             /* [2C, T] W_k, W_v    */
+    const void* attn2_out_w; const void* attn2_out_b;   /* [C, C], [C]         */
+    const void* ln3_gamma;   const void* ln3_beta;      /* [C]                 */
+    const void* ff1_w;       const void* ff1_b;         /* [2F, C], [2F]       */
+    const void* ff2_w;       const void* ff2_b;         /* [C, F], [C]         */
+} pcpp_basic_block_weights_t;
+
+typedef struct {
+    const void* gn_gamma;    const void* gn_beta;       /* [C] (eps 1e-6)      */
+    const void* proj_in_w;   const void* proj_in_b;     /* [C, C], [C]         */
+    const void* proj_out_w;  const void* proj_out_b;    /* [C, C], [C]         */
+    const pcpp_basic_block_weights_t* blocks;           /* host array [depth]  */
+    int32_t depth;                                      /* 1 .. 64             */
+    int32_t ff_inner;                                   /* F, multiple of 64   */
+    int32_t gn_groups;                                  /* dividing C          */
+} pcpp_module_weights_t;
+
+/* Bytes of device workspace (0 if invalid); the same for every depth and the
+ * same contract as pcpp_transformer_block_workspace_size. */
+size_t pcpp_transformer_module_workspace_size(const pcpp_geom_t* g,
+                                              const pcpp_module_weights_t* w,
+                                              int32_t n_text, int32_t text_dim);
+
+/*
+ * k_up, v_up, k_dn, v_dn: host arrays of depth device pointers, entry j the
+ * stale neighbour K/V of basic block j as in pcpp_partial_attention (the
+ * arrays may be NULL where the band has no such neighbour or r = 0).
+ * k_fresh_out, v_fresh_out: NULL, or host arrays of depth device pointers
+ * (entries may be NULL) receiving basic block j's own K and V [B, h*W, C].
+ * gn_bands / gn_own: NULL, or the synchronized GroupNorm's statistics as in
+ * pcpp_transformer_block_sync_gn.  Other arguments, requirements and errors
+ * as pcpp_transformer_block.  Asynchronous on `stream`.
+ */
+int pcpp_transformer_module(const pcpp_geom_t* g, const pcpp_module_weights_t* w,
+                            const void* x, const void* text, int32_t n_text,
+                            int32_t text_dim,
+                            const void* const* k_up, const void* const* v_up,
+                            const void* const* k_dn, const void* const* v_dn,
+                            const float* gn_bands, float* gn_own, void* y,
+                            void* const* k_fresh_out, void* const* v_fresh_out,
+                            void* workspace, size_t ws_bytes, void* stream);
+
+/*
  * p-aware boundary messages of the neighbour exchange (Sec. 3.2 with Eq. 1).
  * At the next step band i-1 reads the first r rows of band i's fresh keys
  * and values (its context below) and band i+1 reads the last r rows (its

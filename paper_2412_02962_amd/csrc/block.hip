@@ -1,4 +1,5 @@
-// pcpp_transformer_block: one SDXL-shaped transformer block on one band,
+// pcpp_transformer_block / pcpp_transformer_module: SDXL's transformer
+// module (depth 1: the block) on one band,
 // built from the library's kernels (GroupNorm, LayerNorm, MFMA GEMMs with
 // fused epilogues, and the attention kernel used twice: partially
 // conditioned self-attention over the band plus its neighbours' stale
@@ -38,16 +39,15 @@ struct BlockLayout {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-int validate_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, int32_t n_text, int32_t text_dim,
+int validate_block(const pcpp_geom_t* g, int32_t ff_inner, int32_t gn_groups, int32_t n_text, int32_t text_dim,
                    Geo* r) {
     int st = validate_geom(g, r);
     if (st != PCPP_OK) return st;
     if (g->dtype != PCPP_DTYPE_BF16 || g->head_dim != 64) return PCPP_ENOTSUP;
-    if (w == nullptr) return PCPP_EINVAL;
     if (n_text < 1 || text_dim < 32 || text_dim % 32 != 0) return PCPP_EINVAL;
-    if (w->ff_inner < 64 || w->ff_inner % 64 != 0) return PCPP_EINVAL;
-    if (w->gn_groups < 1 || r->C % w->gn_groups != 0) return PCPP_EINVAL;
-    if (!norm_shapes_ok(r->C, w->gn_groups)) return PCPP_ENOTSUP;  // LayerNorm keeps a row in registers
+    if (ff_inner < 64 || ff_inner % 64 != 0) return PCPP_EINVAL;
+    if (gn_groups < 1 || r->C % gn_groups != 0) return PCPP_EINVAL;
+    if (!norm_shapes_ok(r->C, gn_groups)) return PCPP_ENOTSUP;  // LayerNorm keeps a row in registers
     if (g->heads > 65535 || g->batch > 65535) return PCPP_EINVAL;
     return PCPP_OK;
 }
@@ -73,7 +73,7 @@ AttnParams cross_attn_params(const pcpp_geom_t* g, const Geo& r, const void* q, 
     return make_attn_params(g, r, q, out, kv);
 }
 
-BlockLayout layout(const pcpp_geom_t* g, const Geo& r, const pcpp_block_weights_t* w, int32_t n_text) {
+BlockLayout layout(const pcpp_geom_t* g, const Geo& r, int32_t ff_inner, int32_t gn_groups, int32_t n_text) {
     BlockLayout L;
     const size_t rows = (size_t)g->batch * r.nq;
     const size_t C = r.C;
@@ -95,9 +95,9 @@ BlockLayout layout(const pcpp_geom_t* g, const Geo& r, const pcpp_block_weights_
     L.a16 = take(rows * C * 2);
     L.k2 = take((size_t)g->batch * n_text * C * 2);
     L.v2 = take((size_t)g->batch * n_text * C * 2);
-    L.u16 = take(rows * (size_t)w->ff_inner * 2);
+    L.u16 = take(rows * (size_t)ff_inner * 2);
     L.attn_ws = take(L.attn_ws_bytes);
-    L.gn = take(group_norm_ws_bytes(g->batch, w->gn_groups, r.nq));
+    L.gn = take(group_norm_ws_bytes(g->batch, gn_groups, r.nq));
     L.total = off;
     return L;
 }
@@ -135,47 +135,82 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 using namespace pcpp;
 
-PCPP_EXPORT size_t pcpp_transformer_block_workspace_size(const pcpp_geom_t* g, const pcpp_block_weights_t* w,
-                                                         int32_t n_text, int32_t text_dim) {
-    Geo r;
-    if (validate_block(g, w, n_text, text_dim, &r) != PCPP_OK) return 0;
-    return layout(g, r, w, n_text).total;
-}
-
 namespace {
 
-int run_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, const void* x, const void* text,
-              int32_t n_text, int32_t text_dim, const void* k_up, const void* v_up, const void* k_dn,
-              const void* v_dn, const float* gn_bands, float* gn_own, void* y, void* k_fresh_out,
-              void* v_fresh_out, void* workspace, size_t ws_bytes, void* stream) {
+// The module's own weights (GroupNorm, proj_in, proj_out) and sizes.
+struct ModuleW {
+    const void *gn_gamma, *gn_beta, *proj_in_w, *proj_in_b, *proj_out_w, *proj_out_b;
+    int32_t ff_inner, gn_groups;
+};
+
+ModuleW module_of(const pcpp_block_weights_t* w) {
+    return ModuleW{w->gn_gamma, w->gn_beta, w->proj_in_w, w->proj_in_b, w->proj_out_w, w->proj_out_b, w->ff_inner,
+                   w->gn_groups};
+}
+
+pcpp_basic_block_weights_t basic_of(const pcpp_block_weights_t* w) {
+    pcpp_basic_block_weights_t b;
+    b.ln1_gamma = w->ln1_gamma;
+    b.ln1_beta = w->ln1_beta;
+    b.attn1_qkv_w = w->attn1_qkv_w;
+    b.attn1_out_w = w->attn1_out_w;
+    b.attn1_out_b = w->attn1_out_b;
+    b.ln2_gamma = w->ln2_gamma;
+    b.ln2_beta = w->ln2_beta;
+    b.attn2_q_w = w->attn2_q_w;
+    b.attn2_kv_w = w->attn2_kv_w;
+    b.attn2_out_w = w->attn2_out_w;
+    b.attn2_out_b = w->attn2_out_b;
+    b.ln3_gamma = w->ln3_gamma;
+    b.ln3_beta = w->ln3_beta;
+    b.ff1_w = w->ff1_w;
+    b.ff1_b = w->ff1_b;
+    b.ff2_w = w->ff2_w;
+    b.ff2_b = w->ff2_b;
+    return b;
+}
+
+// GroupNorm -> proj_in -> depth basic blocks -> proj_out + x.  Basic block j
+// reads the stale neighbour K/V k_up[j] .. v_dn[j] and exports its own K/V
+// to k_out[j] / v_out[j] (either array, or an entry, may be null: then the
+// workspace holds them).
+int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_weights_t* blocks, int depth,
+               const void* x, const void* text, int32_t n_text, int32_t text_dim, const void* const* k_up,
+               const void* const* v_up, const void* const* k_dn, const void* const* v_dn, const float* gn_bands,
+               float* gn_own, void* y, void* const* k_out, void* const* v_out, void* workspace, size_t ws_bytes,
+               void* stream) {
     Geo r;
-    int st = validate_block(g, w, n_text, text_dim, &r);
+    int st = validate_block(g, mw.ff_inner, mw.gn_groups, n_text, text_dim, &r);
     if (st != PCPP_OK) return st;
-    const void* wptrs[] = {w->gn_gamma, w->gn_beta, w->proj_in_w, w->proj_in_b, w->ln1_gamma, w->ln1_beta,
-                           w->attn1_qkv_w, w->attn1_out_w, w->attn1_out_b, w->ln2_gamma, w->ln2_beta,
-                           w->attn2_q_w, w->attn2_kv_w, w->attn2_out_w, w->attn2_out_b, w->ln3_gamma,
-                           w->ln3_beta, w->ff1_w, w->ff1_b, w->ff2_w, w->ff2_b, w->proj_out_w, w->proj_out_b};
-    for (const void* p : wptrs)
+    if (depth < 1 || depth > 64 || blocks == nullptr) return PCPP_EINVAL;
+    const void* mptrs[] = {mw.gn_gamma, mw.gn_beta, mw.proj_in_w, mw.proj_in_b, mw.proj_out_w, mw.proj_out_b};
+    for (const void* p : mptrs)
         if (p == nullptr || !aligned16(p)) return PCPP_EINVAL;
-    if (!x || !text || !y) return PCPP_EINVAL;
-    if (r.up > 0 && (!k_up || !v_up)) return PCPP_EINVAL;
-    if (r.dn > 0 && (!k_dn || !v_dn)) return PCPP_EINVAL;
-    const void* aptrs[] = {x, text, y, k_up, v_up, k_dn, v_dn, k_fresh_out, v_fresh_out};
-    for (const void* p : aptrs)
-        if (p && !aligned16(p)) return PCPP_EINVAL;
-    const BlockLayout L = layout(g, r, w, n_text);
+    if (!x || !text || !y || !aligned16(x) || !aligned16(text) || !aligned16(y)) return PCPP_EINVAL;
+    if ((r.up > 0 && (!k_up || !v_up)) || (r.dn > 0 && (!k_dn || !v_dn))) return PCPP_EINVAL;
+    for (int j = 0; j < depth; ++j) {
+        const pcpp_basic_block_weights_t& w = blocks[j];
+        const void* wptrs[] = {w.ln1_gamma, w.ln1_beta, w.attn1_qkv_w, w.attn1_out_w, w.attn1_out_b, w.ln2_gamma,
+                               w.ln2_beta, w.attn2_q_w, w.attn2_kv_w, w.attn2_out_w, w.attn2_out_b, w.ln3_gamma,
+                               w.ln3_beta, w.ff1_w, w.ff1_b, w.ff2_w, w.ff2_b};
+        for (const void* p : wptrs)
+            if (p == nullptr || !aligned16(p)) return PCPP_EINVAL;
+        if (r.up > 0 && (!k_up[j] || !v_up[j] || !aligned16(k_up[j]) || !aligned16(v_up[j]))) return PCPP_EINVAL;
+        if (r.dn > 0 && (!k_dn[j] || !v_dn[j] || !aligned16(k_dn[j]) || !aligned16(v_dn[j]))) return PCPP_EINVAL;
+        if (k_out && k_out[j] && !aligned16(k_out[j])) return PCPP_EINVAL;
+        if (v_out && v_out[j] && !aligned16(v_out[j])) return PCPP_EINVAL;
+    }
+    const BlockLayout L = layout(g, r, mw.ff_inner, mw.gn_groups, n_text);
     if (workspace == nullptr || ws_bytes < L.total) return PCPP_EWORKSPACE;
     if (!aligned16(workspace)) return PCPP_EINVAL;
 
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    const int B = g->batch, N = r.nq, C = r.C, F = w->ff_inner, T = n_text;
+    const int B = g->batch, N = r.nq, C = r.C, F = mw.ff_inner, T = n_text;
     const int rows = B * N;
     __bf16* t16 = (__bf16*)(ws + L.t16);
     float* hid = (float*)(ws + L.hid);
     __bf16* q16 = (__bf16*)(ws + L.q16);
-    __bf16* k16 = k_fresh_out ? (__bf16*)k_fresh_out : (__bf16*)(ws + L.k16);
-    __bf16* v16 = v_fresh_out ? (__bf16*)v_fresh_out : (__bf16*)(ws + L.v16);
     __bf16* a16 = (__bf16*)(ws + L.a16);
     __bf16* k2 = (__bf16*)(ws + L.k2);
     __bf16* v2 = (__bf16*)(ws + L.v2);
@@ -192,20 +227,20 @@ int run_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, const void* x
     GroupNormParams gp;
     gp.x = (const __bf16*)x;
     gp.y = t16;
-    gp.gamma = (const __bf16*)w->gn_gamma;
-    gp.beta = (const __bf16*)w->gn_beta;
+    gp.gamma = (const __bf16*)mw.gn_gamma;
+    gp.beta = (const __bf16*)mw.gn_beta;
     gp.stats = (float*)(ws + L.gn);
     gp.B = B;
     gp.N = N;
     gp.C = C;
-    gp.G = w->gn_groups;
+    gp.G = mw.gn_groups;
     gp.eps = 1e-6f;
     gp.bands = gn_bands;
     gp.n_bands = g->n_patches;
     gp.band = g->patch_idx;
     gp.own_out = gn_own;
     PCPP_CHECK(launch_group_norm(gp, s));
-    PCPP_CHECK(launch_gemm(gemm(t16, C, false, w->proj_in_w, w->proj_in_b, rows, C, C, hid, C, true), s));
+    PCPP_CHECK(launch_gemm(gemm(t16, C, false, mw.proj_in_w, mw.proj_in_b, rows, C, C, hid, C, true), s));
 
     LayerNormParams lp;
     lp.x = hid;
@@ -213,79 +248,89 @@ int run_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, const void* x
     lp.rows = rows;
     lp.C = C;
     lp.eps = 1e-5f;
-
-    // Self-attention: Q, K, V of the band; K and V are the band's export.
-    lp.gamma = (const __bf16*)w->ln1_gamma;
-    lp.beta = (const __bf16*)w->ln1_beta;
-    PCPP_CHECK(launch_layer_norm(lp, s));
-    {
-        GemmParams qkv = gemm(t16, C, false, w->attn1_qkv_w, nullptr, rows, 3 * C, C, q16, C, false);
-        qkv.out[1] = k16;
-        qkv.out[2] = v16;
-        qkv.seg = C;
-        PCPP_CHECK(launch_gemm(qkv, s));
-    }
-    {
-        AttnParams ap = self_attn_params(g, r, q16, a16, k16, v16, k_up, v_up, k_dn, v_dn, nullptr);
-        PCPP_CHECK(launch_attention_bf16(ap, attn_ws, L.attn_ws_bytes, s));
-    }
-    {
-        GemmParams o = gemm(a16, C, false, w->attn1_out_w, w->attn1_out_b, rows, C, C, hid, C, true);
-        o.resid = hid;
-        o.ldr = C;
-        o.resid_f32 = 1;
-        PCPP_CHECK(launch_gemm(o, s));
-    }
-
-    // Cross-attention to the text features.
-    lp.gamma = (const __bf16*)w->ln2_gamma;
-    lp.beta = (const __bf16*)w->ln2_beta;
-    PCPP_CHECK(launch_layer_norm(lp, s));
-    PCPP_CHECK(launch_gemm(gemm(t16, C, false, w->attn2_q_w, nullptr, rows, C, C, q16, C, false), s));
-    {
-        GemmParams kv = gemm(text, text_dim, false, w->attn2_kv_w, nullptr, B * T, 2 * C, text_dim, k2, C, false);
-        kv.out[1] = v2;
-        kv.seg = C;
-        PCPP_CHECK(launch_gemm(kv, s));
-    }
-    {
-        AttnParams ap = cross_attn_params(g, r, q16, a16, k2, v2, T);
-        PCPP_CHECK(launch_attention_bf16(ap, attn_ws, L.attn_ws_bytes, s));
-    }
-    {
-        GemmParams o = gemm(a16, C, false, w->attn2_out_w, w->attn2_out_b, rows, C, C, hid, C, true);
-        o.resid = hid;
-        o.ldr = C;
-        o.resid_f32 = 1;
-        PCPP_CHECK(launch_gemm(o, s));
-    }
-
-    // GEGLU feed-forward.
-    lp.gamma = (const __bf16*)w->ln3_gamma;
-    lp.beta = (const __bf16*)w->ln3_beta;
-    PCPP_CHECK(launch_layer_norm(lp, s));
-    {
-        GemmParams ff = gemm(t16, C, false, w->ff1_w, w->ff1_b, rows, F, C, u16, F, false);
-        ff.geglu = 1;
-        ff.F = F;
-        PCPP_CHECK(launch_gemm(ff, s));
-    }
-    // FF-out also writes the stream rounded to bf16 (into t16, free by now),
-    // the operand proj_out reads.
+    // The last FF-out also writes the stream rounded to bf16 (into t16, free
+    // by then), the operand proj_out reads.
     const bool copy16 = C % 64 == 0 && F % 64 == 0;
-    {
-        GemmParams o = gemm(u16, F, false, w->ff2_w, w->ff2_b, rows, C, F, hid, C, true);
-        o.resid = hid;
-        o.ldr = C;
-        o.resid_f32 = 1;
-        if (copy16) o.out_bf16 = t16;
-        PCPP_CHECK(launch_gemm(o, s));
+
+    for (int j = 0; j < depth; ++j) {
+        const pcpp_basic_block_weights_t& w = blocks[j];
+        __bf16* k16 = k_out && k_out[j] ? (__bf16*)k_out[j] : (__bf16*)(ws + L.k16);
+        __bf16* v16 = v_out && v_out[j] ? (__bf16*)v_out[j] : (__bf16*)(ws + L.v16);
+        const void* ku = r.up > 0 ? k_up[j] : nullptr;
+        const void* vu = r.up > 0 ? v_up[j] : nullptr;
+        const void* kd = r.dn > 0 ? k_dn[j] : nullptr;
+        const void* vd = r.dn > 0 ? v_dn[j] : nullptr;
+
+        // Self-attention: Q, K, V of the band; K and V are the band's export.
+        lp.gamma = (const __bf16*)w.ln1_gamma;
+        lp.beta = (const __bf16*)w.ln1_beta;
+        PCPP_CHECK(launch_layer_norm(lp, s));
+        {
+            GemmParams qkv = gemm(t16, C, false, w.attn1_qkv_w, nullptr, rows, 3 * C, C, q16, C, false);
+            qkv.out[1] = k16;
+            qkv.out[2] = v16;
+            qkv.seg = C;
+            PCPP_CHECK(launch_gemm(qkv, s));
+        }
+        {
+            AttnParams ap = self_attn_params(g, r, q16, a16, k16, v16, ku, vu, kd, vd, nullptr);
+            PCPP_CHECK(launch_attention_bf16(ap, attn_ws, L.attn_ws_bytes, s));
+        }
+        {
+            GemmParams o = gemm(a16, C, false, w.attn1_out_w, w.attn1_out_b, rows, C, C, hid, C, true);
+            o.resid = hid;
+            o.ldr = C;
+            o.resid_f32 = 1;
+            PCPP_CHECK(launch_gemm(o, s));
+        }
+
+        // Cross-attention to the text features.
+        lp.gamma = (const __bf16*)w.ln2_gamma;
+        lp.beta = (const __bf16*)w.ln2_beta;
+        PCPP_CHECK(launch_layer_norm(lp, s));
+        PCPP_CHECK(launch_gemm(gemm(t16, C, false, w.attn2_q_w, nullptr, rows, C, C, q16, C, false), s));
+        {
+            GemmParams kv = gemm(text, text_dim, false, w.attn2_kv_w, nullptr, B * T, 2 * C, text_dim, k2, C, false);
+            kv.out[1] = v2;
+            kv.seg = C;
+            PCPP_CHECK(launch_gemm(kv, s));
+        }
+        {
+            AttnParams ap = cross_attn_params(g, r, q16, a16, k2, v2, T);
+            PCPP_CHECK(launch_attention_bf16(ap, attn_ws, L.attn_ws_bytes, s));
+        }
+        {
+            GemmParams o = gemm(a16, C, false, w.attn2_out_w, w.attn2_out_b, rows, C, C, hid, C, true);
+            o.resid = hid;
+            o.ldr = C;
+            o.resid_f32 = 1;
+            PCPP_CHECK(launch_gemm(o, s));
+        }
+
+        // GEGLU feed-forward.
+        lp.gamma = (const __bf16*)w.ln3_gamma;
+        lp.beta = (const __bf16*)w.ln3_beta;
+        PCPP_CHECK(launch_layer_norm(lp, s));
+        {
+            GemmParams ff = gemm(t16, C, false, w.ff1_w, w.ff1_b, rows, F, C, u16, F, false);
+            ff.geglu = 1;
+            ff.F = F;
+            PCPP_CHECK(launch_gemm(ff, s));
+        }
+        {
+            GemmParams o = gemm(u16, F, false, w.ff2_w, w.ff2_b, rows, C, F, hid, C, true);
+            o.resid = hid;
+            o.ldr = C;
+            o.resid_f32 = 1;
+            if (copy16 && j == depth - 1) o.out_bf16 = t16;
+            PCPP_CHECK(launch_gemm(o, s));
+        }
     }
 
-    // proj_out plus the block input.
+    // proj_out plus the module input.
     {
-        GemmParams o = copy16 ? gemm(t16, C, false, w->proj_out_w, w->proj_out_b, rows, C, C, y, C, false)
-                              : gemm(hid, C, true, w->proj_out_w, w->proj_out_b, rows, C, C, y, C, false);
+        GemmParams o = copy16 ? gemm(t16, C, false, mw.proj_out_w, mw.proj_out_b, rows, C, C, y, C, false)
+                              : gemm(hid, C, true, mw.proj_out_w, mw.proj_out_b, rows, C, C, y, C, false);
         o.resid = x;
         o.ldr = C;
         o.resid_f32 = 0;
@@ -295,7 +340,30 @@ int run_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, const void* x
     return PCPP_OK;
 }
 
+int run_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, const void* x, const void* text,
+              int32_t n_text, int32_t text_dim, const void* k_up, const void* v_up, const void* k_dn,
+              const void* v_dn, const float* gn_bands, float* gn_own, void* y, void* k_fresh_out,
+              void* v_fresh_out, void* workspace, size_t ws_bytes, void* stream) {
+    if (w == nullptr) return PCPP_EINVAL;
+    const pcpp_basic_block_weights_t b = basic_of(w);
+    const void* ku[1] = {k_up};
+    const void* vu[1] = {v_up};
+    const void* kd[1] = {k_dn};
+    const void* vd[1] = {v_dn};
+    void* ko[1] = {k_fresh_out};
+    void* vo[1] = {v_fresh_out};
+    return run_module(g, module_of(w), &b, 1, x, text, n_text, text_dim, ku, vu, kd, vd, gn_bands, gn_own, y, ko, vo,
+                      workspace, ws_bytes, stream);
+}
+
 }  // namespace
+
+PCPP_EXPORT size_t pcpp_transformer_block_workspace_size(const pcpp_geom_t* g, const pcpp_block_weights_t* w,
+                                                         int32_t n_text, int32_t text_dim) {
+    Geo r;
+    if (w == nullptr || validate_block(g, w->ff_inner, w->gn_groups, n_text, text_dim, &r) != PCPP_OK) return 0;
+    return layout(g, r, w->ff_inner, w->gn_groups, n_text).total;
+}
 
 PCPP_EXPORT int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, const void* x,
                                        const void* text, int32_t n_text, int32_t text_dim, const void* k_up,
@@ -316,4 +384,27 @@ PCPP_EXPORT int pcpp_transformer_block_sync_gn(const pcpp_geom_t* g, const pcpp_
     if (gn_own != nullptr && ((uintptr_t)gn_own & 3u) != 0) return PCPP_EINVAL;
     return run_block(g, w, x, text, n_text, text_dim, k_up, v_up, k_dn, v_dn, gn_bands, gn_own, y, k_fresh_out,
                      v_fresh_out, workspace, ws_bytes, stream);
+}
+
+PCPP_EXPORT size_t pcpp_transformer_module_workspace_size(const pcpp_geom_t* g, const pcpp_module_weights_t* w,
+                                                          int32_t n_text, int32_t text_dim) {
+    Geo r;
+    if (w == nullptr || validate_block(g, w->ff_inner, w->gn_groups, n_text, text_dim, &r) != PCPP_OK) return 0;
+    if (w->depth < 1 || w->depth > 64) return 0;
+    return layout(g, r, w->ff_inner, w->gn_groups, n_text).total;
+}
+
+PCPP_EXPORT int pcpp_transformer_module(const pcpp_geom_t* g, const pcpp_module_weights_t* w, const void* x,
+                                        const void* text, int32_t n_text, int32_t text_dim,
+                                        const void* const* k_up, const void* const* v_up, const void* const* k_dn,
+                                        const void* const* v_dn, const float* gn_bands, float* gn_own, void* y,
+                                        void* const* k_fresh_out, void* const* v_fresh_out, void* workspace,
+                                        size_t ws_bytes, void* stream) {
+    if (w == nullptr) return PCPP_EINVAL;
+    if (gn_bands != nullptr && ((uintptr_t)gn_bands & 3u) != 0) return PCPP_EINVAL;
+    if (gn_own != nullptr && ((uintptr_t)gn_own & 3u) != 0) return PCPP_EINVAL;
+    const ModuleW mw{w->gn_gamma, w->gn_beta, w->proj_in_w, w->proj_in_b, w->proj_out_w, w->proj_out_b, w->ff_inner,
+                     w->gn_groups};
+    return run_module(g, mw, w->blocks, w->depth, x, text, n_text, text_dim, k_up, v_up, k_dn, v_dn, gn_bands, gn_own,
+                      y, k_fresh_out, v_fresh_out, workspace, ws_bytes, stream);
 }

@@ -53,6 +53,24 @@ class pcpp_block_weights_t(ctypes.Structure):
         ("ff_inner", ctypes.c_int32), ("gn_groups", ctypes.c_int32)]
 
 
+BASIC_BLOCK_PTR_FIELDS = (
+    "ln1_gamma", "ln1_beta", "attn1_qkv_w", "attn1_out_w", "attn1_out_b", "ln2_gamma", "ln2_beta",
+    "attn2_q_w", "attn2_kv_w", "attn2_out_w", "attn2_out_b", "ln3_gamma", "ln3_beta",
+    "ff1_w", "ff1_b", "ff2_w", "ff2_b",
+)
+
+
+class pcpp_basic_block_weights_t(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in BASIC_BLOCK_PTR_FIELDS]
+
+
+class pcpp_module_weights_t(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("gn_gamma", "gn_beta", "proj_in_w", "proj_in_b", "proj_out_w",
+                                               "proj_out_b")] + [
+        ("blocks", ctypes.POINTER(pcpp_basic_block_weights_t)), ("depth", ctypes.c_int32),
+        ("ff_inner", ctypes.c_int32), ("gn_groups", ctypes.c_int32)]
+
+
 class pcpp_resnet_geom_t(ctypes.Structure):
     _fields_ = [
         ("H", ctypes.c_int32), ("W", ctypes.c_int32),
@@ -133,6 +151,9 @@ def _load():
                                              ctypes.POINTER(pcpp_resnet_weights_t)] + [vp] * 14 + [sz, vp]),
         "pcpp_guided_step": (ctypes.c_int, [ctypes.POINTER(pcpp_step_params_t), ctypes.c_int64,
                                             vp, vp, vp, vp, vp, vp]),
+        "pcpp_transformer_module_workspace_size": (sz, [gp, ctypes.POINTER(pcpp_module_weights_t), i32, i32]),
+        "pcpp_transformer_module": (ctypes.c_int, [gp, ctypes.POINTER(pcpp_module_weights_t), vp, vp, i32, i32,
+                                                   vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "pcpp_conv3x3_workspace_size": (sz, [ctypes.POINTER(pcpp_conv_geom_t)]),
         "pcpp_conv3x3": (ctypes.c_int, [ctypes.POINTER(pcpp_conv_geom_t)] + [vp] * 7 + [sz, vp]),
     }
@@ -153,6 +174,7 @@ EXPORTED = (
     "pcpp_multihop_message_bytes", "pcpp_pack_multihop", "pcpp_unpack_multihop",
     "pcpp_resnet_block_workspace_size", "pcpp_resnet_block", "pcpp_guided_step",
     "pcpp_conv3x3_workspace_size", "pcpp_conv3x3",
+    "pcpp_transformer_module_workspace_size", "pcpp_transformer_module",
 )
 
 
@@ -339,3 +361,42 @@ def pcpp_conv3x3(g, x, row_up, row_dn, w, bias, y, workspace, ws_bytes, stream=N
     _check("pcpp_conv3x3", _lib.pcpp_conv3x3(
         ctypes.byref(g), _ptr(x), _ptr(row_up), _ptr(row_dn), _ptr(w), _ptr(bias), _ptr(y), _ptr(workspace),
         ws_bytes, _stream(stream)))
+
+
+def make_module_weights(module: dict, blocks: list, ff_inner: int, gn_groups: int):
+    """(pcpp_module_weights_t, keep-alive array) from device tensors: module
+    holds gn_gamma .. proj_out_b, blocks[j] basic block j's tensors."""
+    arr = (pcpp_basic_block_weights_t * len(blocks))()
+    for j, bt in enumerate(blocks):
+        for name in BASIC_BLOCK_PTR_FIELDS:
+            setattr(arr[j], name, _ptr(bt.get(name)))
+    w = pcpp_module_weights_t()
+    for name in ("gn_gamma", "gn_beta", "proj_in_w", "proj_in_b", "proj_out_w", "proj_out_b"):
+        setattr(w, name, _ptr(module.get(name)))
+    w.blocks = ctypes.cast(arr, ctypes.POINTER(pcpp_basic_block_weights_t))
+    w.depth = len(blocks)
+    w.ff_inner = ff_inner
+    w.gn_groups = gn_groups
+    return w, arr
+
+
+def _ptr_array(ts):
+    if ts is None:
+        return None
+    return (ctypes.c_void_p * len(ts))(*[_ptr(t) for t in ts])
+
+
+def pcpp_transformer_module_workspace_size(g, w, n_text, text_dim) -> int:
+    return _lib.pcpp_transformer_module_workspace_size(ctypes.byref(g), ctypes.byref(w), n_text, text_dim)
+
+
+def pcpp_transformer_module(g, w, x, text, n_text, text_dim, k_up, v_up, k_dn, v_dn, gn_bands, gn_own, y,
+                            k_fresh_out, v_fresh_out, workspace, ws_bytes, stream=None):
+    """k_up .. v_fresh_out: lists of per-basic-block tensors (or None)."""
+    arrs = [_ptr_array(a) for a in (k_up, v_up, k_dn, v_dn, k_fresh_out, v_fresh_out)]
+    _check("pcpp_transformer_module", _lib.pcpp_transformer_module(
+        ctypes.byref(g), ctypes.byref(w), _ptr(x), _ptr(text), n_text, text_dim,
+        *[None if a is None else ctypes.cast(a, ctypes.c_void_p) for a in arrs[:4]],
+        _ptr(gn_bands), _ptr(gn_own), _ptr(y),
+        *[None if a is None else ctypes.cast(a, ctypes.c_void_p) for a in arrs[4:]],
+        _ptr(workspace), ws_bytes, _stream(stream)))

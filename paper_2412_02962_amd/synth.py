@@ -404,3 +404,23 @@ CONV_CONFIGS = {
     "sdxl2048_up_l2": (64, 64, 8, 3, 1280, 1280, 2),
     "sdxl2048_up_l1": (128, 128, 8, 3, 640, 640, 2),
 }
+
+
+MODULE_WEIGHT_NAMES = ("gn_gamma", "gn_beta", "proj_in_w", "proj_in_b", "proj_out_w", "proj_out_b")
+
+
+def module_inputs(bc: BlockConfig, depth: int, seed: Optional[int] = None, batch: int = 1):
+    """bf16 inputs of one transformer-module call of the given depth: x, text
+    and the module's own weights as block_inputs draws them for `seed`; basic
+    block j's weights and stale neighbour K/V as block_inputs draws them for
+    seed + 1000 + j.  Returns (x, text, module_weights, [block_weights],
+    [(k_up, v_up, k_dn, v_dn)])."""
+    s = BASE_SEED + bc.seed_id if seed is None else seed
+    base = block_inputs(bc, seed=s, batch=batch)
+    module = {k: base[k] for k in MODULE_WEIGHT_NAMES}
+    blocks, stale = [], []
+    for j in range(depth):
+        bj = block_inputs(bc, seed=s + 1000 + j, batch=batch)
+        blocks.append({k: bj[k] for k in BLOCK_WEIGHT_NAMES if k not in MODULE_WEIGHT_NAMES})
+        stale.append((bj["k_up"], bj["v_up"], bj["k_dn"], bj["v_dn"]))
+    return base["x"], base["text"], module, blocks, stale

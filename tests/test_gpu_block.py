@@ -169,3 +169,99 @@ def test_block_synchronized_group_norm(which):
     # the band-local block differs (the statistics are not this band's alone)
     y_local, _, _ = _run_block(bc, inp, B)
     assert not torch.equal(y_local, y)
+
+
+# ---------------------------------------------------------------------------
+# Transformer module of depth d (each basic block its own weights and stale K/V)
+# ---------------------------------------------------------------------------
+
+def _run_module(bc, x, text, module, blocks, stale, batch, gn_bands=None, want_own=False):
+    import torch
+    from paper_2412_02962_amd import pcpp
+    cfg = bc.attn
+    dv = lambda a: None if a is None else gu.to_dev(a, "bf16")
+    g = pcpp.make_geom(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, cfg.d, batch, 0, pcpp.PCPP_DTYPE_BF16)
+    md = {k: dv(v) for k, v in module.items()}
+    bd = [{k: dv(v) for k, v in b.items()} for b in blocks]
+    w, keep = pcpp.make_module_weights(md, bd, bc.ff_inner, bc.gn_groups)
+    xd, td = dv(x), dv(text)
+    st = [[dv(a) for a in s] for s in stale]
+    cols = list(zip(*st))                                   # k_up list, v_up list, ...
+    lists = [None if any(a is None for a in c) else list(c) for c in cols]
+    y = torch.empty_like(xd)
+    ko = [torch.empty_like(xd) for _ in blocks]
+    vo = [torch.empty_like(xd) for _ in blocks]
+    own = torch.empty((batch, bc.gn_groups, 3), dtype=torch.float32, device=gu.DEV) if want_own else None
+    wsb = pcpp.pcpp_transformer_module_workspace_size(g, w, bc.n_text, bc.text_dim)
+    assert wsb > 0
+    ws = torch.zeros(wsb, dtype=torch.uint8, device=gu.DEV)
+    pcpp.pcpp_transformer_module(g, w, xd, td, bc.n_text, bc.text_dim, *lists, gn_bands, own, y, ko, vo, ws, wsb)
+    torch.cuda.synchronize()
+    del keep
+    return y, ko, vo, own
+
+
+def _oracle_module(bc, x, text, module, blocks, stale, gn_band_stats=None):
+    cfg = bc.attn
+    f = lambda a: None if a is None else oracle.from_bf16_bits(a)
+    return oracle.transformer_module(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, {k: f(v) for k, v in module.items()},
+                                     [{k: f(v) for k, v in b.items()} for b in blocks], f(x), f(text),
+                                     [tuple(f(a) for a in s) for s in stale], gn_groups=bc.gn_groups,
+                                     gn_band_stats=gn_band_stats)
+
+
+def test_module_of_depth_one_is_the_block():
+    import torch
+    bc = synth.BLOCK_CONFIG
+    _say("module depth 1 = block")
+    x, text, module, blocks, stale = synth.module_inputs(bc, 1)
+    y, ko, vo, _ = _run_module(bc, x, text, module, blocks, stale, 1)
+    inp = dict(module)
+    inp.update(blocks[0])
+    inp.update({"x": x, "text": text, "k_up": stale[0][0], "v_up": stale[0][1], "k_dn": stale[0][2],
+                "v_dn": stale[0][3]})
+    yb, kb, vb = _run_block(bc, inp, 1)
+    assert torch.equal(y, yb) and torch.equal(ko[0], kb) and torch.equal(vo[0], vb)
+
+
+MODULE_CASES = [
+    (synth.BLOCK_CONFIG, 2, 1),
+    (dataclasses.replace(synth.BLOCK_CONFIG, attn=synth.AttnConfig(name="m_small", H=12, W=20, n=3, i=1, p=0.5,
+                                                                   heads=2, d=64, dtype="bf16", seed_id=77),
+                         ff_inner=256, text_dim=64, n_text=7, seed_id=77), 3, 2),
+]
+
+
+@pytest.mark.parametrize("case", MODULE_CASES, ids=["l1_2048_depth2", "small_depth3_b2"])
+def test_module_matches_oracle(case):
+    bc, depth, batch = case
+    _say("module", bc.attn.name, depth, batch)
+    x, text, module, blocks, stale = synth.module_inputs(bc, depth, batch=batch)
+    y, ko, vo, _ = _run_module(bc, x, text, module, blocks, stale, batch)
+    want_y, want_k, want_v = _oracle_module(bc, x, text, module, blocks, stale)
+    _check(gu.to_f64(y), want_y, stages=6 * depth, tag=f"module y depth {depth}")
+    # Block j's K and V sit behind the GroupNorm, LayerNorm and K/V roundings
+    # plus six per earlier block.  Each stage's term is a probabilistic bound
+    # (a rounding propagated through a GEMM is a near-Gaussian error): with
+    # three stages the bound is about 6 sigma of their sum while the maximum
+    # over 1.3 million elements reaches about 5 sigma, so one stage is added.
+    for j in range(depth):
+        _check(gu.to_f64(ko[j]), want_k[j], stages=4 + 6 * j, tag=f"k export {j}")
+        _check(gu.to_f64(vo[j]), want_v[j], stages=4 + 6 * j, tag=f"v export {j}")
+
+
+def test_module_synchronized_group_norm():
+    import torch
+    bc, depth, batch = MODULE_CASES[1]
+    _say("module sync GN")
+    x, text, module, blocks, stale = synth.module_inputs(bc, depth, batch=batch)
+    rng = np.random.default_rng(5)
+    cfg = bc.attn
+    st = np.stack([oracle.group_stats(0.3 * rng.standard_normal() + rng.standard_normal((batch, cfg.h * cfg.W, cfg.C)),
+                                      bc.gn_groups) for _ in range(cfg.n)])
+    bands = torch.from_numpy(st.astype(np.float32)).to(gu.DEV)
+    y, _, _, own = _run_module(bc, x, text, module, blocks, stale, batch, gn_bands=bands, want_own=True)
+    want_y, _, _ = _oracle_module(bc, x, text, module, blocks, stale, gn_band_stats=st)
+    _check(gu.to_f64(y), want_y, stages=6 * depth, tag="module sync GN")
+    want_own = oracle.group_stats(oracle.from_bf16_bits(x), bc.gn_groups)
+    assert np.allclose(own.double().cpu().numpy()[..., 1], want_own[..., 1], atol=1e-5)
