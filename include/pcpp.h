@@ -555,6 +555,32 @@ int pcpp_conv3x3(const pcpp_conv_geom_t* g, const void* x, const void* row_up,
                  void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * [rows, ca] and [rows, cb] bf16 side by side into out [rows, ca + cb]: the
+ * U-Net up path's concatenation of a level's state with its skip connection
+ * (the ResNet that follows takes ca + cb channels).  b = NULL fills the cb
+ * channels with zeros (the padding of the 4 latent channels to the 64 the
+ * convolution takes).  ca, cb multiples of 8; pointers 16-byte aligned; out
+ * must not overlap a or b (PCPP_EINVAL).  Asynchronous on `stream`.
+ */
+int pcpp_concat_channels(int64_t rows, const void* a, int32_t ca, const void* b,
+                         int32_t cb, void* out, void* stream);
+
+/*
+ * GroupNorm over each image's tokens (statistics of x itself), affine, then
+ * SiLU if silu = 1: the U-Net's output head before conv_out (SDXL: 32
+ * groups, eps 1e-5).  x, y [batch, tokens, channels] bf16 (y may not
+ * overlap x), gamma/beta [channels]; channels % 8 == 0, <= 2560, groups <=
+ * 256 dividing channels (PCPP_ENOTSUP otherwise).  The workspace needs no
+ * clearing.  Asynchronous on `stream`.
+ */
+size_t pcpp_group_norm_workspace_size(int32_t batch, int32_t tokens,
+                                      int32_t channels, int32_t groups);
+int pcpp_group_norm(int32_t batch, int32_t tokens, int32_t channels,
+                    int32_t groups, float eps, int32_t silu, const void* x,
+                    const void* gamma, const void* beta, void* y,
+                    void* workspace, size_t ws_bytes, void* stream);
+
+/*
  * The update of a band's latent at the end of a step (Sec. 3.1): the two
  * guidance branches' noise predictions are combined by classifier-free
  * guidance (Eq. 2), e = eps_u + s (eps_c - eps_u), and then

@@ -217,3 +217,44 @@ def resnet_weight_shapes(c_in: int, c_out: int, temb_dim: int) -> Dict[str, Tupl
         s["skip_w"] = (c_out, c_in)
         s["skip_b"] = (c_out,)
     return s
+
+
+# ---------------------------------------------------------------------------
+# One band's U-Net forward (SDXL's order of layers), float64
+# ---------------------------------------------------------------------------
+
+def unet_band_step(layers, n: int, i: int, p: float, groups: int, weights, stale,
+                   latent: np.ndarray, temb: np.ndarray, text: np.ndarray) -> np.ndarray:
+    """The noise prediction of band i: the layers in order (`layers`, a list
+    of dicts: name, kind 'conv' / 'resnet' / 'module' / 'gn', input grid H x
+    W, channels, conv mode, module depth, push / pop of skip connections),
+    each with its weights and the band's stale neighbour data of the previous
+    step (convolution rows, ResNet edge rows, every basic block's K/V).  The
+    up path concatenates its state with the skip along the channels before
+    its ResNets.  GroupNorms use the band's own statistics.  latent [B, h*W,
+    64] (4 channels, zero-padded); returns [B, h*W, 64]."""
+    from .pcpp_oracle import group_norm as _gn, transformer_module as _module
+    modes = {0: "same", 1: "down", 2: "up"}
+    hcur = latent
+    skips = []
+    for ly in layers:
+        name, kind, W = ly["name"], ly["kind"], ly["W"]
+        w = weights[name]
+        if kind == "conv":
+            st = stale[name]
+            out = conv3x3_band_mode(hcur, W, w["w"], w["b"], st["row_up"], st["row_dn"], modes[ly["mode"]])
+        elif kind == "resnet":
+            if ly.get("pop"):
+                hcur = np.concatenate([hcur, skips.pop()], axis=-1)
+            st = stale[name]
+            out, _, _ = resnet_block(W, w, hcur, temb, st["edges1_up"], st["edges1_dn"], st["edges2_up"],
+                                     st["edges2_dn"], groups=groups, i=i)
+        elif kind == "module":
+            out, _, _ = _module(ly["H"], W, n, i, p, w["heads"], w["module"], w["blocks"], hcur, text,
+                                stale[name], gn_groups=groups)
+        else:
+            out = silu(_gn(hcur, groups, w["gamma"], w["beta"], eps=RESNET_GN_EPS))
+        if ly.get("push"):
+            skips.append(out)
+        hcur = out
+    return hcur

@@ -154,6 +154,9 @@ def _load():
         "pcpp_transformer_module_workspace_size": (sz, [gp, ctypes.POINTER(pcpp_module_weights_t), i32, i32]),
         "pcpp_transformer_module": (ctypes.c_int, [gp, ctypes.POINTER(pcpp_module_weights_t), vp, vp, i32, i32,
                                                    vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "pcpp_concat_channels": (ctypes.c_int, [ctypes.c_int64, vp, i32, vp, i32, vp, vp]),
+        "pcpp_group_norm_workspace_size": (sz, [i32, i32, i32, i32]),
+        "pcpp_group_norm": (ctypes.c_int, [i32, i32, i32, i32, ctypes.c_float, i32, vp, vp, vp, vp, vp, sz, vp]),
         "pcpp_conv3x3_workspace_size": (sz, [ctypes.POINTER(pcpp_conv_geom_t)]),
         "pcpp_conv3x3": (ctypes.c_int, [ctypes.POINTER(pcpp_conv_geom_t)] + [vp] * 7 + [sz, vp]),
     }
@@ -175,6 +178,7 @@ EXPORTED = (
     "pcpp_resnet_block_workspace_size", "pcpp_resnet_block", "pcpp_guided_step",
     "pcpp_conv3x3_workspace_size", "pcpp_conv3x3",
     "pcpp_transformer_module_workspace_size", "pcpp_transformer_module",
+    "pcpp_concat_channels", "pcpp_group_norm_workspace_size", "pcpp_group_norm",
 )
 
 
@@ -400,3 +404,17 @@ def pcpp_transformer_module(g, w, x, text, n_text, text_dim, k_up, v_up, k_dn, v
         _ptr(gn_bands), _ptr(gn_own), _ptr(y),
         *[None if a is None else ctypes.cast(a, ctypes.c_void_p) for a in arrs[4:]],
         _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def pcpp_concat_channels(rows, a, ca, b, cb, out, stream=None):
+    _check("pcpp_concat_channels", _lib.pcpp_concat_channels(rows, _ptr(a), ca, _ptr(b), cb, _ptr(out),
+                                                              _stream(stream)))
+
+
+def pcpp_group_norm_workspace_size(batch, tokens, channels, groups) -> int:
+    return _lib.pcpp_group_norm_workspace_size(batch, tokens, channels, groups)
+
+
+def pcpp_group_norm(batch, tokens, channels, groups, eps, silu, x, gamma, beta, y, workspace, ws_bytes, stream=None):
+    _check("pcpp_group_norm", _lib.pcpp_group_norm(batch, tokens, channels, groups, eps, silu, _ptr(x), _ptr(gamma),
+                                                    _ptr(beta), _ptr(y), _ptr(workspace), ws_bytes, _stream(stream)))

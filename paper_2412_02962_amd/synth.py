@@ -424,3 +424,146 @@ def module_inputs(bc: BlockConfig, depth: int, seed: Optional[int] = None, batch
         blocks.append({k: bj[k] for k in BLOCK_WEIGHT_NAMES if k not in MODULE_WEIGHT_NAMES})
         stale.append((bj["k_up"], bj["v_up"], bj["k_dn"], bj["v_dn"]))
     return base["x"], base["text"], module, blocks, stale
+
+
+# ---------------------------------------------------------------------------
+# An SDXL-shaped U-Net on one band: topology and seeded random weights / stale
+# neighbour data (shapes and draws only)
+# ---------------------------------------------------------------------------
+
+LATENT_PAD = 64   # the 4 latent channels, zero-padded to the convolution's granularity
+
+
+@dataclasses.dataclass(frozen=True)
+class UNetSpec:
+    """channels / depths per level (depth 0: no attention at that level),
+    the latent grid H0 x W0 split in n bands (band i), p of the attention."""
+    name: str
+    channels: tuple
+    depths: tuple
+    H0: int
+    W0: int
+    n: int
+    i: int
+    p: float = 0.25
+    batch: int = 1
+    temb_dim: int = 1280
+    text_dim: int = 2048
+    n_text: int = 77
+    groups: int = 32
+    seed_id: int = 120
+
+
+UNET_SDXL_2048 = UNetSpec("sdxl2048_unet", (320, 640, 1280), (0, 2, 10), 256, 256, 8, 3)
+UNET_TINY = UNetSpec("tiny_unet", (64, 128, 128), (0, 1, 1), 32, 16, 2, 1, p=0.5, temb_dim=64, text_dim=64,
+                     n_text=7, seed_id=121)
+
+
+def unet_layers(sp: UNetSpec):
+    """SDXL's order of layers on one band: conv_in; per level two (ResNet
+    [+ module]) pairs and a downsampler except at the last level; the middle
+    (ResNet, module, ResNet); per level on the way up three (ResNet on the
+    concatenation with a skip [+ module]) pairs and an upsampler except at
+    level 0; the output GroupNorm + SiLU and conv_out.  Each entry: name,
+    kind ('conv', 'resnet', 'module', 'gn'), grid H x W of its input, c_in,
+    c_out, mode / depth, and whether its output is pushed as a skip or a skip
+    is popped and concatenated to its input first."""
+    L = []
+    ch = sp.channels
+    H, W = sp.H0, sp.W0
+    c = ch[0]
+    L.append(dict(name="conv_in", kind="conv", H=H, W=W, c_in=LATENT_PAD, c_out=c, mode=0, push=True))
+    skip_ch = [c]
+    for lv in range(len(ch)):
+        for r in range(2):
+            L.append(dict(name=f"down{lv}_res{r}", kind="resnet", H=H, W=W, c_in=c, c_out=ch[lv], level=lv,
+                          push=sp.depths[lv] == 0))
+            c = ch[lv]
+            if sp.depths[lv]:
+                L.append(dict(name=f"down{lv}_mod{r}", kind="module", H=H, W=W, c_in=c, c_out=c, level=lv,
+                              depth=sp.depths[lv], push=True))
+            skip_ch.append(c)
+        if lv < len(ch) - 1:
+            L.append(dict(name=f"down{lv}_ds", kind="conv", H=H, W=W, c_in=c, c_out=c, mode=1, push=True))
+            H, W = H // 2, W // 2
+            skip_ch.append(c)
+    top = len(ch) - 1
+    L.append(dict(name="mid_res0", kind="resnet", H=H, W=W, c_in=c, c_out=c, level=top))
+    if sp.depths[top]:
+        L.append(dict(name="mid_mod", kind="module", H=H, W=W, c_in=c, c_out=c, level=top, depth=sp.depths[top]))
+    L.append(dict(name="mid_res1", kind="resnet", H=H, W=W, c_in=c, c_out=c, level=top))
+    for lv in reversed(range(len(ch))):
+        for r in range(3):
+            sc = skip_ch.pop()
+            L.append(dict(name=f"up{lv}_res{r}", kind="resnet", H=H, W=W, c_in=c + sc, c_out=ch[lv], level=lv,
+                          pop=True, skip_c=sc))
+            c = ch[lv]
+            if sp.depths[lv]:
+                L.append(dict(name=f"up{lv}_mod{r}", kind="module", H=H, W=W, c_in=c, c_out=c, level=lv,
+                              depth=sp.depths[lv]))
+        if lv > 0:
+            L.append(dict(name=f"up{lv}_us", kind="conv", H=H, W=W, c_in=c, c_out=c, mode=2))
+            H, W = 2 * H, 2 * W
+    L.append(dict(name="out_gn", kind="gn", H=H, W=W, c_in=c, c_out=c))
+    L.append(dict(name="conv_out", kind="conv", H=H, W=W, c_in=c, c_out=LATENT_PAD, mode=0))
+    return L
+
+
+def _w(g, shape, fan_in):
+    return bf16_bits(g.standard_normal(shape) / np.sqrt(fan_in))
+
+
+def unet_band_inputs(sp: UNetSpec):
+    """Seeded bf16 weights of every layer, the band's stale neighbour data
+    for every layer, the padded latent band, the time embedding and the text:
+    (weights, stale, latent, temb, text).  Draw recipe as the single layers'
+    (weights N(0, 1/fan_in), biases 0.02 N, norm scales 1 + 0.1 N, shifts
+    0.1 N, neighbour rows / K / V N(0, 1)); conv_in's weights are zero on the
+    60 padding channels, conv_out's outputs beyond the first 4 are zero."""
+    s = BASE_SEED + sp.seed_id
+    B = sp.batch
+    weights, stale = {}, {}
+    for idx, ly in enumerate(unet_layers(sp)):
+        g = _stream(s, 1000 + idx)
+        h = ly["H"] // sp.n
+        W, ci, co = ly["W"], ly["c_in"], ly["c_out"]
+        up = sp.i > 0
+        dn = sp.i < sp.n - 1
+        rnd = lambda shape: bf16_bits(g.standard_normal(shape))
+        if ly["kind"] == "conv":
+            w = g.standard_normal((co, 3, 3, ci)) / np.sqrt(9 * ci)
+            if ly["name"] == "conv_in":
+                w[:, :, :, 4:] = 0.0
+            if ly["name"] == "conv_out":
+                w[4:] = 0.0
+            b = 0.02 * g.standard_normal(co)
+            if ly["name"] == "conv_out":
+                b[4:] = 0.0
+            weights[ly["name"]] = {"w": bf16_bits(w), "b": bf16_bits(b)}
+            rows_up = rnd((B, W, ci)) if up else None
+            rows_dn = rnd((B, W, ci)) if dn and ly["mode"] != 1 else None
+            stale[ly["name"]] = {"row_up": rows_up, "row_dn": rows_dn}
+        elif ly["kind"] == "resnet":
+            rc = ResnetConfig(ly["name"], ly["H"], W, sp.n, sp.i, ci, co, temb_dim=sp.temb_dim, groups=sp.groups,
+                              batch=B, seed_id=0)
+            d = resnet_inputs(rc, seed=s + 2000 + idx)
+            weights[ly["name"]] = {k: d[k] for k in resnet_weight_shapes(rc)}
+            stale[ly["name"]] = {k: d[k] for k in ("edges1_up", "edges1_dn", "edges2_up", "edges2_dn")}
+        elif ly["kind"] == "module":
+            heads = co // 64
+            bc = BlockConfig(ly["name"], AttnConfig(name=ly["name"], H=ly["H"], W=W, n=sp.n, i=sp.i, p=sp.p,
+                                                     heads=heads, d=64, dtype=DTYPE_BF16, seed_id=0),
+                             n_text=sp.n_text, text_dim=sp.text_dim, ff_inner=4 * co, gn_groups=sp.groups, seed_id=0)
+            _, _, module, blocks, st = module_inputs(bc, ly["depth"], seed=s + 3000 + 37 * idx, batch=B)
+            weights[ly["name"]] = {"module": module, "blocks": blocks, "ff_inner": 4 * co, "heads": heads}
+            stale[ly["name"]] = st
+        else:  # the output GroupNorm
+            weights[ly["name"]] = {"gamma": bf16_bits(1.0 + 0.1 * g.standard_normal(co)),
+                                   "beta": bf16_bits(0.1 * g.standard_normal(co))}
+    g = _stream(s, 999)
+    h0 = sp.H0 // sp.n
+    lat = np.zeros((B, h0 * sp.W0, LATENT_PAD))
+    lat[:, :, :4] = g.standard_normal((B, h0 * sp.W0, 4))
+    temb = bf16_bits(g.standard_normal((B, sp.temb_dim)))
+    text = bf16_bits(g.standard_normal((B, sp.n_text, sp.text_dim)))
+    return weights, stale, bf16_bits(lat), temb, text

@@ -327,3 +327,69 @@ def test_u6_band_upsample_is_the_whole_image_nearest_then_conv(B, H, W, ci, co, 
         got = uo.conv3x3_band_mode(xb, W, w, b, up, dn, "up")
         assert np.allclose(got.reshape(B, 2 * h, 2 * W, co), want[:, 2 * i * h:2 * (i + 1) * h],
                            rtol=1e-12, atol=1e-12), i
+
+
+# ---------------------------------------------------------------------------
+# U7: one band's U-Net step with n = 1 is the whole image's U-Net, composed
+# from torch operators
+# ---------------------------------------------------------------------------
+
+def _torch_unet(layers, weights, latent, temb, text, H0, W0, groups, p):
+    from tests.test_oracle_block_pins import _torch_module
+    f = lambda a: None if a is None else oracle.from_bf16_bits(a)
+    B = latent.shape[0]
+    cur = f(latent).reshape(B, H0, W0, -1)
+    t_emb, t_text = f(temb), f(text)
+    skips = []
+    for ly in layers:
+        w = weights[ly["name"]]
+        if ly["kind"] == "conv":
+            x = torch.from_numpy(cur).permute(0, 3, 1, 2)
+            k = torch.from_numpy(np.ascontiguousarray(f(w["w"]).transpose(0, 3, 1, 2)))
+            if ly["mode"] == 2:
+                x = F.interpolate(x, scale_factor=2.0, mode="nearest")
+            y = F.conv2d(x, k, torch.from_numpy(f(w["b"])), stride=2 if ly["mode"] == 1 else 1, padding=1)
+            out = y.permute(0, 2, 3, 1).numpy()
+        elif ly["kind"] == "resnet":
+            if ly.get("pop"):
+                cur = np.concatenate([cur, skips.pop()], axis=-1)
+            out, _, _ = _torch_resnet(cur, t_emb, {k: f(v) for k, v in w.items()}, groups)
+        elif ly["kind"] == "module":
+            Hh, Ww, C = cur.shape[1], cur.shape[2], cur.shape[3]
+            zeros = [(np.zeros((B, Hh * Ww, C)), np.zeros((B, Hh * Ww, C))) for _ in w["blocks"]]
+            y = _torch_module(Hh, Ww, 1, 0, p, w["heads"], {k: f(v) for k, v in w["module"].items()},
+                              [{k: f(v) for k, v in b.items()} for b in w["blocks"]], cur.reshape(B, Hh * Ww, C),
+                              t_text, zeros, groups)
+            out = y.reshape(B, Hh, Ww, C)
+        else:
+            x = torch.from_numpy(cur).permute(0, 3, 1, 2)
+            y = F.silu(F.group_norm(x, groups, torch.from_numpy(f(w["gamma"])), torch.from_numpy(f(w["beta"])), eps=1e-5))
+            out = y.permute(0, 2, 3, 1).numpy()
+        if ly.get("push"):
+            skips.append(out)
+        cur = out
+    return cur.reshape(B, H0 * W0, -1)
+
+
+def test_u7_one_band_step_is_the_whole_image_unet():
+    import dataclasses
+    from paper_2412_02962_amd import synth
+    sp = dataclasses.replace(synth.UNET_TINY, n=1, i=0, H0=16, W0=8)
+    layers = synth.unet_layers(sp)
+    weights, stale, latent, temb, text = synth.unet_band_inputs(sp)
+    f = lambda a: None if a is None else oracle.from_bf16_bits(a)
+    fw = {}
+    for ly in layers:
+        w = weights[ly["name"]]
+        if ly["kind"] == "module":
+            fw[ly["name"]] = {"module": {k: f(v) for k, v in w["module"].items()},
+                              "blocks": [{k: f(v) for k, v in b.items()} for b in w["blocks"]], "heads": w["heads"]}
+        else:
+            fw[ly["name"]] = {k: f(v) for k, v in w.items()}
+    fs = {k: ([tuple(f(a) for a in s) for s in v] if isinstance(v, list) else {kk: f(vv) for kk, vv in v.items()})
+          for k, v in stale.items()}
+    got = uo.unet_band_step(layers, 1, 0, sp.p, sp.groups, fw, fs, f(latent), f(temb), f(text))
+    want = _torch_unet(layers, weights, latent, temb, text, sp.H0, sp.W0, sp.groups, sp.p)
+    assert got.shape == (1, sp.H0 * sp.W0, 64)
+    assert np.allclose(got, want, rtol=1e-9, atol=1e-9)
+    assert np.abs(got[..., 4:]).max() == 0.0          # conv_out's padding outputs stay zero
