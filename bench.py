@@ -14,6 +14,7 @@ of whole steps of the same workload.
 import argparse
 import hashlib
 import json
+import math
 import os
 import sys
 import time
@@ -134,6 +135,79 @@ def resnet_call(torch, pcpp, synth, rc, dev):
         pcpp.pcpp_resnet_block(g, w, d["x"], d["temb"], d["edges1_up"], d["edges1_dn"], d["edges2_up"],
                                d["edges2_dn"], None, None, None, None, y, e1, e2, ws, wsb)
     return fn, (d, y, e1, e2, ws)
+
+
+def unet_device_inputs(torch, pcpp, synth, sp, dev, seed=7):
+    """Seeded random weights and stale neighbour data of an SDXL-sized band
+    U-Net drawn on the device (the same shapes and scales as
+    synth.unet_band_inputs; a host draw of 2.6 G parameters would take
+    minutes).  Returns (layers, weights, stale, latent, temb, text, flops)."""
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seed)
+    bf = torch.bfloat16
+    rnd = lambda *shape: torch.randn(*shape, generator=gen, device=dev, dtype=torch.float32)
+    lin = lambda shape, fan: (rnd(*shape) / fan ** 0.5).to(bf)
+    B, n, i = sp.batch, sp.n, sp.i
+    layers = synth.unet_layers(sp)
+    weights, stale, flops = {}, {}, 0.0
+    for ly in layers:
+        H, W, ci, co = ly["H"], ly["W"], ly["c_in"], ly["c_out"]
+        h = H // n
+        up, dn = i > 0, i < n - 1
+        if ly["kind"] == "conv":
+            weights[ly["name"]] = {"w": lin((co, 3, 3, ci), 9 * ci), "b": (0.02 * rnd(co)).to(bf)}
+            stale[ly["name"]] = {"row_up": rnd(B, W, ci).to(bf) if up else None,
+                                 "row_dn": rnd(B, W, ci).to(bf) if dn and ly["mode"] != 1 else None}
+            tok = {0: h * W, 1: (h // 2) * (W // 2), 2: 4 * h * W}[ly["mode"]]
+            flops += 2.0 * B * tok * 9 * ci * co
+        elif ly["kind"] == "resnet":
+            rc = synth.ResnetConfig(ly["name"], H, W, n, i, ci, co, temb_dim=sp.temb_dim, groups=sp.groups, batch=B)
+            wd = {}
+            for k, shp in synth.resnet_weight_shapes(rc).items():
+                if k.endswith("_w"):
+                    wd[k] = lin(shp, math.prod(shp[1:]))
+                elif k.endswith("gamma"):
+                    wd[k] = (1.0 + 0.1 * rnd(*shp)).to(bf)
+                else:
+                    wd[k] = ((0.02 if k.endswith("_b") else 0.1) * rnd(*shp)).to(bf)
+            weights[ly["name"]] = wd
+            stale[ly["name"]] = {"edges1_up": rnd(B, 2, W, ci).clamp_min(-0.28).to(bf) if up else None,
+                                 "edges1_dn": rnd(B, 2, W, ci).clamp_min(-0.28).to(bf) if dn else None,
+                                 "edges2_up": rnd(B, 2, W, co).clamp_min(-0.28).to(bf) if up else None,
+                                 "edges2_dn": rnd(B, 2, W, co).clamp_min(-0.28).to(bf) if dn else None}
+            flops += resnet_flops(rc)
+        elif ly["kind"] == "module":
+            heads, F = co // 64, 4 * co
+            bc = synth.BlockConfig(ly["name"], synth.AttnConfig(name=ly["name"], H=H, W=W, n=n, i=i, p=sp.p,
+                                                                heads=heads, d=64, dtype="bf16", seed_id=0),
+                                   n_text=sp.n_text, text_dim=sp.text_dim, ff_inner=F, gn_groups=sp.groups)
+            shapes = synth.block_weight_shapes(bc)
+
+            def draw(k, shp):
+                if k.endswith("_w"):
+                    return lin(shp, shp[1])
+                if k.endswith("gamma"):
+                    return (1.0 + 0.1 * rnd(*shp)).to(bf)
+                return ((0.02 if k.endswith("_b") else 0.1) * rnd(*shp)).to(bf)
+            module = {k: draw(k, shapes[k]) for k in synth.MODULE_WEIGHT_NAMES}
+            blocks = [{k: draw(k, shp) for k, shp in shapes.items() if k not in synth.MODULE_WEIGHT_NAMES}
+                      for _ in range(ly["depth"])]
+            weights[ly["name"]] = {"module": module, "blocks": blocks, "ff_inner": F, "heads": heads}
+            nb = h * W
+            stale[ly["name"]] = [tuple(rnd(B, nb, co).to(bf) if side else None for side in (up, up, dn, dn))
+                                 for _ in range(ly["depth"])]
+            g = pcpp.make_geom(H, W, n, i, sp.p, heads, 64, B, 0, pcpp.PCPP_DTYPE_BF16)
+            _, _, _, nkv = pcpp.pcpp_context_rows(g)
+            proj = 2.0 * B * nb * co * co * 2
+            flops += ly["depth"] * (block_flops(bc, nkv) - proj) + proj
+        else:  # the output GroupNorm
+            weights[ly["name"]] = {"gamma": (1.0 + 0.1 * rnd(co)).to(bf), "beta": (0.1 * rnd(co)).to(bf)}
+    h0 = sp.H0 // n
+    latent = torch.zeros(B, h0 * sp.W0, synth.LATENT_PAD, device=dev, dtype=bf)
+    latent[:, :, :4] = rnd(B, h0 * sp.W0, 4).to(bf)
+    temb = rnd(B, sp.temb_dim).to(bf)
+    text = rnd(B, sp.n_text, sp.text_dim).to(bf)
+    return layers, weights, stale, latent, temb, text, flops
 
 
 def graph_time_us(torch, fn, K, use_graph=True):
@@ -404,6 +478,17 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
         out[f"conv_{name}_us"] = round(us, 3)
         out[f"conv_{name}_TFLOPs"] = round(2.0 * tokens * 9 * ci * co / us / 1e6, 1)
 
+    # one band's whole U-Net forward at 2048 px (8 bands, band 3, one guidance branch)
+    from paper_2412_02962_amd.unet import BandUNet
+    sp = synth.UNET_SDXL_2048
+    layers, uw, ust, ulat, utemb, utext, uflops = unet_device_inputs(torch, pcpp, synth, sp, dev)
+    net = BandUNet(sp, layers, uw, ust, dev)
+    us = graph_time_us(torch, lambda: net.forward(ulat, utemb, utext), 3, use_graph)
+    out["unet_sdxl2048_band_step_ms"] = round(us / 1e3, 3)
+    out["unet_sdxl2048_band_step_TFLOPs"] = round(uflops / us / 1e6, 1)
+    out["unet_sdxl2048_band_step_gflop"] = round(uflops / 1e9, 1)
+    del net, uw, ust
+
     # the latent update of one band of the 2048 px image (latent 256 x 256 x 4, 8 bands)
     n = 256 // 8 * 256 * 4
     lat = [torch.randn(n, dtype=torch.float32, device=dev) for _ in range(4)]
@@ -530,6 +615,23 @@ def resnet_run(args):
         del keep
 
 
+def unet_run(args):
+    """Workload for a kernel-trace profile of one band's U-Net forward at
+    2048 px (8 bands, band 3): --steps forwards, nothing else."""
+    import torch
+
+    from paper_2412_02962_amd import pcpp, synth
+    from paper_2412_02962_amd.unet import BandUNet
+    sp = synth.UNET_SDXL_2048
+    layers, w, st, lat, temb, text, _ = unet_device_inputs(torch, pcpp, synth, sp, "cuda:0")
+    net = BandUNet(sp, layers, w, st, "cuda:0")
+    torch.cuda.synchronize()
+    for _ in range(args.steps):
+        net.forward(lat, temb, text)
+    torch.cuda.synchronize()
+    print(f"unet run: {args.steps} band steps", flush=True)
+
+
 def gemm_calibration():
     """hipBLASLt (through torch.matmul, bf16, HIP graph of 20 calls) on the
     GEMM shapes of the 2048 px level-1 block and ResNets: a yardstick for the
@@ -594,6 +696,8 @@ def main():
     ap.add_argument("--level", type=int, default=1, choices=(1, 2), help="transformer level of --block-run")
     ap.add_argument("--resnet-run", action="store_true",
                     help="profiling workload: --steps calls of each ResNet block, nothing else")
+    ap.add_argument("--unet-run", action="store_true",
+                    help="profiling workload: --steps band U-Net forwards at 2048 px, nothing else")
     ap.add_argument("--gemm-calibration", action="store_true",
                     help="time hipBLASLt (torch.matmul) on the block's and ResNets' GEMM shapes")
     ap.add_argument("--pmc-report", nargs="+", metavar="DIR",
@@ -613,6 +717,9 @@ def main():
         return
     if args.gemm_calibration:
         gemm_calibration()
+        return
+    if args.unet_run:
+        unet_run(args)
         return
     if args.pmc_run:
         pmc_run(args)

@@ -44,4 +44,5 @@ from .unet_oracle import (  # noqa: F401
     reverse_step_ddpm,
     scaled_linear_alphabar,
     silu,
+    unet_band_step,
 )

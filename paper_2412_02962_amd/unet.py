@@ -1,0 +1,103 @@
+"""One band's SDXL-shaped U-Net forward on the GPU, composed of the
+library's C-ABI calls: pcpp_conv3x3 (conv_in, the down- and upsamplers,
+conv_out), pcpp_resnet_block, pcpp_transformer_module (the partially
+conditioned self-attention of Sec. 3.3 inside), pcpp_concat_channels (the up
+path's skip connections) and pcpp_group_norm (the output head).  This module
+only plans buffers and marshals arguments; every step runs in the library's
+kernels.
+
+The layer order and shapes come from synth.unet_layers; the weights and the
+band's stale neighbour data of the previous step (the rows above and below
+each convolution input, the ResNets' edge rows, every basic block's K/V) are
+inputs, as the neighbour exchange (Sec. 3.2) delivers them.  GroupNorms use
+the band's own statistics.
+"""
+
+from __future__ import annotations
+
+from typing import Dict, List
+
+from . import pcpp
+
+
+class BandUNet:
+    def __init__(self, sp, layers: List[dict], weights: Dict, stale: Dict, device="cuda:0"):
+        import torch
+        self.sp, self.layers = sp, layers
+        self.weights, self.stale = weights, stale
+        B, n, i = sp.batch, sp.n, sp.i
+        self.plans = []
+        ws_max = 0
+        for ly in layers:
+            H, W, ci, co = ly["H"], ly["W"], ly["c_in"], ly["c_out"]
+            h = H // n
+            plan = {"ly": ly}
+            w = weights[ly["name"]]
+            if ly["kind"] == "conv":
+                g = pcpp.make_conv_geom(H, W, n, i, ci, co, B, ly["mode"])
+                tok = {0: h * W, 1: (h // 2) * (W // 2), 2: 4 * h * W}[ly["mode"]]
+                plan.update(g=g, out=torch.empty((B, tok, co), dtype=torch.bfloat16, device=device))
+                wsb = pcpp.pcpp_conv3x3_workspace_size(g)
+            elif ly["kind"] == "resnet":
+                g = pcpp.make_resnet_geom(H, W, n, i, ci, co, sp.temb_dim, sp.groups, B, 1e-5)
+                plan.update(g=g, wts=pcpp.make_resnet_weights(w),
+                            out=torch.empty((B, h * W, co), dtype=torch.bfloat16, device=device))
+                if ly.get("pop"):
+                    plan["cat"] = torch.empty((B, h * W, ci), dtype=torch.bfloat16, device=device)
+                wsb = pcpp.pcpp_resnet_block_workspace_size(g)
+            elif ly["kind"] == "module":
+                g = pcpp.make_geom(H, W, n, i, sp.p, w["heads"], 64, B, 0, pcpp.PCPP_DTYPE_BF16)
+                mw, keep = pcpp.make_module_weights(w["module"], w["blocks"], w["ff_inner"], sp.groups)
+                cols = list(zip(*stale[ly["name"]]))
+                lists = [None if any(a is None for a in c) else list(c) for c in cols]
+                plan.update(g=g, wts=mw, keep=keep, stale_lists=lists,
+                            out=torch.empty((B, h * W, co), dtype=torch.bfloat16, device=device))
+                wsb = pcpp.pcpp_transformer_module_workspace_size(g, mw, sp.n_text, sp.text_dim)
+            else:
+                plan.update(out=torch.empty((B, h * W, co), dtype=torch.bfloat16, device=device))
+                wsb = pcpp.pcpp_group_norm_workspace_size(B, h * W, co, sp.groups)
+            if wsb == 0:
+                raise ValueError(f"layer {ly['name']}: the library rejects its shape")
+            ws_max = max(ws_max, wsb)
+            self.plans.append(plan)
+        # One workspace for all layers (the attention's counters start at zero
+        # and are left at zero).
+        self.ws = torch.zeros(ws_max, dtype=torch.uint8, device=device)
+        self.ws_bytes = ws_max
+
+    def forward(self, latent, temb, text):
+        """latent [B, h*W0, 64] (4 channels, zero-padded), temb [B, T], text
+        [B, n_text, text_dim] (device bf16) -> the band's noise prediction
+        [B, h*W0, 64] (channels 4.. are zero)."""
+        sp, ws, wsb = self.sp, self.ws, self.ws_bytes
+        B = sp.batch
+        cur = latent
+        skips = []
+        for plan in self.plans:
+            ly = plan["ly"]
+            name, out = ly["name"], plan["out"]
+            w = self.weights[name]
+            if ly["kind"] == "conv":
+                st = self.stale[name]
+                pcpp.pcpp_conv3x3(plan["g"], cur, st["row_up"], st["row_dn"], w["w"], w["b"], out, ws, wsb)
+            elif ly["kind"] == "resnet":
+                if ly.get("pop"):
+                    skip = skips.pop()
+                    rows = cur.shape[0] * cur.shape[1]
+                    pcpp.pcpp_concat_channels(rows, cur, cur.shape[2], skip, skip.shape[2], plan["cat"])
+                    cur = plan["cat"]
+                st = self.stale[name]
+                pcpp.pcpp_resnet_block(plan["g"], plan["wts"], cur, temb, st["edges1_up"], st["edges1_dn"],
+                                       st["edges2_up"], st["edges2_dn"], None, None, None, None, out, None, None,
+                                       ws, wsb)
+            elif ly["kind"] == "module":
+                ku, vu, kd, vd = plan["stale_lists"]
+                pcpp.pcpp_transformer_module(plan["g"], plan["wts"], cur, text, sp.n_text, sp.text_dim, ku, vu, kd,
+                                             vd, None, None, out, None, None, ws, wsb)
+            else:
+                pcpp.pcpp_group_norm(B, cur.shape[1], cur.shape[2], sp.groups, 1e-5, 1, cur, w["gamma"], w["beta"],
+                                     out, ws, wsb)
+            if ly.get("push"):
+                skips.append(out)
+            cur = out
+        return cur
