@@ -137,7 +137,7 @@ def resnet_call(torch, pcpp, synth, rc, dev):
     return fn, (d, y, e1, e2, ws)
 
 
-def unet_device_inputs(torch, pcpp, synth, sp, dev, seed=7):
+def unet_device_inputs(torch, pcpp, synth, sp, dev, seed=7, sync_gn=True):
     """Seeded random weights and stale neighbour data of an SDXL-sized band
     U-Net drawn on the device (the same shapes and scales as
     synth.unet_band_inputs; a host draw of 2.6 G parameters would take
@@ -150,6 +150,13 @@ def unet_device_inputs(torch, pcpp, synth, sp, dev, seed=7):
     B, n, i = sp.batch, sp.n, sp.i
     layers = synth.unet_layers(sp)
     weights, stale, flops = {}, {}, 0.0
+
+    def band_stats(G, count):   # every band's (count, mean, M2), as synth._band_stats draws them
+        st = torch.empty(n, B, G, 3, device=dev, dtype=torch.float32)
+        st[..., 0] = count
+        st[..., 1] = 0.1 * rnd(n, B, G)
+        st[..., 2] = count * (0.8 + 0.4 * torch.rand(n, B, G, generator=gen, device=dev))
+        return st
     for ly in layers:
         H, W, ci, co = ly["H"], ly["W"], ly["c_in"], ly["c_out"]
         h = H // n
@@ -175,6 +182,9 @@ def unet_device_inputs(torch, pcpp, synth, sp, dev, seed=7):
                                  "edges1_dn": rnd(B, 2, W, ci).clamp_min(-0.28).to(bf) if dn else None,
                                  "edges2_up": rnd(B, 2, W, co).clamp_min(-0.28).to(bf) if up else None,
                                  "edges2_dn": rnd(B, 2, W, co).clamp_min(-0.28).to(bf) if dn else None}
+            if sync_gn:
+                stale[ly["name"]]["gn1_bands"] = band_stats(sp.groups, h * W * ci / sp.groups)
+                stale[ly["name"]]["gn2_bands"] = band_stats(sp.groups, h * W * co / sp.groups)
             flops += resnet_flops(rc)
         elif ly["kind"] == "module":
             heads, F = co // 64, 4 * co
@@ -200,8 +210,11 @@ def unet_device_inputs(torch, pcpp, synth, sp, dev, seed=7):
             _, _, _, nkv = pcpp.pcpp_context_rows(g)
             proj = 2.0 * B * nb * co * co * 2
             flops += ly["depth"] * (block_flops(bc, nkv) - proj) + proj
+            if sync_gn:
+                stale[ly["name"] + ":gn_bands"] = band_stats(sp.groups, nb * ci / sp.groups)
         else:  # the output GroupNorm
             weights[ly["name"]] = {"gamma": (1.0 + 0.1 * rnd(co)).to(bf), "beta": (0.1 * rnd(co)).to(bf)}
+            stale[ly["name"]] = {"gn_bands": band_stats(sp.groups, h * W * co / sp.groups) if sync_gn else None}
     h0 = sp.H0 // n
     latent = torch.zeros(B, h0 * sp.W0, synth.LATENT_PAD, device=dev, dtype=bf)
     latent[:, :, :4] = rnd(B, h0 * sp.W0, 4).to(bf)
@@ -478,11 +491,12 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
         out[f"conv_{name}_us"] = round(us, 3)
         out[f"conv_{name}_TFLOPs"] = round(2.0 * tokens * 9 * ci * co / us / 1e6, 1)
 
-    # one band's whole U-Net forward at 2048 px (8 bands, band 3, one guidance branch)
+    # one band's whole U-Net forward at 2048 px (8 bands, band 3, one guidance branch,
+    # synchronized GroupNorm)
     from paper_2412_02962_amd.unet import BandUNet
     sp = synth.UNET_SDXL_2048
     layers, uw, ust, ulat, utemb, utext, uflops = unet_device_inputs(torch, pcpp, synth, sp, dev)
-    net = BandUNet(sp, layers, uw, ust, dev)
+    net = BandUNet(sp, layers, uw, ust, dev, sync_gn=True)
     us = graph_time_us(torch, lambda: net.forward(ulat, utemb, utext), 3, use_graph)
     out["unet_sdxl2048_band_step_ms"] = round(us / 1e3, 3)
     out["unet_sdxl2048_band_step_TFLOPs"] = round(uflops / us / 1e6, 1)
@@ -624,7 +638,7 @@ def unet_run(args):
     from paper_2412_02962_amd.unet import BandUNet
     sp = synth.UNET_SDXL_2048
     layers, w, st, lat, temb, text, _ = unet_device_inputs(torch, pcpp, synth, sp, "cuda:0")
-    net = BandUNet(sp, layers, w, st, "cuda:0")
+    net = BandUNet(sp, layers, w, st, "cuda:0", sync_gn=True)
     torch.cuda.synchronize()
     for _ in range(args.steps):
         net.forward(lat, temb, text)

@@ -566,18 +566,22 @@ int pcpp_concat_channels(int64_t rows, const void* a, int32_t ca, const void* b,
                          int32_t cb, void* out, void* stream);
 
 /*
- * GroupNorm over each image's tokens (statistics of x itself), affine, then
- * SiLU if silu = 1: the U-Net's output head before conv_out (SDXL: 32
- * groups, eps 1e-5).  x, y [batch, tokens, channels] bf16 (y may not
- * overlap x), gamma/beta [channels]; channels % 8 == 0, <= 2560, groups <=
- * 256 dividing channels (PCPP_ENOTSUP otherwise).  The workspace needs no
- * clearing.  Asynchronous on `stream`.
+ * GroupNorm over each image's tokens, affine, then SiLU if silu = 1: the
+ * U-Net's output head before conv_out (SDXL: 32 groups, eps 1e-5).
+ * bands = NULL: statistics of x itself.  Else the synchronized GroupNorm
+ * (Sec. 3.3): bands [n_bands][batch][groups] x (count, mean, M2) float32 of
+ * every band, entry `band` replaced by x's own, merged in band order.
+ * own_out: NULL, or [batch][groups] x (count, mean, M2) of x.  x, y [batch,
+ * tokens, channels] bf16 (y may not overlap x), gamma/beta [channels];
+ * channels % 8 == 0, <= 2560, groups <= 256 dividing channels (PCPP_ENOTSUP
+ * otherwise).  The workspace needs no clearing.  Asynchronous on `stream`.
  */
 size_t pcpp_group_norm_workspace_size(int32_t batch, int32_t tokens,
                                       int32_t channels, int32_t groups);
 int pcpp_group_norm(int32_t batch, int32_t tokens, int32_t channels,
                     int32_t groups, float eps, int32_t silu, const void* x,
-                    const void* gamma, const void* beta, void* y,
+                    const void* gamma, const void* beta, const float* bands,
+                    int32_t n_bands, int32_t band, float* own_out, void* y,
                     void* workspace, size_t ws_bytes, void* stream);
 
 /*

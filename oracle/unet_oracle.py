@@ -224,16 +224,18 @@ def resnet_weight_shapes(c_in: int, c_out: int, temb_dim: int) -> Dict[str, Tupl
 # ---------------------------------------------------------------------------
 
 def unet_band_step(layers, n: int, i: int, p: float, groups: int, weights, stale,
-                   latent: np.ndarray, temb: np.ndarray, text: np.ndarray) -> np.ndarray:
+                   latent: np.ndarray, temb: np.ndarray, text: np.ndarray, sync_gn: bool = False) -> np.ndarray:
     """The noise prediction of band i: the layers in order (`layers`, a list
     of dicts: name, kind 'conv' / 'resnet' / 'module' / 'gn', input grid H x
     W, channels, conv mode, module depth, push / pop of skip connections),
     each with its weights and the band's stale neighbour data of the previous
     step (convolution rows, ResNet edge rows, every basic block's K/V).  The
     up path concatenates its state with the skip along the channels before
-    its ResNets.  GroupNorms use the band's own statistics.  latent [B, h*W,
-    64] (4 channels, zero-padded); returns [B, h*W, 64]."""
-    from .pcpp_oracle import group_norm as _gn, transformer_module as _module
+    its ResNets.  GroupNorms use the band's own statistics, or with sync_gn
+    the synchronized ones (every band's statistics from stale: a ResNet's
+    gn1_bands / gn2_bands, stale[module + ':gn_bands'], the head's gn_bands).
+    latent [B, h*W, 64] (4 channels, zero-padded); returns [B, h*W, 64]."""
+    from .pcpp_oracle import group_norm as _gn, group_norm_synchronized as _gns, transformer_module as _module
     modes = {0: "same", 1: "down", 2: "up"}
     hcur = latent
     skips = []
@@ -248,10 +250,15 @@ def unet_band_step(layers, n: int, i: int, p: float, groups: int, weights, stale
                 hcur = np.concatenate([hcur, skips.pop()], axis=-1)
             st = stale[name]
             out, _, _ = resnet_block(W, w, hcur, temb, st["edges1_up"], st["edges1_dn"], st["edges2_up"],
-                                     st["edges2_dn"], groups=groups, i=i)
+                                     st["edges2_dn"], groups=groups, i=i,
+                                     gn1_band_stats=st["gn1_bands"] if sync_gn else None,
+                                     gn2_band_stats=st["gn2_bands"] if sync_gn else None)
         elif kind == "module":
             out, _, _ = _module(ly["H"], W, n, i, p, w["heads"], w["module"], w["blocks"], hcur, text,
-                                stale[name], gn_groups=groups)
+                                stale[name], gn_groups=groups,
+                                gn_band_stats=stale[name + ":gn_bands"] if sync_gn else None)
+        elif sync_gn:
+            out = silu(_gns(hcur, groups, w["gamma"], w["beta"], stale[name]["gn_bands"], i, eps=RESNET_GN_EPS))
         else:
             out = silu(_gn(hcur, groups, w["gamma"], w["beta"], eps=RESNET_GN_EPS))
         if ly.get("push"):

@@ -3,8 +3,9 @@
 //                         into [rows, ca + cb]: the up path's concatenation
 //                         with the skip connection, and the zero padding of
 //                         the 4 latent channels to the convolution's 64
-//   pcpp_group_norm       GroupNorm (optionally with SiLU) over each image's
-//                         tokens: the U-Net's output head before conv_out
+//   pcpp_group_norm       GroupNorm (optionally with SiLU; band-local or
+//                         synchronized statistics): the U-Net's output head
+//                         before conv_out
 // Both are bandwidth-bound; the copy moves 16-byte vectors, all loads of a
 // thread issued before its stores.
 
@@ -86,9 +87,13 @@ PCPP_EXPORT size_t pcpp_group_norm_workspace_size(int32_t batch, int32_t tokens,
 }
 
 PCPP_EXPORT int pcpp_group_norm(int32_t batch, int32_t tokens, int32_t channels, int32_t groups, float eps,
-                                int32_t silu, const void* x, const void* gamma, const void* beta, void* y,
+                                int32_t silu, const void* x, const void* gamma, const void* beta,
+                                const float* bands, int32_t n_bands, int32_t band, float* own_out, void* y,
                                 void* workspace, size_t ws_bytes, void* stream) {
     if (batch < 1 || batch > 65535 || tokens < 1 || !(eps > 0.f) || (silu != 0 && silu != 1)) return PCPP_EINVAL;
+    if (bands != nullptr && (n_bands < 1 || band < 0 || band >= n_bands || ((uintptr_t)bands & 3u) != 0))
+        return PCPP_EINVAL;
+    if (own_out != nullptr && ((uintptr_t)own_out & 3u) != 0) return PCPP_EINVAL;
     if (!gn_shapes_ok(channels, groups)) return PCPP_ENOTSUP;
     if ((int64_t)batch * tokens * channels > ((int64_t)1 << 40)) return PCPP_EINVAL;
     const void* ptrs[] = {x, gamma, beta, y};
@@ -108,10 +113,10 @@ PCPP_EXPORT int pcpp_group_norm(int32_t batch, int32_t tokens, int32_t channels,
     gp.C = channels;
     gp.G = groups;
     gp.eps = eps;
-    gp.bands = nullptr;
-    gp.n_bands = 1;
-    gp.band = 0;
-    gp.own_out = nullptr;
+    gp.bands = bands;
+    gp.n_bands = bands ? n_bands : 1;
+    gp.band = bands ? band : 0;
+    gp.own_out = own_out;
     gp.silu = silu;
     return launch_group_norm(gp, (hipStream_t)stream) == hipSuccess ? PCPP_OK : PCPP_EHIP;
 }

@@ -156,7 +156,8 @@ def _load():
                                                    vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "pcpp_concat_channels": (ctypes.c_int, [ctypes.c_int64, vp, i32, vp, i32, vp, vp]),
         "pcpp_group_norm_workspace_size": (sz, [i32, i32, i32, i32]),
-        "pcpp_group_norm": (ctypes.c_int, [i32, i32, i32, i32, ctypes.c_float, i32, vp, vp, vp, vp, vp, sz, vp]),
+        "pcpp_group_norm": (ctypes.c_int, [i32, i32, i32, i32, ctypes.c_float, i32, vp, vp, vp, vp, i32, i32, vp, vp,
+                                           vp, sz, vp]),
         "pcpp_conv3x3_workspace_size": (sz, [ctypes.POINTER(pcpp_conv_geom_t)]),
         "pcpp_conv3x3": (ctypes.c_int, [ctypes.POINTER(pcpp_conv_geom_t)] + [vp] * 7 + [sz, vp]),
     }
@@ -415,6 +416,8 @@ def pcpp_group_norm_workspace_size(batch, tokens, channels, groups) -> int:
     return _lib.pcpp_group_norm_workspace_size(batch, tokens, channels, groups)
 
 
-def pcpp_group_norm(batch, tokens, channels, groups, eps, silu, x, gamma, beta, y, workspace, ws_bytes, stream=None):
+def pcpp_group_norm(batch, tokens, channels, groups, eps, silu, x, gamma, beta, y, workspace, ws_bytes, stream=None,
+                    bands=None, n_bands=1, band=0, own_out=None):
     _check("pcpp_group_norm", _lib.pcpp_group_norm(batch, tokens, channels, groups, eps, silu, _ptr(x), _ptr(gamma),
-                                                    _ptr(beta), _ptr(y), _ptr(workspace), ws_bytes, _stream(stream)))
+                                                    _ptr(beta), _ptr(bands), n_bands, band, _ptr(own_out), _ptr(y),
+                                                    _ptr(workspace), ws_bytes, _stream(stream)))

@@ -513,13 +513,25 @@ def _w(g, shape, fan_in):
     return bf16_bits(g.standard_normal(shape) / np.sqrt(fan_in))
 
 
-def unet_band_inputs(sp: UNetSpec):
+def _band_stats(g, n: int, B: int, G: int, count: float) -> np.ndarray:
+    """Plausible (count, mean, M2) of every band's GroupNorm input, [n, B, G, 3]
+    float32: means 0.1 N(0, 1), variances 0.8 + 0.4 U(0, 1)."""
+    st = np.empty((n, B, G, 3))
+    st[..., 0] = count
+    st[..., 1] = 0.1 * g.standard_normal((n, B, G))
+    st[..., 2] = count * (0.8 + 0.4 * g.random((n, B, G)))
+    return st.astype(np.float32)
+
+
+def unet_band_inputs(sp: UNetSpec, sync_gn: bool = False):
     """Seeded bf16 weights of every layer, the band's stale neighbour data
     for every layer, the padded latent band, the time embedding and the text:
     (weights, stale, latent, temb, text).  Draw recipe as the single layers'
     (weights N(0, 1/fan_in), biases 0.02 N, norm scales 1 + 0.1 N, shifts
     0.1 N, neighbour rows / K / V N(0, 1)); conv_in's weights are zero on the
-    60 padding channels, conv_out's outputs beyond the first 4 are zero."""
+    60 padding channels, conv_out's outputs beyond the first 4 are zero.
+    With sync_gn, every GroupNorm also gets every band's statistics
+    (_band_stats; entry i is replaced by the band's own in the step)."""
     s = BASE_SEED + sp.seed_id
     B = sp.batch
     weights, stale = {}, {}
@@ -549,6 +561,10 @@ def unet_band_inputs(sp: UNetSpec):
             d = resnet_inputs(rc, seed=s + 2000 + idx)
             weights[ly["name"]] = {k: d[k] for k in resnet_weight_shapes(rc)}
             stale[ly["name"]] = {k: d[k] for k in ("edges1_up", "edges1_dn", "edges2_up", "edges2_dn")}
+            if sync_gn:
+                gs = _stream(s, 4000 + idx)
+                stale[ly["name"]]["gn1_bands"] = _band_stats(gs, sp.n, B, sp.groups, h * W * ci / sp.groups)
+                stale[ly["name"]]["gn2_bands"] = _band_stats(gs, sp.n, B, sp.groups, h * W * co / sp.groups)
         elif ly["kind"] == "module":
             heads = co // 64
             bc = BlockConfig(ly["name"], AttnConfig(name=ly["name"], H=ly["H"], W=W, n=sp.n, i=sp.i, p=sp.p,
@@ -557,9 +573,14 @@ def unet_band_inputs(sp: UNetSpec):
             _, _, module, blocks, st = module_inputs(bc, ly["depth"], seed=s + 3000 + 37 * idx, batch=B)
             weights[ly["name"]] = {"module": module, "blocks": blocks, "ff_inner": 4 * co, "heads": heads}
             stale[ly["name"]] = st
+            if sync_gn:
+                stale[ly["name"] + ":gn_bands"] = _band_stats(_stream(s, 4000 + idx), sp.n, B, sp.groups,
+                                                              h * W * ci / sp.groups)
         else:  # the output GroupNorm
             weights[ly["name"]] = {"gamma": bf16_bits(1.0 + 0.1 * g.standard_normal(co)),
                                    "beta": bf16_bits(0.1 * g.standard_normal(co))}
+            stale[ly["name"]] = {"gn_bands": _band_stats(_stream(s, 4000 + idx), sp.n, B, sp.groups,
+                                                         h * W * co / sp.groups) if sync_gn else None}
     g = _stream(s, 999)
     h0 = sp.H0 // sp.n
     lat = np.zeros((B, h0 * sp.W0, LATENT_PAD))

@@ -10,7 +10,7 @@ The layer order and shapes come from synth.unet_layers; the weights and the
 band's stale neighbour data of the previous step (the rows above and below
 each convolution input, the ResNets' edge rows, every basic block's K/V) are
 inputs, as the neighbour exchange (Sec. 3.2) delivers them.  GroupNorms use
-the band's own statistics.
+the band's own statistics, or with sync_gn every band's (Sec. 3.3).
 """
 
 from __future__ import annotations
@@ -21,10 +21,16 @@ from . import pcpp
 
 
 class BandUNet:
-    def __init__(self, sp, layers: List[dict], weights: Dict, stale: Dict, device="cuda:0"):
+    def __init__(self, sp, layers: List[dict], weights: Dict, stale: Dict, device="cuda:0", sync_gn=False):
+        """sync_gn: every GroupNorm uses the whole image's statistics (Sec. 3.3),
+        from every band's (count, mean, M2) in stale (resnet: gn1_bands and
+        gn2_bands; module NAME: stale[NAME + ':gn_bands']; output head:
+        gn_bands); the band's own statistics are written to self.gn_own."""
         import torch
         self.sp, self.layers = sp, layers
         self.weights, self.stale = weights, stale
+        self.sync_gn = sync_gn
+        self.gn_own = {}
         B, n, i = sp.batch, sp.n, sp.i
         self.plans = []
         ws_max = 0
@@ -58,6 +64,10 @@ class BandUNet:
                 wsb = pcpp.pcpp_group_norm_workspace_size(B, h * W, co, sp.groups)
             if wsb == 0:
                 raise ValueError(f"layer {ly['name']}: the library rejects its shape")
+            if sync_gn:
+                own = lambda: torch.empty((B, sp.groups, 3), dtype=torch.float32, device=device)
+                self.gn_own[ly["name"]] = [own(), own()] if ly["kind"] == "resnet" else (
+                    [own()] if ly["kind"] in ("module", "gn") else [])
             ws_max = max(ws_max, wsb)
             self.plans.append(plan)
         # One workspace for all layers (the attention's counters start at zero
@@ -87,16 +97,21 @@ class BandUNet:
                     pcpp.pcpp_concat_channels(rows, cur, cur.shape[2], skip, skip.shape[2], plan["cat"])
                     cur = plan["cat"]
                 st = self.stale[name]
+                b1, b2 = (st["gn1_bands"], st["gn2_bands"]) if self.sync_gn else (None, None)
+                o1, o2 = self.gn_own[name] if self.sync_gn else (None, None)
                 pcpp.pcpp_resnet_block(plan["g"], plan["wts"], cur, temb, st["edges1_up"], st["edges1_dn"],
-                                       st["edges2_up"], st["edges2_dn"], None, None, None, None, out, None, None,
-                                       ws, wsb)
+                                       st["edges2_up"], st["edges2_dn"], b1, o1, b2, o2, out, None, None, ws, wsb)
             elif ly["kind"] == "module":
                 ku, vu, kd, vd = plan["stale_lists"]
+                bands = self.stale[name + ":gn_bands"] if self.sync_gn else None
+                own = self.gn_own[name][0] if self.sync_gn else None
                 pcpp.pcpp_transformer_module(plan["g"], plan["wts"], cur, text, sp.n_text, sp.text_dim, ku, vu, kd,
-                                             vd, None, None, out, None, None, ws, wsb)
+                                             vd, bands, own, out, None, None, ws, wsb)
             else:
+                bands = self.stale[name]["gn_bands"] if self.sync_gn else None
+                own = self.gn_own[name][0] if self.sync_gn else None
                 pcpp.pcpp_group_norm(B, cur.shape[1], cur.shape[2], sp.groups, 1e-5, 1, cur, w["gamma"], w["beta"],
-                                     out, ws, wsb)
+                                     out, ws, wsb, bands=bands, n_bands=sp.n, band=sp.i, own_out=own)
             if ly.get("push"):
                 skips.append(out)
             cur = out

@@ -39,6 +39,9 @@ def _dev_tree(t):
     if t is None:
         return None
     if isinstance(t, np.ndarray):
+        if t.dtype == np.float32:       # GroupNorm statistics
+            import torch
+            return torch.from_numpy(t).to(gu.DEV)
         return gu.to_dev(t, "bf16")
     if isinstance(t, dict):
         return {k: _dev_tree(v) for k, v in t.items()}
@@ -51,7 +54,7 @@ def _f64_tree(t):
     if t is None:
         return None
     if isinstance(t, np.ndarray):
-        return oracle.from_bf16_bits(t)
+        return t.astype(np.float64) if t.dtype == np.float32 else oracle.from_bf16_bits(t)
     if isinstance(t, dict):
         return {k: _f64_tree(v) for k, v in t.items()}
     if isinstance(t, (list, tuple)):
@@ -59,20 +62,21 @@ def _f64_tree(t):
     return t
 
 
+@pytest.mark.parametrize("sync_gn", [False, True], ids=["local_gn", "sync_gn"])
 @pytest.mark.parametrize("sp", SPECS, ids=["n2_i1", "n2_i0", "n3_i1", "n2_i1_b2"])
-def test_unet_band_step_matches_oracle(sp):
+def test_unet_band_step_matches_oracle(sp, sync_gn):
     import torch
     from paper_2412_02962_amd.unet import BandUNet
-    _say("unet", sp)
+    _say("unet", sp, "sync_gn" if sync_gn else "local_gn")
     layers = synth.unet_layers(sp)
-    weights, stale, latent, temb, text = synth.unet_band_inputs(sp)
-    net = BandUNet(sp, layers, _dev_tree(weights), _dev_tree(stale))
+    weights, stale, latent, temb, text = synth.unet_band_inputs(sp, sync_gn=sync_gn)
+    net = BandUNet(sp, layers, _dev_tree(weights), _dev_tree(stale), sync_gn=sync_gn)
     got = net.forward(gu.to_dev(latent, "bf16"), gu.to_dev(temb, "bf16"), gu.to_dev(text, "bf16"))
     torch.cuda.synchronize()
     got = gu.to_f64(got)
     want = oracle.unet_band_step(layers, sp.n, sp.i, sp.p, sp.groups, _f64_tree(weights), _f64_tree(stale),
                                  oracle.from_bf16_bits(latent), oracle.from_bf16_bits(temb),
-                                 oracle.from_bf16_bits(text))
+                                 oracle.from_bf16_bits(text), sync_gn=sync_gn)
     assert np.abs(got[..., 4:]).max() == 0.0
     g, w = got[..., :4], want[..., :4]
     rel = float(np.linalg.norm(g - w) / np.linalg.norm(w))
