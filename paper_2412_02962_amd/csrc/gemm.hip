@@ -627,11 +627,18 @@ namespace {
 
 constexpr int CUS_PER_XCD = 32;  // gfx950
 
+// Compute units of the current device, asked once per device (a benign race:
+// every thread that asks stores the same value).
 int cu_count() {
-    int dev = 0, cus = 0;
+    constexpr int kMaxDevices = 64;
+    static int cached[kMaxDevices] = {};
+    int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return 256;
+    if (dev >= 0 && dev < kMaxDevices && cached[dev] > 0) return cached[dev];
+    int cus = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
         return 256;
+    if (dev >= 0 && dev < kMaxDevices) cached[dev] = cus;
     return cus;
 }
 
