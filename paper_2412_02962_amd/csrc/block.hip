@@ -33,8 +33,8 @@ namespace pcpp {
 namespace {
 
 struct BlockLayout {
-    size_t t16, hid, q16, k16, v16, a16, k2, v2, u16, attn_ws, gn, total;
-    size_t attn_ws_bytes;
+    size_t t16, hid, q16, k16, v16, a16, k2, v2, u16, attn_ws, gn, split, total;
+    size_t attn_ws_bytes, split_bytes;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -73,7 +73,8 @@ AttnParams cross_attn_params(const pcpp_geom_t* g, const Geo& r, const void* q, 
     return make_attn_params(g, r, q, out, kv);
 }
 
-BlockLayout layout(const pcpp_geom_t* g, const Geo& r, int32_t ff_inner, int32_t gn_groups, int32_t n_text) {
+BlockLayout layout(const pcpp_geom_t* g, const Geo& r, int32_t ff_inner, int32_t gn_groups, int32_t n_text,
+                   int32_t text_dim) {
     BlockLayout L;
     const size_t rows = (size_t)g->batch * r.nq;
     const size_t C = r.C;
@@ -98,6 +99,15 @@ BlockLayout layout(const pcpp_geom_t* g, const Geo& r, int32_t ff_inner, int32_t
     L.u16 = take(rows * (size_t)ff_inner * 2);
     L.attn_ws = take(L.attn_ws_bytes);
     L.gn = take(group_norm_ws_bytes(g->batch, gn_groups, r.nq));
+    // One split-K region serves every GEMM of the call in turn (stream order):
+    // the largest any of them can use.
+    const int M = (int)rows, Ci = (int)C;
+    const size_t sizes[] = {gemm_split_ws_bytes(M, Ci, Ci, false), gemm_split_ws_bytes(M, 3 * Ci, Ci, false),
+                            gemm_split_ws_bytes(M, Ci, ff_inner, false),
+                            gemm_split_ws_bytes(g->batch * n_text, 2 * Ci, text_dim, false)};
+    L.split_bytes = 0;
+    for (size_t b : sizes) L.split_bytes = b > L.split_bytes ? b : L.split_bytes;
+    L.split = L.split_bytes ? take(L.split_bytes) : 0;
     L.total = off;
     return L;
 }
@@ -200,7 +210,7 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
         if (k_out && k_out[j] && !aligned16(k_out[j])) return PCPP_EINVAL;
         if (v_out && v_out[j] && !aligned16(v_out[j])) return PCPP_EINVAL;
     }
-    const BlockLayout L = layout(g, r, mw.ff_inner, mw.gn_groups, n_text);
+    const BlockLayout L = layout(g, r, mw.ff_inner, mw.gn_groups, n_text, text_dim);
     if (workspace == nullptr || ws_bytes < L.total) return PCPP_EWORKSPACE;
     if (!aligned16(workspace)) return PCPP_EINVAL;
 
@@ -216,6 +226,14 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
     __bf16* v2 = (__bf16*)(ws + L.v2);
     __bf16* u16 = (__bf16*)(ws + L.u16);
     void* attn_ws = ws + L.attn_ws;
+    void* split_ws = L.split_bytes ? ws + L.split : nullptr;
+    // Every plain GEMM may split K over the shared region (its counters are
+    // cleared by the GroupNorm statistics launch below).
+    auto gemm_s = [&](GemmParams mm) {
+        mm.split_ws = split_ws;
+        mm.split_ws_bytes = L.split_bytes;
+        return launch_gemm(mm, s);
+    };
     hipError_t e = hipSuccess;
 #define PCPP_CHECK(call)                  \
     do {                                  \
@@ -239,8 +257,10 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
     gp.n_bands = g->n_patches;
     gp.band = g->patch_idx;
     gp.own_out = gn_own;
+    gp.zero = (int*)split_ws;
+    gp.n_zero = split_ws ? GEMM_SPLIT_COUNTERS : 0;
     PCPP_CHECK(launch_group_norm(gp, s));
-    PCPP_CHECK(launch_gemm(gemm(t16, C, false, mw.proj_in_w, mw.proj_in_b, rows, C, C, hid, C, true), s));
+    PCPP_CHECK(gemm_s(gemm(t16, C, false, mw.proj_in_w, mw.proj_in_b, rows, C, C, hid, C, true)));
 
     LayerNormParams lp;
     lp.x = hid;
@@ -270,7 +290,7 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
             qkv.out[1] = k16;
             qkv.out[2] = v16;
             qkv.seg = C;
-            PCPP_CHECK(launch_gemm(qkv, s));
+            PCPP_CHECK(gemm_s(qkv));
         }
         {
             AttnParams ap = self_attn_params(g, r, q16, a16, k16, v16, ku, vu, kd, vd, nullptr);
@@ -281,19 +301,19 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
             o.resid = hid;
             o.ldr = C;
             o.resid_f32 = 1;
-            PCPP_CHECK(launch_gemm(o, s));
+            PCPP_CHECK(gemm_s(o));
         }
 
         // Cross-attention to the text features.
         lp.gamma = (const __bf16*)w.ln2_gamma;
         lp.beta = (const __bf16*)w.ln2_beta;
         PCPP_CHECK(launch_layer_norm(lp, s));
-        PCPP_CHECK(launch_gemm(gemm(t16, C, false, w.attn2_q_w, nullptr, rows, C, C, q16, C, false), s));
+        PCPP_CHECK(gemm_s(gemm(t16, C, false, w.attn2_q_w, nullptr, rows, C, C, q16, C, false)));
         {
             GemmParams kv = gemm(text, text_dim, false, w.attn2_kv_w, nullptr, B * T, 2 * C, text_dim, k2, C, false);
             kv.out[1] = v2;
             kv.seg = C;
-            PCPP_CHECK(launch_gemm(kv, s));
+            PCPP_CHECK(gemm_s(kv));
         }
         {
             AttnParams ap = cross_attn_params(g, r, q16, a16, k2, v2, T);
@@ -304,7 +324,7 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
             o.resid = hid;
             o.ldr = C;
             o.resid_f32 = 1;
-            PCPP_CHECK(launch_gemm(o, s));
+            PCPP_CHECK(gemm_s(o));
         }
 
         // GEGLU feed-forward.
@@ -315,7 +335,7 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
             GemmParams ff = gemm(t16, C, false, w.ff1_w, w.ff1_b, rows, F, C, u16, F, false);
             ff.geglu = 1;
             ff.F = F;
-            PCPP_CHECK(launch_gemm(ff, s));
+            PCPP_CHECK(gemm_s(ff));
         }
         {
             GemmParams o = gemm(u16, F, false, w.ff2_w, w.ff2_b, rows, C, F, hid, C, true);
@@ -323,7 +343,7 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
             o.ldr = C;
             o.resid_f32 = 1;
             if (copy16 && j == depth - 1) o.out_bf16 = t16;
-            PCPP_CHECK(launch_gemm(o, s));
+            PCPP_CHECK(gemm_s(o));
         }
     }
 
@@ -334,7 +354,7 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
         o.resid = x;
         o.ldr = C;
         o.resid_f32 = 0;
-        PCPP_CHECK(launch_gemm(o, s));
+        PCPP_CHECK(gemm_s(o));
     }
 #undef PCPP_CHECK
     return PCPP_OK;
@@ -362,7 +382,7 @@ PCPP_EXPORT size_t pcpp_transformer_block_workspace_size(const pcpp_geom_t* g, c
                                                          int32_t n_text, int32_t text_dim) {
     Geo r;
     if (w == nullptr || validate_block(g, w->ff_inner, w->gn_groups, n_text, text_dim, &r) != PCPP_OK) return 0;
-    return layout(g, r, w->ff_inner, w->gn_groups, n_text).total;
+    return layout(g, r, w->ff_inner, w->gn_groups, n_text, text_dim).total;
 }
 
 PCPP_EXPORT int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, const void* x,
@@ -391,7 +411,7 @@ PCPP_EXPORT size_t pcpp_transformer_module_workspace_size(const pcpp_geom_t* g, 
     Geo r;
     if (w == nullptr || validate_block(g, w->ff_inner, w->gn_groups, n_text, text_dim, &r) != PCPP_OK) return 0;
     if (w->depth < 1 || w->depth > 64) return 0;
-    return layout(g, r, w->ff_inner, w->gn_groups, n_text).total;
+    return layout(g, r, w->ff_inner, w->gn_groups, n_text, text_dim).total;
 }
 
 PCPP_EXPORT int pcpp_transformer_module(const pcpp_geom_t* g, const pcpp_module_weights_t* w, const void* x,

@@ -37,7 +37,7 @@ struct GemmParams {
     // bias2[(m / bias2_rows) * N + n] (16-byte aligned), or null.
     const float* bias2 = nullptr;
     int32_t bias2_rows = 1;
-    // Workspace that lets a convolution split K over several workgroups
+    // Workspace that lets the GEMM split K over several workgroups
     // (gemm_split_ws_bytes; its first bytes are counters that must be zero
     // before the first use and are left zero), or null.
     void* split_ws = nullptr;
@@ -46,10 +46,12 @@ struct GemmParams {
     int32_t splitk = 1, n_xcd = 1, tpx = 0, n_tiles = 0;
 };
 
-// Bytes of split-K workspace a convolution GEMM of this shape can use (0:
-// it runs unsplit); counters come first, at most GEMM_SPLIT_COUNTERS ints.
+// Bytes of split-K workspace a GEMM of this shape can use (0: it runs
+// unsplit); counters come first, at most GEMM_SPLIT_COUNTERS ints.  conv:
+// the implicit convolution (128 x 128 tiles), else a plain bf16 GEMM (64 x 64
+// tiles; GEGLU and fp32 X never split).
 constexpr int GEMM_SPLIT_COUNTERS = 4096;
-size_t gemm_split_ws_bytes(int M, int N, int K);
+size_t gemm_split_ws_bytes(int M, int N, int K, bool conv = true);
 
 bool gemm_shape_ok(const GemmParams& p);
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s);
@@ -80,6 +82,10 @@ struct GroupNormParams {
     const __bf16* frame_up = nullptr;
     const __bf16* frame_dn = nullptr;
     __bf16* edges_out = nullptr;
+    // n_zero ints at zero (if not null) are cleared by the statistics launch:
+    // the split counters of the GEMMs that follow on the stream.
+    int* zero = nullptr;
+    int32_t n_zero = 0;
 };
 size_t group_norm_ws_bytes(int B, int G, int N);
 // C % 8 == 0, C <= 2048, 1 <= G <= 256 divides C.

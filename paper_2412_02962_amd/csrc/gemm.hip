@@ -256,6 +256,24 @@ __device__ __forceinline__ u32x4 lds_b128(uint32_t a) {
     return r;
 }
 
+// s_waitcnt immediate for vmcnt(v) alone (gfx9 layout: low four bits at
+// [3:0], high two at [15:14]; expcnt and lgkmcnt left at their maxima).
+constexpr int vmcnt_imm(int v) { return 0xF70 | (v & 15) | ((v >> 4) << 14); }
+
+// Waits until at most later * PT vector loads of this thread are in flight:
+// the k-tile `later` tiles before the newest issued one has landed.
+template <int PT, int L>
+__device__ __forceinline__ void wait_tiles_after(int later) {
+    if constexpr (L == 0) {
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    } else {
+        if (later >= L)
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(L * PT));
+        else
+            wait_tiles_after<PT, L - 1>(later);
+    }
+}
+
 template <int BM, int BN, int NS, bool GEGLU, bool CONV>
 __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
     constexpr int WMB = BM / 64;                      // 32-token blocks per wavefront
@@ -265,6 +283,7 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
     constexpr int PT = XP + WP;                       // loads per thread per k-tile
     constexpr int STAGE = (BM + BN) * DBK * 2;        // bytes per stage
     constexpr int NOPS = WNB + WMB;                   // operand reads per k-step
+    static_assert((NS - 2) * PT <= 63, "vmcnt holds at most 63 loads");
     static_assert(!GEGLU || WNB == 2, "GEGLU pairs a value block with a gate block");
     __shared__ __attribute__((aligned(16))) char lds[NS * STAGE];
 
@@ -411,13 +430,7 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
         if (kt0 + s < kt1) issue(kt0 + s, s);
     for (int kt = kt0; kt < kt1; ++kt) {
         // k-tiles issued after kt so far: min(kt1 - 1 - kt, NS - 2), PT loads each
-        const int later = min(kt1 - 1 - kt, NS - 2);
-        if (NS >= 4 && later >= 2)
-            __builtin_amdgcn_s_waitcnt(0xF70 | (2 * PT));
-        else if (later >= 1)
-            __builtin_amdgcn_s_waitcnt(0xF70 | PT);
-        else
-            __builtin_amdgcn_s_waitcnt(0xF70);
+        wait_tiles_after<PT, NS - 2>(min(kt1 - 1 - kt, NS - 2));
         __builtin_amdgcn_s_barrier();  // everyone's pieces of tile kt landed; the stage of tile kt-1 is free
         if (kt + NS - 1 < kt1) issue(kt + NS - 1, (kt - kt0 + NS - 1) % NS);
         const uint32_t sbase = lds0 + ((kt - kt0) % NS) * STAGE;
@@ -673,9 +686,42 @@ SplitPlan split_plan(int M, int N, int K) {
     return sp;
 }
 
+// Split of a plain GEMM over 64 x 64 tiles when they are fewer than the
+// compute units (one workgroup per compute unit and the rest idle): about
+// kSplitTarget workgroups per compute unit, each piece at least
+// kSplitMinTiles k-tiles long.  Measured at 512 x 1280 (2048 px level 2):
+// K = 5120 in 3 pieces 21.4 us against 25.8 unsplit; K = 1280 in 2 pieces
+// of 10 k-tiles 10.6 against 9.4, hence the minimum length.  A deeper LDS
+// ring (4, 6 or 8 stages) for the unsplit small launches gained nothing.
+constexpr int kSplitTarget = 2;
+constexpr int kSplitMinTiles = 16;
+
+SplitPlan split_plan_plain(int M, int N, int K) {
+    SplitPlan sp{1, 1, 0, 0, 0};
+    const int cus = cu_count();
+    if (cus % CUS_PER_XCD != 0 || N % 64 != 0 || K % DBK != 0) return sp;
+    const int64_t tiles = (int64_t)((M + 63) / 64) * (N / 64);
+    if (tiles < 1 || tiles >= cus || tiles > GEMM_SPLIT_COUNTERS) return sp;
+    const int n_xcd = cus / CUS_PER_XCD;
+    const int64_t tpx = (tiles + n_xcd - 1) / n_xcd;
+    int64_t k = (int64_t)kSplitTarget * cus / (n_xcd * tpx);
+    const int64_t k_max = (K / DBK) / kSplitMinTiles;
+    if (k > k_max) k = k_max;
+    if (k > 8) k = 8;
+    if (k < 2) return sp;
+    sp.splitk = (int)k;
+    sp.n_xcd = n_xcd;
+    sp.tpx = (int)tpx;
+    sp.n_tiles = (int)tiles;
+    sp.bytes = (size_t)GEMM_SPLIT_COUNTERS * 4 + (size_t)n_xcd * tpx * k * 64 * 64 * 4;
+    return sp;
+}
+
 }  // namespace
 
-size_t gemm_split_ws_bytes(int M, int N, int K) { return split_plan(M, N, K).bytes; }
+size_t gemm_split_ws_bytes(int M, int N, int K, bool conv) {
+    return conv ? split_plan(M, N, K).bytes : split_plan_plain(M, N, K).bytes;
+}
 
 hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
     GemmParams p = p_in;
@@ -694,6 +740,16 @@ hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
     // bf16 X with K % 64 == 0: the pipelined kernel, with the largest tile
     // that still gives about a workgroup per compute unit.
     if (!p.a_f32 && p.K % DBK == 0 && p.seg % 4 == 0) {
+        if (!p.geglu && p.conv_W == 0 && p.split_ws != nullptr && p.N % 64 == 0) {
+            const SplitPlan sp = split_plan_plain(p.M, p.N, p.K);
+            if (sp.splitk > 1 && p.split_ws_bytes >= sp.bytes && ((uintptr_t)p.split_ws & 15u) == 0) {
+                p.splitk = sp.splitk;
+                p.n_xcd = sp.n_xcd;
+                p.tpx = sp.tpx;
+                p.n_tiles = sp.n_tiles;
+                return launch_dma<64, 64, 3, false>(p, s);
+            }
+        }
         if (p.geglu) {
             // value/gate pairs on 64-token tiles at two stages (48 KB of LDS: three
             // workgroups per compute unit): 25.3 us against 28.7 for 128-token

@@ -105,6 +105,48 @@ def test_block_small_shapes(geo, batch):
     _check_kv(gu.to_f64(v), want_v, "v export")
 
 
+@pytest.mark.parametrize("batch", [1, 2])
+def test_block_split_k_gemms(batch):
+    """FF-out (K = 2048) and the text K/V product (K = 2048) split K over two
+    workgroups per tile at these sizes (fewer 64 x 64 tiles than compute
+    units, 32 k-tiles); 80 tokens per image leave a ragged last token tile."""
+    attn = synth.AttnConfig(name="blk", H=12, W=20, n=3, i=1, p=0.5, heads=2, d=64, dtype="bf16", seed_id=56)
+    bc = synth.BlockConfig(name="blk", attn=attn, n_text=7, text_dim=2048, ff_inner=2048, gn_groups=4,
+                           seed_id=57)
+    _say("block split-K", batch)
+    inp = synth.block_inputs(bc, batch=batch)
+    y, k, v = _run_block(bc, inp, batch)
+    want_y, want_k, want_v = _oracle_block(bc, inp)
+    _check(gu.to_f64(y), want_y)
+    _check_kv(gu.to_f64(k), want_k, "k export")
+    _check_kv(gu.to_f64(v), want_v, "v export")
+
+
+def test_block_workspace_is_reusable():
+    """Workspace contract: zero-filled before the first call, left reusable.
+    The attention's and the split GEMMs' counters live there (the level-2
+    block splits FF-out and the text K/V product); three calls on one
+    workspace give the same bits as a call on a fresh one."""
+    import torch
+    from paper_2412_02962_amd import pcpp
+    bc = synth.BLOCK_CONFIG_L2
+    cfg = bc.attn
+    _say("block dirty workspace", bc.name)
+    d = {k: gu.to_dev(v, "bf16") for k, v in synth.block_inputs(bc).items()}
+    g = pcpp.make_geom(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, cfg.d, 1, 0, pcpp.PCPP_DTYPE_BF16)
+    w = pcpp.make_block_weights(d, bc.ff_inner, bc.gn_groups)
+    wsb = pcpp.pcpp_transformer_block_workspace_size(g, w, bc.n_text, bc.text_dim)
+    outs = []
+    shared = torch.zeros(wsb, dtype=torch.uint8, device=gu.DEV)
+    for ws in (torch.zeros(wsb, dtype=torch.uint8, device=gu.DEV), shared, shared, shared):
+        y = torch.empty_like(d["x"])
+        pcpp.pcpp_transformer_block(g, w, d["x"], d["text"], bc.n_text, bc.text_dim, d["k_up"], d["v_up"],
+                                    d["k_dn"], d["v_dn"], y, None, None, ws, wsb)
+        torch.cuda.synchronize()
+        outs.append(y)
+    assert all(torch.equal(outs[0], o) for o in outs[1:])
+
+
 def test_block_without_kv_export_gives_same_output():
     import torch
     attn = synth.AttnConfig(name="blk", H=16, W=16, n=4, i=1, p=0.5, heads=2, d=64, dtype="bf16", seed_id=52)
