@@ -295,11 +295,13 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
     const int col = lane & 31;
     const int half = lane >> 5;
     const int bn_out = GEGLU ? BN / 2 : BN;
-    // Split K: workgroup w runs on XCD w % n_xcd; the tiles of an XCD are a
-    // contiguous range of tpx tiles, and the splitk pieces of a tile follow
-    // each other within it, so all pieces of a tile share one L2.
+    // XCD-contiguous tiles (tpx > 0; always with split K): workgroup w runs
+    // on XCD w % n_xcd; the tiles of an XCD are a contiguous range of tpx
+    // tiles in n-major order (all token tiles of one W tile together), and
+    // the splitk pieces of a tile follow each other within it, so all pieces
+    // of a tile share one L2.
     int m_tile = blockIdx.x, n_tile = blockIdx.y, piece = 0, tile = 0, xcd = 0, tl = 0;
-    if (p.splitk > 1) {
+    if (p.tpx > 0) {
         xcd = blockIdx.x % p.n_xcd;
         const int j = blockIdx.x / p.n_xcd;
         tl = j / p.splitk;
@@ -601,7 +603,7 @@ template <int BM, int BN, int NS, bool GEGLU>
 hipError_t launch_dma(const GemmParams& p, hipStream_t s) {
     const int bn_out = GEGLU ? BN / 2 : BN;
     dim3 grid((p.M + BM - 1) / BM, p.N / bn_out);
-    if (p.splitk > 1) grid = dim3((unsigned)(p.n_xcd * p.tpx * p.splitk), 1);
+    if (p.tpx > 0) grid = dim3((unsigned)(p.n_xcd * p.tpx * p.splitk), 1);
     if (!GEGLU && p.conv_W > 0)
         gemm_dma_kernel<BM, BN, NS, GEGLU, true><<<grid, 256, 0, s>>>(p);
     else
@@ -727,6 +729,7 @@ hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
     GemmParams p = p_in;
     if (p.conv_W > 0 && !gemm_shape_ok(p)) return hipErrorInvalidValue;
     p.splitk = 1;
+    p.tpx = 0;
     if (p.conv_W > 0 && p.split_ws != nullptr) {
         const SplitPlan sp = split_plan(p.M, p.N, p.K);
         if (sp.splitk > 1 && p.split_ws_bytes >= sp.bytes && ((uintptr_t)p.split_ws & 15u) == 0) {
@@ -737,6 +740,24 @@ hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
             return launch_dma<128, 128, 3, false>(p, s);
         }
     }
+    // Unsplit launches: when W (rows x K) is at least four times X (M x K),
+    // each XCD takes a contiguous n-major range of tiles, so a W tile is
+    // fetched into one XCD's L2 (the hardware deals workgroups round-robin
+    // over the XCDs, which with few token tiles sends every W tile to all of
+    // them).  At 512 tokens (2048 px level 2): GEGLU (10240 W rows) 37.4 ->
+    // 25.5 us, Q/K/V (3840) 16.4 -> 13.6 us; at ratios of 1 to 2.5 it
+    // changed nothing measurable.
+    auto map_xcd = [&](int bm, int bn_out) {
+        const int cus = cu_count();
+        const int64_t w_rows = p.geglu ? 2 * (int64_t)p.N : p.N;
+        if (cus % CUS_PER_XCD != 0 || w_rows < 4 * (int64_t)p.M) return;
+        const int64_t tiles = (int64_t)((p.M + bm - 1) / bm) * (p.N / bn_out);
+        const int n_xcd = cus / CUS_PER_XCD;
+        if (tiles < n_xcd || tiles > INT32_MAX / 2) return;
+        p.n_xcd = n_xcd;
+        p.tpx = (int)((tiles + n_xcd - 1) / n_xcd);
+        p.n_tiles = (int)tiles;
+    };
     // bf16 X with K % 64 == 0: the pipelined kernel, with the largest tile
     // that still gives about a workgroup per compute unit.
     if (!p.a_f32 && p.K % DBK == 0 && p.seg % 4 == 0) {
@@ -754,15 +775,23 @@ hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
             // value/gate pairs on 64-token tiles at two stages (48 KB of LDS: three
             // workgroups per compute unit): 25.3 us against 28.7 for 128-token
             // tiles and 35.2 for three stages at the 2048 x 2 x 2560 x 640 shape
-            if (p.N % 64 == 0) return launch_dma<64, 128, 2, true>(p, s);
+            if (p.N % 64 == 0) {
+                map_xcd(64, 64);
+                return launch_dma<64, 128, 2, true>(p, s);
+            }
         } else {
             // 128x128 tiles only with at least two per compute unit; else 64x64
             // tiles at three stages (48 KB of LDS: three workgroups per compute
             // unit), measured faster at M = 2048 for every N from 640 to 1920.
             const int64_t mt128 = (p.M + 127) / 128;
-            if (p.N % 128 == 0 && mt128 * (p.N / 128) >= 2 * (int64_t)cu_count())
+            if (p.N % 128 == 0 && mt128 * (p.N / 128) >= 2 * (int64_t)cu_count()) {
+                map_xcd(128, 128);
                 return launch_dma<128, 128, 3, false>(p, s);
-            if (p.N % 64 == 0) return launch_dma<64, 64, 3, false>(p, s);
+            }
+            if (p.N % 64 == 0) {
+                map_xcd(64, 64);
+                return launch_dma<64, 64, 3, false>(p, s);
+            }
         }
     }
     // only the pipelined kernel writes a bf16 copy, adds bias2 or convolves
