@@ -189,7 +189,8 @@ def unet_device_inputs(torch, pcpp, synth, sp, dev, seed=7, sync_gn=True):
         elif ly["kind"] == "module":
             heads, F = co // 64, 4 * co
             bc = synth.BlockConfig(ly["name"], synth.AttnConfig(name=ly["name"], H=H, W=W, n=n, i=i, p=sp.p,
-                                                                heads=heads, d=64, dtype="bf16", seed_id=0),
+                                                                heads=heads, d=64, dtype="bf16", seed_id=0,
+                                                                batch=B),
                                    n_text=sp.n_text, text_dim=sp.text_dim, ff_inner=F, gn_groups=sp.groups)
             shapes = synth.block_weight_shapes(bc)
 
@@ -501,7 +502,16 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
     out["unet_sdxl2048_band_step_ms"] = round(us / 1e3, 3)
     out["unet_sdxl2048_band_step_TFLOPs"] = round(uflops / us / 1e6, 1)
     out["unet_sdxl2048_band_step_gflop"] = round(uflops / 1e9, 1)
-    del net, uw, ust
+    del net, uw, ust, ulat, utemb, utext
+    # the same band step with both guidance branches (unconditional and
+    # conditional, Eq. 2) stacked as a batch of 2 in one pass
+    sp2 = dataclasses.replace(sp, batch=2)
+    layers, uw, ust, ulat, utemb, utext, uflops2 = unet_device_inputs(torch, pcpp, synth, sp2, dev)
+    net = BandUNet(sp2, layers, uw, ust, dev, sync_gn=True)
+    us = graph_time_us(torch, lambda: net.forward(ulat, utemb, utext), 3, use_graph)
+    out["unet_sdxl2048_band_step_cfg_batch2_ms"] = round(us / 1e3, 3)
+    out["unet_sdxl2048_band_step_cfg_batch2_TFLOPs"] = round(uflops2 / us / 1e6, 1)
+    del net, uw, ust, ulat, utemb, utext
 
     # the latent update of one band of the 2048 px image (latent 256 x 256 x 4, 8 bands)
     n = 256 // 8 * 256 * 4

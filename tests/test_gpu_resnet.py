@@ -146,7 +146,8 @@ def _other_band_stats(rc, G, C, seed):
     return np.stack(out)
 
 
-@pytest.mark.parametrize("rc", [SMALL[0], SMALL[2], FULL[1]], ids=lambda r: r.name)
+# FULL[2] (8192 tokens of 320 channels) applies 32 tokens per workgroup
+@pytest.mark.parametrize("rc", [SMALL[0], SMALL[2], FULL[1], FULL[2]], ids=lambda r: r.name)
 def test_resnet_synchronized_group_norm(rc):
     import torch
     _say("resnet sync GN", rc)
