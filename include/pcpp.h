@@ -317,8 +317,9 @@ typedef struct {
     int32_t gn_groups;                                  /* dividing C          */
 } pcpp_module_weights_t;
 
-/* Bytes of device workspace (0 if invalid); the same for every depth and the
- * same contract as pcpp_transformer_block_workspace_size. */
+/* Bytes of device workspace (0 if invalid), the same contract as
+ * pcpp_transformer_block_workspace_size. It grows with the depth up to 16
+ * basic blocks: the text K/V of up to 16 blocks come from one product. */
 size_t pcpp_transformer_module_workspace_size(const pcpp_geom_t* g,
                                               const pcpp_module_weights_t* w,
                                               int32_t n_text, int32_t text_dim);

@@ -33,8 +33,10 @@ namespace pcpp {
 namespace {
 
 struct BlockLayout {
-    size_t t16, hid, q16, k16, v16, a16, k2, v2, u16, attn_ws, gn, split, total;
+    size_t t16, hid, q16, k16, v16, a16, kv2, u16, attn_ws, gn, split, total;
     size_t attn_ws_bytes, split_bytes;
+    int kv_slots;  // basic blocks whose text K/V one launch computes
+    bool kv_grouped;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -73,8 +75,10 @@ AttnParams cross_attn_params(const pcpp_geom_t* g, const Geo& r, const void* q, 
     return make_attn_params(g, r, q, out, kv);
 }
 
+// The text K/V of up to GEMM_MAX_WSEG basic blocks come from one grouped
+// product (text_dim % 64 == 0; else one product per block into one slot).
 BlockLayout layout(const pcpp_geom_t* g, const Geo& r, int32_t ff_inner, int32_t gn_groups, int32_t n_text,
-                   int32_t text_dim) {
+                   int32_t text_dim, int32_t depth) {
     BlockLayout L;
     const size_t rows = (size_t)g->batch * r.nq;
     const size_t C = r.C;
@@ -94,8 +98,9 @@ BlockLayout layout(const pcpp_geom_t* g, const Geo& r, int32_t ff_inner, int32_t
     L.k16 = take(rows * C * 2);
     L.v16 = take(rows * C * 2);
     L.a16 = take(rows * C * 2);
-    L.k2 = take((size_t)g->batch * n_text * C * 2);
-    L.v2 = take((size_t)g->batch * n_text * C * 2);
+    L.kv_grouped = text_dim % 64 == 0;
+    L.kv_slots = L.kv_grouped ? (depth < GEMM_MAX_WSEG ? depth : GEMM_MAX_WSEG) : 1;
+    L.kv2 = take((size_t)L.kv_slots * 2 * g->batch * n_text * C * 2);
     L.u16 = take(rows * (size_t)ff_inner * 2);
     L.attn_ws = take(L.attn_ws_bytes);
     L.gn = take(group_norm_ws_bytes(g->batch, gn_groups, r.nq));
@@ -103,10 +108,13 @@ BlockLayout layout(const pcpp_geom_t* g, const Geo& r, int32_t ff_inner, int32_t
     // the largest any of them can use.
     const int M = (int)rows, Ci = (int)C;
     const size_t sizes[] = {gemm_split_ws_bytes(M, Ci, Ci, false), gemm_split_ws_bytes(M, 3 * Ci, Ci, false),
-                            gemm_split_ws_bytes(M, Ci, ff_inner, false),
-                            gemm_split_ws_bytes(g->batch * n_text, 2 * Ci, text_dim, false)};
+                            gemm_split_ws_bytes(M, Ci, ff_inner, false)};
     L.split_bytes = 0;
     for (size_t b : sizes) L.split_bytes = b > L.split_bytes ? b : L.split_bytes;
+    for (int nb = 1; nb <= L.kv_slots; ++nb) {  // every chunk size, the last one may be short
+        const size_t b = gemm_split_ws_bytes(g->batch * n_text, nb * 2 * Ci, text_dim, false);
+        L.split_bytes = b > L.split_bytes ? b : L.split_bytes;
+    }
     L.split = L.split_bytes ? take(L.split_bytes) : 0;
     L.total = off;
     return L;
@@ -210,7 +218,7 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
         if (k_out && k_out[j] && !aligned16(k_out[j])) return PCPP_EINVAL;
         if (v_out && v_out[j] && !aligned16(v_out[j])) return PCPP_EINVAL;
     }
-    const BlockLayout L = layout(g, r, mw.ff_inner, mw.gn_groups, n_text, text_dim);
+    const BlockLayout L = layout(g, r, mw.ff_inner, mw.gn_groups, n_text, text_dim, depth);
     if (workspace == nullptr || ws_bytes < L.total) return PCPP_EWORKSPACE;
     if (!aligned16(workspace)) return PCPP_EINVAL;
 
@@ -222,8 +230,8 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
     float* hid = (float*)(ws + L.hid);
     __bf16* q16 = (__bf16*)(ws + L.q16);
     __bf16* a16 = (__bf16*)(ws + L.a16);
-    __bf16* k2 = (__bf16*)(ws + L.k2);
-    __bf16* v2 = (__bf16*)(ws + L.v2);
+    __bf16* kv2 = (__bf16*)(ws + L.kv2);
+    const int64_t kv_elems = (int64_t)B * T * C;  // one K or V of the text
     __bf16* u16 = (__bf16*)(ws + L.u16);
     void* attn_ws = ws + L.attn_ws;
     void* split_ws = L.split_bytes ? ws + L.split : nullptr;
@@ -281,6 +289,22 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
         const void* kd = r.dn > 0 ? k_dn[j] : nullptr;
         const void* vd = r.dn > 0 ? v_dn[j] : nullptr;
 
+        // Text K/V of this block and the next ones of its chunk: one product
+        // over their stacked weights, block u's K at slot 2u, V at 2u + 1.
+        const int slot = j % L.kv_slots;
+        if (L.kv_grouped && slot == 0) {
+            const int nb = depth - j < L.kv_slots ? depth - j : L.kv_slots;
+            GemmParams kv = gemm(text, text_dim, false, w.attn2_kv_w, nullptr, B * T, nb * 2 * C, text_dim, kv2, C,
+                                 false);
+            kv.seg = C;
+            kv.seg_stride = kv_elems;
+            kv.w_seg_rows = 2 * C;
+            for (int u = 0; u < nb; ++u) kv.w_seg[u] = (const __bf16*)blocks[j + u].attn2_kv_w;
+            PCPP_CHECK(gemm_s(kv));
+        }
+        __bf16* k2 = kv2 + 2 * slot * kv_elems;
+        __bf16* v2 = k2 + kv_elems;
+
         // Self-attention: Q, K, V of the band; K and V are the band's export.
         lp.gamma = (const __bf16*)w.ln1_gamma;
         lp.beta = (const __bf16*)w.ln1_beta;
@@ -309,7 +333,7 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
         lp.beta = (const __bf16*)w.ln2_beta;
         PCPP_CHECK(launch_layer_norm(lp, s));
         PCPP_CHECK(gemm_s(gemm(t16, C, false, w.attn2_q_w, nullptr, rows, C, C, q16, C, false)));
-        {
+        if (!L.kv_grouped) {
             GemmParams kv = gemm(text, text_dim, false, w.attn2_kv_w, nullptr, B * T, 2 * C, text_dim, k2, C, false);
             kv.out[1] = v2;
             kv.seg = C;
@@ -382,7 +406,7 @@ PCPP_EXPORT size_t pcpp_transformer_block_workspace_size(const pcpp_geom_t* g, c
                                                          int32_t n_text, int32_t text_dim) {
     Geo r;
     if (w == nullptr || validate_block(g, w->ff_inner, w->gn_groups, n_text, text_dim, &r) != PCPP_OK) return 0;
-    return layout(g, r, w->ff_inner, w->gn_groups, n_text, text_dim).total;
+    return layout(g, r, w->ff_inner, w->gn_groups, n_text, text_dim, 1).total;
 }
 
 PCPP_EXPORT int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w, const void* x,
@@ -411,7 +435,7 @@ PCPP_EXPORT size_t pcpp_transformer_module_workspace_size(const pcpp_geom_t* g, 
     Geo r;
     if (w == nullptr || validate_block(g, w->ff_inner, w->gn_groups, n_text, text_dim, &r) != PCPP_OK) return 0;
     if (w->depth < 1 || w->depth > 64) return 0;
-    return layout(g, r, w->ff_inner, w->gn_groups, n_text, text_dim).total;
+    return layout(g, r, w->ff_inner, w->gn_groups, n_text, text_dim, w->depth).total;
 }
 
 PCPP_EXPORT int pcpp_transformer_module(const pcpp_geom_t* g, const pcpp_module_weights_t* w, const void* x,

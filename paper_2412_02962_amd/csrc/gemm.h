@@ -6,6 +6,8 @@
 
 namespace pcpp {
 
+constexpr int GEMM_MAX_WSEG = 16;
+
 // Y[m, n] = X[m, :] . W[n, :] (+ bias[n]) (+ resid[m, n]), optionally
 // value * GELU(gate) with the gate taken from W rows F + n.
 struct GemmParams {
@@ -42,6 +44,15 @@ struct GemmParams {
     // before the first use and are left zero), or null.
     void* split_ws = nullptr;
     size_t split_ws_bytes = 0;
+    // Several W matrices sharing X (plain bf16 GEMMs on the pipelined kernel
+    // only): W rows [j * w_seg_rows, (j + 1) * w_seg_rows) are the rows of
+    // w_seg[j] (w_seg_rows % 128 == 0, N / w_seg_rows <= GEMM_MAX_WSEG);
+    // w_seg_rows = 0: w alone.
+    const __bf16* w_seg[GEMM_MAX_WSEG] = {};
+    int32_t w_seg_rows = 0;
+    // > 0: output segment s at out[0] + s * seg_stride elements (out[1..2]
+    // unused), for any number of segments.
+    int64_t seg_stride = 0;
     // Set by launch_gemm for a split launch.
     int32_t splitk = 1, n_xcd = 1, tpx = 0, n_tiles = 0;
 };

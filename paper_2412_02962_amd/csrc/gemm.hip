@@ -351,12 +351,21 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
         iss_kx = t - 3 * ky;
         iss_xoff = ((int64_t)(ky * (p.conv_W + 2) + iss_kx) * cin + iss_cb * DBK) * 2;
     }
+    // W of this tile: one of several matrices when w_seg_rows > 0 (a tile's
+    // BN rows never straddle two of them).
+    const __bf16* wmat = p.w;
+    int wrow0 = n0;
+    if (!GEGLU && p.w_seg_rows > 0) {
+        const int j = n0 / p.w_seg_rows;
+        wmat = p.w_seg[j];
+        wrow0 = n0 - j * p.w_seg_rows;
+    }
 #pragma unroll
     for (int i = 0; i < WP; ++i) {
         const int r = 8 * (wave + 4 * i) + (lane >> 3);
-        const int wr = GEGLU ? (r < BN / 2 ? n0 + r : p.F + n0 + (r - BN / 2)) : n0 + r;
+        const int wr = GEGLU ? (r < BN / 2 ? n0 + r : p.F + n0 + (r - BN / 2)) : wrow0 + r;
         const int c = (lane & 7) ^ ((r >> 1) & 7);
-        wsrc[i] = (const char*)p.w + ((int64_t)wr * p.K + 8 * c) * 2;
+        wsrc[i] = (const char*)wmat + ((int64_t)wr * p.K + 8 * c) * 2;
     }
     auto issue = [&](int kt, int stage) {
         char* st = lds + stage * STAGE;
@@ -582,7 +591,9 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
                 for (int e = 0; e < 4; ++e) v[e] += res_v[i][j][c][e];
                 const int seg = n / p.seg;
                 const int ns = n - seg * p.seg;
-                void* dst = p.out[seg];
+                void* dst = p.seg_stride > 0
+                                ? (void*)((char*)p.out[0] + (int64_t)seg * p.seg_stride * (p.out_f32 ? 4 : 2))
+                                : p.out[seg];
                 if (p.out_f32) {
                     f32x4 o = {v[0], v[1], v[2], v[3]};
                     *(f32x4*)((float*)dst + (int64_t)m * p.ldo + ns) = o;
@@ -728,6 +739,14 @@ size_t gemm_split_ws_bytes(int M, int N, int K, bool conv) {
 hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
     GemmParams p = p_in;
     if (p.conv_W > 0 && !gemm_shape_ok(p)) return hipErrorInvalidValue;
+    if (p.w_seg_rows != 0 || p.seg_stride != 0) {  // the pipelined kernel's plain form only
+        if (p.a_f32 || p.geglu || p.conv_W > 0 || p.K % DBK != 0 || p.seg % 4 != 0 || p.N % 64 != 0 ||
+            p.seg_stride < 0 || p.w_seg_rows < 0)
+            return hipErrorInvalidValue;
+        if (p.w_seg_rows > 0 &&
+            (p.w_seg_rows % 128 != 0 || p.N % p.w_seg_rows != 0 || p.N / p.w_seg_rows > GEMM_MAX_WSEG))
+            return hipErrorInvalidValue;
+    }
     p.splitk = 1;
     p.tpx = 0;
     if (p.conv_W > 0 && p.split_ws != nullptr) {
