@@ -284,7 +284,7 @@ constexpr int LN_MAX_VEC = 8;  // 16-byte fp32 vectors per lane: C <= 2048
 
 template <int NV>  // 16-byte vectors per lane: C <= 256 * NV
 __global__ __launch_bounds__(256) void ln_kernel(LayerNormParams p) {
-    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int row = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (row >= p.rows) return;
     const int nv = p.C / 4;
@@ -382,16 +382,18 @@ hipError_t launch_group_norm(GroupNormParams p, hipStream_t s) {
 
 hipError_t launch_layer_norm(const LayerNormParams& p, hipStream_t s) {
     if (p.C % 4 != 0 || p.C > 4 * 64 * LN_MAX_VEC) return hipErrorInvalidValue;
-    const unsigned grid = (unsigned)((p.rows + 3) / 4);
+    // One row per wavefront; one wavefront per workgroup, so that short
+    // launches still spread over every compute unit.
+    const unsigned grid = (unsigned)p.rows;
     switch ((p.C + 255) / 256) {
-        case 1: ln_kernel<1><<<grid, 256, 0, s>>>(p); break;
-        case 2: ln_kernel<2><<<grid, 256, 0, s>>>(p); break;
-        case 3: ln_kernel<3><<<grid, 256, 0, s>>>(p); break;
-        case 4: ln_kernel<4><<<grid, 256, 0, s>>>(p); break;
-        case 5: ln_kernel<5><<<grid, 256, 0, s>>>(p); break;
-        case 6: ln_kernel<6><<<grid, 256, 0, s>>>(p); break;
-        case 7: ln_kernel<7><<<grid, 256, 0, s>>>(p); break;
-        default: ln_kernel<8><<<grid, 256, 0, s>>>(p); break;
+        case 1: ln_kernel<1><<<grid, 64, 0, s>>>(p); break;
+        case 2: ln_kernel<2><<<grid, 64, 0, s>>>(p); break;
+        case 3: ln_kernel<3><<<grid, 64, 0, s>>>(p); break;
+        case 4: ln_kernel<4><<<grid, 64, 0, s>>>(p); break;
+        case 5: ln_kernel<5><<<grid, 64, 0, s>>>(p); break;
+        case 6: ln_kernel<6><<<grid, 64, 0, s>>>(p); break;
+        case 7: ln_kernel<7><<<grid, 64, 0, s>>>(p); break;
+        default: ln_kernel<8><<<grid, 64, 0, s>>>(p); break;
     }
     return hipGetLastError();
 }
