@@ -556,6 +556,20 @@ int pcpp_conv3x3(const pcpp_conv_geom_t* g, const void* x, const void* row_up,
                  void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * pcpp_conv3x3 that also exports the band's first and last input rows (Sec.
+ * 3.2: what the neighbours read as row_dn and row_up at the next step):
+ *   first_out, last_out  [B, W, c_in] (either may be NULL), 16-byte aligned,
+ *                        not overlapping the inputs, y or each other
+ *                        (PCPP_EINVAL).  UP exports the rows before upsampling.
+ * Otherwise the same as pcpp_conv3x3 (which is this call without exports).
+ */
+int pcpp_conv3x3_export(const pcpp_conv_geom_t* g, const void* x,
+                        const void* row_up, const void* row_dn, const void* w,
+                        const void* bias, void* y, void* first_out,
+                        void* last_out, void* workspace, size_t ws_bytes,
+                        void* stream);
+
+/*
  * [rows, ca] and [rows, cb] bf16 side by side into out [rows, ca + cb]: the
  * U-Net up path's concatenation of a level's state with its skip connection
  * (the ResNet that follows takes ca + cb channels).  b = NULL fills the cb

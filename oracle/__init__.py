@@ -45,4 +45,5 @@ from .unet_oracle import (  # noqa: F401
     scaled_linear_alphabar,
     silu,
     unet_band_step,
+    image_step,
 )

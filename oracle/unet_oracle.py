@@ -33,7 +33,7 @@ from typing import Dict, Optional, Tuple
 
 import numpy as np
 
-from .pcpp_oracle import group_norm, group_norm_synchronized, linear
+from .pcpp_oracle import group_norm, group_norm_synchronized, group_stats, linear
 
 
 def silu(x: np.ndarray) -> np.ndarray:
@@ -134,7 +134,7 @@ def resnet_block(W: int, wts: Dict[str, np.ndarray], x: np.ndarray, temb: np.nda
                  edges2_up: Optional[np.ndarray], edges2_dn: Optional[np.ndarray],
                  groups: int = 32, i: int = 0,
                  gn1_band_stats: Optional[np.ndarray] = None,
-                 gn2_band_stats: Optional[np.ndarray] = None):
+                 gn2_band_stats: Optional[np.ndarray] = None, stats_out: Optional[list] = None):
     """One SDXL-shaped ResNet block on a row band, float64.
 
     x [B, h*W, C_in]; temb [B, T] (the step's time embedding).  edges*_up is
@@ -144,18 +144,23 @@ def resnet_block(W: int, wts: Dict[str, np.ndarray], x: np.ndarray, temb: np.nda
     GroupNorm is the synchronized one (every band's statistics, this band's
     own, index i, in its place).
     Returns (y [B, h*W, C_out], edges1, edges2): the output and this band's
-    own exports of the two convolution inputs.
+    own exports of the two convolution inputs.  stats_out, if a list, gets
+    this band's own statistics of the two GroupNorm inputs (group_stats).
     """
     def gn(t, gamma, beta, stats):
         if stats is None:
             return group_norm(t, groups, gamma, beta, eps=RESNET_GN_EPS)
         return group_norm_synchronized(t, groups, gamma, beta, stats, i, eps=RESNET_GN_EPS)
 
+    if stats_out is not None:
+        stats_out.append(group_stats(x, groups))
     a1 = silu(gn(x, wts["gn1_gamma"], wts["gn1_beta"], gn1_band_stats))
     hid = conv3x3_band(a1, W, wts["conv1_w"], wts["conv1_b"],
                        None if edges1_up is None else edges1_up[:, 1],
                        None if edges1_dn is None else edges1_dn[:, 0])
     hid = hid + linear(silu(temb), wts["temb_w"], wts["temb_b"])[:, None, :]
+    if stats_out is not None:
+        stats_out.append(group_stats(hid, groups))
     a2 = silu(gn(hid, wts["gn2_gamma"], wts["gn2_beta"], gn2_band_stats))
     hid = conv3x3_band(a2, W, wts["conv2_w"], wts["conv2_b"],
                        None if edges2_up is None else edges2_up[:, 1],
@@ -224,7 +229,8 @@ def resnet_weight_shapes(c_in: int, c_out: int, temb_dim: int) -> Dict[str, Tupl
 # ---------------------------------------------------------------------------
 
 def unet_band_step(layers, n: int, i: int, p: float, groups: int, weights, stale,
-                   latent: np.ndarray, temb: np.ndarray, text: np.ndarray, sync_gn: bool = False) -> np.ndarray:
+                   latent: np.ndarray, temb: np.ndarray, text: np.ndarray, sync_gn: bool = False,
+                   exports: Optional[dict] = None) -> np.ndarray:
     """The noise prediction of band i: the layers in order (`layers`, a list
     of dicts: name, kind 'conv' / 'resnet' / 'module' / 'gn', input grid H x
     W, channels, conv mode, module depth, push / pop of skip connections),
@@ -234,7 +240,11 @@ def unet_band_step(layers, n: int, i: int, p: float, groups: int, weights, stale
     its ResNets.  GroupNorms use the band's own statistics, or with sync_gn
     the synchronized ones (every band's statistics from stale: a ResNet's
     gn1_bands / gn2_bands, stale[module + ':gn_bands'], the head's gn_bands).
-    latent [B, h*W, 64] (4 channels, zero-padded); returns [B, h*W, 64]."""
+    latent [B, h*W, 64] (4 channels, zero-padded); returns [B, h*W, 64].
+    exports, if a dict, gets per layer what the neighbours read at the next
+    step (Sec. 3.2): a convolution's first and last input rows, a ResNet's
+    edges1 / edges2, a module's per-block K and V, and the band's own
+    GroupNorm statistics ('gn', a list in the layer's order)."""
     from .pcpp_oracle import group_norm as _gn, group_norm_synchronized as _gns, transformer_module as _module
     modes = {0: "same", 1: "down", 2: "up"}
     hcur = latent
@@ -244,24 +254,103 @@ def unet_band_step(layers, n: int, i: int, p: float, groups: int, weights, stale
         w = weights[name]
         if kind == "conv":
             st = stale[name]
+            if exports is not None:
+                rows = hcur.reshape(hcur.shape[0], -1, W, hcur.shape[2])
+                exports[name] = {"first": rows[:, 0], "last": rows[:, -1]}
             out = conv3x3_band_mode(hcur, W, w["w"], w["b"], st["row_up"], st["row_dn"], modes[ly["mode"]])
         elif kind == "resnet":
             if ly.get("pop"):
                 hcur = np.concatenate([hcur, skips.pop()], axis=-1)
             st = stale[name]
-            out, _, _ = resnet_block(W, w, hcur, temb, st["edges1_up"], st["edges1_dn"], st["edges2_up"],
-                                     st["edges2_dn"], groups=groups, i=i,
-                                     gn1_band_stats=st["gn1_bands"] if sync_gn else None,
-                                     gn2_band_stats=st["gn2_bands"] if sync_gn else None)
+            stats = []
+            out, e1, e2 = resnet_block(W, w, hcur, temb, st["edges1_up"], st["edges1_dn"], st["edges2_up"],
+                                       st["edges2_dn"], groups=groups, i=i,
+                                       gn1_band_stats=st["gn1_bands"] if sync_gn else None,
+                                       gn2_band_stats=st["gn2_bands"] if sync_gn else None, stats_out=stats)
+            if exports is not None:
+                exports[name] = {"edges1": e1, "edges2": e2, "gn": stats}
         elif kind == "module":
-            out, _, _ = _module(ly["H"], W, n, i, p, w["heads"], w["module"], w["blocks"], hcur, text,
-                                stale[name], gn_groups=groups,
-                                gn_band_stats=stale[name + ":gn_bands"] if sync_gn else None)
-        elif sync_gn:
-            out = silu(_gns(hcur, groups, w["gamma"], w["beta"], stale[name]["gn_bands"], i, eps=RESNET_GN_EPS))
+            out, ks, vs = _module(ly["H"], W, n, i, p, w["heads"], w["module"], w["blocks"], hcur, text,
+                                  stale[name], gn_groups=groups,
+                                  gn_band_stats=stale[name + ":gn_bands"] if sync_gn else None)
+            if exports is not None:
+                exports[name] = {"k": ks, "v": vs, "gn": [group_stats(hcur, groups)]}
         else:
-            out = silu(_gn(hcur, groups, w["gamma"], w["beta"], eps=RESNET_GN_EPS))
+            if exports is not None:
+                exports[name] = {"gn": [group_stats(hcur, groups)]}
+            if sync_gn:
+                out = silu(_gns(hcur, groups, w["gamma"], w["beta"], stale[name]["gn_bands"], i, eps=RESNET_GN_EPS))
+            else:
+                out = silu(_gn(hcur, groups, w["gamma"], w["beta"], eps=RESNET_GN_EPS))
         if ly.get("push"):
             skips.append(out)
         hcur = out
     return hcur
+
+
+def image_step(layers, n: int, p: float, groups: int, weights, prev, latents, temb: np.ndarray,
+               text: np.ndarray, sync_gn: bool = False):
+    """One denoising step of the whole image under PCPP (Sec. 3.1-3.3): every
+    band i runs unet_band_step with the stale data its neighbours exported
+    at the previous step (Sec. 3.2: the step's exchange).  prev[j] is band
+    j's exports of that step, or None for every band before the first step
+    (nothing received: zero rows, zero K/V, statistics of count 0).  latents[i]
+    is band i's [B, h*W, 64] input.  Returns (outputs, exports), one per band.
+    Band i reads from band i-1 the last rows it exported (convolutions: its
+    last input row; ResNets: its edge rows, of which the last is used; the
+    attention: its K/V, of which the last r rows are used) and from band i+1
+    the first ones; with sync_gn every band's statistics of every GroupNorm.
+    """
+    def nb_export(j, name):
+        if j < 0 or j >= n or prev is None or prev[j] is None:
+            return None
+        return prev[j][name]
+
+    outs, exps = [], []
+    for i in range(n):
+        B = latents[i].shape[0]
+        stale = {}
+        for ly in layers:
+            name, kind, H, W, ci, co = ly["name"], ly["kind"], ly["H"], ly["W"], ly["c_in"], ly["c_out"]
+            h = H // n
+            up, dn = nb_export(i - 1, name), nb_export(i + 1, name)
+
+            def gn_stack(k):  # [n, B, G, 3]: entry j = band j's k-th statistics (count 0 if none)
+                st = np.zeros((n, B, groups, 3))
+                for j in range(n):
+                    e = nb_export(j, name)
+                    if e is not None:
+                        st[j] = e["gn"][k]
+                return st
+
+            if kind == "conv":
+                zero = np.zeros((B, W, ci))
+                stale[name] = {"row_up": (up["last"] if up else zero) if i > 0 else None,
+                               "row_dn": (dn["first"] if dn else zero) if i < n - 1 and ly["mode"] != 1 else None}
+            elif kind == "resnet":
+                z1, z2 = np.zeros((B, 2, W, ci)), np.zeros((B, 2, W, co))
+                stale[name] = {"edges1_up": (up["edges1"] if up else z1) if i > 0 else None,
+                               "edges1_dn": (dn["edges1"] if dn else z1) if i < n - 1 else None,
+                               "edges2_up": (up["edges2"] if up else z2) if i > 0 else None,
+                               "edges2_dn": (dn["edges2"] if dn else z2) if i < n - 1 else None}
+                if sync_gn:
+                    stale[name]["gn1_bands"], stale[name]["gn2_bands"] = gn_stack(0), gn_stack(1)
+            elif kind == "module":
+                zkv = np.zeros((B, h * W, co))
+                st = []
+                for j in range(ly["depth"]):
+                    ku = (up["k"][j] if up else zkv) if i > 0 else None
+                    vu = (up["v"][j] if up else zkv) if i > 0 else None
+                    kd = (dn["k"][j] if dn else zkv) if i < n - 1 else None
+                    vd = (dn["v"][j] if dn else zkv) if i < n - 1 else None
+                    st.append((ku, vu, kd, vd))
+                stale[name] = st
+                if sync_gn:
+                    stale[name + ":gn_bands"] = gn_stack(0)
+            else:
+                stale[name] = {"gn_bands": gn_stack(0) if sync_gn else None}
+        ex = {}
+        outs.append(unet_band_step(layers, n, i, p, groups, weights, stale, latents[i], temb, text,
+                                   sync_gn=sync_gn, exports=ex))
+        exps.append(ex)
+    return outs, exps

@@ -31,9 +31,12 @@ constexpr int kThreads = 256;
 // ((fy - 1) / u, (fx - 1) / u) (u = 2 when upsampling, else 1); framed row 0
 // takes row_up [B][W][C] at column (fx - 1) / u, row Hf + 1 row_dn (zeros
 // when null); columns 0 and Wf + 1 are zeros.  Block 0 also clears the
-// convolution's split counters (n_zero ints).
+// convolution's split counters (n_zero ints).  first_out / last_out [B][W][C]
+// (if not null) receive the band's first and last rows, what its neighbours
+// read as row_dn and row_up at the next step.
 __global__ __launch_bounds__(kThreads) void frame_copy(bf16* f, const bf16* x, const bf16* row_up, const bf16* row_dn,
-                                                       int h, int W, int C, int u, int* zero, int n_zero) {
+                                                       int h, int W, int C, int u, int* zero, int n_zero,
+                                                       bf16* first_out, bf16* last_out) {
     if (blockIdx.x == 0 && blockIdx.y == 0 && zero != nullptr)
         for (int i = threadIdx.x; i < n_zero; i += kThreads) zero[i] = 0;
     const int b = blockIdx.y;
@@ -55,6 +58,11 @@ __global__ __launch_bounds__(kThreads) void frame_copy(bf16* f, const bf16* x, c
             else
                 src = x + (((int64_t)b * h + (fy - 1) / u) * W + col) * C;
             if (src != nullptr) v = *(const u32x4*)(src + c);
+            if ((fx - 1) % u == 0) {  // once per band token
+                const int64_t o = ((int64_t)b * W + col) * C + c;
+                if (fy == 1 && first_out != nullptr) *(u32x4*)(first_out + o) = v;
+                if (fy == Hf && last_out != nullptr) *(u32x4*)(last_out + o) = v;
+            }
         }
         *(u32x4*)(fb + cell * C + c) = v;
     }
@@ -106,6 +114,11 @@ int validate_conv(const pcpp_conv_geom_t* g) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+bool overlap(const void* a, int64_t na, const void* b, int64_t nb) {
+    if (!a || !b) return false;
+    return (uintptr_t)a < (uintptr_t)b + (uintptr_t)nb && (uintptr_t)b < (uintptr_t)a + (uintptr_t)na;
+}
+
 }  // namespace
 
 }  // namespace pcpp
@@ -117,17 +130,31 @@ PCPP_EXPORT size_t pcpp_conv3x3_workspace_size(const pcpp_conv_geom_t* g) {
     return conv_layout(g).total;
 }
 
-PCPP_EXPORT int pcpp_conv3x3(const pcpp_conv_geom_t* g, const void* x, const void* row_up, const void* row_dn,
-                             const void* w, const void* bias, void* y, void* workspace, size_t ws_bytes,
-                             void* stream) {
+PCPP_EXPORT int pcpp_conv3x3_export(const pcpp_conv_geom_t* g, const void* x, const void* row_up,
+                                    const void* row_dn, const void* w, const void* bias, void* y, void* first_out,
+                                    void* last_out, void* workspace, size_t ws_bytes, void* stream) {
     int st = validate_conv(g);
     if (st != PCPP_OK) return st;
     const bool need_up = g->patch_idx > 0;
     const bool need_dn = g->patch_idx < g->n_patches - 1 && g->mode != PCPP_CONV_DOWN;
     if (!x || !w || !y || (need_up && !row_up) || (need_dn && !row_dn)) return PCPP_EINVAL;
-    const void* ptrs[] = {x, row_up, row_dn, w, bias, y};
+    const void* ptrs[] = {x, row_up, row_dn, w, bias, y, first_out, last_out};
     for (const void* p : ptrs)
         if (p && !aligned16(p)) return PCPP_EINVAL;
+    {  // the exported rows must not overlap the inputs, the output or each other
+        const int hb = g->H / g->n_patches;
+        const int64_t row_b = (int64_t)g->batch * g->W * g->c_in * 2;
+        const int64_t x_b = row_b * hb;
+        const int st_o = g->mode == PCPP_CONV_DOWN ? 2 : 1, u_o = g->mode == PCPP_CONV_UP ? 2 : 1;
+        const int64_t y_b = (int64_t)g->batch * (hb * u_o / st_o) * (g->W * u_o / st_o) * g->c_out * 2;
+        for (void* e : {first_out, last_out}) {
+            if (!e) continue;
+            if (overlap(e, row_b, x, x_b) || overlap(e, row_b, row_up, need_up ? row_b : 0) ||
+                overlap(e, row_b, row_dn, need_dn ? row_b : 0) || overlap(e, row_b, y, y_b))
+                return PCPP_EINVAL;
+        }
+        if (overlap(first_out, row_b, last_out, row_b)) return PCPP_EINVAL;
+    }
     const ConvLayout L = conv_layout(g);
     if (workspace == nullptr || ws_bytes < L.total) return PCPP_EWORKSPACE;
     if (!aligned16(workspace)) return PCPP_EINVAL;
@@ -142,7 +169,8 @@ PCPP_EXPORT int pcpp_conv3x3(const pcpp_conv_geom_t* g, const void* x, const voi
     if (blocks > 2048) blocks = 2048;
     frame_copy<<<dim3((unsigned)blocks, (unsigned)g->batch), kThreads, 0, s>>>(
         framed, (const bf16*)x, need_up ? (const bf16*)row_up : nullptr, need_dn ? (const bf16*)row_dn : nullptr,
-        L.h, g->W, g->c_in, u, (int*)split_ws, split_ws ? GEMM_SPLIT_COUNTERS : 0);
+        L.h, g->W, g->c_in, u, (int*)split_ws, split_ws ? GEMM_SPLIT_COUNTERS : 0, (bf16*)first_out,
+        (bf16*)last_out);
     if (hipGetLastError() != hipSuccess) return PCPP_EHIP;
 
     GemmParams p;
@@ -171,4 +199,10 @@ PCPP_EXPORT int pcpp_conv3x3(const pcpp_conv_geom_t* g, const void* x, const voi
     p.split_ws = split_ws;
     p.split_ws_bytes = L.split_bytes;
     return launch_gemm(p, s) == hipSuccess ? PCPP_OK : PCPP_EHIP;
+}
+
+PCPP_EXPORT int pcpp_conv3x3(const pcpp_conv_geom_t* g, const void* x, const void* row_up, const void* row_dn,
+                             const void* w, const void* bias, void* y, void* workspace, size_t ws_bytes,
+                             void* stream) {
+    return pcpp_conv3x3_export(g, x, row_up, row_dn, w, bias, y, nullptr, nullptr, workspace, ws_bytes, stream);
 }

@@ -160,6 +160,7 @@ def _load():
                                            vp, sz, vp]),
         "pcpp_conv3x3_workspace_size": (sz, [ctypes.POINTER(pcpp_conv_geom_t)]),
         "pcpp_conv3x3": (ctypes.c_int, [ctypes.POINTER(pcpp_conv_geom_t)] + [vp] * 7 + [sz, vp]),
+        "pcpp_conv3x3_export": (ctypes.c_int, [ctypes.POINTER(pcpp_conv_geom_t)] + [vp] * 9 + [sz, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -177,7 +178,7 @@ EXPORTED = (
     "pcpp_partial_attention_multihop_workspace_size", "pcpp_partial_attention_multihop",
     "pcpp_multihop_message_bytes", "pcpp_pack_multihop", "pcpp_unpack_multihop",
     "pcpp_resnet_block_workspace_size", "pcpp_resnet_block", "pcpp_guided_step",
-    "pcpp_conv3x3_workspace_size", "pcpp_conv3x3",
+    "pcpp_conv3x3_workspace_size", "pcpp_conv3x3", "pcpp_conv3x3_export",
     "pcpp_transformer_module_workspace_size", "pcpp_transformer_module",
     "pcpp_concat_channels", "pcpp_group_norm_workspace_size", "pcpp_group_norm",
 )
@@ -366,6 +367,13 @@ def pcpp_conv3x3(g, x, row_up, row_dn, w, bias, y, workspace, ws_bytes, stream=N
     _check("pcpp_conv3x3", _lib.pcpp_conv3x3(
         ctypes.byref(g), _ptr(x), _ptr(row_up), _ptr(row_dn), _ptr(w), _ptr(bias), _ptr(y), _ptr(workspace),
         ws_bytes, _stream(stream)))
+
+
+def pcpp_conv3x3_export(g, x, row_up, row_dn, w, bias, y, first_out, last_out, workspace, ws_bytes,
+                        stream=None):
+    _check("pcpp_conv3x3_export", _lib.pcpp_conv3x3_export(
+        ctypes.byref(g), _ptr(x), _ptr(row_up), _ptr(row_dn), _ptr(w), _ptr(bias), _ptr(y), _ptr(first_out),
+        _ptr(last_out), _ptr(workspace), ws_bytes, _stream(stream)))
 
 
 def make_module_weights(module: dict, blocks: list, ff_inner: int, gn_groups: int):

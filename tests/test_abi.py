@@ -361,3 +361,11 @@ def test_conv3x3_geometry_and_validation():
     d = pcpp.make_conv_geom(16, 20, 4, 1, 64, 64, 1, pcpp.PCPP_CONV_DOWN)
     assert lib.pcpp_conv3x3(ctypes.byref(d), FAKE, FAKE, None, FAKE, None, FAKE, FAKE, 16, None) == \
         pcpp.PCPP_EWORKSPACE                                                                  # no row below needed
+    # pcpp_conv3x3_export: x, row_up, row_dn, w, bias, y, first_out, last_out, workspace, bytes
+    ex = lambda *a: lib.pcpp_conv3x3_export(ctypes.byref(g), *a, None)
+    A = [1 << k for k in range(21, 31)]  # distinct, far apart, aligned
+    assert ex(A[0], A[1], A[2], A[3], None, A[4], A[0], None, A[7], 1 << 30) == pcpp.PCPP_EINVAL  # first_out on x
+    assert ex(A[0], A[1], A[2], A[3], None, A[4], None, A[4], A[7], 1 << 30) == pcpp.PCPP_EINVAL  # last_out on y
+    assert ex(A[0], A[1], A[2], A[3], None, A[4], A[5], A[5], A[7], 1 << 30) == pcpp.PCPP_EINVAL  # on each other
+    assert ex(A[0], A[1], A[2], A[3], None, A[4], A[5] + 8, None, A[7], 1 << 30) == pcpp.PCPP_EINVAL  # misaligned
+    assert ex(A[0], A[1], A[2], A[3], None, A[4], A[5], A[6], A[7], 16) == pcpp.PCPP_EWORKSPACE  # valid exports

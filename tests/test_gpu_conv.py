@@ -92,3 +92,29 @@ def test_down_ignores_the_row_below():
         outs.append(y)
     torch.cuda.synchronize()
     assert torch.equal(outs[0], outs[1])
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2], ids=["same", "down", "up"])
+def test_conv_exports_first_and_last_rows(mode):
+    """pcpp_conv3x3_export: the same output as pcpp_conv3x3, and the band's
+    first and last input rows (before upsampling) bit for bit."""
+    import torch
+    from paper_2412_02962_amd import pcpp
+    H, W, n, i, ci, co, B = 12, 10, 3, 1, 64, 128, 2
+    _say("conv export", mode)
+    d = {k: gu.to_dev(v, "bf16") for k, v in synth.conv_inputs(H, W, n, i, ci, co, B, 61).items()}
+    g = pcpp.make_conv_geom(H, W, n, i, ci, co, B, mode)
+    h = H // n
+    tok = {0: h * W, 1: (h // 2) * (W // 2), 2: 4 * h * W}[mode]
+    wsb = pcpp.pcpp_conv3x3_workspace_size(g)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=gu.DEV)
+    y0 = torch.empty((B, tok, co), dtype=torch.bfloat16, device=gu.DEV)
+    y1 = torch.empty_like(y0)
+    first = torch.empty((B, W, ci), dtype=torch.bfloat16, device=gu.DEV)
+    last = torch.empty_like(first)
+    pcpp.pcpp_conv3x3(g, d["x"], d["row_up"], d["row_dn"], d["w"], d["b"], y0, ws, wsb)
+    pcpp.pcpp_conv3x3_export(g, d["x"], d["row_up"], d["row_dn"], d["w"], d["b"], y1, first, last, ws, wsb)
+    torch.cuda.synchronize()
+    x = d["x"].view(B, h, W, ci)
+    assert torch.equal(y0, y1)
+    assert torch.equal(first, x[:, 0]) and torch.equal(last, x[:, h - 1])

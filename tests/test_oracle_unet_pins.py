@@ -393,3 +393,43 @@ def test_u7_one_band_step_is_the_whole_image_unet():
     assert got.shape == (1, sp.H0 * sp.W0, 64)
     assert np.allclose(got, want, rtol=1e-9, atol=1e-9)
     assert np.abs(got[..., 4:]).max() == 0.0          # conv_out's padding outputs stay zero
+
+
+def test_u8_image_steps_reach_the_whole_image_unet():
+    """Repeated PCPP image steps on constant inputs: each step hands every
+    band its neighbours' exports of the step before, so once nothing changes
+    the stale data equal the fresh data.  With n = 2, p = 1 (a band attends
+    to the whole other band) and synchronized GroupNorm that fixed point is
+    the whole-image U-Net, composed here from torch operators; the bands'
+    outputs stop changing after finitely many steps (the exchange delays
+    each layer's inputs by one step at most per hop)."""
+    import dataclasses
+    from paper_2412_02962_amd import synth
+    sp = dataclasses.replace(synth.UNET_TINY, n=2, i=0, H0=16, W0=8, p=1.0)
+    layers = synth.unet_layers(sp)
+    weights, _, latent, temb, text = synth.unet_band_inputs(dataclasses.replace(sp, n=1))
+    f = lambda a: None if a is None else oracle.from_bf16_bits(a)
+    fw = {}
+    for ly in layers:
+        w = weights[ly["name"]]
+        if ly["kind"] == "module":
+            fw[ly["name"]] = {"module": {k: f(v) for k, v in w["module"].items()},
+                              "blocks": [{k: f(v) for k, v in b.items()} for b in w["blocks"]], "heads": w["heads"]}
+        else:
+            fw[ly["name"]] = {k: f(v) for k, v in w.items()}
+    lat = f(latent)
+    h0 = sp.H0 // sp.n
+    latents = [lat[:, i * h0 * sp.W0:(i + 1) * h0 * sp.W0] for i in range(sp.n)]
+    prev, last, steps = None, None, 0
+    while steps < 200:
+        outs, prev = uo.image_step(layers, sp.n, sp.p, sp.groups, fw, prev, latents, f(temb), f(text), sync_gn=True)
+        steps += 1
+        cur = np.concatenate(outs, axis=1)
+        if last is not None and np.array_equal(cur, last):
+            break
+        last = cur
+    assert steps < 200, "no fixed point"
+    want = _torch_unet(layers, weights, latent, temb, text, sp.H0, sp.W0, sp.groups, sp.p)
+    assert np.allclose(cur, want, rtol=1e-9, atol=1e-9)
+    first, _ = uo.image_step(layers, sp.n, sp.p, sp.groups, fw, None, latents, f(temb), f(text), sync_gn=True)
+    assert not np.allclose(np.concatenate(first, axis=1), want, atol=1e-3)  # the stale data matter
