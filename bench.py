@@ -137,6 +137,32 @@ def resnet_call(torch, pcpp, synth, rc, dev):
     return fn, (d, y, e1, e2, ws)
 
 
+def unet_flops(pcpp, synth, sp):
+    """Algorithmic FLOPs of band sp.i's U-Net forward (the accounting of
+    unet_device_inputs, without drawing anything)."""
+    B, n, i, flops = sp.batch, sp.n, sp.i, 0.0
+    for ly in synth.unet_layers(sp):
+        H, W, ci, co = ly["H"], ly["W"], ly["c_in"], ly["c_out"]
+        h = H // n
+        if ly["kind"] == "conv":
+            tok = {0: h * W, 1: (h // 2) * (W // 2), 2: 4 * h * W}[ly["mode"]]
+            flops += 2.0 * B * tok * 9 * ci * co
+        elif ly["kind"] == "resnet":
+            flops += resnet_flops(synth.ResnetConfig(ly["name"], H, W, n, i, ci, co, temb_dim=sp.temb_dim,
+                                                     groups=sp.groups, batch=B))
+        elif ly["kind"] == "module":
+            heads = co // 64
+            bc = synth.BlockConfig(ly["name"], synth.AttnConfig(name=ly["name"], H=H, W=W, n=n, i=i, p=sp.p,
+                                                                heads=heads, d=64, dtype="bf16", seed_id=0,
+                                                                batch=B),
+                                   n_text=sp.n_text, text_dim=sp.text_dim, ff_inner=4 * co, gn_groups=sp.groups)
+            g = pcpp.make_geom(H, W, n, i, sp.p, heads, 64, B, 0, pcpp.PCPP_DTYPE_BF16)
+            _, _, _, nkv = pcpp.pcpp_context_rows(g)
+            proj = 2.0 * B * h * W * co * co * 2
+            flops += ly["depth"] * (block_flops(bc, nkv) - proj) + proj
+    return flops
+
+
 def unet_device_inputs(torch, pcpp, synth, sp, dev, seed=7, sync_gn=True):
     """Seeded random weights and stale neighbour data of an SDXL-sized band
     U-Net drawn on the device (the same shapes and scales as
@@ -512,6 +538,18 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
     out["unet_sdxl2048_band_step_cfg_batch2_ms"] = round(us / 1e3, 3)
     out["unet_sdxl2048_band_step_cfg_batch2_TFLOPs"] = round(uflops2 / us / 1e6, 1)
     del net, uw, ust, ulat, utemb, utext
+    # one whole-image PCPP step at 2048 px on this one device: the 8 bands'
+    # U-Net forwards in turn, each with its neighbours' exports of the step
+    # before (the exchange as zero-copy buffers), synchronized GroupNorm
+    from paper_2412_02962_amd.image_step import ImageStep
+    layers, uw, _, ulat, utemb, utext, _ = unet_device_inputs(torch, pcpp, synth, sp, dev)
+    net = ImageStep(sp, layers, uw, dev, sync_gn=True)
+    bands = [ulat.clone() for _ in range(sp.n)]
+    flops_img = sum(unet_flops(pcpp, synth, dataclasses.replace(sp, i=i)) for i in range(sp.n))
+    us = graph_time_us(torch, lambda: net.step(bands, utemb, utext), 2, use_graph)
+    out["image_step_sdxl2048_8bands_one_gpu_ms"] = round(us / 1e3, 3)
+    out["image_step_sdxl2048_8bands_one_gpu_TFLOPs"] = round(flops_img / us / 1e6, 1)
+    del net, uw, ulat, utemb, utext, bands
 
     # the latent update of one band of the 2048 px image (latent 256 x 256 x 4, 8 bands)
     n = 256 // 8 * 256 * 4

@@ -54,9 +54,7 @@ class BandUNet:
             elif ly["kind"] == "module":
                 g = pcpp.make_geom(H, W, n, i, sp.p, w["heads"], 64, B, 0, pcpp.PCPP_DTYPE_BF16)
                 mw, keep = pcpp.make_module_weights(w["module"], w["blocks"], w["ff_inner"], sp.groups)
-                cols = list(zip(*stale[ly["name"]]))
-                lists = [None if any(a is None for a in c) else list(c) for c in cols]
-                plan.update(g=g, wts=mw, keep=keep, stale_lists=lists,
+                plan.update(g=g, wts=mw, keep=keep,
                             out=torch.empty((B, h * W, co), dtype=torch.bfloat16, device=device))
                 wsb = pcpp.pcpp_transformer_module_workspace_size(g, mw, sp.n_text, sp.text_dim)
             else:
@@ -75,41 +73,57 @@ class BandUNet:
         self.ws = torch.zeros(ws_max, dtype=torch.uint8, device=device)
         self.ws_bytes = ws_max
 
-    def forward(self, latent, temb, text):
+    def forward(self, latent, temb, text, stale=None, exports=None, gn_own=None):
         """latent [B, h*W0, 64] (4 channels, zero-padded), temb [B, T], text
         [B, n_text, text_dim] (device bf16) -> the band's noise prediction
-        [B, h*W0, 64] (channels 4.. are zero)."""
+        [B, h*W0, 64] (channels 4.. are zero; the buffer is reused by the
+        next call).  stale replaces the constructor's stale data for this
+        call.  exports (per layer, optional) receives what the neighbours
+        read at the next step: a convolution's first / last input rows
+        ('first', 'last' [B, W, c_in]), a ResNet's 'edges1' / 'edges2', a
+        module's per-block 'k' / 'v' lists.  gn_own replaces self.gn_own (the
+        band's own GroupNorm statistics, per layer a list)."""
         sp, ws, wsb = self.sp, self.ws, self.ws_bytes
         B = sp.batch
+        stale = self.stale if stale is None else stale
+        own_all = self.gn_own if gn_own is None else gn_own
         cur = latent
         skips = []
         for plan in self.plans:
             ly = plan["ly"]
             name, out = ly["name"], plan["out"]
             w = self.weights[name]
+            ex = exports.get(name) if exports is not None else None
             if ly["kind"] == "conv":
-                st = self.stale[name]
-                pcpp.pcpp_conv3x3(plan["g"], cur, st["row_up"], st["row_dn"], w["w"], w["b"], out, ws, wsb)
+                st = stale[name]
+                if ex is not None:
+                    pcpp.pcpp_conv3x3_export(plan["g"], cur, st["row_up"], st["row_dn"], w["w"], w["b"], out,
+                                             ex["first"], ex["last"], ws, wsb)
+                else:
+                    pcpp.pcpp_conv3x3(plan["g"], cur, st["row_up"], st["row_dn"], w["w"], w["b"], out, ws, wsb)
             elif ly["kind"] == "resnet":
                 if ly.get("pop"):
                     skip = skips.pop()
                     rows = cur.shape[0] * cur.shape[1]
                     pcpp.pcpp_concat_channels(rows, cur, cur.shape[2], skip, skip.shape[2], plan["cat"])
                     cur = plan["cat"]
-                st = self.stale[name]
+                st = stale[name]
                 b1, b2 = (st["gn1_bands"], st["gn2_bands"]) if self.sync_gn else (None, None)
-                o1, o2 = self.gn_own[name] if self.sync_gn else (None, None)
+                o1, o2 = own_all[name] if self.sync_gn else (None, None)
+                e1, e2 = (ex["edges1"], ex["edges2"]) if ex is not None else (None, None)
                 pcpp.pcpp_resnet_block(plan["g"], plan["wts"], cur, temb, st["edges1_up"], st["edges1_dn"],
-                                       st["edges2_up"], st["edges2_dn"], b1, o1, b2, o2, out, None, None, ws, wsb)
+                                       st["edges2_up"], st["edges2_dn"], b1, o1, b2, o2, out, e1, e2, ws, wsb)
             elif ly["kind"] == "module":
-                ku, vu, kd, vd = plan["stale_lists"]
-                bands = self.stale[name + ":gn_bands"] if self.sync_gn else None
-                own = self.gn_own[name][0] if self.sync_gn else None
+                cols = list(zip(*stale[name]))
+                ku, vu, kd, vd = [None if any(a is None for a in c) else list(c) for c in cols]
+                bands = stale[name + ":gn_bands"] if self.sync_gn else None
+                own = own_all[name][0] if self.sync_gn else None
+                ko, vo = (ex["k"], ex["v"]) if ex is not None else (None, None)
                 pcpp.pcpp_transformer_module(plan["g"], plan["wts"], cur, text, sp.n_text, sp.text_dim, ku, vu, kd,
-                                             vd, bands, own, out, None, None, ws, wsb)
+                                             vd, bands, own, out, ko, vo, ws, wsb)
             else:
-                bands = self.stale[name]["gn_bands"] if self.sync_gn else None
-                own = self.gn_own[name][0] if self.sync_gn else None
+                bands = stale[name]["gn_bands"] if self.sync_gn else None
+                own = own_all[name][0] if self.sync_gn else None
                 pcpp.pcpp_group_norm(B, cur.shape[1], cur.shape[2], sp.groups, 1e-5, 1, cur, w["gamma"], w["beta"],
                                      out, ws, wsb, bands=bands, n_bands=sp.n, band=sp.i, own_out=own)
             if ly.get("push"):
