@@ -65,3 +65,39 @@ def test_image_steps_match_oracle(case):
             print(f"step {t} band {i}: relative L2 {rel:.3e} (bound {bound})")
             assert rel <= bound
             assert np.abs(g[..., 4:]).max() == 0.0
+
+
+def test_image_steps_settle_on_the_whole_image_unet():
+    """On constant inputs the exchange hands every band the neighbours' data
+    of the step before; once those stop changing they equal the fresh data.
+    With n = 2, p = 1 and synchronized GroupNorm the bands then compute the
+    whole-image U-Net (the oracle's pin U8), here the library's own n = 1
+    forward: the same bound as one band step against the oracle (5.5e-2),
+    while the first step (nothing received yet) is further away.  (Observed:
+    after 100 steps the bands' outputs equal the whole-image forward bit
+    for bit; the first step is 0.73 away.)"""
+    import torch
+    from paper_2412_02962_amd.image_step import ImageStep
+    from paper_2412_02962_amd.unet import BandUNet
+    sp = dataclasses.replace(synth.UNET_TINY, n=2, i=0, H0=16, W0=8, p=1.0)
+    sp1 = dataclasses.replace(sp, n=1)
+    _say("image steps settle", sp.n, sp.p)
+    layers = synth.unet_layers(sp)
+    weights, stale1, latent, temb, text = synth.unet_band_inputs(sp1, sync_gn=True)
+    wd = _dev_tree(weights)
+    temb_d, text_d, lat_d = gu.to_dev(temb, "bf16"), gu.to_dev(text, "bf16"), gu.to_dev(latent, "bf16")
+    whole = BandUNet(sp1, layers, wd, _dev_tree(stale1), gu.DEV, sync_gn=True)
+    want = gu.to_f64(whole.forward(lat_d, temb_d, text_d).clone())[..., :4]
+    tok = (sp.H0 // sp.n) * sp.W0
+    bands = [lat_d[:, i * tok:(i + 1) * tok].contiguous() for i in range(sp.n)]
+    net = ImageStep(sp, layers, wd, gu.DEV, sync_gn=True)
+    rels = []
+    for t in range(100):  # the oracle's image step reaches its fixed point after 93 here
+        outs = net.step(bands, temb_d, text_d)
+        if t in (0, 99):
+            got = np.concatenate([gu.to_f64(o) for o in outs], axis=1)[..., :4]
+            rels.append(np.linalg.norm(got - want) / np.linalg.norm(want))
+    torch.cuda.synchronize()
+    print(f"relative L2 to the whole image: first step {rels[0]:.3e}, after 100 steps {rels[1]:.3e}")
+    assert rels[1] <= 5.5e-2
+    assert rels[0] > 2 * rels[1]
