@@ -68,34 +68,49 @@ def load_traffic():
         return None
 
 
-def cpu_baseline(cfg, inputs, budget_s=12.0):
-    import numpy as np  # noqa: F401
-
-    import oracle
+def cpu_model():
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([t.get("num_threads", 1) for t in threadpool_info() if t.get("user_api") == "blas"] or [1])
-    except Exception:
-        threads = os.cpu_count() or 1
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cfg, inputs, budget_s=8.0):
+    """The float64 oracle on the host: whole steps of the workload with every
+    BLAS thread, then with one (threadpoolctl), each timed for about
+    budget_s after one warm-up step."""
+    import oracle
+    from threadpoolctl import threadpool_info, threadpool_limits
     f = {k: oracle.as_f64(v, cfg.dtype) for k, v in inputs.items()}
 
     def step():
         return oracle.partial_attention(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, f["q"], f["k_fresh"],
                                         f["v_fresh"], f["k_up"], f["v_up"], f["k_dn"], f["v_dn"])
 
-    step()  # warm
-    n, t0 = 0, time.perf_counter()
-    while True:
-        step()
-        n += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or n >= 50:
-            break
+    def timed(max_steps):
+        step()  # warm
+        n, t0 = 0, time.perf_counter()
+        while True:
+            step()
+            n += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s or n >= max_steps:
+                return n, el
+
+    threads = max([t.get("num_threads", 1) for t in threadpool_info() if t.get("user_api") == "blas"] or [1])
+    n_all, el_all = timed(50)
+    with threadpool_limits(limits=1, user_api="blas"):
+        n_one, el_one = timed(5)
     _, _, _, rows = oracle.context_rows(cfg.H, cfg.n, cfg.i, cfg.p)
     fl = attn_flops(cfg, rows * cfg.W)
-    return {"value": round(fl * n / el / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{n} whole steps of {WORKLOAD} (float64 numpy oracle, BLAS threads={threads}), "
-                      f"{el:.1f} s, {el / n * 1e3:.1f} ms/step"}
+    return {"value": round(fl * n_all / el_all / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "value_1thread": round(fl * n_one / el_one / 1e12, 6), "ms_per_step": round(el_all / n_all * 1e3, 2),
+            "ms_per_step_1thread": round(el_one / n_one * 1e3, 2), "nproc": os.cpu_count(), "cpu_model": cpu_model(),
+            "sample": f"whole steps of {WORKLOAD} (float64 numpy oracle): {n_all} steps with {threads} BLAS threads "
+                      f"in {el_all:.1f} s, {n_one} steps with 1 thread in {el_one:.1f} s"}
 
 
 def block_flops(bc, n_kv):

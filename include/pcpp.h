@@ -16,8 +16,9 @@
  *     C = heads * head_dim; head a owns channels [a*head_dim, (a+1)*head_dim).
  *     Tokens of a band are ordered row by row (token = row * W + col).
  *   - Tensor pointers are DEVICE pointers owned by the caller.  The library
- *     never frees, retains or writes through an input pointer, and holds no
- *     global mutable state.
+ *     never frees, retains or writes through an input pointer.  Its only
+ *     state between calls is a per-device cache of the device's compute-unit
+ *     count (read once, then constant).
  *   - Neighbour buffers hold the WHOLE neighbouring band, [B, h*W, C], as
  *     received from that neighbour; only its boundary rows are read.  A
  *     missing neighbour (top or bottom band) or a zero row count allows NULL.
@@ -30,6 +31,17 @@
  *     launched and no output is touched.  No exception crosses the ABI.
  *   - Element types: PCPP_DTYPE_BF16 (bfloat16 storage, float32
  *     accumulation) or PCPP_DTYPE_F32 (float32 throughout).
+ *   - Work split across workgroups.  Some launches (the bf16 attention's key
+ *     ranges, the split-K GEMMs inside the block, module, ResNet and
+ *     convolution calls) split one tile's work over several workgroups and
+ *     merge the pieces through one XCD's L2 cache.  That relies on the gfx950
+ *     dispatcher dealing the workgroups of a launch round-robin over the
+ *     device's XCDs of 32 compute units (workgroup w on XCD w % n_xcd).  The
+ *     library splits only when the device's compute units are whole XCDs and
+ *     the stream has no CU mask (hipExtStreamGetCUMask reports every compute
+ *     unit); otherwise the same calls run unsplit, with the same results up
+ *     to the order of float32 additions.  Do not run these calls on a device
+ *     partitioned or masked in any way the CU mask does not show.
  */
 #ifndef PCPP_H
 #define PCPP_H
@@ -162,6 +174,20 @@ int pcpp_partial_attention(const pcpp_geom_t* g, const void* q,
                            void* stream);
 
 /*
+ * Launch plan of the bf16 partially conditioned attention (host only, no GPU
+ * work; for diagnostics and tests).  cus > 0: a device of `cus` compute
+ * units of which `cus_enabled` may run the launch (a stream's CU mask);
+ * cus == 0: the current device and the CU mask of `stream` (PCPP_EHIP if
+ * the device cannot be queried).  Outputs (any may be NULL): queries per
+ * block (a block is one workgroup's share of one image and head), pieces
+ * per block (key ranges merged through one XCD's L2; 1 = unsplit) and the
+ * launch's workgroups.  PCPP_ENOTSUP unless bf16 with head_dim 64.
+ */
+int pcpp_partial_attention_plan(const pcpp_geom_t* g, int32_t cus, int32_t cus_enabled,
+                                void* stream, int32_t* block_queries,
+                                int32_t* pieces, int32_t* workgroups);
+
+/*
  * Multi-hop partially conditioned attention: p may exceed 1, the context
  * reaching past the immediate neighbours (Sec. 6 hypothesises that many
  * bands need it), up to the whole image at p = n - 1.  The band attends to
@@ -218,8 +244,9 @@ typedef struct pcpp_block_weights {
 } pcpp_block_weights_t;
 
 /* Bytes of device workspace pcpp_transformer_block needs (0 if g invalid).
- * Same contract as the attention workspace: zero-filled before first use,
- * reusable afterwards without clearing. */
+ * The workspace needs no clearing: each call clears the work counters its
+ * launches use before the first of them, so the buffer may hold anything on
+ * entry (another call's scratch, say). */
 size_t pcpp_transformer_block_workspace_size(const pcpp_geom_t* g,
                                              const pcpp_block_weights_t* w,
                                              int32_t n_text, int32_t text_dim);
@@ -247,7 +274,7 @@ size_t pcpp_transformer_block_workspace_size(const pcpp_geom_t* g,
  * C <= 2048 and gn_groups <= 256 (PCPP_ENOTSUP), text_dim >= 32 with text_dim % 32 == 0,
  * n_text >= 1, ff_inner % 64 == 0, C % gn_groups == 0 (PCPP_EINVAL).  All
  * pointers, weights included, must be 16-byte aligned (PCPP_EINVAL).
- * The workspace follows the contract above (zero-filled before first use).
+ * The workspace needs no clearing (see pcpp_transformer_block_workspace_size).
  */
 int pcpp_transformer_block(const pcpp_geom_t* g, const pcpp_block_weights_t* w,
                            const void* x, const void* text, int32_t n_text,
@@ -317,8 +344,8 @@ typedef struct {
     int32_t gn_groups;                                  /* dividing C          */
 } pcpp_module_weights_t;
 
-/* Bytes of device workspace (0 if invalid), the same contract as
- * pcpp_transformer_block_workspace_size. It grows with the depth up to 16
+/* Bytes of device workspace (0 if invalid); no clearing needed, as for
+ * pcpp_transformer_block_workspace_size.  It grows with the depth up to 16
  * basic blocks: the text K/V of up to 16 blocks come from one product. */
 size_t pcpp_transformer_module_workspace_size(const pcpp_geom_t* g,
                                               const pcpp_module_weights_t* w,

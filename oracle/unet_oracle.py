@@ -293,9 +293,13 @@ def image_step(layers, n: int, p: float, groups: int, weights, prev, latents, te
     """One denoising step of the whole image under PCPP (Sec. 3.1-3.3): every
     band i runs unet_band_step with the stale data its neighbours exported
     at the previous step (Sec. 3.2: the step's exchange).  prev[j] is band
-    j's exports of that step, or None for every band before the first step
-    (nothing received: zero rows, zero K/V, statistics of count 0).  latents[i]
-    is band i's [B, h*W, 64] input.  Returns (outputs, exports), one per band.
+    j's exports of that step, or prev is None before the first step: then
+    nothing has been received and, as in Fig. 1 where no synchronous warm-up
+    step runs, the bands are computed separately: the attention takes no
+    stale rows (p = 0 for this step), the convolutions see zero rows beyond
+    the band (the zero padding of an image of its own) and the GroupNorms
+    the band's own statistics (the others have count 0).  latents[i] is band
+    i's [B, h*W, 64] input.  Returns (outputs, exports), one per band.
     Band i reads from band i-1 the last rows it exported (convolutions: its
     last input row; ResNets: its edge rows, of which the last is used; the
     attention: its K/V, of which the last r rows are used) and from band i+1
@@ -336,13 +340,12 @@ def image_step(layers, n: int, p: float, groups: int, weights, prev, latents, te
                 if sync_gn:
                     stale[name]["gn1_bands"], stale[name]["gn2_bands"] = gn_stack(0), gn_stack(1)
             elif kind == "module":
-                zkv = np.zeros((B, h * W, co))
                 st = []
                 for j in range(ly["depth"]):
-                    ku = (up["k"][j] if up else zkv) if i > 0 else None
-                    vu = (up["v"][j] if up else zkv) if i > 0 else None
-                    kd = (dn["k"][j] if dn else zkv) if i < n - 1 else None
-                    vd = (dn["v"][j] if dn else zkv) if i < n - 1 else None
+                    ku = up["k"][j] if up else None
+                    vu = up["v"][j] if up else None
+                    kd = dn["k"][j] if dn else None
+                    vd = dn["v"][j] if dn else None
                     st.append((ku, vu, kd, vd))
                 stale[name] = st
                 if sync_gn:
@@ -350,7 +353,8 @@ def image_step(layers, n: int, p: float, groups: int, weights, prev, latents, te
             else:
                 stale[name] = {"gn_bands": gn_stack(0) if sync_gn else None}
         ex = {}
-        outs.append(unet_band_step(layers, n, i, p, groups, weights, stale, latents[i], temb, text,
+        p_step = p if prev is not None else 0.0
+        outs.append(unet_band_step(layers, n, i, p_step, groups, weights, stale, latents[i], temb, text,
                                    sync_gn=sync_gn, exports=ex))
         exps.append(ex)
     return outs, exps

@@ -72,7 +72,6 @@ constexpr int SLOTS = 4;                    // LDS slots for K tiles, and for V 
 constexpr int V_REGION = SLOTS * TILE_BYTES;
 constexpr float P_LIMIT = 1048576.0f;       // 2^20: bound on a lane's probability sum per half-tile
 constexpr int MIN_TILES_PER_PIECE = 3;
-constexpr int CUS_PER_XCD = 32;             // gfx950
 
 constexpr int PIECES = TILE_BYTES / 1024 / NW;  // 1 KB pieces of a tile each wavefront stages
 static_assert(WG_PER_CU * 2 * V_REGION + 64 <= 160 * 1024, "the workgroups of a compute unit share its LDS");
@@ -550,20 +549,12 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
 }
 
 struct Plan {
-    int32_t n_xcd, bpx, k, grid, max_grid, n_tiles, nqb, n_blocks;
+    int32_t n_xcd, bpx, k, grid, n_tiles, nqb, n_blocks;
     size_t off_counters, off_o, off_ml, ws_bytes;
     bool fits;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
-
-int device_cus() {
-    int dev = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return 256;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-        return 256;
-    return cus;
-}
 
 // Pieces per block.  A launch runs in waves of max_grid workgroups (one per
 // compute unit); with k pieces per block it takes ceil(blocks * k / max_grid)
@@ -591,22 +582,20 @@ int64_t pick_k(int64_t slots, int64_t max_grid, int64_t n_tiles) {
 // counters: MAX_SPLIT_BLOCKS ints, always at offset 0, left zero by every
 // call][partial outputs: one per workgroup][partial row statistics: same].
 // The partial regions grow with the grid of a split launch; their contents
-// need no clearing.
-Plan make_plan(const AttnParams& p) {
+// need no clearing.  Pieces are merged only where the device layout says
+// that workgroup w runs on XCD w % n_xcd; otherwise every workgroup
+// computes whole blocks.
+Plan make_plan(const AttnParams& p, const DeviceLayout& d) {
     Plan pl;
-    const int cus = device_cus();
-    pl.max_grid = WG_PER_CU * cus;
+    const int64_t max_grid = (int64_t)WG_PER_CU * d.cus;
     pl.n_tiles = (p.kv.n_kv + KT - 1) / KT;
     pl.nqb = (p.nq + QB - 1) / QB;
     const int64_t n_blocks = (int64_t)p.batch * p.heads * pl.nqb;
     pl.n_blocks = (int32_t)(n_blocks < INT32_MAX ? n_blocks : INT32_MAX);
-    // Merging pieces needs the XCD layout of a gfx950 device (32 compute
-    // units per XCD); otherwise every workgroup computes whole blocks.
-    const bool xcd_known = cus % CUS_PER_XCD == 0;
-    pl.n_xcd = xcd_known ? cus / CUS_PER_XCD : 1;
+    pl.n_xcd = d.xcd_merge ? d.n_xcd : 1;
     const int64_t bpx = (n_blocks + pl.n_xcd - 1) / pl.n_xcd;
     int64_t k = 1;
-    if (xcd_known && n_blocks <= MAX_SPLIT_BLOCKS) k = pick_k(pl.n_xcd * bpx, pl.max_grid, pl.n_tiles);
+    if (d.xcd_merge && n_blocks <= MAX_SPLIT_BLOCKS) k = pick_k(pl.n_xcd * bpx, max_grid, pl.n_tiles);
     pl.k = (int32_t)k;
     pl.bpx = (int32_t)(bpx < INT32_MAX ? bpx : INT32_MAX);
     const int64_t grid = (int64_t)pl.n_xcd * bpx * k;
@@ -626,10 +615,15 @@ Plan make_plan(const AttnParams& p) {
 
 }  // namespace
 
-size_t attention_bf16_ws_bytes(const AttnParams& p) { return make_plan(p).ws_bytes; }
+size_t attention_bf16_ws_bytes(const AttnParams& p) { return make_plan(p, device_layout_unmasked()).ws_bytes; }
+
+AttnPlanInfo attention_bf16_plan(const AttnParams& p, const DeviceLayout& d) {
+    const Plan pl = make_plan(p, d);
+    return AttnPlanInfo{QB, pl.k, pl.grid, pl.k > 1 ? pl.n_blocks : 0};
+}
 
 hipError_t launch_attention_bf16(const AttnParams& p, void* ws, size_t ws_bytes, hipStream_t stream) {
-    const Plan pl = make_plan(p);
+    const Plan pl = make_plan(p, device_layout(stream));
     if (ws == nullptr || ws_bytes < pl.ws_bytes) return hipErrorInvalidValue;
     if (!pl.fits) return hipErrorInvalidValue;
     Sched sc;

@@ -235,8 +235,10 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
     __bf16* u16 = (__bf16*)(ws + L.u16);
     void* attn_ws = ws + L.attn_ws;
     void* split_ws = L.split_bytes ? ws + L.split : nullptr;
-    // Every plain GEMM may split K over the shared region (its counters are
-    // cleared by the GroupNorm statistics launch below).
+    // Every plain GEMM may split K over the shared region, and the attention
+    // launches merge key pieces through theirs: the GroupNorm statistics
+    // launch below clears both sets of counters, so the workspace needs no
+    // clearing between calls.
     auto gemm_s = [&](GemmParams mm) {
         mm.split_ws = split_ws;
         mm.split_ws_bytes = L.split_bytes;
@@ -267,6 +269,18 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
     gp.own_out = gn_own;
     gp.zero = (int*)split_ws;
     gp.n_zero = split_ws ? GEMM_SPLIT_COUNTERS : 0;
+    // The attention launches' work counters too: the workspace may hold
+    // anything on entry (a caller may share it with calls that use it as
+    // plain scratch), and every launch below leaves its counters at zero.
+    {
+        const DeviceLayout dl = device_layout(s);
+        const AttnParams sa = self_attn_params(g, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                               nullptr, nullptr);
+        const AttnParams ca = cross_attn_params(g, r, nullptr, nullptr, nullptr, nullptr, n_text);
+        const int n1 = attention_bf16_plan(sa, dl).counters, n2 = attention_bf16_plan(ca, dl).counters;
+        gp.zero2 = (int*)attn_ws;
+        gp.n_zero2 = n1 > n2 ? n1 : n2;
+    }
     PCPP_CHECK(launch_group_norm(gp, s));
     PCPP_CHECK(gemm_s(gemm(t16, C, false, mw.proj_in_w, mw.proj_in_b, rows, C, C, hid, C, true)));
 

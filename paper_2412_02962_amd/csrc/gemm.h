@@ -93,10 +93,13 @@ struct GroupNormParams {
     const __bf16* frame_up = nullptr;
     const __bf16* frame_dn = nullptr;
     __bf16* edges_out = nullptr;
-    // n_zero ints at zero (if not null) are cleared by the statistics launch:
-    // the split counters of the GEMMs that follow on the stream.
+    // n_zero ints at zero and n_zero2 ints at zero2 (if not null) are cleared
+    // by the statistics launch: the work counters of the split GEMMs and of
+    // the attention launches that follow on the stream.
     int* zero = nullptr;
     int32_t n_zero = 0;
+    int* zero2 = nullptr;
+    int32_t n_zero2 = 0;
 };
 size_t group_norm_ws_bytes(int B, int G, int N);
 // C % 8 == 0, C <= 2048, 1 <= G <= 256 divides C.

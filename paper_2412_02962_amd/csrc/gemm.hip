@@ -15,6 +15,7 @@
 
 #include "common.h"
 #include "gemm.h"
+#include "kernels.h"
 
 namespace pcpp {
 
@@ -651,23 +652,6 @@ bool gemm_shape_ok(const GemmParams& p) {
 
 namespace {
 
-constexpr int CUS_PER_XCD = 32;  // gfx950
-
-// Compute units of the current device, asked once per device (a benign race:
-// every thread that asks stores the same value).
-int cu_count() {
-    constexpr int kMaxDevices = 64;
-    static int cached[kMaxDevices] = {};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return 256;
-    if (dev >= 0 && dev < kMaxDevices && cached[dev] > 0) return cached[dev];
-    int cus = 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-        return 256;
-    if (dev >= 0 && dev < kMaxDevices) cached[dev] = cus;
-    return cus;
-}
-
 // Split of a convolution GEMM over 128 x 128 tiles: as many pieces per tile
 // as still fit one workgroup per compute unit, each at least 16 k-tiles
 // long, used only when the split launch fills at least 90% of the compute
@@ -678,13 +662,13 @@ struct SplitPlan {
     size_t bytes;
 };
 
-SplitPlan split_plan(int M, int N, int K) {
+SplitPlan split_plan(int M, int N, int K, const DeviceLayout& d) {
     SplitPlan sp{1, 1, 0, 0, 0};
-    const int cus = cu_count();
-    if (cus % CUS_PER_XCD != 0 || N % 128 != 0 || K % DBK != 0) return sp;
+    const int cus = d.cus;
+    if (!d.xcd_merge || N % 128 != 0 || K % DBK != 0) return sp;
     const int64_t tiles = (int64_t)((M + 127) / 128) * (N / 128);
     if (tiles < 1 || tiles > GEMM_SPLIT_COUNTERS) return sp;
-    const int n_xcd = cus / CUS_PER_XCD;
+    const int n_xcd = d.n_xcd;
     const int64_t tpx = (tiles + n_xcd - 1) / n_xcd;
     int64_t k = cus / (n_xcd * tpx);
     const int64_t k_max = (K / DBK) / 16;
@@ -709,13 +693,13 @@ SplitPlan split_plan(int M, int N, int K) {
 constexpr int kSplitTarget = 2;
 constexpr int kSplitMinTiles = 16;
 
-SplitPlan split_plan_plain(int M, int N, int K) {
+SplitPlan split_plan_plain(int M, int N, int K, const DeviceLayout& d) {
     SplitPlan sp{1, 1, 0, 0, 0};
-    const int cus = cu_count();
-    if (cus % CUS_PER_XCD != 0 || N % 64 != 0 || K % DBK != 0) return sp;
+    const int cus = d.cus;
+    if (!d.xcd_merge || N % 64 != 0 || K % DBK != 0) return sp;
     const int64_t tiles = (int64_t)((M + 63) / 64) * (N / 64);
     if (tiles < 1 || tiles >= cus || tiles > GEMM_SPLIT_COUNTERS) return sp;
-    const int n_xcd = cus / CUS_PER_XCD;
+    const int n_xcd = d.n_xcd;
     const int64_t tpx = (tiles + n_xcd - 1) / n_xcd;
     int64_t k = (int64_t)kSplitTarget * cus / (n_xcd * tpx);
     const int64_t k_max = (K / DBK) / kSplitMinTiles;
@@ -732,8 +716,11 @@ SplitPlan split_plan_plain(int M, int N, int K) {
 
 }  // namespace
 
+// Sized for a launch that may use every compute unit (a CU-masked stream
+// only ever needs less).
 size_t gemm_split_ws_bytes(int M, int N, int K, bool conv) {
-    return conv ? split_plan(M, N, K).bytes : split_plan_plain(M, N, K).bytes;
+    const DeviceLayout d = device_layout_unmasked();
+    return conv ? split_plan(M, N, K, d).bytes : split_plan_plain(M, N, K, d).bytes;
 }
 
 hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
@@ -749,8 +736,9 @@ hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
     }
     p.splitk = 1;
     p.tpx = 0;
+    const DeviceLayout dl = device_layout(s);
     if (p.conv_W > 0 && p.split_ws != nullptr) {
-        const SplitPlan sp = split_plan(p.M, p.N, p.K);
+        const SplitPlan sp = split_plan(p.M, p.N, p.K, dl);
         if (sp.splitk > 1 && p.split_ws_bytes >= sp.bytes && ((uintptr_t)p.split_ws & 15u) == 0) {
             p.splitk = sp.splitk;
             p.n_xcd = sp.n_xcd;
@@ -767,11 +755,10 @@ hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
     // 25.5 us, Q/K/V (3840) 16.4 -> 13.6 us; at ratios of 1 to 2.5 it
     // changed nothing measurable.
     auto map_xcd = [&](int bm, int bn_out) {
-        const int cus = cu_count();
         const int64_t w_rows = p.geglu ? 2 * (int64_t)p.N : p.N;
-        if (cus % CUS_PER_XCD != 0 || w_rows < 4 * (int64_t)p.M) return;
+        if (!dl.xcd_merge || w_rows < 4 * (int64_t)p.M) return;
         const int64_t tiles = (int64_t)((p.M + bm - 1) / bm) * (p.N / bn_out);
-        const int n_xcd = cus / CUS_PER_XCD;
+        const int n_xcd = dl.n_xcd;
         if (tiles < n_xcd || tiles > INT32_MAX / 2) return;
         p.n_xcd = n_xcd;
         p.tpx = (int)((tiles + n_xcd - 1) / n_xcd);
@@ -781,7 +768,7 @@ hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
     // that still gives about a workgroup per compute unit.
     if (!p.a_f32 && p.K % DBK == 0 && p.seg % 4 == 0) {
         if (!p.geglu && p.conv_W == 0 && p.split_ws != nullptr && p.N % 64 == 0) {
-            const SplitPlan sp = split_plan_plain(p.M, p.N, p.K);
+            const SplitPlan sp = split_plan_plain(p.M, p.N, p.K, dl);
             if (sp.splitk > 1 && p.split_ws_bytes >= sp.bytes && ((uintptr_t)p.split_ws & 15u) == 0) {
                 p.splitk = sp.splitk;
                 p.n_xcd = sp.n_xcd;
@@ -803,7 +790,7 @@ hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
             // tiles at three stages (48 KB of LDS: three workgroups per compute
             // unit), measured faster at M = 2048 for every N from 640 to 1920.
             const int64_t mt128 = (p.M + 127) / 128;
-            if (p.N % 128 == 0 && mt128 * (p.N / 128) >= 2 * (int64_t)cu_count()) {
+            if (p.N % 128 == 0 && mt128 * (p.N / 128) >= 2 * (int64_t)dl.cus) {
                 map_xcd(128, 128);
                 return launch_dma<128, 128, 3, false>(p, s);
             }

@@ -34,10 +34,32 @@ struct AttnParams {
     float scale;          // 1 / sqrt(head_dim)
 };
 
+// Where the workgroups of a launch run (device.hip).  n_xcd > 1 only when
+// workgroup w of a launch is known to run on XCD w % n_xcd: a device whose
+// compute units are whole XCDs (32 each) and a stream without a CU mask.
+// Only then may a launch merge the pieces of one tile through an XCD's L2.
+struct DeviceLayout {
+    int32_t cus;       // compute units of the device
+    int32_t n_xcd;     // XCDs the workgroups are dealt over, or 1
+    bool xcd_merge;    // pieces of a tile may be merged through one XCD's L2
+};
+DeviceLayout layout_for(int cus, int cus_enabled);  // pure: for planning and tests
+int device_cus();                                    // current device, cached per device; 0 if unknown
+DeviceLayout device_layout(hipStream_t stream);      // current device, the stream's CU mask
+DeviceLayout device_layout_unmasked();               // current device, every compute unit (workspace sizing)
+
 // bf16 path: workspace bytes it needs (work counters and float32 partial
-// results of query blocks split across workgroups) and the launch.
+// results of query blocks split across workgroups; sized for a launch that
+// may use every compute unit) and the launch.
 size_t attention_bf16_ws_bytes(const AttnParams& p);
 hipError_t launch_attention_bf16(const AttnParams& p, void* ws, size_t ws_bytes, hipStream_t stream);
+// Launch plan for a device layout: queries per block, pieces per block,
+// workgroups, and the work counters a launch uses (they must be zero at the
+// launch and are left zero).
+struct AttnPlanInfo {
+    int32_t block_queries, pieces, workgroups, counters;
+};
+AttnPlanInfo attention_bf16_plan(const AttnParams& p, const DeviceLayout& d);
 hipError_t launch_attention_f32(const AttnParams& p, hipStream_t stream);
 
 // Context assembly: contiguous segment copies plus the index set.

@@ -64,8 +64,12 @@ __global__ __launch_bounds__(GN_THREADS) void gn_stats(GroupNormParams p) {
     __shared__ float g_mean[GN_MAX_G];
     const int ch = blockIdx.x, b = blockIdx.y;
     const int tid = threadIdx.x;
-    if (ch == 0 && b == 0 && p.zero != nullptr)
-        for (int i = tid; i < p.n_zero; i += GN_THREADS) p.zero[i] = 0;
+    if (ch == 0 && b == 0) {
+        if (p.zero != nullptr)
+            for (int i = tid; i < p.n_zero; i += GN_THREADS) p.zero[i] = 0;
+        if (p.zero2 != nullptr)
+            for (int i = tid; i < p.n_zero2; i += GN_THREADS) p.zero2[i] = 0;
+    }
     const int C = p.C, G = p.G, cg = C / G, np = C / 2;
     const int t0 = ch * GN_CHUNK_TOKENS;
     const int nt = min(GN_CHUNK_TOKENS, p.N - t0);

@@ -197,6 +197,28 @@ PCPP_EXPORT size_t pcpp_partial_attention_workspace_size(const pcpp_geom_t* g) {
     return attention_bf16_ws_bytes(make_attn_params(g, r, nullptr, nullptr, kv));
 }
 
+PCPP_EXPORT int pcpp_partial_attention_plan(const pcpp_geom_t* g, int32_t cus, int32_t cus_enabled, void* stream,
+                                            int32_t* block_queries, int32_t* pieces, int32_t* workgroups) {
+    Geo r;
+    int st = validate_geom(g, &r);
+    if (st != PCPP_OK) return st;
+    if (g->dtype != PCPP_DTYPE_BF16 || g->head_dim != 64) return PCPP_ENOTSUP;
+    if (cus < 0 || (cus > 0 && cus_enabled < 0)) return PCPP_EINVAL;
+    DeviceLayout d;
+    if (cus > 0) {
+        d = layout_for(cus, cus_enabled);
+    } else {
+        d = device_layout((hipStream_t)stream);
+        if (device_cus() <= 0) return PCPP_EHIP;
+    }
+    KvSource kv = make_kv_source(g, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
+    const AttnPlanInfo pi = attention_bf16_plan(make_attn_params(g, r, nullptr, nullptr, kv), d);
+    if (block_queries) *block_queries = pi.block_queries;
+    if (pieces) *pieces = pi.pieces;
+    if (workgroups) *workgroups = pi.workgroups;
+    return PCPP_OK;
+}
+
 PCPP_EXPORT size_t pcpp_partial_attention_multihop_workspace_size(const pcpp_geom_t* g) {
     Geo r;
     if (validate_geom_hops(g, true, &r) != PCPP_OK) return 0;

@@ -15,8 +15,11 @@ What band i reads from band i-1 (from band i+1 the mirror image):
                   last r rows)
   GroupNorm       with synchronized statistics, every band's (count, mean,
                   M2) of the step before, stacked [n, B, G, 3]
-Before the first step nothing has been received: zero rows, zero K/V and
-statistics of count 0 (which the merge skips).
+Before the first step nothing has been received, and with no synchronous
+warm-up step the bands are computed separately (as in the paper's Fig. 1):
+the attention layers take no stale rows (p = 0 for that step), the
+convolutions read zero rows beyond the band and the GroupNorm statistics of
+the other bands have count 0 (the merge skips them).
 """
 
 from __future__ import annotations
@@ -96,6 +99,6 @@ class ImageStep:
             own = ({name: [s[i] for s in stacks] for name, stacks in self.stats[cur].items()}
                    if self.sync_gn else None)
             outs.append(net.forward(latents[i], temb, text, stale=self._stale(i, prev),
-                                    exports=self.exports[cur][i], gn_own=own))
+                                    exports=self.exports[cur][i], gn_own=own, separate=self.t == 0))
         self.t += 1
         return outs

@@ -132,6 +132,7 @@ def _load():
         "pcpp_context_rows": (ctypes.c_int, [gp, i32p, i32p, i32p, i32p]),
         "pcpp_gather_context": (ctypes.c_int, [gp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
         "pcpp_partial_attention_workspace_size": (sz, [gp]),
+        "pcpp_partial_attention_plan": (ctypes.c_int, [gp, i32, i32, vp, i32p, i32p, i32p]),
         "pcpp_partial_attention": (ctypes.c_int, [gp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "pcpp_transformer_block_workspace_size": (sz, [gp, wp, i32, i32]),
         "pcpp_transformer_block": (ctypes.c_int, [gp, wp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp,
@@ -172,7 +173,7 @@ def _load():
 _lib = _load()
 EXPORTED = (
     "pcpp_version", "pcpp_strerror", "pcpp_context_rows", "pcpp_gather_context",
-    "pcpp_partial_attention_workspace_size", "pcpp_partial_attention",
+    "pcpp_partial_attention_workspace_size", "pcpp_partial_attention", "pcpp_partial_attention_plan",
     "pcpp_transformer_block_workspace_size", "pcpp_transformer_block",
     "pcpp_boundary_bytes", "pcpp_pack_boundary", "pcpp_unpack_boundary", "pcpp_transformer_block_sync_gn",
     "pcpp_partial_attention_multihop_workspace_size", "pcpp_partial_attention_multihop",
@@ -239,6 +240,17 @@ def pcpp_gather_context(g, k_fresh, v_fresh, k_up, v_up, k_dn, v_dn, idx_out, k_
 
 def pcpp_partial_attention_workspace_size(g) -> int:
     return _lib.pcpp_partial_attention_workspace_size(ctypes.byref(g))
+
+
+def pcpp_partial_attention_plan(g, cus=0, cus_enabled=0, stream=None):
+    """(queries per block, pieces per block, workgroups) of the bf16 attention's
+    launch: on a device of `cus` compute units with `cus_enabled` usable, or
+    (cus = 0) on the current device with the CU mask of `stream`."""
+    bq, k, wg = (ctypes.c_int32() for _ in range(3))
+    st = _stream(stream) if cus == 0 else None
+    _check("pcpp_partial_attention_plan", _lib.pcpp_partial_attention_plan(
+        ctypes.byref(g), cus, cus_enabled, st, ctypes.byref(bq), ctypes.byref(k), ctypes.byref(wg)))
+    return bq.value, k.value, wg.value
 
 
 def pcpp_partial_attention(g, q, k_fresh, v_fresh, k_up, v_up, k_dn, v_dn, out, workspace=None,

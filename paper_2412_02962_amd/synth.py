@@ -138,8 +138,9 @@ def bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round to bfloat16 (round to nearest even via float32) and return the
     16-bit patterns as uint16.  NaN inputs are not expected here."""
     f = np.ascontiguousarray(x, dtype=np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    u = f.view(np.uint32)
+    # finite values stay below 2^32 after adding the rounding bias
+    u = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
     return u.astype(np.uint16)
 
 

@@ -53,8 +53,10 @@ class BandUNet:
                 wsb = pcpp.pcpp_resnet_block_workspace_size(g)
             elif ly["kind"] == "module":
                 g = pcpp.make_geom(H, W, n, i, sp.p, w["heads"], 64, B, 0, pcpp.PCPP_DTYPE_BF16)
+                # p = 0: the band's attention without stale rows (a band computed on its own)
+                g0 = pcpp.make_geom(H, W, n, i, 0.0, w["heads"], 64, B, 0, pcpp.PCPP_DTYPE_BF16)
                 mw, keep = pcpp.make_module_weights(w["module"], w["blocks"], w["ff_inner"], sp.groups)
-                plan.update(g=g, wts=mw, keep=keep,
+                plan.update(g=g, g0=g0, wts=mw, keep=keep,
                             out=torch.empty((B, h * W, co), dtype=torch.bfloat16, device=device))
                 wsb = pcpp.pcpp_transformer_module_workspace_size(g, mw, sp.n_text, sp.text_dim)
             else:
@@ -68,12 +70,12 @@ class BandUNet:
                     [own()] if ly["kind"] in ("module", "gn") else [])
             ws_max = max(ws_max, wsb)
             self.plans.append(plan)
-        # One workspace for all layers (the attention's counters start at zero
-        # and are left at zero).
-        self.ws = torch.zeros(ws_max, dtype=torch.uint8, device=device)
+        # One workspace for all layers: every call treats it as scratch (the
+        # module clears the work counters its launches use).
+        self.ws = torch.empty(ws_max, dtype=torch.uint8, device=device)
         self.ws_bytes = ws_max
 
-    def forward(self, latent, temb, text, stale=None, exports=None, gn_own=None):
+    def forward(self, latent, temb, text, stale=None, exports=None, gn_own=None, separate=False):
         """latent [B, h*W0, 64] (4 channels, zero-padded), temb [B, T], text
         [B, n_text, text_dim] (device bf16) -> the band's noise prediction
         [B, h*W0, 64] (channels 4.. are zero; the buffer is reused by the
@@ -82,7 +84,10 @@ class BandUNet:
         read at the next step: a convolution's first / last input rows
         ('first', 'last' [B, W, c_in]), a ResNet's 'edges1' / 'edges2', a
         module's per-block 'k' / 'v' lists.  gn_own replaces self.gn_own (the
-        band's own GroupNorm statistics, per layer a list)."""
+        band's own GroupNorm statistics, per layer a list).  separate: the
+        attention layers take no stale rows (p = 0), as for a band computed
+        on its own before anything has been exchanged; the modules' stale
+        K/V are then not read."""
         sp, ws, wsb = self.sp, self.ws, self.ws_bytes
         B = sp.batch
         stale = self.stale if stale is None else stale
@@ -114,12 +119,15 @@ class BandUNet:
                 pcpp.pcpp_resnet_block(plan["g"], plan["wts"], cur, temb, st["edges1_up"], st["edges1_dn"],
                                        st["edges2_up"], st["edges2_dn"], b1, o1, b2, o2, out, e1, e2, ws, wsb)
             elif ly["kind"] == "module":
-                cols = list(zip(*stale[name]))
-                ku, vu, kd, vd = [None if any(a is None for a in c) else list(c) for c in cols]
+                if separate:
+                    ku = vu = kd = vd = None
+                else:
+                    cols = list(zip(*stale[name]))
+                    ku, vu, kd, vd = [None if any(a is None for a in c) else list(c) for c in cols]
                 bands = stale[name + ":gn_bands"] if self.sync_gn else None
                 own = own_all[name][0] if self.sync_gn else None
                 ko, vo = (ex["k"], ex["v"]) if ex is not None else (None, None)
-                pcpp.pcpp_transformer_module(plan["g"], plan["wts"], cur, text, sp.n_text, sp.text_dim, ku, vu, kd,
+                pcpp.pcpp_transformer_module(plan["g0"] if separate else plan["g"], plan["wts"], cur, text, sp.n_text, sp.text_dim, ku, vu, kd,
                                              vd, bands, own, out, ko, vo, ws, wsb)
             else:
                 bands = stale[name]["gn_bands"] if self.sync_gn else None

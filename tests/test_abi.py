@@ -369,3 +369,27 @@ def test_conv3x3_geometry_and_validation():
     assert ex(A[0], A[1], A[2], A[3], None, A[4], A[5], A[5], A[7], 1 << 30) == pcpp.PCPP_EINVAL  # on each other
     assert ex(A[0], A[1], A[2], A[3], None, A[4], A[5] + 8, None, A[7], 1 << 30) == pcpp.PCPP_EINVAL  # misaligned
     assert ex(A[0], A[1], A[2], A[3], None, A[4], A[5], A[6], A[7], 16) == pcpp.PCPP_EWORKSPACE  # valid exports
+
+
+def test_attention_plan_splits_only_on_whole_unmasked_xcds():
+    """Key pieces are merged through one XCD's L2 only when workgroup w is
+    known to run on XCD w % n_xcd: compute units in whole XCDs of 32 and a
+    stream that may use all of them.  Otherwise the launch runs whole blocks
+    (one piece each, no merging)."""
+    from paper_2412_02962_amd import pcpp
+    g = pcpp.make_geom(128, 128, 8, 3, 0.25, 10)           # 2048 queries x 3072 keys, 10 heads
+    bq, k, wg = pcpp.pcpp_partial_attention_plan(g, 256, 256)
+    blocks = 10 * math.ceil(2048 / bq)
+    assert k > 1 and wg >= blocks * k                       # split: pieces of every block
+    for cus, enabled in ((256, 255), (256, 128), (256, 0), (80, 80), (250, 250), (33, 33)):
+        bq2, k2, wg2 = pcpp.pcpp_partial_attention_plan(g, cus, enabled)
+        assert (bq2, k2, wg2) == (bq, 1, blocks), (cus, enabled)
+    _, k4, _ = pcpp.pcpp_partial_attention_plan(g, 128, 128)  # a 4-XCD partition: still whole XCDs
+    assert k4 > 1
+    # one key tile per block cannot be split
+    small = pcpp.make_geom(16, 16, 4, 1, 0.25, 2)
+    assert pcpp.pcpp_partial_attention_plan(small, 256, 256)[1] == 1
+    with pytest.raises(pcpp.PcppError):
+        pcpp.pcpp_partial_attention_plan(g, -1, 0)
+    with pytest.raises(pcpp.PcppError):
+        pcpp.pcpp_partial_attention_plan(pcpp.make_geom(128, 128, 8, 3, 0.25, 10, dtype=pcpp.PCPP_DTYPE_F32), 256, 256)

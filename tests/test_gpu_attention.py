@@ -172,8 +172,11 @@ def test_largest_workload_sampled_rows():
                            seed_id=42)
     _say("3840px level-1, sampled")
     inp = synth.attention_inputs(cfg)
-    got = gu.to_f64(gu.run_attention(cfg, inp))
-    rows = np.sort(np.random.default_rng(5).choice(cfg.n_q, 96, replace=False))
+    out = gu.run_attention(cfg, inp)
+    assert bool(out.isfinite().all())
+    got = gu.to_f64(out)
+    # every workgroup block of queries: its first and last row and one more
+    rows = gu.block_rows(cfg.n_q, gu.attention_block_queries(cfg), np.random.default_rng(5))
     f = {k: oracle.as_f64(v, cfg.dtype) for k, v in inp.items()}
     want = oracle.partial_attention(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, f["q"][:, rows],
                                     f["k_fresh"], f["v_fresh"], f["k_up"], f["v_up"], f["k_dn"], f["v_dn"])
@@ -235,13 +238,14 @@ def test_paper_geometries(name):
     cfg = synth.PAPER_GEOMETRIES[name]
     _say("paper geometry", name)
     inp = synth.attention_inputs(cfg)
-    got = gu.to_f64(gu.run_attention(cfg, inp))
+    out = gu.run_attention(cfg, inp)
+    assert bool(out.isfinite().all())
+    got = gu.to_f64(out)
     f = {k: oracle.as_f64(v, cfg.dtype) for k, v in inp.items()}
     if cfg.n_q <= 1024:
         rows = np.arange(cfg.n_q)
-    else:
-        rows = np.sort(np.random.default_rng(6).choice(cfg.n_q, 128, replace=False))
-        rows[0], rows[-1] = 0, cfg.n_q - 1
+    else:  # every workgroup block of queries: first, last and two more rows
+        rows = gu.block_rows(cfg.n_q, gu.attention_block_queries(cfg), np.random.default_rng(6), extra=2)
     want = oracle.partial_attention(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, f["q"][:, rows],
                                     f["k_fresh"], f["v_fresh"], f["k_up"], f["v_up"], f["k_dn"], f["v_dn"])
     gu.assert_close(cfg, got[:, rows], want, name)
@@ -268,7 +272,8 @@ def test_workspace_reuse_with_multi_wave_launches():
         pcpp.pcpp_partial_attention(gu.geom(cfg), d["q"], d["k_fresh"], d["v_fresh"], d["k_up"], d["v_up"],
                                     d["k_dn"], d["v_dn"], out, ws, need)
         torch.cuda.synchronize()
-        rows = np.sort(rows_rng.choice(cfg.n_q, min(cfg.n_q, 96), replace=False))
+        assert bool(out.isfinite().all())
+        rows = gu.block_rows(cfg.n_q, gu.attention_block_queries(cfg), rows_rng)
         f = {k: oracle.as_f64(v, cfg.dtype) for k, v in inp.items()}
         want = oracle.partial_attention(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, f["q"][:, rows],
                                         f["k_fresh"], f["v_fresh"], f["k_up"], f["v_up"], f["k_dn"], f["v_dn"])
@@ -323,3 +328,56 @@ def test_multihop_equals_neighbour_form_for_p_up_to_one():
                                          d["k_dn"][:, :dn * W].contiguous(), d["v_dn"][:, :dn * W].contiguous(), out, ws, wsb)
     torch.cuda.synchronize()
     assert torch.equal(out, ref)
+
+
+def test_plan_splits_on_the_default_stream():
+    """The CU-mask query works on this device: an unmasked stream gets the
+    split plan the bench workload needs (pieces merged per XCD)."""
+    from paper_2412_02962_amd import pcpp
+    cfg = synth.ATTN_CONFIGS["sdxl2048_l1_p25"]
+    _say("plan on the default stream")
+    bq, k, wg = pcpp.pcpp_partial_attention_plan(gu.geom(cfg))
+    cus = torch_cus()
+    assert (bq, k, wg) == pcpp.pcpp_partial_attention_plan(gu.geom(cfg), cus, cus)
+    assert k > 1
+
+
+def torch_cus():
+    import torch
+    return torch.cuda.get_device_properties(0).multi_processor_count
+
+
+def _masked_stream(n_enabled):
+    """A HIP stream restricted to the first n_enabled compute units."""
+    import ctypes
+
+    import torch
+    hip = ctypes.CDLL("libamdhip64.so")
+    words = (torch_cus() + 31) // 32
+    mask = (ctypes.c_uint32 * words)()
+    for c in range(n_enabled):
+        mask[c // 32] |= 1 << (c % 32)
+    s = ctypes.c_void_p()
+    assert hip.hipExtStreamCreateWithCUMask(ctypes.byref(s), ctypes.c_uint32(words), mask) == 0
+    return hip, s
+
+
+@pytest.mark.parametrize("name", ["sdxl2048_l1_p25", "sdxl2048_l2_edge"])
+def test_attention_on_a_cu_masked_stream_runs_unsplit(name):
+    """On a stream with a CU mask the dispatch of workgroups to XCDs is not
+    known: the launch computes whole blocks (no merge through an L2) and
+    still matches the oracle."""
+    import torch
+    from paper_2412_02962_amd import pcpp
+    cfg = synth.ATTN_CONFIGS[name]
+    _say("CU-masked stream", name)
+    hip, s = _masked_stream(torch_cus() // 2)
+    try:
+        assert pcpp.pcpp_partial_attention_plan(gu.geom(cfg), stream=s.value)[1] == 1
+        inp = synth.attention_inputs(cfg)
+        out = gu.run_attention(cfg, inp, stream=s.value)
+        assert hip.hipStreamSynchronize(s) == 0
+        gu.assert_close(cfg, gu.to_f64(out), gu.oracle_attention(cfg, inp), f"masked {name}")
+        torch.cuda.synchronize()
+    finally:
+        hip.hipStreamDestroy(s)

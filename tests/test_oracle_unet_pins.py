@@ -433,3 +433,37 @@ def test_u8_image_steps_reach_the_whole_image_unet():
     assert np.allclose(cur, want, rtol=1e-9, atol=1e-9)
     first, _ = uo.image_step(layers, sp.n, sp.p, sp.groups, fw, None, latents, f(temb), f(text), sync_gn=True)
     assert not np.allclose(np.concatenate(first, axis=1), want, atol=1e-3)  # the stale data matter
+
+
+def test_u9_first_image_step_computes_each_band_as_an_image_of_its_own():
+    """Before the first exchange nothing has been received.  Without
+    synchronous warm-up steps the bands are then computed separately (the
+    setting of Fig. 1): the first image step of band i equals the whole
+    U-Net, composed here from torch operators, run on that band alone as an
+    image of h rows (no stale rows in any attention, zero padding around the
+    band in every convolution, the band's own GroupNorm statistics)."""
+    import dataclasses
+    from paper_2412_02962_amd import synth
+    sp = dataclasses.replace(synth.UNET_TINY, n=2, i=0, H0=16, W0=8, p=0.5)
+    layers = synth.unet_layers(sp)
+    weights, _, latent, temb, text = synth.unet_band_inputs(dataclasses.replace(sp, n=1))
+    f = lambda a: None if a is None else oracle.from_bf16_bits(a)
+    fw = {}
+    for ly in layers:
+        w = weights[ly["name"]]
+        if ly["kind"] == "module":
+            fw[ly["name"]] = {"module": {k: f(v) for k, v in w["module"].items()},
+                              "blocks": [{k: f(v) for k, v in b.items()} for b in w["blocks"]], "heads": w["heads"]}
+        else:
+            fw[ly["name"]] = {k: f(v) for k, v in w.items()}
+    lat = f(latent)
+    h0 = sp.H0 // sp.n
+    tok = h0 * sp.W0
+    latents = [lat[:, i * tok:(i + 1) * tok] for i in range(sp.n)]
+    band_layers = synth.unet_layers(dataclasses.replace(sp, H0=h0, n=1))
+    for sync_gn in (False, True):
+        outs, _ = uo.image_step(layers, sp.n, sp.p, sp.groups, fw, None, latents, f(temb), f(text), sync_gn=sync_gn)
+        for i in range(sp.n):
+            want = _torch_unet(band_layers, weights, latent[:, i * tok:(i + 1) * tok], temb, text, h0, sp.W0,
+                               sp.groups, sp.p)
+            assert np.allclose(outs[i], want, rtol=1e-9, atol=1e-9), (sync_gn, i)
