@@ -318,8 +318,9 @@ def test_level2_module_on_a_garbage_workspace():
     dv = lambda a: None if a is None else gu.to_dev(a, "bf16")
     g = pcpp.make_geom(cfg.H, cfg.W, cfg.n, cfg.i, cfg.p, cfg.heads, cfg.d, 1, 0, pcpp.PCPP_DTYPE_BF16)
     assert pcpp.pcpp_partial_attention_plan(g)[1] > 1           # the merge path is exercised
-    w, keep = pcpp.make_module_weights({k: dv(v) for k, v in module.items()},
-                                       [{k: dv(v) for k, v in b.items()} for b in blocks], bc.ff_inner, bc.gn_groups)
+    md = {k: dv(v) for k, v in module.items()}               # device weights, alive for the whole test
+    bd = [{k: dv(v) for k, v in b.items()} for b in blocks]
+    w, keep = pcpp.make_module_weights(md, bd, bc.ff_inner, bc.gn_groups)
     xd, td = dv(x), dv(text)
     cols = list(zip(*[[dv(a) for a in s_] for s_ in stale]))
     lists = [None if any(a is None for a in c) else list(c) for c in cols]
@@ -337,7 +338,7 @@ def test_level2_module_on_a_garbage_workspace():
     assert torch.equal(outs[0][0], outs[1][0])
     want_y, want_k, want_v = _oracle_module(bc, x, text, module, blocks, stale)
     _check_module(bc, depth, *outs[0], want_y, want_k, want_v)
-    del keep
+    del keep, md, bd
 
 
 def test_module_bound_rejects_a_planted_mistake():
