@@ -94,6 +94,20 @@ __device__ __forceinline__ void dma16(const void* g, const char* lds) {
     asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(a) : "memory");
 }
 
+// The same with a wave-uniform 64-bit base in SGPRs and a 32-bit per-lane
+// byte offset (the load's saddr form): no per-lane address arithmetic.
+// lds is the wave-uniform LDS byte address.
+__device__ __forceinline__ void dma16_s(uint64_t base, uint32_t voff, uint32_t lds) {
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "{m0}"(lds) : "memory");
+}
+
+// A wave-uniform value known to the compiler as such (kept in SGPRs).
+__device__ __forceinline__ uint64_t uniform64(uint64_t x) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+
 // LDS swizzles: 16-byte chunk c of tile row r is stored at slot c ^ mask(r).
 // K rows are read 16 bytes per lane by 32 consecutive rows at one chunk; V
 // rows by four rows x 32 bytes per 16 lanes (transposing read).  Both masks
@@ -164,7 +178,7 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
     const int col = lane & 31;
     const int half = lane >> 5;
     const int C = p.C;
@@ -245,11 +259,35 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
         const int64_t va1 = (int64_t)(uintptr_t)p.kv.v[1] + o1 * 2;
         const int64_t va2 = (int64_t)(uintptr_t)p.kv.v[2] + o2 * 2;
 
+        // Sources whose boundaries fall on tile boundaries (the usual case:
+        // W * rows a multiple of 64) take every tile from one source, picked
+        // by comparing the tile index with two precomputed tile numbers and
+        // addressed with scalar arithmetic only.
+        const bool aligned = end0 % KT == 0 && end1 % KT == 0 && kv_end % KT == 0;
+        const int tb0 = end0 / KT, tb1 = end1 / KT;
+        const uint32_t tile_g = (uint32_t)(KT * C * 2);  // bytes between consecutive tiles of a source (C <= 2^20 / 64)
+        const uint64_t sk0 = uniform64((uint64_t)ka0), sk1 = uniform64((uint64_t)ka1), sk2 = uniform64((uint64_t)ka2);
+        const uint64_t sv0 = uniform64((uint64_t)va0), sv1 = uniform64((uint64_t)va1), sv2 = uniform64((uint64_t)va2);
+        // LDS byte addresses of the slots' parts this wavefront stages.
+        auto lds_of = [&](const char* slot) {
+            return (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lptr_t)slot) +
+                   (uint32_t)(PIECES * wave * 1024);
+        };
+
         // Stage tile t of K (is_v = false) or V into the slot at dst.
         auto issue = [&](int t_in, char* slot, bool is_v) {
             const int t = __builtin_amdgcn_readfirstlane(t_in);
             char* dst = slot + PIECES * wave * 1024;
             const uint32_t* off = is_v ? ld_voff : ld_koff;
+            if (aligned) {
+                const uint64_t a0 = is_v ? sv0 : sk0, a1 = is_v ? sv1 : sk1, a2 = is_v ? sv2 : sk2;
+                const uint64_t src = t < tb0 ? a0 : (t < tb1 ? a1 : a2);
+                const uint64_t base = src + (uint64_t)(uint32_t)t * tile_g;
+                const uint32_t lds = lds_of(slot);
+#pragma unroll
+                for (int i = 0; i < PIECES; ++i) dma16_s(base, off[i], lds + i * 1024);
+                return;
+            }
             const int j0 = t * KT, j1 = j0 + KT;
             const bool one_src = j1 <= kv_end && (j1 <= end0 || j0 >= end0) && (j1 <= end1 || j0 >= end1);
             if (one_src) {
@@ -334,7 +372,6 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
         auto step = [&](int h, f32x16& s_cur, f32x16& s_nxt, bf16x8 (&p_prev)[2], bf16x8 (&p_cur)[2],
                         Operands& op_cur, Operands& op_nxt, const char* nk, int nk_half, const char* nv, int nv_half) {
             SCHED_FENCE();
-            read_step(nk, nk_half, nv, nv_half, op_nxt);
             float acc0 = 0.f, acc1 = 0.f;
             float mneg = -m_run;
             // probabilities of elements 2i, 2i+1 and their bf16 sum
@@ -363,6 +400,16 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
                     s_nxt = mfma32x32x16(op_cur.k[kk], qop[kk], kk == 0 ? f32x16{} : s_nxt);
                 }
                 SCHED_FENCE();
+                // The operand that product i of the next step uses, read a
+                // whole step ahead; one or two LDS reads per product keep
+                // the LDS queue from filling up.
+                if ((i & 1) == 0) {
+                    const int nst = i >> 2, nmb = (i >> 1) & 1;
+                    op_nxt.v[nmb][nst] = read_vt(nv + nv_half * (TILE_BYTES / 2) + v_rel[nmb] + nst * 2048);
+                } else {
+                    const int nkk = i >> 1;
+                    op_nxt.k[nkk] = *(const bf16x8*)(nk + nk_half * (TILE_BYTES / 2) + k_rel[nkk]);
+                }
                 if (i < 6) pair(i + 2);
                 SCHED_FENCE();
             }
