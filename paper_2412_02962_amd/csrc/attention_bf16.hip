@@ -7,25 +7,30 @@
 // lies inside one source is fetched from that source's base; a tile that
 // straddles two sources (or the end) picks the source row by row.
 //
-// Work decomposition.  A block is 256 queries of one (image, head); its key
+// Work decomposition.  A block is 128 queries of one (image, head); its key
 // tiles are cut into k equal pieces and a workgroup computes one piece of one
-// block.  One workgroup fits a compute unit, so a launch runs in waves of as
-// many workgroups as there are compute units; k is chosen by a cost estimate
-// (waves x (tiles per piece + a fixed cost per piece)): at the 2048 px
-// level-1 shape k = 3 fills one wave, larger shapes take several waves of
-// smaller pieces instead of a ragged last wave of whole blocks.  The blocks are dealt out to the XCDs in contiguous ranges
-// and all pieces of a block run on one XCD: workgroup w runs on XCD w % n_xcd
-// (the hardware deals workgroups out round-robin), so the pieces of a block
-// are merged through that XCD's L2 with ordinary stores and one counter per
-// block (the last piece to arrive merges and resets the counter to zero).
-// Pieces of the blocks of one head start on the same key tiles, so their
-// tiles are fetched from HBM once and then hit in the L2.
+// block.  Two workgroups share a compute unit (two wavefronts per SIMD, from
+// different workgroups, so that their tile barriers are independent), so a
+// launch runs in waves of twice as many workgroups as there are compute
+// units; k is chosen by a cost estimate (waves x (tiles per piece + a fixed
+// cost per piece)): at the 2048 px level-1 shape k = 3 (480 workgroups, one
+// wave); larger shapes take several waves of smaller pieces instead of a
+// ragged last wave of whole blocks.  The blocks are dealt out to the XCDs in
+// contiguous ranges and all pieces of a block run on one XCD: workgroup w
+// runs on XCD w % n_xcd (the hardware deals workgroups out round-robin), so
+// the pieces of a block are merged through that XCD's L2 with ordinary
+// stores and one counter per block (the last piece to arrive merges and
+// resets the counter to zero).  Pieces of the blocks of one head start on
+// the same key tiles, so their tiles are fetched from HBM once and then hit
+// in the L2.
 //
-// Inside a workgroup the eight wavefronts (two per SIMD) own 32 queries each
+// Inside a workgroup the four wavefronts (one per SIMD) own 32 queries each
 // and walk the same key tiles, staged once per workgroup in LDS by direct
 // global->LDS loads into four K and four V slots (tile t+3's keys and tile
-// t+2's values load while tile t is computed; one barrier per tile, which
-// keeps the two wavefronts of a SIMD in step).
+// t+2's values load while tile t is computed; one barrier per tile).  Tiles
+// that lie inside one key source (the usual case) are addressed with scalar
+// arithmetic only: a wave-uniform 64-bit base and the per-lane offsets of
+// the load's saddr form.
 
 // Software pipeline over 32-key half-tiles h.  Step h holds S(h) (scores of
 // half h) and P(h-1) (bf16 probabilities of half h-1) in registers and
@@ -60,13 +65,10 @@ namespace {
 constexpr int D = 64;
 constexpr int KT = 64;                      // keys per tile
 constexpr int QW = 32;                      // queries per wavefront
-#ifndef PCPP_ATTN_WAVES
-#define PCPP_ATTN_WAVES 8
-#endif
-constexpr int NW = PCPP_ATTN_WAVES;         // wavefronts per workgroup
+constexpr int NW = 4;                       // wavefronts per workgroup (one per SIMD)
 constexpr int QB = QW * NW;                 // queries per block
 constexpr int NTHREADS = 64 * NW;
-constexpr int WG_PER_CU = 8 / NW;           // two wavefronts per SIMD
+constexpr int WG_PER_CU = 8 / NW;           // two workgroups per compute unit: two wavefronts per SIMD
 constexpr int TILE_BYTES = KT * D * 2;      // 8 KB of K or of V
 constexpr int SLOTS = 4;                    // LDS slots for K tiles, and for V tiles
 constexpr int V_REGION = SLOTS * TILE_BYTES;
@@ -447,8 +449,8 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
         // kn, V(pt) in vc; K(pt+3) and V(pt+2) are staged into kl and vl, so
         // every tile has two periods to arrive.
         auto period = [&](int pt, char* kc, char* kn, char* kl, char* vc, char* vl) {
-            // Two wavefronts share each SIMD and the barrier waits for the
-            // slower one; issue favours the older wavefront at equal
+            // Two wavefronts (one of each workgroup on the compute unit)
+            // share each SIMD; issue favours the older one at equal
             // priority.  Raising the priority for the first half-tile and
             // dropping it for the second lets the one behind catch up.
             __builtin_amdgcn_s_setprio(1);
