@@ -188,6 +188,31 @@ int pcpp_partial_attention_plan(const pcpp_geom_t* g, int32_t cus, int32_t cus_e
                                 int32_t* pieces, int32_t* workgroups);
 
 /*
+ * pcpp_partial_attention for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same computation and arguments without the workspace.
+ * The library keeps, on each GPU it runs on, one device array of
+ * PCPP_NOALLOC_SCRATCH_BYTES for this entry point's workspace, held until
+ * the process ends; the first call on a device looks up its address and
+ * clears it (a fill kernel on `stream`).  Nothing is allocated by any call.
+ *   - Geometries whose workspace (pcpp_partial_attention_workspace_size)
+ *     exceeds PCPP_NOALLOC_SCRATCH_BYTES fail with PCPP_EWORKSPACE before
+ *     anything is launched; use pcpp_partial_attention with a caller
+ *     workspace for them.
+ *   - Every call on one GPU shares that GPU's array: calls that overlap on
+ *     one GPU (different streams, different host threads) race and must be
+ *     ordered by the caller.  Calls in one stream, graph replays included,
+ *     are fine: each leaves the array ready for the next.
+ * Other arguments, requirements and errors as pcpp_partial_attention.
+ */
+#define PCPP_NOALLOC_SCRATCH_BYTES (32u * 1024u * 1024u)
+int pcpp_partial_attention_noalloc(const pcpp_geom_t* g, const void* q,
+                                   const void* k_fresh, const void* v_fresh,
+                                   const void* k_up, const void* v_up,
+                                   const void* k_dn, const void* v_dn,
+                                   void* out, void* stream);
+
+/*
  * Multi-hop partially conditioned attention: p may exceed 1, the context
  * reaching past the immediate neighbours (Sec. 6 hypothesises that many
  * bands need it), up to the whole image at p = n - 1.  The band attends to

@@ -25,5 +25,9 @@ KvSource make_kv_source(const pcpp_geom_t* g, const Geo& r, const void* k_fresh,
                         const void* k_up, const void* v_up, const void* k_dn, const void* v_dn);
 AttnParams make_attn_params(const pcpp_geom_t* g, const Geo& r, const void* q, void* out,
                             const KvSource& kv);
+// Argument checks of pcpp_partial_attention (geometry, dtype, head_dim,
+// pointers, 16-byte alignment); PCPP_OK or the status to return.
+int check_attention(const pcpp_geom_t* g, Geo* r, const void* q, const void* k_fresh, const void* v_fresh,
+                    const void* k_up, const void* v_up, const void* k_dn, const void* v_dn, const void* out);
 
 }  // namespace pcpp

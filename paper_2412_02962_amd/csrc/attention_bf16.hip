@@ -666,6 +666,8 @@ Plan make_plan(const AttnParams& p, const DeviceLayout& d) {
 
 size_t attention_bf16_ws_bytes(const AttnParams& p) { return make_plan(p, device_layout_unmasked()).ws_bytes; }
 
+size_t attention_bf16_counter_bytes() { return align256((size_t)MAX_SPLIT_BLOCKS * sizeof(int)); }
+
 AttnPlanInfo attention_bf16_plan(const AttnParams& p, const DeviceLayout& d) {
     const Plan pl = make_plan(p, d);
     return AttnPlanInfo{QB, pl.k, pl.grid, pl.k > 1 ? pl.n_blocks : 0};

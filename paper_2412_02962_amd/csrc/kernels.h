@@ -52,6 +52,9 @@ DeviceLayout device_layout_unmasked();               // current device, every co
 // results of query blocks split across workgroups; sized for a launch that
 // may use every compute unit) and the launch.
 size_t attention_bf16_ws_bytes(const AttnParams& p);
+// Bytes at the start of every bf16 attention workspace that hold its work
+// counters (the same for every geometry).
+size_t attention_bf16_counter_bytes();
 hipError_t launch_attention_bf16(const AttnParams& p, void* ws, size_t ws_bytes, hipStream_t stream);
 // Launch plan for a device layout: queries per block, pieces per block,
 // workgroups, and the work counters a launch uses (they must be zero at the

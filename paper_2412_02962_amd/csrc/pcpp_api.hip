@@ -98,8 +98,8 @@ KvSource make_kv_source_compact(const pcpp_geom_t* g, const Geo& r, const void* 
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-// Shared argument checks of the attention entry point.
-static int check_attention(const pcpp_geom_t* g, Geo* r, const void* q, const void* k_fresh,
+// Shared argument checks of the attention entry points.
+int check_attention(const pcpp_geom_t* g, Geo* r, const void* q, const void* k_fresh,
                            const void* v_fresh, const void* k_up, const void* v_up, const void* k_dn,
                            const void* v_dn, const void* out) {
     int st = validate_geom(g, r);

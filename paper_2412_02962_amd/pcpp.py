@@ -133,6 +133,7 @@ def _load():
         "pcpp_gather_context": (ctypes.c_int, [gp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
         "pcpp_partial_attention_workspace_size": (sz, [gp]),
         "pcpp_partial_attention_plan": (ctypes.c_int, [gp, i32, i32, vp, i32p, i32p, i32p]),
+        "pcpp_partial_attention_noalloc": (ctypes.c_int, [gp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
         "pcpp_partial_attention": (ctypes.c_int, [gp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "pcpp_transformer_block_workspace_size": (sz, [gp, wp, i32, i32]),
         "pcpp_transformer_block": (ctypes.c_int, [gp, wp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp,
@@ -174,6 +175,7 @@ _lib = _load()
 EXPORTED = (
     "pcpp_version", "pcpp_strerror", "pcpp_context_rows", "pcpp_gather_context",
     "pcpp_partial_attention_workspace_size", "pcpp_partial_attention", "pcpp_partial_attention_plan",
+    "pcpp_partial_attention_noalloc",
     "pcpp_transformer_block_workspace_size", "pcpp_transformer_block",
     "pcpp_boundary_bytes", "pcpp_pack_boundary", "pcpp_unpack_boundary", "pcpp_transformer_block_sync_gn",
     "pcpp_partial_attention_multihop_workspace_size", "pcpp_partial_attention_multihop",
@@ -258,6 +260,15 @@ def pcpp_partial_attention(g, q, k_fresh, v_fresh, k_up, v_up, k_dn, v_dn, out, 
     _check("pcpp_partial_attention", _lib.pcpp_partial_attention(
         ctypes.byref(g), _ptr(q), _ptr(k_fresh), _ptr(v_fresh), _ptr(k_up), _ptr(v_up), _ptr(k_dn),
         _ptr(v_dn), _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+PCPP_NOALLOC_SCRATCH_BYTES = 32 * 1024 * 1024
+
+
+def pcpp_partial_attention_noalloc(g, q, k_fresh, v_fresh, k_up, v_up, k_dn, v_dn, out, stream=None):
+    _check("pcpp_partial_attention_noalloc", _lib.pcpp_partial_attention_noalloc(
+        ctypes.byref(g), _ptr(q), _ptr(k_fresh), _ptr(v_fresh), _ptr(k_up), _ptr(v_up), _ptr(k_dn),
+        _ptr(v_dn), _ptr(out), _stream(stream)))
 
 
 def make_block_weights(tensors: dict, ff_inner: int, gn_groups: int) -> pcpp_block_weights_t:

@@ -393,3 +393,25 @@ def test_attention_plan_splits_only_on_whole_unmasked_xcds():
         pcpp.pcpp_partial_attention_plan(g, -1, 0)
     with pytest.raises(pcpp.PcppError):
         pcpp.pcpp_partial_attention_plan(pcpp.make_geom(128, 128, 8, 3, 0.25, 10, dtype=pcpp.PCPP_DTYPE_F32), 256, 256)
+
+
+def test_noalloc_attention_validates_before_any_gpu_work():
+    """The allocation-free entry point checks its arguments like
+    pcpp_partial_attention, and refuses geometries whose workspace exceeds
+    its fixed device array, before touching the device."""
+    from paper_2412_02962_amd import pcpp
+    lib = pcpp.lib()
+    fake = 1 << 40  # never dereferenced: every call below fails validation first
+    g = pcpp.make_geom(128, 128, 8, 3, 0.25, 10)
+    args = [fake] * 8
+    assert lib.pcpp_partial_attention_noalloc(ctypes.byref(g), None, *args[1:], None) == pcpp.PCPP_EINVAL
+    bad = pcpp.make_geom(128, 128, 8, 3, 1.5, 10)
+    assert lib.pcpp_partial_attention_noalloc(ctypes.byref(bad), *args, None) == pcpp.PCPP_EINVAL
+    d32 = pcpp.make_geom(128, 128, 8, 3, 0.25, 10, head_dim=32)
+    assert lib.pcpp_partial_attention_noalloc(ctypes.byref(d32), *args, None) == pcpp.PCPP_ENOTSUP
+    # 3840 px level 1, 2 bands: a workspace far above the fixed array
+    big = pcpp.make_geom(240, 240, 2, 0, 0.3, 10)
+    assert pcpp.pcpp_partial_attention_workspace_size(big) > pcpp.PCPP_NOALLOC_SCRATCH_BYTES
+    assert lib.pcpp_partial_attention_noalloc(ctypes.byref(big), *args, None) == pcpp.PCPP_EWORKSPACE
+    # the bench workload fits
+    assert pcpp.pcpp_partial_attention_workspace_size(g) <= pcpp.PCPP_NOALLOC_SCRATCH_BYTES
