@@ -42,6 +42,7 @@ def attn_bytes(cfg, n_kv):
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_bf16_sdxl2048_l1_p25_traffic.txt")
 CALIB_BYTES = 256 << 20      # plain device-to-device copy used to scale the memory counters
+MEM_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "memory_kernels_sdxl2048_traffic.txt")
 
 
 def kernel_source_hash():
@@ -356,6 +357,22 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
     out["pack_flushed_GBps"] = round(2 * 2 * nb / us / 1e3, 1)
     del flush
 
+    # GroupNorm of the block's input alone (pcpp_group_norm: the statistics
+    # kernel reads x, the apply kernel reads x and writes y; 2048 tokens x 640
+    # channels, 32 groups): algorithmic bytes 3 x 2.6 MB.
+    gx = torch.randn(1, cfg.n_q, cfg.C, device=dev).to(torch.bfloat16)
+    gy = torch.empty_like(gx)
+    gam = torch.ones(cfg.C, dtype=torch.bfloat16, device=dev)
+    bet = torch.zeros(cfg.C, dtype=torch.bfloat16, device=dev)
+    gws = pcpp.pcpp_group_norm_workspace_size(1, cfg.n_q, cfg.C, 32)
+    gwsb = torch.empty(gws, dtype=torch.uint8, device=dev)
+    us = graph_time_us(torch, lambda: pcpp.pcpp_group_norm(1, cfg.n_q, cfg.C, 32, 1e-6, 0, gx, gam, bet, gy, gwsb,
+                                                           gws), reps, use_graph)
+    gbytes = 3 * cfg.n_q * cfg.C * 2
+    out["group_norm_us"] = round(us, 3)
+    out["group_norm_GBps"] = round(gbytes / us / 1e3, 1)
+    out["group_norm_frac_hbm"] = round(gbytes / us / 1e3 / PEAK_HBM_GBS, 4)
+
     c50 = synth.ATTN_CONFIGS["sdxl2048_l1_p50"]
     d50 = {k: to_dev(v) for k, v in synth.attention_inputs(c50).items()}
     g50 = pcpp.make_geom(c50.H, c50.W, c50.n, c50.i, c50.p, c50.heads, c50.d, 1, 0, pcpp.PCPP_DTYPE_BF16)
@@ -603,6 +620,25 @@ def pmc_run(args):
         pcpp.pcpp_partial_attention(g, d["q"], d["k_fresh"], d["v_fresh"], d["k_up"], d["v_up"], d["k_dn"],
                                     d["v_dn"], out, ws, wsb, None)
     torch.cuda.synchronize()
+    # the memory-bound kernels: the materialised gather of the same band, a
+    # GroupNorm of the block's input shape, and whole blocks (their GroupNorm
+    # and LayerNorm kernels)
+    _, _, _, n_kv = pcpp.pcpp_context_rows(g)
+    idx = torch.empty(n_kv, dtype=torch.int32, device=dev)
+    kc = torch.empty((1, n_kv, cfg.C), dtype=torch.bfloat16, device=dev)
+    vc = torch.empty_like(kc)
+    gx = torch.randn(1, cfg.n_q, cfg.C, device=dev).to(torch.bfloat16)
+    gy = torch.empty_like(gx)
+    gam = torch.ones(cfg.C, dtype=torch.bfloat16, device=dev)
+    bet = torch.zeros(cfg.C, dtype=torch.bfloat16, device=dev)
+    gws = pcpp.pcpp_group_norm_workspace_size(1, cfg.n_q, cfg.C, 32)
+    gwsb = torch.empty(gws, dtype=torch.uint8, device=dev)
+    for _ in range(args.steps):
+        pcpp.pcpp_gather_context(g, d["k_fresh"], d["v_fresh"], d["k_up"], d["v_up"], d["k_dn"], d["v_dn"], idx, kc,
+                                 vc)
+        pcpp.pcpp_group_norm(1, cfg.n_q, cfg.C, 32, 1e-6, 0, gx, gam, bet, gy, gwsb, gws)
+    torch.cuda.synchronize()
+    block_run(argparse.Namespace(level=1, steps=max(2, args.steps // 4)))
     print("pmc run done", flush=True)
 
 
@@ -649,6 +685,38 @@ def pmc_summarize(fetch_dir, write_dir):
         f"kernel_source_sha256_16: {kernel_source_hash()}\n")
     open(TRAFFIC_FILE, "w").write(text)
     print(text)
+
+    # Memory-bound kernels of the same run: median scaled HBM bytes per
+    # dispatch against their algorithmic bytes at these shapes.
+    cfg_c, tokens = 640, 2048
+    algo = {
+        "gather_copy": 4 * 3072 * cfg_c * 2 + 4 * 3072,      # read + write K and V context, indices
+        "gn_stats": tokens * cfg_c * 2,                        # read x
+        "gn_apply": 2 * tokens * cfg_c * 2,                    # read x, write y
+        "ln_kernel": tokens * cfg_c * 4 + tokens * cfg_c * 2,  # read the fp32 stream, write bf16
+    }
+    fv = per_kernel(fetch_dir, "FETCH_SIZE")
+    wv = per_kernel(write_dir, "WRITE_SIZE")
+    rows = ["# HBM traffic of the memory-bound kernels (one dispatch; median over the run's dispatches of each),",
+            "# FETCH_SIZE and WRITE_SIZE scaled as above; shapes of the 2048 px level-1 band (gather: 3072 keys x 640",
+            "# channels, K and V; GroupNorm and LayerNorm: 2048 tokens x 640 channels, the block's and pcpp_group_norm's).",
+            f"fetch_scale: {fetch[2]:.4f}",
+            f"write_scale: {write[2]:.4f}",
+            "kernel | fetched MB | written MB | HBM MB | algorithmic MB | HBM / algorithmic"]
+    for key, ab in algo.items():
+        fk = [sorted(x.values()) for k, x in fv.items() if key in k]
+        wk = [sorted(x.values()) for k, x in wv.items() if key in k]
+        if not fk or not wk:
+            continue
+        fmed = sorted(v for lst in fk for v in lst)
+        wmed = sorted(v for lst in wk for v in lst)
+        fb = fmed[len(fmed) // 2] / fetch[2] * 1024.0
+        wb = wmed[len(wmed) // 2] / write[2] * 1024.0
+        rows.append(f"{key} | {fb / 1e6:.2f} | {wb / 1e6:.2f} | {(fb + wb) / 1e6:.2f} | {ab / 1e6:.2f} | "
+                    f"{(fb + wb) / ab:.2f}")
+    mem = "\n".join(rows) + "\n"
+    open(MEM_TRAFFIC_FILE, "w").write(mem)
+    print(mem)
 
 
 def block_run(args):
@@ -765,7 +833,8 @@ def main():
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead of a graph")
     ap.add_argument("--no-extras", action="store_true", help="skip the gather / p=0.5 / block context lines")
     ap.add_argument("--pmc-run", action="store_true",
-                    help="counter-collection workload: a calibration copy, then --steps attention calls")
+                    help="counter-collection workload: a calibration copy, --steps attention calls, then the "
+                         "gather, GroupNorm and block calls whose memory-bound kernels the summary covers")
     ap.add_argument("--pmc-summarize", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the traffic summary from two rocprofv3 --pmc output folders")
     ap.add_argument("--block-run", action="store_true",

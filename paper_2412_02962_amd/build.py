@@ -2,6 +2,7 @@
 
 import concurrent.futures
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -34,13 +35,38 @@ def sources():
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
+# the compiler's per-kernel resource report (one remark line per field)
+RESOURCE_REMARKS = ["-Rpass-analysis=kernel-resource-usage", "-fno-caret-diagnostics"]
+
+
+def scratch_users(remarks):
+    """Kernels of one compile whose waves need per-lane private (scratch)
+    memory, from the resource report: [(kernel, bytes per lane)].  Such
+    memory lives in HBM; no kernel of this library is meant to use it (a
+    spill or a struct copied to private memory is a performance bug)."""
+    out, name = [], None
+    for line in remarks.splitlines():
+        m = re.search(r"remark: Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            continue
+        m = re.search(r"remark:\s+ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and name is not None and int(m.group(1)) > 0:
+            out.append((name, int(m.group(1))))
+    return out
+
+
 def _compile(src):
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [hipcc()] + HIPCC_FLAGS + ["-c", src, "-o", obj]
+    cmd = [hipcc()] + HIPCC_FLAGS + RESOURCE_REMARKS + ["-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
-    errs = "\n".join(l for l in (r.stderr or "").splitlines() if "packed-fp32-ops" not in l)
+    lines = (r.stderr or "").splitlines()
+    errs = "\n".join(l for l in lines if "packed-fp32-ops" not in l and "kernel-resource-usage" not in l)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{errs}")
+    bad = scratch_users(r.stderr or "")
+    if bad:
+        raise RuntimeError(f"{os.path.basename(src)}: kernels use per-lane scratch memory: {bad}")
     return obj, errs
 
 

@@ -21,17 +21,25 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kUnroll = 4;
 
+// One tensor's three source runs.  The kernel turns them into three
+// per-image base pointers held in scalar registers before the copy loop; a
+// run picked per lane by indexing an array (or a local struct) would make
+// the compiler keep the struct in per-lane private memory, whose stores
+// reach HBM.
 struct Seg3 {
-    const char* base[3];
-    int64_t bstride_bytes[3];
-    int64_t end0;  // byte offsets of segment boundaries within one image
+    const char* base0;
+    const char* base1;
+    const char* base2;
+    int64_t bstride0, bstride1, bstride2;  // bytes between images
+    int64_t end0;  // byte offsets of the run boundaries within one image
     int64_t end1;
 };
 
-__device__ __forceinline__ const char* seg_addr(const Seg3& s, int b, int64_t off) {
-    int k = off < s.end0 ? 0 : (off < s.end1 ? 1 : 2);
-    int64_t begin = k == 0 ? 0 : (k == 1 ? s.end0 : s.end1);
-    return s.base[k] + (int64_t)b * s.bstride_bytes[k] + (off - begin);
+// Source address of byte `off` of the context: run 0 below e0, run 1 below
+// e1, run 2 after (p0..p2 already point at this image's runs).
+__device__ __forceinline__ const char* seg_addr(const char* p0, const char* p1, const char* p2, int64_t e0,
+                                                int64_t e1, int64_t off) {
+    return off < e0 ? p0 + off : (off < e1 ? p1 + (off - e0) : p2 + (off - e1));
 }
 
 template <typename V>
@@ -41,23 +49,37 @@ __global__ __launch_bounds__(kThreads) void gather_copy(Seg3 ks, Seg3 vs, char* 
     const int b = blockIdx.z;
     const bool is_v = blockIdx.y == 1;
     const Seg3& s = is_v ? vs : ks;
+    const char* p0 = s.base0 + (int64_t)b * s.bstride0;
+    const char* p1 = s.base1 + (int64_t)b * s.bstride1;
+    const char* p2 = s.base2 + (int64_t)b * s.bstride2;
+    const int64_t e0 = ks.end0, e1 = ks.end1;
     char* dst = (is_v ? vdst : kdst);
     if (dst != nullptr) {
         dst += (int64_t)b * image_bytes;
         const int64_t nvec = image_bytes / (int64_t)sizeof(V);
-        const int64_t stride = (int64_t)gridDim.x * kThreads;
-        int64_t v0 = (int64_t)blockIdx.x * kThreads * kUnroll + threadIdx.x;
-        for (; v0 < nvec; v0 += stride * kUnroll) {
+        const int64_t chunk = (int64_t)kThreads * kUnroll;
+        for (int64_t c = (int64_t)blockIdx.x * chunk; c < nvec; c += (int64_t)gridDim.x * chunk) {
+            const int64_t v0 = c + threadIdx.x;
             V buf[kUnroll];
+            if (c + chunk <= nvec) {
+                // whole chunk: every load issued before the first store
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                int64_t v = v0 + (int64_t)u * kThreads;
-                if (v < nvec) buf[u] = *(const V*)seg_addr(s, b, v * (int64_t)sizeof(V));
-            }
+                for (int u = 0; u < kUnroll; ++u)
+                    buf[u] = *(const V*)seg_addr(p0, p1, p2, e0, e1, (v0 + (int64_t)u * kThreads) * (int64_t)sizeof(V));
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                int64_t v = v0 + (int64_t)u * kThreads;
-                if (v < nvec) *(V*)(dst + v * (int64_t)sizeof(V)) = buf[u];
+                for (int u = 0; u < kUnroll; ++u)
+                    *(V*)(dst + (v0 + (int64_t)u * kThreads) * (int64_t)sizeof(V)) = buf[u];
+            } else {
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) {
+                    const int64_t v = v0 + (int64_t)u * kThreads;
+                    if (v < nvec) buf[u] = *(const V*)seg_addr(p0, p1, p2, e0, e1, v * (int64_t)sizeof(V));
+                }
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) {
+                    const int64_t v = v0 + (int64_t)u * kThreads;
+                    if (v < nvec) *(V*)(dst + v * (int64_t)sizeof(V)) = buf[u];
+                }
             }
         }
     }
@@ -74,18 +96,22 @@ hipError_t launch_gather(const GatherParams& p, hipStream_t stream) {
     const int64_t row = (int64_t)p.C * p.esize;
     const int64_t image = row * p.src.n_kv;
     Seg3 ks, vs;
-    for (int k = 0; k < 3; ++k) {
-        ks.base[k] = (const char*)p.src.k[k];
-        vs.base[k] = (const char*)p.src.v[k];
-        ks.bstride_bytes[k] = vs.bstride_bytes[k] = p.src.bstride[k] * p.esize;
-    }
+    ks.base0 = (const char*)p.src.k[0];
+    ks.base1 = (const char*)p.src.k[1];
+    ks.base2 = (const char*)p.src.k[2];
+    vs.base0 = (const char*)p.src.v[0];
+    vs.base1 = (const char*)p.src.v[1];
+    vs.base2 = (const char*)p.src.v[2];
+    ks.bstride0 = vs.bstride0 = p.src.bstride[0] * p.esize;
+    ks.bstride1 = vs.bstride1 = p.src.bstride[1] * p.esize;
+    ks.bstride2 = vs.bstride2 = p.src.bstride[2] * p.esize;
     ks.end0 = vs.end0 = row * p.src.end0;
     ks.end1 = vs.end1 = row * p.src.end1;
 
     bool vec16 = (row % 16) == 0;
     for (int k = 0; k < 3; ++k) {
-        vec16 = vec16 && ((uintptr_t)ks.base[k] % 16 == 0) && ((uintptr_t)vs.base[k] % 16 == 0) &&
-                ((ks.bstride_bytes[k] % 16) == 0);
+        vec16 = vec16 && ((uintptr_t)p.src.k[k] % 16 == 0) && ((uintptr_t)p.src.v[k] % 16 == 0) &&
+                ((p.src.bstride[k] * p.esize) % 16 == 0);
     }
     vec16 = vec16 && ((uintptr_t)p.k_ctx % 16 == 0) && ((uintptr_t)p.v_ctx % 16 == 0);
     const int vbytes = vec16 ? 16 : p.esize;
