@@ -412,6 +412,34 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
         out[f"l2_{name}_TFLOPs"] = round(attn_flops(c2, nkv2) / us / 1e6, 1)
     out["derived_unet_selfattn_ms_per_band_step"] = round((10 * out_l1_us + 60 * l2["interior"]) / 1e3, 4)
 
+    # The same shapes with both guidance branches of a step in one launch
+    # (batch 2: the conditional and unconditional images, as the U-Net step
+    # with classifier-free guidance runs them); per-image time is half the
+    # launch.
+    cfg2 = {}
+    for name, base, band in (("l1", WORKLOAD, None), ("l2_edge", "sdxl2048_l2_edge", None),
+                             ("l2_interior", "sdxl2048_l2_edge", 3)):
+        import dataclasses
+        cb = dataclasses.replace(synth.ATTN_CONFIGS[base], batch=2)
+        if band is not None:
+            cb = dataclasses.replace(cb, i=band)
+        db = {k: to_dev(v) for k, v in synth.attention_inputs(cb).items()}
+        gb = pcpp.make_geom(cb.H, cb.W, cb.n, cb.i, cb.p, cb.heads, cb.d, 2, 0, pcpp.PCPP_DTYPE_BF16)
+        _, _, _, nkvb = pcpp.pcpp_context_rows(gb)
+        ob = torch.empty_like(db["q"])
+        wb = pcpp.pcpp_partial_attention_workspace_size(gb)
+        wsb_ = torch.zeros(max(wb, 1), dtype=torch.uint8, device=dev)
+        us = graph_time_us(torch, lambda: pcpp.pcpp_partial_attention(gb, db["q"], db["k_fresh"], db["v_fresh"],
+                                                                      db["k_up"], db["v_up"], db["k_dn"],
+                                                                      db["v_dn"], ob, wsb_, wb), reps, use_graph)
+        cfg2[name] = us / 2
+        out[f"{name}_cfg_batch2_us"] = round(us, 3)
+        out[f"{name}_cfg_batch2_us_per_image"] = round(us / 2, 3)
+        out[f"{name}_cfg_batch2_TFLOPs"] = round(attn_flops(cb, nkvb) / us / 1e6, 1)
+        del db, ob, wsb_
+    out["derived_unet_selfattn_ms_per_band_step_cfg_batch2_per_image"] = round(
+        (10 * cfg2["l1"] + 60 * cfg2["l2_interior"]) / 1e3, 4)
+
     # Multi-hop context (p > 1): 8 bands at 2048 px level 1, p = 1.5 (24 rows
     # on each side, from two bands), the stale rows given compactly.
     import dataclasses
@@ -642,6 +670,17 @@ def pmc_run(args):
     print("pmc run done", flush=True)
 
 
+def headline_attention(rows):
+    """Dispatch ids of the attention calls of the timed workload in a
+    --pmc-run counter file: the attention dispatches before the first gather
+    (the block calls later in the run launch the same kernel on their own
+    inputs, and a cross-attention shape)."""
+    ids = sorted(int(r["Dispatch_Id"]) for r in rows if "attn_bf16_kernel" in r["Kernel_Name"])
+    later = [int(r["Dispatch_Id"]) for r in rows if "gather_copy" in r["Kernel_Name"]]
+    first_other = min(later) if later else None
+    return {str(i) for i in ids if first_other is None or i < first_other}
+
+
 def pmc_summarize(fetch_dir, write_dir):
     """Writes the traffic summary from two rocprofv3 --pmc outputs
     (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch), each scaled by what the
@@ -651,9 +690,13 @@ def pmc_summarize(fetch_dir, write_dir):
 
     def per_kernel(d, counter):
         f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+        rows = list(csv.DictReader(open(f)))
+        head = headline_attention(rows)
         vals = {}
-        for r in csv.DictReader(open(f)):
+        for r in rows:
             if r["Counter_Name"] != counter:
+                continue
+            if "attn_bf16_kernel" in r["Kernel_Name"] and r["Dispatch_Id"] not in head:
                 continue
             vals.setdefault(r["Kernel_Name"], {}).setdefault(r["Dispatch_Id"], 0.0)
             vals[r["Kernel_Name"]][r["Dispatch_Id"]] += float(r["Counter_Value"])
@@ -807,9 +850,11 @@ def pmc_report(dirs):
              "(rocprofv3 --pmc; averages over the dispatches of each pass)"]
     for d in dirs:
         f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+        rows = list(csv.DictReader(open(f)))
+        head = headline_attention(rows)
         vals, durs = {}, {}
-        for r in csv.DictReader(open(f)):
-            if "attn_bf16_kernel" not in r["Kernel_Name"]:
+        for r in rows:
+            if r["Dispatch_Id"] not in head:
                 continue
             vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
             durs[r["Dispatch_Id"]] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3

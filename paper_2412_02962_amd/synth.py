@@ -22,6 +22,7 @@ abstract and Sec. 2.2).
 from __future__ import annotations
 
 import dataclasses
+import os
 from typing import Dict, Optional
 
 import numpy as np
@@ -535,8 +536,10 @@ def unet_band_inputs(sp: UNetSpec, sync_gn: bool = False):
     (_band_stats; entry i is replaced by the band's own in the step)."""
     s = BASE_SEED + sp.seed_id
     B = sp.batch
-    weights, stale = {}, {}
-    for idx, ly in enumerate(unet_layers(sp)):
+
+    def one(idx, ly):
+        """Weights and stale data of layer idx, from the layer's own streams."""
+        weights, stale = {}, {}
         g = _stream(s, 1000 + idx)
         h = ly["H"] // sp.n
         W, ci, co = ly["W"], ly["c_in"], ly["c_out"]
@@ -582,6 +585,19 @@ def unet_band_inputs(sp: UNetSpec, sync_gn: bool = False):
                                    "beta": bf16_bits(0.1 * g.standard_normal(co))}
             stale[ly["name"]] = {"gn_bands": _band_stats(_stream(s, 4000 + idx), sp.n, B, sp.groups,
                                                          h * W * co / sp.groups) if sync_gn else None}
+        return weights, stale
+
+    # Layers are independent draws: fill them on a few threads (numpy's
+    # generators and array arithmetic release the GIL on large arrays); the
+    # values do not depend on the order.
+    import concurrent.futures
+    layers = unet_layers(sp)
+    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:
+        parts = list(ex.map(lambda a: one(*a), list(enumerate(layers))))
+    weights, stale = {}, {}
+    for w_, s_ in parts:
+        weights.update(w_)
+        stale.update(s_)
     g = _stream(s, 999)
     h0 = sp.H0 // sp.n
     lat = np.zeros((B, h0 * sp.W0, LATENT_PAD))

@@ -63,6 +63,18 @@ def test_attention_batched(batch):
     gu.assert_close(cfg, got, gu.oracle_attention(cfg, inp), "batched")
 
 
+@pytest.mark.parametrize("band", [0, 3])
+def test_attention_level2_guidance_pair(band):
+    """Both guidance branches of a step in one launch (batch 2) at the full
+    2048 px level-2 shape (64 x 64 grid, 20 heads), an edge and an interior
+    band: every output element against the oracle."""
+    cfg = _cfg("sdxl2048_l2_edge", batch=2, i=band)
+    _say("level-2 guidance pair, band", band)
+    inp = synth.attention_inputs(cfg)
+    got = gu.to_f64(gu.run_attention(cfg, inp))
+    gu.assert_close(cfg, got, gu.oracle_attention(cfg, inp), f"l2 batch 2 band {band}")
+
+
 def test_attention_f32_at_workload_shape():
     cfg = _cfg("sdxl1024_l1", dtype="f32")
     _say("f32 at 1024px level-1 shape")
