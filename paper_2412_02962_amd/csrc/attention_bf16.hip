@@ -605,20 +605,44 @@ struct Plan {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Pieces per block.  A launch runs in waves of max_grid workgroups (one per
-// compute unit); with k pieces per block it takes ceil(blocks * k / max_grid)
-// waves of ceil(tiles / k) tiles each, plus a fixed cost per piece (first
-// loads, partial store and merge) of about PIECE_COST_TILES tile periods.
-// The k with the smallest estimate wins (the smallest such k on ties).
+// Pieces per block, from a cost estimate; the k with the smallest estimate
+// wins (the smallest such k on ties).  A launch of W workgroups runs in
+// ceil(W / max_grid) waves (max_grid = two workgroups per compute unit).
+//   Shapes whose whole blocks fit one wave (the 2048 px level-1 and level-2
+//   bands): in hundredths of the time a tile takes when two workgroups share
+//   a compute unit (1.09 us at level 1), a workgroup that has its compute
+//   unit to itself (W <= compute units) runs a tile in 0.64 of that time, a
+//   split costs about 2.6 tile times per wave (partial stores, counter,
+//   merge), and a launch with compute units holding two workgroups about
+//   1.8 more (measured on the level-2 bands at batch 1 and 2: 10 to 12 tiles,
+//   80 or 160 blocks).
+//   Larger shapes: waves x (tiles per piece + 4), in tile times; they take
+//   several waves of smaller pieces rather than a ragged last wave of whole
+//   blocks.
+constexpr int64_t TILE_COST_SHARED = 100;
+constexpr int64_t TILE_COST_ALONE = 64;
+constexpr int64_t PIECE_COST = 257;
+constexpr int64_t SHARED_CU_COST = 183;
 constexpr int64_t PIECE_COST_TILES = 4;
 constexpr int64_t MAX_SPLIT_BLOCKS = 65536;  // work counters kept at a fixed place
 
-int64_t pick_k(int64_t slots, int64_t max_grid, int64_t n_tiles) {
+int64_t pick_k(int64_t slots, int64_t cus, int64_t n_tiles) {
+    const int64_t max_grid = (int64_t)WG_PER_CU * cus;
     const int64_t k_max = n_tiles / MIN_TILES_PER_PIECE;
+    const bool one_wave = slots <= max_grid;
     int64_t best_k = 1, best = -1;
-    for (int64_t k = 1; k <= k_max && k <= 64; ++k) {
-        const int64_t waves = (slots * k + max_grid - 1) / max_grid;
-        const int64_t cost = waves * ((n_tiles + k - 1) / k + PIECE_COST_TILES);
+    for (int64_t k = 1; k == 1 || (k <= k_max && k <= 64); ++k) {
+        const int64_t w = slots * k;
+        const int64_t waves = (w + max_grid - 1) / max_grid;
+        const int64_t tiles = (n_tiles + k - 1) / k;
+        int64_t cost;
+        if (one_wave) {
+            const bool alone = w <= cus;
+            cost = waves * (tiles * (alone ? TILE_COST_ALONE : TILE_COST_SHARED) + (k > 1 ? PIECE_COST : 0)) +
+                   (alone ? 0 : SHARED_CU_COST);
+        } else {
+            cost = waves * (tiles + PIECE_COST_TILES);
+        }
         if (best < 0 || cost < best) {
             best = cost;
             best_k = k;
@@ -636,7 +660,6 @@ int64_t pick_k(int64_t slots, int64_t max_grid, int64_t n_tiles) {
 // computes whole blocks.
 Plan make_plan(const AttnParams& p, const DeviceLayout& d) {
     Plan pl;
-    const int64_t max_grid = (int64_t)WG_PER_CU * d.cus;
     pl.n_tiles = (p.kv.n_kv + KT - 1) / KT;
     pl.nqb = (p.nq + QB - 1) / QB;
     const int64_t n_blocks = (int64_t)p.batch * p.heads * pl.nqb;
@@ -644,7 +667,7 @@ Plan make_plan(const AttnParams& p, const DeviceLayout& d) {
     pl.n_xcd = d.xcd_merge ? d.n_xcd : 1;
     const int64_t bpx = (n_blocks + pl.n_xcd - 1) / pl.n_xcd;
     int64_t k = 1;
-    if (d.xcd_merge && n_blocks <= MAX_SPLIT_BLOCKS) k = pick_k(pl.n_xcd * bpx, max_grid, pl.n_tiles);
+    if (d.xcd_merge && n_blocks <= MAX_SPLIT_BLOCKS) k = pick_k(pl.n_xcd * bpx, d.cus, pl.n_tiles);
     pl.k = (int32_t)k;
     pl.bpx = (int32_t)(bpx < INT32_MAX ? bpx : INT32_MAX);
     const int64_t grid = (int64_t)pl.n_xcd * bpx * k;
