@@ -244,6 +244,23 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
         mm.split_ws_bytes = L.split_bytes;
         return launch_gemm(mm, s);
     };
+    auto gemm_pair_s = [&](GemmParams a, GemmParams b) {
+        a.split_ws = b.split_ws = split_ws;
+        a.split_ws_bytes = b.split_ws_bytes = L.split_bytes;
+        return launch_gemm_pair(a, b, s);
+    };
+    // Text K/V of blocks j.. (the rest of its chunk of kv_slots blocks): one
+    // product over their stacked weights, block u's K at slot 2u, V at 2u + 1.
+    auto text_kv = [&](int j) {
+        const int nb = depth - j < L.kv_slots ? depth - j : L.kv_slots;
+        GemmParams kv = gemm(text, text_dim, false, blocks[j].attn2_kv_w, nullptr, B * T, nb * 2 * C, text_dim, kv2, C,
+                             false);
+        kv.seg = C;
+        kv.seg_stride = kv_elems;
+        kv.w_seg_rows = 2 * C;
+        for (int u = 0; u < nb; ++u) kv.w_seg[u] = (const __bf16*)blocks[j + u].attn2_kv_w;
+        return kv;
+    };
     hipError_t e = hipSuccess;
 #define PCPP_CHECK(call)                  \
     do {                                  \
@@ -281,8 +298,34 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
         gp.zero2 = (int*)attn_ws;
         gp.n_zero2 = n1 > n2 ? n1 : n2;
     }
-    PCPP_CHECK(launch_group_norm(gp, s));
-    PCPP_CHECK(gemm_s(gemm(t16, C, false, mw.proj_in_w, mw.proj_in_b, rows, C, C, hid, C, true)));
+    // proj_in, and beside it in the same launch the first chunk's text K/V
+    // (independent of the band).  When the band's tokens fill whole 64-token
+    // tiles, proj_in applies the GroupNorm itself while staging x (from the
+    // statistics launch's records), else a separate apply writes it to t16.
+    {
+        const bool gn_in_gemm = N % 64 == 0 && C % 64 == 0 && C <= GEMM_GN_MAXC;
+        GemmParams pin = gemm(t16, C, false, mw.proj_in_w, mw.proj_in_b, rows, C, C, hid, C, true);
+        if (gn_in_gemm) {
+            PCPP_CHECK(launch_group_norm_stats(gp, s));
+            pin.a = x;
+            pin.a_mode = 1;
+            pin.gn.stats = gp.stats;
+            pin.gn.chunks = gp.chunks;
+            pin.gn.G = gp.G;
+            pin.gn.B = gp.B;
+            pin.gn.eps = gp.eps;
+            pin.gn.bands = gp.bands;
+            pin.gn.n_bands = gp.n_bands;
+            pin.gn.band = gp.band;
+            pin.gn.own_out = gp.own_out;
+            pin.gn_gamma = gp.gamma;
+            pin.gn_beta = gp.beta;
+            pin.gn_N = N;
+        } else {
+            PCPP_CHECK(launch_group_norm(gp, s));
+        }
+        PCPP_CHECK(L.kv_grouped && depth > 0 ? gemm_pair_s(pin, text_kv(0)) : gemm_s(pin));
+    }
 
     LayerNormParams lp;
     lp.x = hid;
@@ -303,19 +346,9 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
         const void* kd = r.dn > 0 ? k_dn[j] : nullptr;
         const void* vd = r.dn > 0 ? v_dn[j] : nullptr;
 
-        // Text K/V of this block and the next ones of its chunk: one product
-        // over their stacked weights, block u's K at slot 2u, V at 2u + 1.
+        // Text K/V of this block's chunk (the first chunk's came with proj_in).
         const int slot = j % L.kv_slots;
-        if (L.kv_grouped && slot == 0) {
-            const int nb = depth - j < L.kv_slots ? depth - j : L.kv_slots;
-            GemmParams kv = gemm(text, text_dim, false, w.attn2_kv_w, nullptr, B * T, nb * 2 * C, text_dim, kv2, C,
-                                 false);
-            kv.seg = C;
-            kv.seg_stride = kv_elems;
-            kv.w_seg_rows = 2 * C;
-            for (int u = 0; u < nb; ++u) kv.w_seg[u] = (const __bf16*)blocks[j + u].attn2_kv_w;
-            PCPP_CHECK(gemm_s(kv));
-        }
+        if (L.kv_grouped && slot == 0 && j > 0) PCPP_CHECK(gemm_s(text_kv(j)));
         __bf16* k2 = kv2 + 2 * slot * kv_elems;
         __bf16* v2 = k2 + kv_elems;
 

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "gn_merge.h"
+
 namespace pcpp {
 
 constexpr int GEMM_MAX_WSEG = 16;
@@ -53,9 +55,23 @@ struct GemmParams {
     // > 0: output segment s at out[0] + s * seg_stride elements (out[1..2]
     // unused), for any number of segments.
     int64_t seg_stride = 0;
+    // a_mode 1: GroupNorm of X applied while X is staged (bf16 X; K = C <=
+    // GEMM_GN_MAXC channels, G <= 256 groups; gn_N tokens per image, a
+    // multiple of 64): channel k of token m becomes X * sc + sh with the
+    // scale and shift of m's image, from the statistics launch's records in
+    // gn (and the other bands' for the synchronized form), in the arithmetic
+    // of the GroupNorm apply kernel (the same bits).  Runs on the 64 x 64
+    // pipelined kernel; the workgroup holding image b's first token tile and
+    // the first W tile writes the band's own statistics to gn.own_out.
+    int32_t a_mode = 0;
+    GnStatsSrc gn = {};
+    const __bf16* gn_gamma = nullptr;
+    const __bf16* gn_beta = nullptr;
+    int32_t gn_N = 0;
     // Set by launch_gemm for a split launch.
     int32_t splitk = 1, n_xcd = 1, tpx = 0, n_tiles = 0;
 };
+constexpr int GEMM_GN_MAXC = 1280;
 
 // Bytes of split-K workspace a GEMM of this shape can use (0: it runs
 // unsplit); counters come first, at most GEMM_SPLIT_COUNTERS ints.  conv:
@@ -66,6 +82,9 @@ size_t gemm_split_ws_bytes(int M, int N, int K, bool conv = true);
 
 bool gemm_shape_ok(const GemmParams& p);
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s);
+// Two independent products (neither reads what the other writes) in one
+// launch when both run on the same pipelined kernel, else one after the other.
+hipError_t launch_gemm_pair(const GemmParams& a, const GemmParams& b, hipStream_t s);
 
 // GroupNorm with statistics over one image's tokens (per image and group):
 // writes bf16 y = (x - mean) * rsqrt(var + eps) * gamma + beta.
@@ -106,6 +125,9 @@ size_t group_norm_ws_bytes(int B, int G, int N);
 bool norm_shapes_ok(int C, int G);  // GroupNorm and LayerNorm: C <= 2048
 bool gn_shapes_ok(int C, int G);    // GroupNorm alone: C <= 2560
 hipError_t launch_group_norm(GroupNormParams p, hipStream_t s);
+// The statistics launch alone (sets p.chunks): for a GEMM that applies the
+// GroupNorm while staging its operand (GemmParams::a_mode).
+hipError_t launch_group_norm_stats(GroupNormParams& p, hipStream_t s);
 
 // LayerNorm over the channel axis of fp32 rows, bf16 output.
 struct LayerNormParams {

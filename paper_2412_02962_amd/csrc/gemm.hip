@@ -275,8 +275,24 @@ __device__ __forceinline__ void wait_tiles_after(int later) {
     }
 }
 
-template <int BM, int BN, int NS, bool GEGLU, bool CONV>
-__global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
+// LDS floats of the GroupNorm table of a_mode 1: scale and shift per
+// channel (the merge's 256 x 3 scratch shares their space), then the group
+// means and reciprocal deviations.
+constexpr int GN_TAB_FLOATS = 2 * GEMM_GN_MAXC + 2 * 256;
+static_assert(2 * GEMM_GN_MAXC >= 3 * 256, "the merge scratch fits the scale and shift tables");
+
+// One workgroup's tile of the product; (bx, by) is its place in the
+// product's own grid (blockIdx of a single launch); lds holds NS stages,
+// gn_tab GN_TAB_FLOATS floats when AMODE is 1.
+//
+// AMODE 1 applies GroupNorm to X in its LDS stage: after the products of
+// k-tile kt every lane rewrites the pieces of k-tile kt + 1 its own direct
+// loads brought, published by the next barrier.
+template <int BM, int BN, int NS, bool GEGLU, bool CONV, int AMODE>
+__device__ __forceinline__ void gemm_dma_body(const GemmParams& p, const int bx, const int by, char* lds,
+                                              float* gn_tab) {
+    constexpr bool AGN = AMODE == 1;
+    static_assert(!AGN || (BM == 64 && BN == 64 && !GEGLU && !CONV), "GroupNorm staging: plain 64 x 64 tiles");
     constexpr int WMB = BM / 64;                      // 32-token blocks per wavefront
     constexpr int WNB = BN / 64;                      // 32-row W blocks per wavefront
     constexpr int XP = BM / 32;                       // 1 KB X pieces per wavefront per k-tile
@@ -286,7 +302,6 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
     constexpr int NOPS = WNB + WMB;                   // operand reads per k-step
     static_assert((NS - 2) * PT <= 63, "vmcnt holds at most 63 loads");
     static_assert(!GEGLU || WNB == 2, "GEGLU pairs a value block with a gate block");
-    __shared__ __attribute__((aligned(16))) char lds[NS * STAGE];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -301,10 +316,10 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
     // tiles in n-major order (all token tiles of one W tile together), and
     // the splitk pieces of a tile follow each other within it, so all pieces
     // of a tile share one L2.
-    int m_tile = blockIdx.x, n_tile = blockIdx.y, piece = 0, tile = 0, xcd = 0, tl = 0;
+    int m_tile = bx, n_tile = by, piece = 0, tile = 0, xcd = 0, tl = 0;
     if (p.tpx > 0) {
-        xcd = blockIdx.x % p.n_xcd;
-        const int j = blockIdx.x / p.n_xcd;
+        xcd = bx % p.n_xcd;
+        const int j = bx / p.n_xcd;
         tl = j / p.splitk;
         piece = j - tl * p.splitk;
         tile = xcd * p.tpx + tl;
@@ -437,15 +452,8 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-#pragma unroll
-    for (int s = 0; s < NS - 1; ++s)
-        if (kt0 + s < kt1) issue(kt0 + s, s);
-    for (int kt = kt0; kt < kt1; ++kt) {
-        // k-tiles issued after kt so far: min(kt1 - 1 - kt, NS - 2), PT loads each
-        wait_tiles_after<PT, NS - 2>(min(kt1 - 1 - kt, NS - 2));
-        __builtin_amdgcn_s_barrier();  // everyone's pieces of tile kt landed; the stage of tile kt-1 is free
-        if (kt + NS - 1 < kt1) issue(kt + NS - 1, (kt - kt0 + NS - 1) % NS);
-        const uint32_t sbase = lds0 + ((kt - kt0) % NS) * STAGE;
+    // The MFMAs of the k-tile in the stage at LDS address sbase.
+    auto mfma_tile = [&](uint32_t sbase) {
         Ops o[2];
         read_ops(sbase, 0, o[0]);
 #pragma unroll
@@ -464,6 +472,85 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
                     acc[i][j] = mfma32x32x16(__builtin_bit_cast(bf16x8, cur.w[i]), __builtin_bit_cast(bf16x8, cur.x[j]),
                                              acc[i][j]);
         }
+    };
+
+    if constexpr (AGN) {
+        // X arrives with the direct loads like W; each lane then rewrites in
+        // place the 16-byte pieces its own loads brought (so its own wait
+        // suffices), with the GroupNorm applied, before the barrier that
+        // publishes the stage.  Piece i of the lane: row 8 (wave + 4 i) +
+        // lane / 8, source chunk (lane % 8) ^ ((row / 2) % 8).
+        float* sc = gn_tab;
+        float* sh = gn_tab + GEMM_GN_MAXC;
+        auto gn_rewrite = [&](int kt, int stage) {
+#pragma unroll
+            for (int i = 0; i < XP; ++i) {
+                const int r = 8 * (wave + 4 * i) + (lane >> 3);
+                const int c0 = kt * DBK + 8 * ((lane & 7) ^ ((r >> 1) & 7));
+                bf16x8* at = (bf16x8*)(lds + stage * STAGE + (wave + 4 * i) * 1024 + lane * 16);
+                const bf16x8 v = *at;
+                float a[8], b[8];
+                *(f32x4*)&a[0] = *(const f32x4*)(sc + c0);
+                *(f32x4*)&a[4] = *(const f32x4*)(sc + c0 + 4);
+                *(f32x4*)&b[0] = *(const f32x4*)(sh + c0);
+                *(f32x4*)&b[4] = *(const f32x4*)(sh + c0 + 4);
+                bf16x8 y;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) y[e] = f32_to_bf16(__builtin_fmaf((float)v[e], a[e], b[e]));
+                *at = y;
+            }
+        };
+        // The first two k-tiles in flight while the statistics are merged.
+        const int nkt = kt1 - kt0;
+        issue(kt0, 0);
+        if (nkt > 1) issue(kt0 + 1, 1);
+        {
+            const int img = m0 / p.gn_N;
+            float* g_mean = gn_tab + 2 * GEMM_GN_MAXC;
+            float* g_rstd = g_mean + 256;
+            gn_group_stats(p.gn, img, m0 == img * p.gn_N && n0 == 0 && piece == 0, gn_tab, g_mean, g_rstd);
+            const int cg = p.K / p.gn.G;
+            for (int c = tid; c < p.K; c += 256) {
+                const int g = c / cg;
+                const float a = g_rstd[g] * bf16_to_f32(p.gn_gamma[c]);
+                sc[c] = a;
+                sh[c] = bf16_to_f32(p.gn_beta[c]) - g_mean[g] * a;
+            }
+            __syncthreads();
+        }
+        // X(kt0) landed: after it W(kt0) and, if issued, k-tile kt0 + 1.
+        if (nkt > 1)
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(WP + PT));
+        else
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(WP));
+        gn_rewrite(kt0, 0);
+        for (int kt = kt0; kt < kt1; ++kt) {
+            const int i = kt - kt0;
+            wait_tiles_after<PT, NS - 2>(min(kt1 - 1 - kt, NS - 2));
+            __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this lane's rewrite of X(kt)
+            __builtin_amdgcn_s_barrier();
+            if (kt + NS - 1 < kt1) issue(kt + NS - 1, (i + NS - 1) % NS);
+            mfma_tile(lds0 + (i % NS) * STAGE);
+            if (kt + 1 < kt1) {
+                // X(kt + 1) landed: after it W(kt + 1) and, if issued, k-tile kt + 2.
+                if (kt + 2 < kt1)
+                    __builtin_amdgcn_s_waitcnt(vmcnt_imm(WP + PT));
+                else
+                    __builtin_amdgcn_s_waitcnt(vmcnt_imm(WP));
+                gn_rewrite(kt + 1, (i + 1) % NS);
+            }
+        }
+    } else {
+#pragma unroll
+        for (int s = 0; s < NS - 1; ++s)
+            if (kt0 + s < kt1) issue(kt0 + s, s);
+        for (int kt = kt0; kt < kt1; ++kt) {
+            // k-tiles issued after kt so far: min(kt1 - 1 - kt, NS - 2), PT loads each
+            wait_tiles_after<PT, NS - 2>(min(kt1 - 1 - kt, NS - 2));
+            __builtin_amdgcn_s_barrier();  // everyone's pieces of tile kt landed; the stage of tile kt-1 is free
+            if (kt + NS - 1 < kt1) issue(kt + NS - 1, (kt - kt0 + NS - 1) % NS);
+            mfma_tile(lds0 + ((kt - kt0) % NS) * STAGE);
+        }
     }
 
     // Split K: every piece stores its partial tile (fp32, 1 KB per wavefront
@@ -474,7 +561,7 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
         constexpr int NQ = WNB * WMB * 4;  // f32x4 chunks per lane
         auto part_of = [&](int wg) { return (float*)p.split_ws + GEMM_SPLIT_COUNTERS + (int64_t)wg * BM * BN; };
         {
-            float* dst = part_of(blockIdx.x) + (wave * 64 + lane) * 4;
+            float* dst = part_of(bx) + (wave * 64 + lane) * 4;
 #pragma unroll
             for (int q = 0; q < NQ; ++q) {
                 const f32x16& a = acc[q / (4 * WMB)][(q / 4) % WMB];
@@ -611,15 +698,49 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
     }
 }
 
+template <int BM, int BN, int NS, bool GEGLU, bool CONV, int AMODE>
+__global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
+    __shared__ __attribute__((aligned(16))) char lds[NS * (BM + BN) * DBK * 2];
+    __shared__ __attribute__((aligned(16))) float gn_tab[AMODE == 1 ? GN_TAB_FLOATS : 4];
+    gemm_dma_body<BM, BN, NS, GEGLU, CONV, AMODE>(p, blockIdx.x, blockIdx.y, lds, gn_tab);
+}
+
+// Two independent plain products in one launch (so that neither pays a
+// launch's fixed cost alone): workgroups [0, n_a) run `a`, [b0, b0 + n_b)
+// run `b`, each product's grid linearised x-fastest; b0 is a multiple of the
+// XCD count, so a product on XCD-ordered tiles keeps its workgroup-to-XCD
+// map; the workgroups in between exit at once.
+struct GemmPair {
+    GemmParams a, b;
+    int32_t gx_a, n_a, gx_b, b0;
+};
+
+template <int BM, int BN, int NS, int AMODE_A>
+__global__ __launch_bounds__(256) void gemm_dma_pair_kernel(GemmPair pp) {
+    __shared__ __attribute__((aligned(16))) char lds[NS * (BM + BN) * DBK * 2];
+    __shared__ __attribute__((aligned(16))) float gn_tab[AMODE_A == 1 ? GN_TAB_FLOATS : 4];
+    const int id = blockIdx.x;
+    if (id < pp.n_a)
+        gemm_dma_body<BM, BN, NS, false, false, AMODE_A>(pp.a, id % pp.gx_a, id / pp.gx_a, lds, gn_tab);
+    else if (id >= pp.b0)
+        gemm_dma_body<BM, BN, NS, false, false, 0>(pp.b, (id - pp.b0) % pp.gx_b, (id - pp.b0) / pp.gx_b, lds, gn_tab);
+}
+
 template <int BM, int BN, int NS, bool GEGLU>
 hipError_t launch_dma(const GemmParams& p, hipStream_t s) {
     const int bn_out = GEGLU ? BN / 2 : BN;
     dim3 grid((p.M + BM - 1) / BM, p.N / bn_out);
     if (p.tpx > 0) grid = dim3((unsigned)(p.n_xcd * p.tpx * p.splitk), 1);
+    if constexpr (!GEGLU && BM == 64 && BN == 64) {
+        if (p.a_mode == 1) {
+            gemm_dma_kernel<BM, BN, NS, false, false, 1><<<grid, 256, 0, s>>>(p);
+            return hipGetLastError();
+        }
+    }
     if (!GEGLU && p.conv_W > 0)
-        gemm_dma_kernel<BM, BN, NS, GEGLU, true><<<grid, 256, 0, s>>>(p);
+        gemm_dma_kernel<BM, BN, NS, GEGLU, true, 0><<<grid, 256, 0, s>>>(p);
     else
-        gemm_dma_kernel<BM, BN, NS, GEGLU, false><<<grid, 256, 0, s>>>(p);
+        gemm_dma_kernel<BM, BN, NS, GEGLU, false, 0><<<grid, 256, 0, s>>>(p);
     return hipGetLastError();
 }
 
@@ -723,9 +844,22 @@ size_t gemm_split_ws_bytes(int M, int N, int K, bool conv) {
     return conv ? split_plan(M, N, K, d).bytes : split_plan_plain(M, N, K, d).bytes;
 }
 
-hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
-    GemmParams p = p_in;
+namespace {
+
+// The kernel a product runs on.
+enum GemmKind { GK_DMA_128, GK_DMA_64, GK_DMA_GEGLU, GK_REG_22, GK_REG_12, GK_REG_11 };
+
+// Validates p, picks its kernel, and sets the fields of a split or
+// XCD-ordered launch.
+hipError_t plan_gemm(GemmParams& p, hipStream_t s, GemmKind& kind) {
     if (p.conv_W > 0 && !gemm_shape_ok(p)) return hipErrorInvalidValue;
+    if (p.a_mode != 0) {  // GroupNorm staging: the 64 x 64 pipelined kernel only
+        if (p.a_mode != 1 || p.a_f32 || p.geglu || p.conv_W > 0 || p.K % DBK != 0 || p.K > GEMM_GN_MAXC ||
+            p.N % 64 != 0 || p.seg % 4 != 0 || p.gn_N <= 0 || p.gn_N % 64 != 0 || p.M % p.gn_N != 0 || p.gn.G < 1 ||
+            p.gn.G > 256 || p.K % p.gn.G != 0 || p.gn.stats == nullptr || p.gn_gamma == nullptr ||
+            p.gn_beta == nullptr)
+            return hipErrorInvalidValue;
+    }
     if (p.w_seg_rows != 0 || p.seg_stride != 0) {  // the pipelined kernel's plain form only
         if (p.a_f32 || p.geglu || p.conv_W > 0 || p.K % DBK != 0 || p.seg % 4 != 0 || p.N % 64 != 0 ||
             p.seg_stride < 0 || p.w_seg_rows < 0)
@@ -744,7 +878,8 @@ hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
             p.n_xcd = sp.n_xcd;
             p.tpx = sp.tpx;
             p.n_tiles = sp.n_tiles;
-            return launch_dma<128, 128, 3, false>(p, s);
+            kind = GK_DMA_128;
+            return hipSuccess;
         }
     }
     // Unsplit launches: when W (rows x K) is at least four times X (M x K),
@@ -774,7 +909,8 @@ hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
                 p.n_xcd = sp.n_xcd;
                 p.tpx = sp.tpx;
                 p.n_tiles = sp.n_tiles;
-                return launch_dma<64, 64, 3, false>(p, s);
+                kind = GK_DMA_64;
+                return hipSuccess;
             }
         }
         if (p.geglu) {
@@ -783,20 +919,23 @@ hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
             // tiles and 35.2 for three stages at the 2048 x 2 x 2560 x 640 shape
             if (p.N % 64 == 0) {
                 map_xcd(64, 64);
-                return launch_dma<64, 128, 2, true>(p, s);
+                kind = GK_DMA_GEGLU;
+                return hipSuccess;
             }
         } else {
             // 128x128 tiles only with at least two per compute unit; else 64x64
             // tiles at three stages (48 KB of LDS: three workgroups per compute
             // unit), measured faster at M = 2048 for every N from 640 to 1920.
             const int64_t mt128 = (p.M + 127) / 128;
-            if (p.N % 128 == 0 && mt128 * (p.N / 128) >= 2 * (int64_t)dl.cus) {
+            if (p.a_mode == 0 && p.N % 128 == 0 && mt128 * (p.N / 128) >= 2 * (int64_t)dl.cus) {
                 map_xcd(128, 128);
-                return launch_dma<128, 128, 3, false>(p, s);
+                kind = GK_DMA_128;
+                return hipSuccess;
             }
             if (p.N % 64 == 0) {
                 map_xcd(64, 64);
-                return launch_dma<64, 64, 3, false>(p, s);
+                kind = GK_DMA_64;
+                return hipSuccess;
             }
         }
     }
@@ -804,11 +943,79 @@ hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
     if (p.out_bf16 != nullptr || p.bias2 != nullptr || p.conv_W > 0) return hipErrorInvalidValue;
     // 128x128 tiles when they still give about a workgroup per compute unit,
     // else 64x128 / 64x64.
-    if (p.geglu) return launch_shape<2, 2>(p, s);
+    kind = GK_REG_11;
+    if (p.geglu) kind = GK_REG_22;
     const int64_t t128 = (int64_t)((p.M + 127) / 128) * (p.N / 128);
-    if (p.N % 128 == 0 && t128 >= 200) return launch_shape<2, 2>(p, s);
-    if (p.N % 128 == 0 && (int64_t)((p.M + 63) / 64) * (p.N / 128) >= 160) return launch_shape<1, 2>(p, s);
-    return launch_shape<1, 1>(p, s);
+    if (!p.geglu && p.N % 128 == 0 && t128 >= 200)
+        kind = GK_REG_22;
+    else if (!p.geglu && p.N % 128 == 0 && (int64_t)((p.M + 63) / 64) * (p.N / 128) >= 160)
+        kind = GK_REG_12;
+    return hipSuccess;
+}
+
+hipError_t launch_planned(const GemmParams& p, GemmKind kind, hipStream_t s) {
+    switch (kind) {
+        case GK_DMA_128: return launch_dma<128, 128, 3, false>(p, s);
+        case GK_DMA_64: return launch_dma<64, 64, 3, false>(p, s);
+        case GK_DMA_GEGLU: return launch_dma<64, 128, 2, true>(p, s);
+        case GK_REG_22: return launch_shape<2, 2>(p, s);
+        case GK_REG_12: return launch_shape<1, 2>(p, s);
+        default: return launch_shape<1, 1>(p, s);
+    }
+}
+
+// Workgroups along x and y of a 64 x 64 pipelined launch (launch_dma).
+void dma64_grid(const GemmParams& p, int& gx, int& gy) {
+    if (p.tpx > 0) {
+        gx = p.n_xcd * p.tpx * p.splitk;
+        gy = 1;
+    } else {
+        gx = (p.M + 63) / 64;
+        gy = p.N / 64;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_gemm(const GemmParams& p_in, hipStream_t s) {
+    GemmParams p = p_in;
+    GemmKind kind;
+    const hipError_t e = plan_gemm(p, s, kind);
+    return e != hipSuccess ? e : launch_planned(p, kind, s);
+}
+
+hipError_t launch_gemm_pair(const GemmParams& a_in, const GemmParams& b_in, hipStream_t s) {
+    GemmParams a = a_in, b = b_in;
+    GemmKind ka, kb;
+    hipError_t e = plan_gemm(a, s, ka);
+    if (e != hipSuccess) return e;
+    e = plan_gemm(b, s, kb);
+    if (e != hipSuccess) return e;
+    // One launch when both run on the 64 x 64 pipelined kernel and at most
+    // one of them splits K (the split region holds one product's partials);
+    // only the first may stage its X with GroupNorm.
+    if (ka == GK_DMA_64 && kb == GK_DMA_64 && a.conv_W == 0 && b.conv_W == 0 && !(a.splitk > 1 && b.splitk > 1) &&
+        b.a_mode == 0) {
+        GemmPair pp;
+        pp.a = a;
+        pp.b = b;
+        int gy_a, gy_b;
+        dma64_grid(a, pp.gx_a, gy_a);
+        dma64_grid(b, pp.gx_b, gy_b);
+        pp.n_a = pp.gx_a * gy_a;
+        const DeviceLayout dl = device_layout(s);
+        const int n_xcd = dl.n_xcd > 0 ? dl.n_xcd : 1;
+        pp.b0 = (pp.n_a + n_xcd - 1) / n_xcd * n_xcd;
+        const int64_t total = (int64_t)pp.b0 + (int64_t)pp.gx_b * gy_b;
+        if (total > INT32_MAX) return hipErrorInvalidValue;
+        if (a.a_mode == 1)
+            gemm_dma_pair_kernel<64, 64, 3, 1><<<dim3((unsigned)total), 256, 0, s>>>(pp);
+        else
+            gemm_dma_pair_kernel<64, 64, 3, 0><<<dim3((unsigned)total), 256, 0, s>>>(pp);
+        return hipGetLastError();
+    }
+    e = launch_planned(a, ka, s);
+    return e != hipSuccess ? e : launch_planned(b, kb, s);
 }
 
 }  // namespace pcpp

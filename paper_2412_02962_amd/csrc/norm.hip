@@ -26,6 +26,7 @@
 
 #include "common.h"
 #include "gemm.h"
+#include "gn_merge.h"
 
 namespace pcpp {
 
@@ -46,17 +47,6 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // Workspace of GroupNorm: [B][chunks][G] x (count, mean, M2).
 size_t gn_part_bytes(int B, int G, int chunks) { return (size_t)B * G * chunks * 3 * sizeof(float); }
-
-// Chan et al.'s pairwise update of (n, mean, M2) with (nb, mb, m2b).
-__device__ __forceinline__ void chan_merge(float& n, float& mean, float& m2, float nb, float mb, float m2b) {
-    if (nb <= 0.f) return;
-    const float nn = n + nb;
-    const float r = __builtin_amdgcn_rcpf(nn);  // statistics: a 1-ulp reciprocal is plenty
-    const float d = mb - mean;
-    mean += d * (nb * r);
-    m2 += m2b + d * d * (n * nb * r);
-    n = nn;
-}
 
 template <int GN_CHUNK_TOKENS, int PP>  // PP: channel pairs per thread, ceil(C / 2 / GN_THREADS)
 __global__ __launch_bounds__(GN_THREADS) void gn_stats(GroupNormParams p) {
@@ -163,60 +153,20 @@ __global__ __launch_bounds__(GN_THREADS) void gn_apply(GroupNormParams p) {
             xv[k] = *(const bf16x8*)(p.x + base + (int64_t)t * C + c);
         }
     }
-    // Thread (g, j) of S = GN_THREADS / G per group merges chunks j, j + S, ...
-    // (records of one chunk are consecutive in g: coalesced), then thread g
-    // merges the S results in order j = 0, 1, ...
+    // The image's statistics (chunks, then bands), the same code as the GEMM
+    // that applies GroupNorm while staging its operand.
     {
-        const int S = GN_THREADS / G;
-        const int g = tid % G, j = tid / G;
-        float n = 0.f, mean = 0.f, m2 = 0.f;
-        if (j < S) {
-            const float* st = p.stats + ((int64_t)b * p.chunks * G + g) * 3;
-            for (int k0 = j; k0 < p.chunks; k0 += 8 * S) {
-                float cn[8], cm[8], cq[8];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    const int k = k0 + u * S;
-                    const bool ok = k < p.chunks;
-                    const float* r = st + (int64_t)k * G * 3;
-                    cn[u] = ok ? r[0] : 0.f;
-                    cm[u] = ok ? r[1] : 0.f;
-                    cq[u] = ok ? r[2] : 0.f;
-                }
-#pragma unroll
-                for (int u = 0; u < 8; ++u) chan_merge(n, mean, m2, cn[u], cm[u], cq[u]);
-            }
-        }
-        mrg[tid][0] = n;
-        mrg[tid][1] = mean;
-        mrg[tid][2] = m2;
-        __syncthreads();
-        if (tid < G) {
-            for (int k = 1; k < S; ++k) chan_merge(n, mean, m2, mrg[tid + k * G][0], mrg[tid + k * G][1], mrg[tid + k * G][2]);
-            if (p.own_out != nullptr && blockIdx.x == 0) {
-                float* o = p.own_out + ((int64_t)b * G + tid) * 3;
-                o[0] = n;
-                o[1] = mean;
-                o[2] = m2;
-            }
-            if (p.bands != nullptr) {
-                float tn = 0.f, tm = 0.f, tq = 0.f;
-                for (int jb = 0; jb < p.n_bands; ++jb) {
-                    if (jb == p.band) {
-                        chan_merge(tn, tm, tq, n, mean, m2);
-                    } else {
-                        const float* o = p.bands + (((int64_t)jb * p.B + b) * G + tid) * 3;
-                        chan_merge(tn, tm, tq, o[0], o[1], o[2]);
-                    }
-                }
-                n = tn;
-                mean = tm;
-                m2 = tq;
-            }
-            g_mean[tid] = mean;
-            g_rstd[tid] = n > 0.f ? rsqrtf(m2 / n + p.eps) : 0.f;
-        }
-        __syncthreads();
+        GnStatsSrc src;
+        src.stats = p.stats;
+        src.chunks = p.chunks;
+        src.G = G;
+        src.B = p.B;
+        src.eps = p.eps;
+        src.bands = p.bands;
+        src.n_bands = p.n_bands;
+        src.band = p.band;
+        src.own_out = p.own_out;
+        gn_group_stats(src, b, blockIdx.x == 0, &mrg[0][0], g_mean, g_rstd);
     }
     for (int c = tid; c < C; c += GN_THREADS) {
         const int g = c / cg;
@@ -355,7 +305,7 @@ bool gn_shapes_ok(int C, int G) {
 
 bool norm_shapes_ok(int C, int G) { return gn_shapes_ok(C, G) && C <= 4 * 64 * LN_MAX_VEC; }
 
-hipError_t launch_group_norm(GroupNormParams p, hipStream_t s) {
+hipError_t launch_group_norm_stats(GroupNormParams& p, hipStream_t s) {
     if (!gn_shapes_ok(p.C, p.G)) return hipErrorInvalidValue;
     if (p.pad_W < 0 || (p.pad_W > 0 && p.N % p.pad_W != 0)) return hipErrorInvalidValue;
     p.chunks = gn_chunks(p.N);
@@ -378,7 +328,11 @@ hipError_t launch_group_norm(GroupNormParams p, hipStream_t s) {
         default:
             return hipErrorInvalidValue;
     }
-    hipError_t e = hipGetLastError();
+    return hipGetLastError();
+}
+
+hipError_t launch_group_norm(GroupNormParams p, hipStream_t s) {
+    const hipError_t e = launch_group_norm_stats(p, s);
     if (e != hipSuccess) return e;
     gn_apply<<<dim3((p.N + GN_TOKENS_PER_APPLY - 1) / GN_TOKENS_PER_APPLY, p.B), GN_THREADS, 0, s>>>(p);
     return hipGetLastError();
