@@ -726,6 +726,170 @@ __global__ __launch_bounds__(256) void gemm_dma_pair_kernel(GemmPair pp) {
         gemm_dma_body<BM, BN, NS, false, false, 0>(pp.b, (id - pp.b0) % pp.gx_b, (id - pp.b0) / pp.gx_b, lds, gn_tab);
 }
 
+// ---------------------------------------------------------------------------
+// Balanced tiles for products whose 64 x 64 tiles do not divide evenly over
+// the compute units: 64 tokens x 80 W rows per workgroup, so that a
+// 2048 x 640 product is 256 tiles, one per compute unit (64 x 64 tiles give
+// 320: a quarter of the compute units would run two, and the launch lasts
+// as long as they do).  Y^T = W X^T with 16x16x32 MFMAs (a lane ends up with
+// four consecutive outputs of one token).  Eight wavefronts: wavefront w
+// takes tokens 16 (w % 4) .. + 15 and k-step w / 4 of the two 32-long steps
+// of every 64-long k-tile, for all 80 rows (five 16-row blocks); the two
+// k-steps' sums meet through LDS at the end.  X and W go straight into LDS
+// in the row layout and swizzle of the kernel above: 18 pieces of 1 KB per
+// k-tile (8 of X, 10 of W), piece j loaded by wavefront j % 8.
+// ---------------------------------------------------------------------------
+constexpr int G80_BM = 64, G80_BN = 80, G80_NS = 4;
+constexpr int G80_STAGE = (G80_BM + G80_BN) * DBK * 2;  // 18 KB
+
+__device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__global__ __launch_bounds__(512) void gemm80_kernel(GemmParams p) {
+    __shared__ __attribute__((aligned(16))) char lds[G80_NS * G80_STAGE];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int tb = wave & 3, kg = wave >> 2;
+    const int m0 = blockIdx.x * G80_BM, n0 = blockIdx.y * G80_BN;
+    const int nk = p.K / DBK;
+
+    // Pieces j = wave + 8 q of this wavefront: LDS rows 8 j .. 8 j + 7 of the
+    // stage (X rows 0..63, then W rows 64..143); lane: row 8 j + lane / 8,
+    // chunk (lane % 8) ^ ((row / 2) % 8).
+    const char* src[3];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+        const int j = wave + 8 * q;
+        const int row = 8 * j + (lane >> 3);
+        const int c = (lane & 7) ^ ((row >> 1) & 7);
+        if (row < G80_BM) {
+            const int m = min(m0 + row, p.M - 1);
+            src[q] = (const char*)p.a + ((int64_t)m * p.lda + 8 * c) * 2;
+        } else {
+            src[q] = (const char*)p.w + ((int64_t)(n0 + min(row, G80_BM + G80_BN - 1) - G80_BM) * p.K + 8 * c) * 2;
+        }
+    }
+    const bool three = wave < 2;  // 18 pieces: wavefronts 0 and 1 load a third
+    auto issue = [&](int kt, int stage) {
+        char* st = lds + stage * G80_STAGE;
+        const int koff = kt * DBK * 2;
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+            __builtin_amdgcn_global_load_lds((gvoid)(src[q] + koff), (lvoid)(st + (wave + 8 * q) * 1024), 16, 0, 0);
+        if (three)
+            __builtin_amdgcn_global_load_lds((gvoid)(src[2] + koff), (lvoid)(st + (wave + 16) * 1024), 16, 0, 0);
+    };
+
+    // Operands of k-step kg: X rows 16 tb + lane % 16 (B, tokens), W rows
+    // 64 + 16 fb + lane % 16 (A, W rows), k-octet lane / 16 of the step.
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
+    const int chunk = 4 * kg + (lane >> 4);
+    const int xr = 16 * tb + (lane & 15);
+    const uint32_t xoff = xr * 128 + ((chunk ^ ((xr >> 1) & 7)) << 4);
+    uint32_t woff[5];
+#pragma unroll
+    for (int fb = 0; fb < 5; ++fb) {
+        const int r = G80_BM + 16 * fb + (lane & 15);
+        woff[fb] = r * 128 + ((chunk ^ ((r >> 1) & 7)) << 4);
+    }
+    f32x4 acc[5];
+#pragma unroll
+    for (int fb = 0; fb < 5; ++fb) acc[fb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+    for (int st = 0; st < G80_NS - 1; ++st)
+        if (st < nk) issue(st, st);
+    for (int kt = 0; kt < nk; ++kt) {
+        const int later = min(nk - 1 - kt, G80_NS - 2);
+        if (three)
+            wait_tiles_after<3, G80_NS - 2>(later);
+        else
+            wait_tiles_after<2, G80_NS - 2>(later);
+        __builtin_amdgcn_s_barrier();  // everyone's pieces of tile kt landed; the stage of tile kt-1 is free
+        if (kt + G80_NS - 1 < nk) issue(kt + G80_NS - 1, (kt + G80_NS - 1) % G80_NS);
+        const uint32_t sb = lds0 + (kt % G80_NS) * G80_STAGE;
+        u32x4 x = lds_b128<0>(sb + xoff);
+        u32x4 w0 = lds_b128<0>(sb + woff[0]);
+        u32x4 w1 = lds_b128<0>(sb + woff[1]);
+        u32x4 w2 = lds_b128<0>(sb + woff[2]);
+        u32x4 w3 = lds_b128<0>(sb + woff[3]);
+        u32x4 w4 = lds_b128<0>(sb + woff[4]);
+        asm volatile("s_waitcnt lgkmcnt(4)" : "+v"(x), "+v"(w0));
+        acc[0] = mfma16x16x32(__builtin_bit_cast(bf16x8, w0), __builtin_bit_cast(bf16x8, x), acc[0]);
+        asm volatile("s_waitcnt lgkmcnt(3)" : "+v"(w1));
+        acc[1] = mfma16x16x32(__builtin_bit_cast(bf16x8, w1), __builtin_bit_cast(bf16x8, x), acc[1]);
+        asm volatile("s_waitcnt lgkmcnt(2)" : "+v"(w2));
+        acc[2] = mfma16x16x32(__builtin_bit_cast(bf16x8, w2), __builtin_bit_cast(bf16x8, x), acc[2]);
+        asm volatile("s_waitcnt lgkmcnt(1)" : "+v"(w3));
+        acc[3] = mfma16x16x32(__builtin_bit_cast(bf16x8, w3), __builtin_bit_cast(bf16x8, x), acc[3]);
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(w4));
+        acc[4] = mfma16x16x32(__builtin_bit_cast(bf16x8, w4), __builtin_bit_cast(bf16x8, x), acc[4]);
+    }
+
+    // The two k-steps' sums: wavefront (tb, 0) finishes blocks 0-2, (tb, 1)
+    // blocks 3-4; each hands the other its sums of the other's blocks.
+    __syncthreads();  // every wavefront is past its last LDS operand read
+    float* red = (float*)lds;  // [tb][block][lane] x 4 floats (20 KB)
+    auto owned = [&](int fb) { return kg == 0 ? fb < 3 : fb >= 3; };
+#pragma unroll
+    for (int fb = 0; fb < 5; ++fb)
+        if (!owned(fb)) *(f32x4*)(red + ((tb * 5 + fb) * 64 + lane) * 4) = acc[fb];
+    __syncthreads();
+#pragma unroll
+    for (int fb = 0; fb < 5; ++fb)
+        if (owned(fb)) acc[fb] += *(const f32x4*)(red + ((tb * 5 + fb) * 64 + lane) * 4);
+
+    // Epilogue: token m0 + 16 tb + lane % 16, W rows n0 + 16 fb + 4 (lane / 16)
+    // + 0..3; all bias and residual loads before the first store (the output
+    // may be the residual buffer itself).
+    const int m = m0 + 16 * tb + (lane & 15);
+    const int mc = min(m, p.M - 1);
+    // The epilogue keeps the order of the 64 x 64 kernel: (acc + bias) + residual.
+    f32x4 bias_v[5], res_v[5];
+#pragma unroll
+    for (int fb = 0; fb < 5; ++fb) {
+        bias_v[fb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        res_v[fb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (!owned(fb)) continue;
+        const int n = n0 + 16 * fb + 4 * (lane >> 4);
+        if (p.bias != nullptr) {
+            const bf16x4 bv = *(const bf16x4*)(p.bias + n);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) bias_v[fb][e] = bf16_to_f32(bv[e]);
+        }
+        if (p.resid != nullptr) {
+            if (p.resid_f32) {
+                res_v[fb] = *(const f32x4*)((const float*)p.resid + (int64_t)mc * p.ldr + n);
+            } else {
+                const bf16x4 rb = *(const bf16x4*)((const bf16*)p.resid + (int64_t)mc * p.ldr + n);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) res_v[fb][e] = bf16_to_f32(rb[e]);
+            }
+        }
+    }
+    if (m >= p.M) return;
+#pragma unroll
+    for (int fb = 0; fb < 5; ++fb) {
+        if (!owned(fb)) continue;
+        const int n = n0 + 16 * fb + 4 * (lane >> 4);
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = (acc[fb][e] + bias_v[fb][e]) + res_v[fb][e];
+        if (p.out_f32) {
+            *(f32x4*)((float*)p.out[0] + (int64_t)m * p.ldo + n) = f32x4{v[0], v[1], v[2], v[3]};
+        } else {
+            const bf16x4 o = {f32_to_bf16(v[0]), f32_to_bf16(v[1]), f32_to_bf16(v[2]), f32_to_bf16(v[3])};
+            *(bf16x4*)((bf16*)p.out[0] + (int64_t)m * p.ldo + n) = o;
+        }
+        if (p.out_bf16 != nullptr) {
+            const bf16x4 o = {f32_to_bf16(v[0]), f32_to_bf16(v[1]), f32_to_bf16(v[2]), f32_to_bf16(v[3])};
+            *(bf16x4*)((bf16*)p.out_bf16 + (int64_t)m * p.ldo + n) = o;
+        }
+    }
+}
+
 template <int BM, int BN, int NS, bool GEGLU>
 hipError_t launch_dma(const GemmParams& p, hipStream_t s) {
     const int bn_out = GEGLU ? BN / 2 : BN;
@@ -847,7 +1011,7 @@ size_t gemm_split_ws_bytes(int M, int N, int K, bool conv) {
 namespace {
 
 // The kernel a product runs on.
-enum GemmKind { GK_DMA_128, GK_DMA_64, GK_DMA_GEGLU, GK_REG_22, GK_REG_12, GK_REG_11 };
+enum GemmKind { GK_DMA_128, GK_DMA_64, GK_G80, GK_DMA_GEGLU, GK_REG_22, GK_REG_12, GK_REG_11 };
 
 // Validates p, picks its kernel, and sets the fields of a split or
 // XCD-ordered launch.
@@ -926,6 +1090,18 @@ hipError_t plan_gemm(GemmParams& p, hipStream_t s, GemmKind& kind) {
             // 128x128 tiles only with at least two per compute unit; else 64x64
             // tiles at three stages (48 KB of LDS: three workgroups per compute
             // unit), measured faster at M = 2048 for every N from 640 to 1920.
+            // Balanced 64 x 80 tiles when the 64 x 64 ones would give some
+            // compute units a second tile while the 80-row tiles fit one per
+            // compute unit and fill at least three quarters of them (a
+            // 2048 x 640 product: 256 tiles instead of 320).
+            const int64_t mt64 = (p.M + 63) / 64;
+            const int64_t t80 = p.N % 80 == 0 ? mt64 * (p.N / 80) : 0;
+            if (p.a_mode == 0 && p.conv_W == 0 && p.w_seg_rows == 0 && p.seg_stride == 0 && p.bias2 == nullptr &&
+                p.seg >= p.N && t80 > 0 && t80 <= dl.cus && 4 * t80 >= 3 * (int64_t)dl.cus &&
+                mt64 * (p.N / 64) > dl.cus) {
+                kind = GK_G80;
+                return hipSuccess;
+            }
             const int64_t mt128 = (p.M + 127) / 128;
             if (p.a_mode == 0 && p.N % 128 == 0 && mt128 * (p.N / 128) >= 2 * (int64_t)dl.cus) {
                 map_xcd(128, 128);
@@ -957,6 +1133,9 @@ hipError_t launch_planned(const GemmParams& p, GemmKind kind, hipStream_t s) {
     switch (kind) {
         case GK_DMA_128: return launch_dma<128, 128, 3, false>(p, s);
         case GK_DMA_64: return launch_dma<64, 64, 3, false>(p, s);
+        case GK_G80:
+            gemm80_kernel<<<dim3((unsigned)((p.M + G80_BM - 1) / G80_BM), (unsigned)(p.N / G80_BN)), 512, 0, s>>>(p);
+            return hipGetLastError();
         case GK_DMA_GEGLU: return launch_dma<64, 128, 2, true>(p, s);
         case GK_REG_22: return launch_shape<2, 2>(p, s);
         case GK_REG_12: return launch_shape<1, 2>(p, s);
