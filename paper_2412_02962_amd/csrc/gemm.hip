@@ -737,17 +737,19 @@ __global__ __launch_bounds__(256) void gemm_dma_pair_kernel(GemmPair pp) {
 // of every 64-long k-tile, for all 80 rows (five 16-row blocks); the two
 // k-steps' sums meet through LDS at the end.  X and W go straight into LDS
 // in the row layout and swizzle of the kernel above: 18 pieces of 1 KB per
-// k-tile (8 of X, 10 of W), piece j loaded by wavefront j % 8.
+// k-tile (8 of X, 10 of W), piece j loaded by wavefront j % 8; NS stages
+// (4 with one tile per compute unit, 2 when several share one).
 // ---------------------------------------------------------------------------
-constexpr int G80_BM = 64, G80_BN = 80, G80_NS = 4;
+constexpr int G80_BM = 64, G80_BN = 80;
 constexpr int G80_STAGE = (G80_BM + G80_BN) * DBK * 2;  // 18 KB
 
 __device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+template <int NS>
 __global__ __launch_bounds__(512) void gemm80_kernel(GemmParams p) {
-    __shared__ __attribute__((aligned(16))) char lds[G80_NS * G80_STAGE];
+    __shared__ __attribute__((aligned(16))) char lds[NS * G80_STAGE];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -799,17 +801,17 @@ __global__ __launch_bounds__(512) void gemm80_kernel(GemmParams p) {
     for (int fb = 0; fb < 5; ++fb) acc[fb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
 #pragma unroll
-    for (int st = 0; st < G80_NS - 1; ++st)
+    for (int st = 0; st < NS - 1; ++st)
         if (st < nk) issue(st, st);
     for (int kt = 0; kt < nk; ++kt) {
-        const int later = min(nk - 1 - kt, G80_NS - 2);
+        const int later = min(nk - 1 - kt, NS - 2);
         if (three)
-            wait_tiles_after<3, G80_NS - 2>(later);
+            wait_tiles_after<3, NS - 2>(later);
         else
-            wait_tiles_after<2, G80_NS - 2>(later);
+            wait_tiles_after<2, NS - 2>(later);
         __builtin_amdgcn_s_barrier();  // everyone's pieces of tile kt landed; the stage of tile kt-1 is free
-        if (kt + G80_NS - 1 < nk) issue(kt + G80_NS - 1, (kt + G80_NS - 1) % G80_NS);
-        const uint32_t sb = lds0 + (kt % G80_NS) * G80_STAGE;
+        if (kt + NS - 1 < nk) issue(kt + NS - 1, (kt + NS - 1) % NS);
+        const uint32_t sb = lds0 + (kt % NS) * G80_STAGE;
         u32x4 x = lds_b128<0>(sb + xoff);
         u32x4 w0 = lds_b128<0>(sb + woff[0]);
         u32x4 w1 = lds_b128<0>(sb + woff[1]);
@@ -870,6 +872,7 @@ __global__ __launch_bounds__(512) void gemm80_kernel(GemmParams p) {
         }
     }
     if (m >= p.M) return;
+    const int sg = n0 / p.seg;  // output segment of the whole tile (80 divides the segment width)
 #pragma unroll
     for (int fb = 0; fb < 5; ++fb) {
         if (!owned(fb)) continue;
@@ -877,15 +880,156 @@ __global__ __launch_bounds__(512) void gemm80_kernel(GemmParams p) {
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = (acc[fb][e] + bias_v[fb][e]) + res_v[fb][e];
+        const int ns = n - sg * p.seg;
         if (p.out_f32) {
-            *(f32x4*)((float*)p.out[0] + (int64_t)m * p.ldo + n) = f32x4{v[0], v[1], v[2], v[3]};
+            *(f32x4*)((float*)p.out[sg] + (int64_t)m * p.ldo + ns) = f32x4{v[0], v[1], v[2], v[3]};
         } else {
             const bf16x4 o = {f32_to_bf16(v[0]), f32_to_bf16(v[1]), f32_to_bf16(v[2]), f32_to_bf16(v[3])};
-            *(bf16x4*)((bf16*)p.out[0] + (int64_t)m * p.ldo + n) = o;
+            *(bf16x4*)((bf16*)p.out[sg] + (int64_t)m * p.ldo + ns) = o;
         }
         if (p.out_bf16 != nullptr) {
             const bf16x4 o = {f32_to_bf16(v[0]), f32_to_bf16(v[1]), f32_to_bf16(v[2]), f32_to_bf16(v[3])};
             *(bf16x4*)((bf16*)p.out_bf16 + (int64_t)m * p.ldo + n) = o;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// GEGLU on balanced tiles: 128 tokens x 160 outputs (their 160 value rows
+// and 160 gate rows of W) per workgroup, so that the 2048 x 2560 product of
+// the block is 256 tiles, one per compute unit, fetching half the bytes of
+// the 64-token tiles.  16x16x32 MFMAs, Y^T = W X^T; eight wavefronts:
+// wavefront w takes tokens 32 (w % 4) .. + 31 (two 16-token blocks) and
+// outputs 80 (w / 4) .. + 79 (five 16-row blocks) of both the value and the
+// gate rows, so every lane holds the value and the gate of the same outputs.
+// LDS stage: X rows 0..127, value rows 128..287, gate rows 288..447 (448 rows
+// of 128 bytes, the swizzle above), two stages (112 KB); 56 direct-load
+// pieces per k-tile, seven per wavefront.
+// ---------------------------------------------------------------------------
+constexpr int GG_BM = 128, GG_BN = 160, GG_NS = 2;
+constexpr int GG_ROWS = GG_BM + 2 * GG_BN;
+constexpr int GG_STAGE = GG_ROWS * DBK * 2;  // 56 KB
+constexpr int GG_PT = GG_ROWS / 8 / 8;        // pieces per wavefront per k-tile
+
+__global__ __launch_bounds__(512) void geglu160_kernel(GemmParams p) {
+    __shared__ __attribute__((aligned(16))) char lds[GG_NS * GG_STAGE];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int tb = wave & 3, vg = wave >> 2;
+    const int m0 = blockIdx.x * GG_BM, n0 = blockIdx.y * GG_BN;
+    const int nk = p.K / DBK;
+
+    const char* src[GG_PT];
+#pragma unroll
+    for (int q = 0; q < GG_PT; ++q) {
+        const int row = 8 * (wave + 8 * q) + (lane >> 3);
+        const int c = (lane & 7) ^ ((row >> 1) & 7);
+        int64_t grow;
+        const __bf16* base;
+        if (row < GG_BM) {
+            base = (const __bf16*)p.a;
+            grow = (int64_t)min(m0 + row, p.M - 1) * p.lda;
+        } else {
+            base = p.w;
+            const int r = row - GG_BM;
+            grow = (int64_t)(r < GG_BN ? n0 + r : p.F + n0 + (r - GG_BN)) * p.K;
+        }
+        src[q] = (const char*)(base + grow + 8 * c);
+    }
+    auto issue = [&](int kt, int stage) {
+        char* st = lds + stage * GG_STAGE;
+        const int koff = kt * DBK * 2;
+#pragma unroll
+        for (int q = 0; q < GG_PT; ++q)
+            __builtin_amdgcn_global_load_lds((gvoid)(src[q] + koff), (lvoid)(st + (wave + 8 * q) * 1024), 16, 0, 0);
+    };
+
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
+    // Row offsets (chunk added per k-step): X blocks j, value and gate blocks fb.
+    uint32_t xrow[2], vrow[5], grow_[5];
+    int xsw[2], vsw[5], gsw[5];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int r = 32 * tb + 16 * j + (lane & 15);
+        xrow[j] = r * 128;
+        xsw[j] = (r >> 1) & 7;
+    }
+#pragma unroll
+    for (int fb = 0; fb < 5; ++fb) {
+        const int rv = GG_BM + 80 * vg + 16 * fb + (lane & 15);
+        const int rg = rv + GG_BN;
+        vrow[fb] = rv * 128;
+        vsw[fb] = (rv >> 1) & 7;
+        grow_[fb] = rg * 128;
+        gsw[fb] = (rg >> 1) & 7;
+    }
+    f32x4 accv[2][5], accg[2][5];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int fb = 0; fb < 5; ++fb) accv[j][fb] = accg[j][fb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    issue(0, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+        __builtin_amdgcn_s_barrier();  // everyone's pieces of tile kt landed; the stage of tile kt-1 is free
+        if (kt + 1 < nk) issue(kt + 1, (kt + 1) % GG_NS);
+        const uint32_t sb = lds0 + (kt % GG_NS) * GG_STAGE;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const int chunk = 4 * ks + (lane >> 4);
+            u32x4 x[2], v[5], g[5];
+#pragma unroll
+            for (int j = 0; j < 2; ++j) x[j] = lds_b128<0>(sb + xrow[j] + ((chunk ^ xsw[j]) << 4));
+#pragma unroll
+            for (int fb = 0; fb < 5; ++fb) {
+                v[fb] = lds_b128<0>(sb + vrow[fb] + ((chunk ^ vsw[fb]) << 4));
+                g[fb] = lds_b128<0>(sb + grow_[fb] + ((chunk ^ gsw[fb]) << 4));
+            }
+            asm volatile("s_waitcnt lgkmcnt(0)"
+                         : "+v"(x[0]), "+v"(x[1]), "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]),
+                           "+v"(g[0]), "+v"(g[1]), "+v"(g[2]), "+v"(g[3]), "+v"(g[4]));
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+                for (int fb = 0; fb < 5; ++fb) {
+                    accv[j][fb] = mfma16x16x32(__builtin_bit_cast(bf16x8, v[fb]), __builtin_bit_cast(bf16x8, x[j]),
+                                               accv[j][fb]);
+                    accg[j][fb] = mfma16x16x32(__builtin_bit_cast(bf16x8, g[fb]), __builtin_bit_cast(bf16x8, x[j]),
+                                               accg[j][fb]);
+                }
+        }
+    }
+
+    // Epilogue: token m0 + 32 tb + 16 j + lane % 16, outputs n0 + 80 vg + 16 fb
+    // + 4 (lane / 16) + 0..3: (value + bias) * GELU(gate + gate bias).
+#pragma unroll
+    for (int fb = 0; fb < 5; ++fb) {
+        const int n = n0 + 80 * vg + 16 * fb + 4 * (lane >> 4);
+        float bv[4] = {0.f, 0.f, 0.f, 0.f}, bg[4] = {0.f, 0.f, 0.f, 0.f};
+        if (p.bias != nullptr) {
+            const bf16x4 b1 = *(const bf16x4*)(p.bias + n);
+            const bf16x4 b2 = *(const bf16x4*)(p.bias + p.F + n);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                bv[e] = bf16_to_f32(b1[e]);
+                bg[e] = bf16_to_f32(b2[e]);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int m = m0 + 32 * tb + 16 * j + (lane & 15);
+            if (m >= p.M) continue;
+            float o[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e] = (accv[j][fb][e] + bv[e]) * gelu_erf(accg[j][fb][e] + bg[e]);
+            if (p.out_f32) {
+                *(f32x4*)((float*)p.out[0] + (int64_t)m * p.ldo + n) = f32x4{o[0], o[1], o[2], o[3]};
+            } else {
+                const bf16x4 ob = {f32_to_bf16(o[0]), f32_to_bf16(o[1]), f32_to_bf16(o[2]), f32_to_bf16(o[3])};
+                *(bf16x4*)((bf16*)p.out[0] + (int64_t)m * p.ldo + n) = ob;
+            }
         }
     }
 }
@@ -1011,7 +1155,7 @@ size_t gemm_split_ws_bytes(int M, int N, int K, bool conv) {
 namespace {
 
 // The kernel a product runs on.
-enum GemmKind { GK_DMA_128, GK_DMA_64, GK_G80, GK_DMA_GEGLU, GK_REG_22, GK_REG_12, GK_REG_11 };
+enum GemmKind { GK_DMA_128, GK_DMA_64, GK_G80, GK_DMA_GEGLU, GK_GEGLU160, GK_REG_22, GK_REG_12, GK_REG_11 };
 
 // Validates p, picks its kernel, and sets the fields of a split or
 // XCD-ordered launch.
@@ -1078,6 +1222,16 @@ hipError_t plan_gemm(GemmParams& p, hipStream_t s, GemmKind& kind) {
             }
         }
         if (p.geglu) {
+            // 128 tokens x 160 outputs when those tiles fit one per compute
+            // unit and fill at least three quarters of them (the block's
+            // 2048 x 2560 product: 256 tiles).
+            const int64_t t160 = p.N % 160 == 0 ? (int64_t)((p.M + 127) / 128) * (p.N / 160) : 0;
+            if (t160 > 0 && t160 <= dl.cus && 4 * t160 >= 3 * (int64_t)dl.cus && p.resid == nullptr &&
+                p.out_bf16 == nullptr && p.bias2 == nullptr && p.seg >= p.N && p.w_seg_rows == 0 &&
+                p.seg_stride == 0 && 2 * (int64_t)p.N < 4 * (int64_t)p.M) {
+                kind = GK_GEGLU160;
+                return hipSuccess;
+            }
             // value/gate pairs on 64-token tiles at two stages (48 KB of LDS: three
             // workgroups per compute unit): 25.3 us against 28.7 for 128-token
             // tiles and 35.2 for three stages at the 2048 x 2 x 2560 x 640 shape
@@ -1090,14 +1244,16 @@ hipError_t plan_gemm(GemmParams& p, hipStream_t s, GemmKind& kind) {
             // 128x128 tiles only with at least two per compute unit; else 64x64
             // tiles at three stages (48 KB of LDS: three workgroups per compute
             // unit), measured faster at M = 2048 for every N from 640 to 1920.
-            // Balanced 64 x 80 tiles when the 64 x 64 ones would give some
-            // compute units a second tile while the 80-row tiles fit one per
-            // compute unit and fill at least three quarters of them (a
-            // 2048 x 640 product: 256 tiles instead of 320).
+            // Balanced 64 x 80 tiles when the 64 x 64 ones would divide
+            // unevenly over the compute units while the 80-row tiles come to
+            // at most three per compute unit and fill at least three quarters
+            // of them: a 2048 x 640 product is 256 tiles instead of 320, the
+            // 2048 x 1920 Q/K/V product 768 instead of 960.  Not when W has
+            // four times X's rows: those keep the XCD-contiguous 64 x 64 tiles.
             const int64_t mt64 = (p.M + 63) / 64;
             const int64_t t80 = p.N % 80 == 0 ? mt64 * (p.N / 80) : 0;
             if (p.a_mode == 0 && p.conv_W == 0 && p.w_seg_rows == 0 && p.seg_stride == 0 && p.bias2 == nullptr &&
-                p.seg >= p.N && t80 > 0 && t80 <= dl.cus && 4 * t80 >= 3 * (int64_t)dl.cus &&
+                (p.seg >= p.N || (p.seg % 80 == 0 && p.N / p.seg <= 3)) && p.N < 4 * (int64_t)p.M && t80 > 0 && t80 <= 3 * dl.cus && 4 * t80 >= 3 * (int64_t)dl.cus &&
                 mt64 * (p.N / 64) > dl.cus) {
                 kind = GK_G80;
                 return hipSuccess;
@@ -1134,9 +1290,16 @@ hipError_t launch_planned(const GemmParams& p, GemmKind kind, hipStream_t s) {
         case GK_DMA_128: return launch_dma<128, 128, 3, false>(p, s);
         case GK_DMA_64: return launch_dma<64, 64, 3, false>(p, s);
         case GK_G80:
-            gemm80_kernel<<<dim3((unsigned)((p.M + G80_BM - 1) / G80_BM), (unsigned)(p.N / G80_BN)), 512, 0, s>>>(p);
+            // two stages (36 KB of LDS) when the tiles need several per compute unit
+            if ((int64_t)((p.M + 63) / 64) * (p.N / 80) > device_layout(s).cus)
+                gemm80_kernel<2><<<dim3((unsigned)((p.M + G80_BM - 1) / G80_BM), (unsigned)(p.N / G80_BN)), 512, 0, s>>>(p);
+            else
+                gemm80_kernel<4><<<dim3((unsigned)((p.M + G80_BM - 1) / G80_BM), (unsigned)(p.N / G80_BN)), 512, 0, s>>>(p);
             return hipGetLastError();
         case GK_DMA_GEGLU: return launch_dma<64, 128, 2, true>(p, s);
+        case GK_GEGLU160:
+            geglu160_kernel<<<dim3((unsigned)((p.M + GG_BM - 1) / GG_BM), (unsigned)(p.N / GG_BN)), 512, 0, s>>>(p);
+            return hipGetLastError();
         case GK_REG_22: return launch_shape<2, 2>(p, s);
         case GK_REG_12: return launch_shape<1, 2>(p, s);
         default: return launch_shape<1, 1>(p, s);
