@@ -379,14 +379,26 @@ int run_module(const pcpp_geom_t* g, const ModuleW& mw, const pcpp_basic_block_w
         lp.gamma = (const __bf16*)w.ln2_gamma;
         lp.beta = (const __bf16*)w.ln2_beta;
         PCPP_CHECK(launch_layer_norm(lp, s));
-        PCPP_CHECK(gemm_s(gemm(t16, C, false, w.attn2_q_w, nullptr, rows, C, C, q16, C, false)));
         if (!L.kv_grouped) {
             GemmParams kv = gemm(text, text_dim, false, w.attn2_kv_w, nullptr, B * T, 2 * C, text_dim, k2, C, false);
             kv.out[1] = v2;
             kv.seg = C;
             PCPP_CHECK(gemm_s(kv));
         }
-        {
+        // Q of the cross-attention; with at most GEMM_XA_MAXT text tokens and
+        // whole 64-token tiles, the Q product's workgroups go on to the
+        // attention itself (one head per tile), else it runs separately.
+        if (T <= GEMM_XA_MAXT && N % 64 == 0) {
+            GemmParams xq = gemm(t16, C, false, w.attn2_q_w, nullptr, rows, C, C, a16, C, false);
+            xq.a_mode = 2;
+            xq.xa_k = k2;
+            xq.xa_v = v2;
+            xq.xa_T = T;
+            xq.xa_N = N;
+            xq.xa_ldkv = C;
+            PCPP_CHECK(gemm_s(xq));
+        } else {
+            PCPP_CHECK(gemm_s(gemm(t16, C, false, w.attn2_q_w, nullptr, rows, C, C, q16, C, false)));
             AttnParams ap = cross_attn_params(g, r, q16, a16, k2, v2, T);
             PCPP_CHECK(launch_attention_bf16(ap, attn_ws, L.attn_ws_bytes, s));
         }

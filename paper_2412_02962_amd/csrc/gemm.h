@@ -68,10 +68,21 @@ struct GemmParams {
     const __bf16* gn_gamma = nullptr;
     const __bf16* gn_beta = nullptr;
     int32_t gn_N = 0;
+    // a_mode 2: cross-attention in the epilogue (bf16 X and output, N = heads
+    // x 64, xa_N tokens per image, a multiple of 64; no bias, residual or
+    // copy): the product is the attention's Q, and the workgroup of token
+    // tile m and head h goes on to softmax(Q K_h^T / 8) V_h over the xa_T <=
+    // 96 keys of its image (xa_k, xa_v: [B][xa_T][xa_ldkv], head h at columns
+    // 64 h) and writes that to out[0] in Q's place.
+    const __bf16* xa_k = nullptr;
+    const __bf16* xa_v = nullptr;
+    int32_t xa_T = 0, xa_N = 0;
+    int64_t xa_ldkv = 0;
     // Set by launch_gemm for a split launch.
     int32_t splitk = 1, n_xcd = 1, tpx = 0, n_tiles = 0;
 };
 constexpr int GEMM_GN_MAXC = 1280;
+constexpr int GEMM_XA_MAXT = 96;  // keys of the cross-attention epilogue
 
 // Bytes of split-K workspace a GEMM of this shape can use (0: it runs
 // unsplit); counters come first, at most GEMM_SPLIT_COUNTERS ints.  conv:

@@ -279,6 +279,8 @@ __device__ __forceinline__ void wait_tiles_after(int later) {
 // channel (the merge's 256 x 3 scratch shares their space), then the group
 // means and reciprocal deviations.
 constexpr int GN_TAB_FLOATS = 2 * GEMM_GN_MAXC + 2 * 256;
+// LDS floats of the cross-attention epilogue's K rows and transposed V.
+constexpr int XA_TAB_FLOATS = (GEMM_XA_MAXT * 128 + 64 * 200) / 4;
 static_assert(2 * GEMM_GN_MAXC >= 3 * 256, "the merge scratch fits the scale and shift tables");
 
 // One workgroup's tile of the product; (bx, by) is its place in the
@@ -292,7 +294,8 @@ template <int BM, int BN, int NS, bool GEGLU, bool CONV, int AMODE>
 __device__ __forceinline__ void gemm_dma_body(const GemmParams& p, const int bx, const int by, char* lds,
                                               float* gn_tab) {
     constexpr bool AGN = AMODE == 1;
-    static_assert(!AGN || (BM == 64 && BN == 64 && !GEGLU && !CONV), "GroupNorm staging: plain 64 x 64 tiles");
+    constexpr bool XATT = AMODE == 2;
+    static_assert(!(AGN || XATT) || (BM == 64 && BN == 64 && !GEGLU && !CONV), "plain 64 x 64 tiles only");
     constexpr int WMB = BM / 64;                      // 32-token blocks per wavefront
     constexpr int WNB = BN / 64;                      // 32-row W blocks per wavefront
     constexpr int XP = BM / 32;                       // 1 KB X pieces per wavefront per k-tile
@@ -474,6 +477,118 @@ __device__ __forceinline__ void gemm_dma_body(const GemmParams& p, const int bx,
         }
     };
 
+    // Cross-attention (AMODE 2).  gn_tab holds K_h as rows of 128 bytes (the
+    // operand swizzle; keys past xa_T zero) and V_h transposed, a row of
+    // 200 bytes per head dimension (keys along the row; 200 keeps the eight-
+    // byte reads of 32 dimensions on distinct banks).
+    constexpr int XA_VT_STRIDE = 200;
+    char* xa = (char*)gn_tab;
+    char* xa_vt = xa + GEMM_XA_MAXT * 128;
+    auto xatt_stage = [&]() {
+        const int img = m0 / p.xa_N;
+        const int64_t kvo = (int64_t)img * p.xa_T * p.xa_ldkv + n0;
+#pragma unroll
+        for (int it = 0; it < GEMM_XA_MAXT * 8 / 256; ++it) {
+            const int i = tid + 256 * it;
+            const int key = i >> 3, c = i & 7;
+            u32x4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
+            if (key < p.xa_T) {
+                kv = *(const u32x4*)(p.xa_k + kvo + (int64_t)key * p.xa_ldkv + 8 * c);
+                vv = *(const u32x4*)(p.xa_v + kvo + (int64_t)key * p.xa_ldkv + 8 * c);
+            }
+            *(u32x4*)(xa + key * 128 + ((c ^ ((key >> 1) & 7)) << 4)) = kv;
+            const bf16x8 v8 = __builtin_bit_cast(bf16x8, vv);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) *(bf16*)(xa_vt + (8 * c + e) * XA_VT_STRIDE + key * 2) = v8[e];
+        }
+    };
+    // After the product: Q (bf16, rows of 128 bytes) into the first stage,
+    // then wavefront (qb, dh) = (w % 2, w / 2) computes S^T = K Q^T for
+    // queries 32 qb .. + 31 over all keys (a lane holds one query), the
+    // softmax in registers (the key halves meet across lanes l and l ^ 32),
+    // and O^T = V^T P^T for head dimensions 32 dh .. + 31.  P^T feeds the
+    // matrix product straight from the S^T registers: its k-slot e of lane
+    // half h is key 16 u + 8 (e / 4) + 4 h + e % 4 of the step, and V^T is
+    // read with the same key order.
+    auto xatt_epilogue = [&]() {
+        __syncthreads();  // every operand read of the last stage is done
+        {
+            const int t = 32 * wm + col;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int chunk = 4 * wn + c;  // head dimensions 32 wn + 8 c + 4 half + 0..3
+                const bf16x4 q4 = {f32_to_bf16(acc[0][0][4 * c]), f32_to_bf16(acc[0][0][4 * c + 1]),
+                                   f32_to_bf16(acc[0][0][4 * c + 2]), f32_to_bf16(acc[0][0][4 * c + 3])};
+                *(bf16x4*)(lds + t * 128 + ((chunk ^ ((t >> 1) & 7)) << 4) + 8 * half) = q4;
+            }
+        }
+        __syncthreads();
+        const int qb = wave & 1, dh = wave >> 1;
+        f32x16 sc[3];
+#pragma unroll
+        for (int kb = 0; kb < 3; ++kb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) sc[kb][r] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            const int ch = 2 * ks + half;
+            const int qr = 32 * qb + col;
+            const u32x4 qv = *(const u32x4*)(lds + qr * 128 + ((ch ^ ((qr >> 1) & 7)) << 4));
+#pragma unroll
+            for (int kb = 0; kb < 3; ++kb) {
+                const int kr = 32 * kb + col;
+                const u32x4 kv = *(const u32x4*)(xa + kr * 128 + ((ch ^ ((kr >> 1) & 7)) << 4));
+                sc[kb] = mfma32x32x16(__builtin_bit_cast(bf16x8, kv), __builtin_bit_cast(bf16x8, qv), sc[kb]);
+            }
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 3; ++kb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int key = 32 * kb + 8 * (r >> 2) + 4 * half + (r & 3);
+                if (key >= p.xa_T) sc[kb][r] = -INFINITY;
+                mx = fmaxf(mx, sc[kb][r]);
+            }
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float cl = 1.4426950408889634f * 0.125f;  // log2(e) / sqrt(64)
+        const float mcl = mx * cl;
+        float l = 0.f;
+        bf16x8 pb[3][2];
+#pragma unroll
+        for (int kb = 0; kb < 3; ++kb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const bf16 pr = f32_to_bf16(fast_exp2(__builtin_fmaf(sc[kb][r], cl, -mcl)));
+                pb[kb][r >> 3][r & 7] = pr;
+                l += bf16_to_f32(pr);  // the weights the products use
+            }
+        l += __shfl_xor(l, 32);
+        f32x16 o;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[r] = 0.f;
+        const int d = 32 * dh + col;
+#pragma unroll
+        for (int kb = 0; kb < 3; ++kb)
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int k0 = 32 * kb + 16 * u + 4 * half;
+                const u32x2 a0 = *(const u32x2*)(xa_vt + d * XA_VT_STRIDE + k0 * 2);
+                const u32x2 a1 = *(const u32x2*)(xa_vt + d * XA_VT_STRIDE + (k0 + 8) * 2);
+                const u32x4 av = {a0[0], a0[1], a1[0], a1[1]};
+                o = mfma32x32x16(__builtin_bit_cast(bf16x8, av), pb[kb][u], o);
+            }
+        const int m = m0 + 32 * qb + col;
+        if (m >= p.M) return;
+        const float inv = 1.f / l;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const bf16x4 ov = {f32_to_bf16(o[4 * q] * inv), f32_to_bf16(o[4 * q + 1] * inv),
+                               f32_to_bf16(o[4 * q + 2] * inv), f32_to_bf16(o[4 * q + 3] * inv)};
+            *(bf16x4*)((bf16*)p.out[0] + (int64_t)m * p.ldo + n0 + 32 * dh + 8 * q + 4 * half) = ov;
+        }
+    };
+
     if constexpr (AGN) {
         // X arrives with the direct loads like W; each lane then rewrites in
         // place the 16-byte pieces its own loads brought (so its own wait
@@ -544,6 +659,7 @@ __device__ __forceinline__ void gemm_dma_body(const GemmParams& p, const int bx,
 #pragma unroll
         for (int s = 0; s < NS - 1; ++s)
             if (kt0 + s < kt1) issue(kt0 + s, s);
+        if constexpr (XATT) xatt_stage();  // its loads wait behind the first k-tiles'
         for (int kt = kt0; kt < kt1; ++kt) {
             // k-tiles issued after kt so far: min(kt1 - 1 - kt, NS - 2), PT loads each
             wait_tiles_after<PT, NS - 2>(min(kt1 - 1 - kt, NS - 2));
@@ -551,6 +667,11 @@ __device__ __forceinline__ void gemm_dma_body(const GemmParams& p, const int bx,
             if (kt + NS - 1 < kt1) issue(kt + NS - 1, (kt - kt0 + NS - 1) % NS);
             mfma_tile(lds0 + ((kt - kt0) % NS) * STAGE);
         }
+    }
+
+    if constexpr (XATT) {
+        xatt_epilogue();
+        return;
     }
 
     // Split K: every piece stores its partial tile (fp32, 1 KB per wavefront
@@ -701,7 +822,7 @@ __device__ __forceinline__ void gemm_dma_body(const GemmParams& p, const int bx,
 template <int BM, int BN, int NS, bool GEGLU, bool CONV, int AMODE>
 __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmParams p) {
     __shared__ __attribute__((aligned(16))) char lds[NS * (BM + BN) * DBK * 2];
-    __shared__ __attribute__((aligned(16))) float gn_tab[AMODE == 1 ? GN_TAB_FLOATS : 4];
+    __shared__ __attribute__((aligned(16))) float gn_tab[AMODE == 1 ? GN_TAB_FLOATS : AMODE == 2 ? XA_TAB_FLOATS : 4];
     gemm_dma_body<BM, BN, NS, GEGLU, CONV, AMODE>(p, blockIdx.x, blockIdx.y, lds, gn_tab);
 }
 
@@ -1044,6 +1165,10 @@ hipError_t launch_dma(const GemmParams& p, hipStream_t s) {
             gemm_dma_kernel<BM, BN, NS, false, false, 1><<<grid, 256, 0, s>>>(p);
             return hipGetLastError();
         }
+        if (p.a_mode == 2) {
+            gemm_dma_kernel<BM, BN, NS, false, false, 2><<<grid, 256, 0, s>>>(p);
+            return hipGetLastError();
+        }
     }
     if (!GEGLU && p.conv_W > 0)
         gemm_dma_kernel<BM, BN, NS, GEGLU, true, 0><<<grid, 256, 0, s>>>(p);
@@ -1161,7 +1286,14 @@ enum GemmKind { GK_DMA_128, GK_DMA_64, GK_G80, GK_DMA_GEGLU, GK_GEGLU160, GK_REG
 // XCD-ordered launch.
 hipError_t plan_gemm(GemmParams& p, hipStream_t s, GemmKind& kind) {
     if (p.conv_W > 0 && !gemm_shape_ok(p)) return hipErrorInvalidValue;
-    if (p.a_mode != 0) {  // GroupNorm staging: the 64 x 64 pipelined kernel only
+    if (p.a_mode == 2) {  // cross-attention epilogue: the 64 x 64 pipelined kernel, unsplit
+        if (p.a_f32 || p.geglu || p.conv_W > 0 || p.K % DBK != 0 || p.N % 64 != 0 || p.seg < p.N || p.out_f32 ||
+            p.resid != nullptr || p.out_bf16 != nullptr || p.bias != nullptr || p.bias2 != nullptr ||
+            p.w_seg_rows != 0 || p.seg_stride != 0 || p.xa_k == nullptr || p.xa_v == nullptr || p.xa_T < 1 ||
+            p.xa_T > GEMM_XA_MAXT || p.xa_N <= 0 || p.xa_N % 64 != 0 || p.M % p.xa_N != 0 || p.xa_ldkv < p.N ||
+            p.xa_ldkv % 8 != 0)
+            return hipErrorInvalidValue;
+    } else if (p.a_mode != 0) {  // GroupNorm staging: the 64 x 64 pipelined kernel only
         if (p.a_mode != 1 || p.a_f32 || p.geglu || p.conv_W > 0 || p.K % DBK != 0 || p.K > GEMM_GN_MAXC ||
             p.N % 64 != 0 || p.seg % 4 != 0 || p.gn_N <= 0 || p.gn_N % 64 != 0 || p.M % p.gn_N != 0 || p.gn.G < 1 ||
             p.gn.G > 256 || p.K % p.gn.G != 0 || p.gn.stats == nullptr || p.gn_gamma == nullptr ||
@@ -1210,7 +1342,7 @@ hipError_t plan_gemm(GemmParams& p, hipStream_t s, GemmKind& kind) {
     // bf16 X with K % 64 == 0: the pipelined kernel, with the largest tile
     // that still gives about a workgroup per compute unit.
     if (!p.a_f32 && p.K % DBK == 0 && p.seg % 4 == 0) {
-        if (!p.geglu && p.conv_W == 0 && p.split_ws != nullptr && p.N % 64 == 0) {
+        if (!p.geglu && p.conv_W == 0 && p.split_ws != nullptr && p.N % 64 == 0 && p.a_mode != 2) {
             const SplitPlan sp = split_plan_plain(p.M, p.N, p.K, dl);
             if (sp.splitk > 1 && p.split_ws_bytes >= sp.bytes && ((uintptr_t)p.split_ws & 15u) == 0) {
                 p.splitk = sp.splitk;
