@@ -20,7 +20,7 @@
 //             workgroups also fill the frame (neighbour edge rows or zeros)
 //             and export the band's own first and last rows.
 // LayerNorm: one wavefront per fp32 row, 16-byte loads, two passes over
-// registers, 8-byte bf16 stores.
+// registers (wavefront sums by DPP and lane swaps), 8-byte bf16 stores.
 
 #include <math.h>
 
@@ -236,6 +236,24 @@ __global__ __launch_bounds__(GN_THREADS) void gn_apply(GroupNormParams p) {
 
 constexpr int LN_MAX_VEC = 8;  // 16-byte fp32 vectors per lane: C <= 2048
 
+// Sum over the 64 lanes of a wavefront, the same bits in every lane:
+// quad permutes, the half-row and row mirrors (DPP), then the 16- and
+// 32-lane swaps; no LDS round trip.
+template <int CTRL>
+__device__ __forceinline__ float dpp_add(float v) {
+    return v + __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float wave_sum(float v) {
+    v = dpp_add<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+    v = dpp_add<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+    v = dpp_add<0x141>(v);  // row_half_mirror
+    v = dpp_add<0x140>(v);  // row_mirror
+    const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+    const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
+}
+
 template <int NV>  // 16-byte vectors per lane: C <= 256 * NV
 __global__ __launch_bounds__(256) void ln_kernel(LayerNormParams p) {
     const int row = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
@@ -243,12 +261,17 @@ __global__ __launch_bounds__(256) void ln_kernel(LayerNormParams p) {
     if (row >= p.rows) return;
     const int nv = p.C / 4;
     const f32x4* xr = (const f32x4*)(p.x + (int64_t)row * p.C);
+    // The row's loads first (all in flight together), then gamma and beta.
     f32x4 v[NV];
-    bf16x4 gm[NV], bt[NV];
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
         const int j = lane + 64 * k;
         v[k] = j < nv ? xr[j] : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    bf16x4 gm[NV], bt[NV];
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        const int j = lane + 64 * k;
         if (j < nv) {
             gm[k] = *(const bf16x4*)(p.gamma + 4 * j);
             bt[k] = *(const bf16x4*)(p.beta + 4 * j);
@@ -257,10 +280,7 @@ __global__ __launch_bounds__(256) void ln_kernel(LayerNormParams p) {
     float s = 0.f;
 #pragma unroll
     for (int k = 0; k < NV; ++k) s += (v[k][0] + v[k][1]) + (v[k][2] + v[k][3]);
-    float t = s;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) t += __shfl_xor(t, o);
-    const float mean = t / (float)p.C;
+    const float mean = wave_sum(s) / (float)p.C;
     float q = 0.f;
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
@@ -273,9 +293,7 @@ __global__ __launch_bounds__(256) void ln_kernel(LayerNormParams p) {
             }
         }
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) q += __shfl_xor(q, o);
-    const float rstd = rsqrtf(q / (float)p.C + p.eps);
+    const float rstd = rsqrtf(wave_sum(q) / (float)p.C + p.eps);
     bf16* yr = p.y + (int64_t)row * p.C;
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
