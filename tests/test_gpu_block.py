@@ -125,6 +125,40 @@ def test_block_split_k_gemms(batch):
     _check_kv(gu.to_f64(v), want_v, "v export")
 
 
+@pytest.mark.parametrize("n_text", [1, 64, 96, 97])
+def test_block_cross_attention_text_lengths(n_text):
+    """64 tokens per band: up to 96 text tokens the cross-attention runs
+    inside its Q product (keys past the text masked: 1, 64 and 96 fill one,
+    two and all three 32-key blocks), 97 goes to the separate Q product and
+    attention launch."""
+    attn = synth.AttnConfig(name="blk", H=16, W=16, n=4, i=1, p=0.25, heads=2, d=64, dtype="bf16", seed_id=58)
+    bc = synth.BlockConfig(name="blk", attn=attn, n_text=n_text, text_dim=64, ff_inner=128, gn_groups=4,
+                           seed_id=59)
+    _say("block text length", n_text)
+    inp = synth.block_inputs(bc, batch=2)
+    y, k, v = _run_block(bc, inp, 2)
+    want_y, want_k, want_v = _oracle_block(bc, inp)
+    _check(gu.to_f64(y), want_y)
+    _check_kv(gu.to_f64(k), want_k, "k export")
+
+
+def test_block_balanced_tiles_with_a_ragged_last_tile():
+    """2000 tokens of 640 channels (one band of 100 x 20): the 640-wide
+    products and Q/K/V run on 64 x 80 tiles and the GEGLU on 128 x 160 tiles,
+    each with a ragged last token tile (2000 = 31 x 64 + 16 = 15 x 128 + 80);
+    the GroupNorm and the cross-attention take their separate launches (the
+    band is not whole 64-token tiles)."""
+    attn = synth.AttnConfig(name="blk", H=100, W=20, n=1, i=0, p=0.0, heads=10, d=64, dtype="bf16", seed_id=60)
+    bc = synth.BlockConfig(name="blk", attn=attn, seed_id=61)
+    _say("block ragged balanced tiles")
+    inp = synth.block_inputs(bc)
+    y, k, v = _run_block(bc, inp, 1)
+    want_y, want_k, want_v = _oracle_block(bc, inp)
+    _check(gu.to_f64(y), want_y)
+    _check_kv(gu.to_f64(k), want_k, "k export")
+    _check_kv(gu.to_f64(v), want_v, "v export")
+
+
 def test_block_workspace_is_reusable():
     """Workspace contract: no clearing needed.  The attention's and the split
     GEMMs' counters live there (the level-2 block splits FF-out and the text
