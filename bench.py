@@ -373,6 +373,16 @@ def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
     out["group_norm_GBps"] = round(gbytes / us / 1e3, 1)
     out["group_norm_frac_hbm"] = round(gbytes / us / 1e3 / PEAK_HBM_GBS, 4)
 
+    # LayerNorm of a block's float32 stream alone (pcpp_layer_norm, 2048 x 640:
+    # fp32 rows read, bf16 rows written): algorithmic bytes 6 x 2048 x 640.
+    lx = torch.randn(cfg.n_q, cfg.C, device=dev)
+    ly = torch.empty(cfg.n_q, cfg.C, dtype=torch.bfloat16, device=dev)
+    us = graph_time_us(torch, lambda: pcpp.pcpp_layer_norm(cfg.n_q, cfg.C, 1e-5, lx, gam, bet, ly), reps, use_graph)
+    lbytes = cfg.n_q * cfg.C * (4 + 2)
+    out["layer_norm_us"] = round(us, 3)
+    out["layer_norm_GBps"] = round(lbytes / us / 1e3, 1)
+    out["layer_norm_frac_hbm"] = round(lbytes / us / 1e3 / PEAK_HBM_GBS, 4)
+
     c50 = synth.ATTN_CONFIGS["sdxl2048_l1_p50"]
     d50 = {k: to_dev(v) for k, v in synth.attention_inputs(c50).items()}
     g50 = pcpp.make_geom(c50.H, c50.W, c50.n, c50.i, c50.p, c50.heads, c50.d, 1, 0, pcpp.PCPP_DTYPE_BF16)

@@ -643,6 +643,19 @@ int pcpp_concat_channels(int64_t rows, const void* a, int32_t ca, const void* b,
  * channels % 8 == 0, <= 2560, groups <= 256 dividing channels (PCPP_ENOTSUP
  * otherwise).  The workspace needs no clearing.  Asynchronous on `stream`.
  */
+/*
+ * LayerNorm over the channel axis of float32 rows, affine, bf16 output: the
+ * normalization in front of each of the transformer block's three branches
+ * (SDXL: eps 1e-5; the block runs it internally), here on its own.  x [rows,
+ * channels] float32, y [rows, channels] bf16 (y may not overlap x),
+ * gamma/beta [channels] bf16; 1 <= rows <= 2^24; channels % 4 == 0 and
+ * <= 2048 (PCPP_ENOTSUP otherwise); eps > 0; pointers 16-byte aligned
+ * (PCPP_EINVAL).  Asynchronous on `stream`.
+ */
+int pcpp_layer_norm(int64_t rows, int32_t channels, float eps, const float* x,
+                    const void* gamma, const void* beta, void* y,
+                    void* stream);
+
 size_t pcpp_group_norm_workspace_size(int32_t batch, int32_t tokens,
                                       int32_t channels, int32_t groups);
 int pcpp_group_norm(int32_t batch, int32_t tokens, int32_t channels,

@@ -6,7 +6,8 @@
 //   pcpp_group_norm       GroupNorm (optionally with SiLU; band-local or
 //                         synchronized statistics): the U-Net's output head
 //                         before conv_out
-// Both are bandwidth-bound; the copy moves 16-byte vectors, all loads of a
+//   pcpp_layer_norm       the transformer block's LayerNorm on its own
+// All are bandwidth-bound; the copy moves 16-byte vectors, all loads of a
 // thread issued before its stores.
 
 #include <stdint.h>
@@ -79,6 +80,27 @@ PCPP_EXPORT int pcpp_concat_channels(int64_t rows, const void* a, int32_t ca, co
     concat_channels<<<(unsigned)blocks, kThreads, 0, (hipStream_t)stream>>>((bf16*)out, (const bf16*)a,
                                                                             (const bf16*)b, rows, ca, cb);
     return hipGetLastError() == hipSuccess ? PCPP_OK : PCPP_EHIP;
+}
+
+PCPP_EXPORT int pcpp_layer_norm(int64_t rows, int32_t channels, float eps, const float* x, const void* gamma,
+                                const void* beta, void* y, void* stream) {
+    if (rows < 1 || rows > ((int64_t)1 << 24) || !(eps > 0.f)) return PCPP_EINVAL;
+    if (channels < 4 || channels % 4 != 0 || channels > 2048) return PCPP_ENOTSUP;
+    const void* ptrs[] = {x, gamma, beta, y};
+    for (const void* p : ptrs)
+        if (!p || !aligned16(p)) return PCPP_EINVAL;
+    const char* xb = (const char*)x;
+    const char* yb = (const char*)y;
+    if (yb < xb + rows * channels * 4 && xb < yb + rows * channels * 2) return PCPP_EINVAL;
+    LayerNormParams lp;
+    lp.x = x;
+    lp.y = (__bf16*)y;
+    lp.gamma = (const __bf16*)gamma;
+    lp.beta = (const __bf16*)beta;
+    lp.rows = (int32_t)rows;
+    lp.C = channels;
+    lp.eps = eps;
+    return launch_layer_norm(lp, (hipStream_t)stream) == hipSuccess ? PCPP_OK : PCPP_EHIP;
 }
 
 PCPP_EXPORT size_t pcpp_group_norm_workspace_size(int32_t batch, int32_t tokens, int32_t channels, int32_t groups) {

@@ -157,6 +157,7 @@ def _load():
         "pcpp_transformer_module": (ctypes.c_int, [gp, ctypes.POINTER(pcpp_module_weights_t), vp, vp, i32, i32,
                                                    vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "pcpp_concat_channels": (ctypes.c_int, [ctypes.c_int64, vp, i32, vp, i32, vp, vp]),
+        "pcpp_layer_norm": (ctypes.c_int, [ctypes.c_int64, i32, ctypes.c_float, vp, vp, vp, vp, vp]),
         "pcpp_group_norm_workspace_size": (sz, [i32, i32, i32, i32]),
         "pcpp_group_norm": (ctypes.c_int, [i32, i32, i32, i32, ctypes.c_float, i32, vp, vp, vp, vp, i32, i32, vp, vp,
                                            vp, sz, vp]),
@@ -183,7 +184,7 @@ EXPORTED = (
     "pcpp_resnet_block_workspace_size", "pcpp_resnet_block", "pcpp_guided_step",
     "pcpp_conv3x3_workspace_size", "pcpp_conv3x3", "pcpp_conv3x3_export",
     "pcpp_transformer_module_workspace_size", "pcpp_transformer_module",
-    "pcpp_concat_channels", "pcpp_group_norm_workspace_size", "pcpp_group_norm",
+    "pcpp_concat_channels", "pcpp_layer_norm", "pcpp_group_norm_workspace_size", "pcpp_group_norm",
 )
 
 
@@ -441,6 +442,11 @@ def pcpp_transformer_module(g, w, x, text, n_text, text_dim, k_up, v_up, k_dn, v
 def pcpp_concat_channels(rows, a, ca, b, cb, out, stream=None):
     _check("pcpp_concat_channels", _lib.pcpp_concat_channels(rows, _ptr(a), ca, _ptr(b), cb, _ptr(out),
                                                               _stream(stream)))
+
+
+def pcpp_layer_norm(rows, channels, eps, x, gamma, beta, y, stream=None):
+    _check("pcpp_layer_norm", _lib.pcpp_layer_norm(rows, channels, eps, _ptr(x), _ptr(gamma), _ptr(beta), _ptr(y),
+                                                    _stream(stream)))
 
 
 def pcpp_group_norm_workspace_size(batch, tokens, channels, groups) -> int:

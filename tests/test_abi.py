@@ -201,6 +201,22 @@ def test_boundary_bytes_follow_eq1_rows():
     assert pcpp.pcpp_boundary_bytes(pcpp.make_geom(16, 8, 1, 0, 0.5, 2)) == 0        # one band: no neighbour
 
 
+def test_layer_norm_validation_errors_before_launch():
+    from paper_2412_02962_amd import pcpp
+    lib = pcpp.lib()
+    ln = lambda rows, C, eps, x, g, b, y: lib.pcpp_layer_norm(rows, C, eps, x, g, b, y, None)
+    A = FAKE
+    Y = FAKE + (1 << 30)
+    assert ln(0, 640, 1e-5, A, A, A, Y) == pcpp.PCPP_EINVAL                # no rows
+    assert ln((1 << 24) + 1, 640, 1e-5, A, A, A, Y) == pcpp.PCPP_EINVAL    # too many rows
+    assert ln(16, 640, 0.0, A, A, A, Y) == pcpp.PCPP_EINVAL                # eps must be positive
+    assert ln(16, 642, 1e-5, A, A, A, Y) == pcpp.PCPP_ENOTSUP              # channels not a multiple of 4
+    assert ln(16, 4096, 1e-5, A, A, A, Y) == pcpp.PCPP_ENOTSUP             # channels beyond 2048
+    assert ln(16, 640, 1e-5, None, A, A, Y) == pcpp.PCPP_EINVAL            # missing input
+    assert ln(16, 640, 1e-5, A + 8, A, A, Y) == pcpp.PCPP_EINVAL           # misaligned input
+    assert ln(16, 640, 1e-5, A, A, A, A + 64) == pcpp.PCPP_EINVAL          # output overlaps the input
+
+
 def test_boundary_validation_errors_before_launch():
     from paper_2412_02962_amd import pcpp
     lib = pcpp.lib()

@@ -1,0 +1,133 @@
+"""GPU parity of the stand-alone norm entry points, pcpp_layer_norm and
+pcpp_group_norm, against the float64 oracle, element by element, through the
+C ABI.
+
+Each output element is one bf16 rounding (at most 2^-8 of its magnitude) of
+a float32 computation whose own error (the statistics over at most a few
+thousand values) is far below that; the bound used is
+|dy| <= 2^-8 |y| + 2^-12 rms(y).  The inputs carry a per-row (LayerNorm) or
+per-group (GroupNorm) offset of several standard deviations, so that the
+centering is exercised, and seeded random scale and shift."""
+
+import numpy as np
+import pytest
+
+import oracle
+from tests import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+def _bf16_bits(a):
+    """float64 -> bf16 bit patterns (round to nearest even), uint16."""
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(torch.bfloat16).view(torch.int16).numpy() \
+        .view(np.uint16)
+
+
+def _check(got, want, tag):
+    err = np.abs(got - want)
+    rms = float(np.sqrt(np.mean(want ** 2)))
+    bound = 2.0 ** -8 * np.abs(want) + 2.0 ** -12 * rms
+    worst = float((err / bound).max())
+    print(f"{tag}: max-abs {err.max():.3e}, worst err/bound {worst:.3f}, rms {rms:.3f}")
+    assert np.isfinite(got).all(), tag
+    assert worst <= 1.0, f"{tag}: error exceeds the bound by {worst:.2f}x"
+
+
+@pytest.mark.parametrize("rows,C", [(2048, 640), (512, 1280), (77, 64), (1, 2048), (300, 324)])
+def test_layer_norm_matches_oracle(rows, C):
+    import torch
+    from paper_2412_02962_amd import pcpp
+    _say("layer norm", rows, C)
+    rng = np.random.default_rng(1000 + C + rows)
+    x = (rng.standard_normal((rows, C)) * 2.0 + rng.uniform(-6, 6, (rows, 1))).astype(np.float32)
+    gamma = oracle.from_bf16_bits(_bf16_bits(1.0 + 0.3 * rng.standard_normal(C)))
+    beta = oracle.from_bf16_bits(_bf16_bits(0.2 * rng.standard_normal(C)))
+    xd = torch.from_numpy(x).to(gu.DEV)
+    gd = gu.to_dev(_bf16_bits(gamma), "bf16")
+    bd = gu.to_dev(_bf16_bits(beta), "bf16")
+    y = torch.empty(rows, C, dtype=torch.bfloat16, device=gu.DEV)
+    pcpp.pcpp_layer_norm(rows, C, 1e-5, xd, gd, bd, y)
+    torch.cuda.synchronize()
+    want = oracle.layer_norm(x.astype(np.float64), gamma, beta, 1e-5)
+    _check(gu.to_f64(y), want, f"layer norm {rows} x {C}")
+
+
+@pytest.mark.parametrize("B,N,C,G,silu,sync", [
+    (1, 2048, 640, 32, 0, False),
+    (2, 512, 1280, 32, 1, False),
+    (1, 100, 64, 8, 0, False),
+    (2, 256, 320, 32, 0, True),
+    (1, 8192, 320, 32, 1, True),
+])
+def test_group_norm_matches_oracle(B, N, C, G, silu, sync):
+    import torch
+    from paper_2412_02962_amd import pcpp
+    _say("group norm", B, N, C, G, silu, sync)
+    rng = np.random.default_rng(2000 + N + C + G)
+    off = np.repeat(rng.uniform(-4, 4, (B, 1, G)), C // G, axis=2)
+    x = oracle.from_bf16_bits(_bf16_bits(rng.standard_normal((B, N, C)) * 1.5 + off))
+    gamma = oracle.from_bf16_bits(_bf16_bits(1.0 + 0.3 * rng.standard_normal(C)))
+    beta = oracle.from_bf16_bits(_bf16_bits(0.2 * rng.standard_normal(C)))
+    xd = gu.to_dev(_bf16_bits(x), "bf16")
+    gd = gu.to_dev(_bf16_bits(gamma), "bf16")
+    bd = gu.to_dev(_bf16_bits(beta), "bf16")
+    y = torch.empty(B, N, C, dtype=torch.bfloat16, device=gu.DEV)
+    ws_bytes = pcpp.pcpp_group_norm_workspace_size(B, N, C, G)
+    ws = torch.full((ws_bytes,), 0xA5, dtype=torch.uint8, device=gu.DEV)   # needs no clearing
+    if sync:
+        # three bands; this one is band 1, the others' statistics as exchanged
+        n_bands, band = 3, 1
+        others = [oracle.from_bf16_bits(_bf16_bits(rng.standard_normal((B, N, C)) + off + 0.5 * j))
+                  for j in range(n_bands)]
+        stats = np.stack([oracle.group_stats(o, G) for o in others])           # [n, B, G, 3]
+        bands = torch.from_numpy(stats.astype(np.float32)).to(gu.DEV)
+        own = torch.empty(B, G, 3, dtype=torch.float32, device=gu.DEV)
+        pcpp.pcpp_group_norm(B, N, C, G, 1e-6, silu, xd, gd, bd, y, ws, ws_bytes, bands=bands, n_bands=n_bands,
+                             band=band, own_out=own)
+        torch.cuda.synchronize()
+        want = oracle.group_norm_synchronized(x, G, gamma, beta, stats, band, eps=1e-6)
+        own_want = oracle.group_stats(x, G)
+        got_own = own.cpu().double().numpy()
+        assert np.allclose(got_own[..., 0], own_want[..., 0])
+        assert np.allclose(got_own[..., 1], own_want[..., 1], rtol=1e-5, atol=1e-5)
+        assert np.allclose(got_own[..., 2], own_want[..., 2], rtol=1e-4)
+    else:
+        pcpp.pcpp_group_norm(B, N, C, G, 1e-6, silu, xd, gd, bd, y, ws, ws_bytes)
+        torch.cuda.synchronize()
+        want = oracle.group_norm(x, G, gamma, beta, eps=1e-6)
+    if silu:
+        want = oracle.silu(want)
+    _check(gu.to_f64(y), want, f"group norm {B} x {N} x {C} / {G}{' silu' if silu else ''}{' sync' if sync else ''}")
+
+
+def test_norm_bound_rejects_a_planted_mistake():
+    """Negative control: the LayerNorm output checked against an oracle with
+    one planted mistake (the shift dropped; the statistics of the next row)
+    must fail the bound."""
+    import torch
+    from paper_2412_02962_amd import pcpp
+    rows, C = 512, 640
+    rng = np.random.default_rng(3001)
+    x = (rng.standard_normal((rows, C)) * 2.0 + rng.uniform(-6, 6, (rows, 1))).astype(np.float32)
+    gamma = oracle.from_bf16_bits(_bf16_bits(1.0 + 0.3 * rng.standard_normal(C)))
+    beta = oracle.from_bf16_bits(_bf16_bits(0.2 * rng.standard_normal(C)))
+    y = torch.empty(rows, C, dtype=torch.bfloat16, device=gu.DEV)
+    pcpp.pcpp_layer_norm(rows, C, 1e-5, torch.from_numpy(x).to(gu.DEV), gu.to_dev(_bf16_bits(gamma), "bf16"),
+                         gu.to_dev(_bf16_bits(beta), "bf16"), y)
+    torch.cuda.synchronize()
+    got = gu.to_f64(y)
+    xd = x.astype(np.float64)
+    _check(got, oracle.layer_norm(xd, gamma, beta, 1e-5), "layer norm, right oracle")
+    no_shift = oracle.layer_norm(xd, gamma, np.zeros_like(beta), 1e-5)
+    mean = np.roll(xd.mean(axis=1, keepdims=True), -1, axis=0)
+    var = np.roll(((xd - xd.mean(axis=1, keepdims=True)) ** 2).mean(axis=1, keepdims=True), -1, axis=0)
+    next_row_stats = (xd - mean) / np.sqrt(var + 1e-5) * gamma + beta
+    for wrong, tag in ((no_shift, "shift dropped"), (next_row_stats, "next row's statistics")):
+        with pytest.raises(AssertionError):
+            _check(got, wrong, f"layer norm, {tag}")
