@@ -45,6 +45,14 @@ __host__ __device__ inline int gn_chunk_tokens(int N) { return N >= 64 * GN_CHUN
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
+// Lanes that sum one group's channel totals in gn_stats: the largest power of
+// two with G of them in the workgroup, at most a wavefront.
+__host__ __device__ inline int gn_group_lanes(int G) {
+    int t = 1;
+    while (2 * t * G <= GN_THREADS && 2 * t <= 64) t *= 2;
+    return t;
+}
+
 // Workspace of GroupNorm: [B][chunks][G] x (count, mean, M2).
 size_t gn_part_bytes(int B, int G, int chunks) { return (size_t)B * G * chunks * 3 * sizeof(float); }
 
@@ -94,11 +102,21 @@ __global__ __launch_bounds__(GN_THREADS) void gn_stats(GroupNormParams p) {
         chan_acc[2 * cp + 1] = s1;
     }
     __syncthreads();
+    // Per group: T consecutive lanes (a power of two, within one wavefront)
+    // each add every T-th channel of the group, then a fixed shuffle tree.
+    const int T = gn_group_lanes(G);
+    const int gg = tid / T, gu = tid % T;
+    auto group_sum = [&]() {
+        float v = 0.f;
+        if (gg < G)
+            for (int c = gg * cg + gu; c < (gg + 1) * cg; c += T) v += chan_acc[c];
+        for (int o = 1; o < T; o <<= 1) v += __shfl_xor(v, o);
+        return v;
+    };
     const float n_chunk = (float)nt * (float)cg;
-    for (int g = tid; g < G; g += GN_THREADS) {
-        float s = 0.f;
-        for (int c = g * cg; c < (g + 1) * cg; ++c) s += chan_acc[c];
-        g_mean[g] = s / n_chunk;
+    {
+        const float v = group_sum();
+        if (gg < G && gu == 0) g_mean[gg] = v / n_chunk;
     }
     __syncthreads();
     // Pass 2: squared deviations from the chunk mean of the channel's group.
@@ -120,13 +138,14 @@ __global__ __launch_bounds__(GN_THREADS) void gn_stats(GroupNormParams p) {
         chan_acc[2 * cp + 1] = q1;
     }
     __syncthreads();
-    for (int g = tid; g < G; g += GN_THREADS) {
-        float q = 0.f;
-        for (int c = g * cg; c < (g + 1) * cg; ++c) q += chan_acc[c];
-        float* st = p.stats + (((int64_t)b * p.chunks + ch) * G + g) * 3;
-        st[0] = n_chunk;
-        st[1] = g_mean[g];
-        st[2] = q;
+    {
+        const float q = group_sum();
+        if (gg < G && gu == 0) {
+            float* st = p.stats + (((int64_t)b * p.chunks + ch) * G + gg) * 3;
+            st[0] = n_chunk;
+            st[1] = g_mean[gg];
+            st[2] = q;
+        }
     }
 }
 
