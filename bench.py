@@ -266,9 +266,10 @@ def unet_device_inputs(torch, pcpp, synth, sp, dev, seed=7, sync_gn=True):
     return layers, weights, stale, latent, temb, text, flops
 
 
-def graph_time_us(torch, fn, K, use_graph=True):
-    """Average microseconds per call of fn: K calls captured in one HIP graph
-    and replayed (or K eager calls)."""
+def graph_time_us(torch, fn, K, use_graph=True, replays=5):
+    """Microseconds per call of fn: K calls captured in one HIP graph, the
+    graph replayed `replays` times after one untimed replay, the median replay
+    divided by K (or K eager calls)."""
     for _ in range(3):
         fn()
     torch.cuda.synchronize()
@@ -287,13 +288,16 @@ def graph_time_us(torch, fn, K, use_graph=True):
             fn()
     gr.replay()
     torch.cuda.synchronize()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    e0.record()
-    gr.replay()
-    e1.record()
-    torch.cuda.synchronize()
-    return e0.elapsed_time(e1) / K * 1e3
+    times = []
+    for _ in range(replays):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        gr.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    return sorted(times)[len(times) // 2] / K * 1e3
 
 
 def extras(torch, pcpp, synth, dev, out_l1_us, use_graph=True, reps=200):
