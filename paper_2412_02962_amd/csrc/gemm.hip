@@ -1384,8 +1384,9 @@ hipError_t plan_gemm(GemmParams& p, hipStream_t s, GemmKind& kind) {
             // four times X's rows: those keep the XCD-contiguous 64 x 64 tiles.
             const int64_t mt64 = (p.M + 63) / 64;
             const int64_t t80 = p.N % 80 == 0 ? mt64 * (p.N / 80) : 0;
-            if (p.a_mode == 0 && p.conv_W == 0 && p.w_seg_rows == 0 && p.seg_stride == 0 && p.bias2 == nullptr &&
-                (p.seg >= p.N || (p.seg % 80 == 0 && p.N / p.seg <= 3)) && p.N < 4 * (int64_t)p.M && t80 > 0 && t80 <= 3 * dl.cus && 4 * t80 >= 3 * (int64_t)dl.cus &&
+            const bool g80_form = p.a_mode == 0 && p.conv_W == 0 && p.w_seg_rows == 0 && p.seg_stride == 0 &&
+                                  p.bias2 == nullptr && (p.seg >= p.N || (p.seg % 80 == 0 && p.N / p.seg <= 3));
+            if (g80_form && p.N < 4 * (int64_t)p.M && t80 > 0 && t80 <= 3 * dl.cus && 4 * t80 >= 3 * (int64_t)dl.cus &&
                 mt64 * (p.N / 64) > dl.cus) {
                 kind = GK_G80;
                 return hipSuccess;
@@ -1421,13 +1422,15 @@ hipError_t launch_planned(const GemmParams& p, GemmKind kind, hipStream_t s) {
     switch (kind) {
         case GK_DMA_128: return launch_dma<128, 128, 3, false>(p, s);
         case GK_DMA_64: return launch_dma<64, 64, 3, false>(p, s);
-        case GK_G80:
+        case GK_G80: {
             // two stages (36 KB of LDS) when the tiles need several per compute unit
-            if ((int64_t)((p.M + 63) / 64) * (p.N / 80) > device_layout(s).cus)
-                gemm80_kernel<2><<<dim3((unsigned)((p.M + G80_BM - 1) / G80_BM), (unsigned)(p.N / G80_BN)), 512, 0, s>>>(p);
+            const dim3 grid((unsigned)((p.M + G80_BM - 1) / G80_BM), (unsigned)(p.N / G80_BN));
+            if ((int64_t)grid.x * grid.y > device_layout(s).cus)
+                gemm80_kernel<2><<<grid, 512, 0, s>>>(p);
             else
-                gemm80_kernel<4><<<dim3((unsigned)((p.M + G80_BM - 1) / G80_BM), (unsigned)(p.N / G80_BN)), 512, 0, s>>>(p);
+                gemm80_kernel<4><<<grid, 512, 0, s>>>(p);
             return hipGetLastError();
+        }
         case GK_DMA_GEGLU: return launch_dma<64, 128, 2, true>(p, s);
         case GK_GEGLU160:
             geglu160_kernel<<<dim3((unsigned)((p.M + GG_BM - 1) / GG_BM), (unsigned)(p.N / GG_BN)), 512, 0, s>>>(p);
@@ -1467,9 +1470,10 @@ hipError_t launch_gemm_pair(const GemmParams& a_in, const GemmParams& b_in, hipS
     if (e != hipSuccess) return e;
     // One launch when both run on the 64 x 64 pipelined kernel and at most
     // one of them splits K (the split region holds one product's partials);
-    // only the first may stage its X with GroupNorm.
+    // only the first may stage its X with GroupNorm, and neither carries the
+    // cross-attention epilogue.
     if (ka == GK_DMA_64 && kb == GK_DMA_64 && a.conv_W == 0 && b.conv_W == 0 && !(a.splitk > 1 && b.splitk > 1) &&
-        b.a_mode == 0) {
+        a.a_mode <= 1 && b.a_mode == 0) {
         GemmPair pp;
         pp.a = a;
         pp.b = b;
