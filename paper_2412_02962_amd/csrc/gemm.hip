@@ -1016,53 +1016,77 @@ __global__ __launch_bounds__(512) void gemm80_kernel(GemmParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// GEGLU on balanced tiles: 128 tokens x 160 outputs (their 160 value rows
-// and 160 gate rows of W) per workgroup, so that the 2048 x 2560 product of
-// the block is 256 tiles, one per compute unit, fetching half the bytes of
-// the 64-token tiles.  16x16x32 MFMAs, Y^T = W X^T; eight wavefronts:
-// wavefront w takes tokens 32 (w % 4) .. + 31 (two 16-token blocks) and
-// outputs 80 (w / 4) .. + 79 (five 16-row blocks) of both the value and the
-// gate rows, so every lane holds the value and the gate of the same outputs.
-// LDS stage: X rows 0..127, value rows 128..287, gate rows 288..447 (448 rows
-// of 128 bytes, the swizzle above), two stages (112 KB); 56 direct-load
-// pieces per k-tile, seven per wavefront.
+// GEGLU on balanced tiles: BM tokens x 160 outputs (their 160 value rows and
+// 160 gate rows of W) per workgroup, so that the block's 2048 x 2560 product
+// (BM = 128) and the level-2 512 x 5120 product (BM = 64) are 256 tiles, one
+// per compute unit.  16x16x32 MFMAs, Y^T = W X^T; eight wavefronts, each
+// holding the value and the gate of the same outputs, so the GELU product is
+// formed in registers.  BM = 128: wavefront w takes tokens 32 (w % 4) .. + 31
+// and outputs 80 (w / 4) .. + 79.  BM = 64: wavefront w takes tokens
+// 32 (w % 2) .. + 31, outputs 80 ((w / 2) % 2) .. + 79 and k-step w / 4 of
+// the two 32-long steps of each k-tile; the two k-steps' sums meet through
+// LDS at the end.  LDS stage: X rows, then value rows, then gate rows, 128
+// bytes each (the swizzle above): 448 rows (56 KB, two stages) or 384 rows
+// (48 KB, three stages); 1 KB direct-load pieces, the same number per
+// wavefront.  With tpx > 0 the tiles run in XCD-contiguous n-major order (W
+// at least four times X: a W tile is then fetched into one XCD's L2).
 // ---------------------------------------------------------------------------
-constexpr int GG_BM = 128, GG_BN = 160, GG_NS = 2;
-constexpr int GG_ROWS = GG_BM + 2 * GG_BN;
-constexpr int GG_STAGE = GG_ROWS * DBK * 2;  // 56 KB
-constexpr int GG_PT = GG_ROWS / 8 / 8;        // pieces per wavefront per k-tile
+constexpr int GG_BN = 160;
 
+template <int GBM>
+struct GegluShape {
+    static constexpr int ROWS = GBM + 2 * GG_BN;
+    static constexpr int STAGE = ROWS * DBK * 2;
+    static constexpr int NS = GBM == 128 ? 2 : 3;
+    static constexpr int PT = ROWS / 8 / 8;  // pieces per wavefront per k-tile
+    static constexpr bool KSPLIT = GBM == 64;
+};
+
+template <int GBM>
 __global__ __launch_bounds__(512) void geglu160_kernel(GemmParams p) {
-    __shared__ __attribute__((aligned(16))) char lds[GG_NS * GG_STAGE];
+    using SH = GegluShape<GBM>;
+    __shared__ __attribute__((aligned(16))) char lds[SH::NS * SH::STAGE];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int tb = wave & 3, vg = wave >> 2;
-    const int m0 = blockIdx.x * GG_BM, n0 = blockIdx.y * GG_BN;
+    const int tb = SH::KSPLIT ? (wave & 1) : (wave & 3);
+    const int vg = SH::KSPLIT ? ((wave >> 1) & 1) : (wave >> 2);
+    const int kg = SH::KSPLIT ? (wave >> 2) : 0;
+    int m_tile = blockIdx.x, n_tile = blockIdx.y;
+    if (p.tpx > 0) {  // XCD-contiguous: workgroup w on XCD w % n_xcd, n-major within an XCD
+        const int xcd = blockIdx.x % p.n_xcd;
+        const int tl = blockIdx.x / p.n_xcd;
+        const int tile = xcd * p.tpx + tl;
+        if (tl >= p.tpx || tile >= p.n_tiles) return;  // idle slot of the last XCD (uniform)
+        const int mt = (p.M + GBM - 1) / GBM;
+        n_tile = tile / mt;
+        m_tile = tile - n_tile * mt;
+    }
+    const int m0 = m_tile * GBM, n0 = n_tile * GG_BN;
     const int nk = p.K / DBK;
 
-    const char* src[GG_PT];
+    const char* src[SH::PT];
 #pragma unroll
-    for (int q = 0; q < GG_PT; ++q) {
+    for (int q = 0; q < SH::PT; ++q) {
         const int row = 8 * (wave + 8 * q) + (lane >> 3);
         const int c = (lane & 7) ^ ((row >> 1) & 7);
         int64_t grow;
         const __bf16* base;
-        if (row < GG_BM) {
+        if (row < GBM) {
             base = (const __bf16*)p.a;
             grow = (int64_t)min(m0 + row, p.M - 1) * p.lda;
         } else {
             base = p.w;
-            const int r = row - GG_BM;
+            const int r = row - GBM;
             grow = (int64_t)(r < GG_BN ? n0 + r : p.F + n0 + (r - GG_BN)) * p.K;
         }
         src[q] = (const char*)(base + grow + 8 * c);
     }
     auto issue = [&](int kt, int stage) {
-        char* st = lds + stage * GG_STAGE;
+        char* st = lds + stage * SH::STAGE;
         const int koff = kt * DBK * 2;
 #pragma unroll
-        for (int q = 0; q < GG_PT; ++q)
+        for (int q = 0; q < SH::PT; ++q)
             __builtin_amdgcn_global_load_lds((gvoid)(src[q] + koff), (lvoid)(st + (wave + 8 * q) * 1024), 16, 0, 0);
     };
 
@@ -1078,7 +1102,7 @@ __global__ __launch_bounds__(512) void geglu160_kernel(GemmParams p) {
     }
 #pragma unroll
     for (int fb = 0; fb < 5; ++fb) {
-        const int rv = GG_BM + 80 * vg + 16 * fb + (lane & 15);
+        const int rv = GBM + 80 * vg + 16 * fb + (lane & 15);
         const int rg = rv + GG_BN;
         vrow[fb] = rv * 128;
         vsw[fb] = (rv >> 1) & 7;
@@ -1091,36 +1115,70 @@ __global__ __launch_bounds__(512) void geglu160_kernel(GemmParams p) {
 #pragma unroll
         for (int fb = 0; fb < 5; ++fb) accv[j][fb] = accg[j][fb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    issue(0, 0);
-    for (int kt = 0; kt < nk; ++kt) {
-        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-        __builtin_amdgcn_s_barrier();  // everyone's pieces of tile kt landed; the stage of tile kt-1 is free
-        if (kt + 1 < nk) issue(kt + 1, (kt + 1) % GG_NS);
-        const uint32_t sb = lds0 + (kt % GG_NS) * GG_STAGE;
+    // The MFMAs of k-step ks of the stage at sb.
+    auto kstep = [&](uint32_t sb, int ks) {
+        const int chunk = 4 * ks + (lane >> 4);
+        u32x4 x[2], v[5], g[5];
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            const int chunk = 4 * ks + (lane >> 4);
-            u32x4 x[2], v[5], g[5];
+        for (int j = 0; j < 2; ++j) x[j] = lds_b128<0>(sb + xrow[j] + ((chunk ^ xsw[j]) << 4));
 #pragma unroll
-            for (int j = 0; j < 2; ++j) x[j] = lds_b128<0>(sb + xrow[j] + ((chunk ^ xsw[j]) << 4));
+        for (int fb = 0; fb < 5; ++fb) {
+            v[fb] = lds_b128<0>(sb + vrow[fb] + ((chunk ^ vsw[fb]) << 4));
+            g[fb] = lds_b128<0>(sb + grow_[fb] + ((chunk ^ gsw[fb]) << 4));
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(x[0]), "+v"(x[1]), "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]),
+                       "+v"(g[0]), "+v"(g[1]), "+v"(g[2]), "+v"(g[3]), "+v"(g[4]));
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int fb = 0; fb < 5; ++fb) {
-                v[fb] = lds_b128<0>(sb + vrow[fb] + ((chunk ^ vsw[fb]) << 4));
-                g[fb] = lds_b128<0>(sb + grow_[fb] + ((chunk ^ gsw[fb]) << 4));
+                accv[j][fb] = mfma16x16x32(__builtin_bit_cast(bf16x8, v[fb]), __builtin_bit_cast(bf16x8, x[j]),
+                                           accv[j][fb]);
+                accg[j][fb] = mfma16x16x32(__builtin_bit_cast(bf16x8, g[fb]), __builtin_bit_cast(bf16x8, x[j]),
+                                           accg[j][fb]);
             }
-            asm volatile("s_waitcnt lgkmcnt(0)"
-                         : "+v"(x[0]), "+v"(x[1]), "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]),
-                           "+v"(g[0]), "+v"(g[1]), "+v"(g[2]), "+v"(g[3]), "+v"(g[4]));
+    };
+
+#pragma unroll
+    for (int st = 0; st < SH::NS - 1; ++st)
+        if (st < nk) issue(st, st);
+    for (int kt = 0; kt < nk; ++kt) {
+        wait_tiles_after<SH::PT, SH::NS - 2>(min(nk - 1 - kt, SH::NS - 2));
+        __builtin_amdgcn_s_barrier();  // everyone's pieces of tile kt landed; the stage of tile kt-1 is free
+        if (kt + SH::NS - 1 < nk) issue(kt + SH::NS - 1, (kt + SH::NS - 1) % SH::NS);
+        const uint32_t sb = lds0 + (kt % SH::NS) * SH::STAGE;
+        if constexpr (SH::KSPLIT) {
+            kstep(sb, kg);
+        } else {
+            kstep(sb, 0);
+            kstep(sb, 1);
+        }
+    }
+
+    // BM = 64: wavefront (tb, vg, 1) hands its sums to (tb, vg, 0), which
+    // finishes the outputs.
+    if constexpr (SH::KSPLIT) {
+        __syncthreads();  // every wavefront is past its last LDS operand read
+        float* red = (float*)lds + ((tb * 2 + vg) * 20) * 64 * 4;  // 20 f32x4 per lane
+        if (kg == 1) {
 #pragma unroll
             for (int j = 0; j < 2; ++j)
 #pragma unroll
                 for (int fb = 0; fb < 5; ++fb) {
-                    accv[j][fb] = mfma16x16x32(__builtin_bit_cast(bf16x8, v[fb]), __builtin_bit_cast(bf16x8, x[j]),
-                                               accv[j][fb]);
-                    accg[j][fb] = mfma16x16x32(__builtin_bit_cast(bf16x8, g[fb]), __builtin_bit_cast(bf16x8, x[j]),
-                                               accg[j][fb]);
+                    *(f32x4*)(red + ((j * 5 + fb) * 64 + lane) * 4) = accv[j][fb];
+                    *(f32x4*)(red + ((10 + j * 5 + fb) * 64 + lane) * 4) = accg[j][fb];
                 }
         }
+        __syncthreads();
+        if (kg == 1) return;
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int fb = 0; fb < 5; ++fb) {
+                accv[j][fb] += *(const f32x4*)(red + ((j * 5 + fb) * 64 + lane) * 4);
+                accg[j][fb] += *(const f32x4*)(red + ((10 + j * 5 + fb) * 64 + lane) * 4);
+            }
     }
 
     // Epilogue: token m0 + 32 tb + 16 j + lane % 16, outputs n0 + 80 vg + 16 fb
@@ -1280,7 +1338,7 @@ size_t gemm_split_ws_bytes(int M, int N, int K, bool conv) {
 namespace {
 
 // The kernel a product runs on.
-enum GemmKind { GK_DMA_128, GK_DMA_64, GK_G80, GK_DMA_GEGLU, GK_GEGLU160, GK_REG_22, GK_REG_12, GK_REG_11 };
+enum GemmKind { GK_DMA_128, GK_DMA_64, GK_G80, GK_DMA_GEGLU, GK_GEGLU160, GK_GEGLU160_64, GK_REG_22, GK_REG_12, GK_REG_11 };
 
 // Validates p, picks its kernel, and sets the fields of a split or
 // XCD-ordered launch.
@@ -1354,14 +1412,25 @@ hipError_t plan_gemm(GemmParams& p, hipStream_t s, GemmKind& kind) {
             }
         }
         if (p.geglu) {
-            // 128 tokens x 160 outputs when those tiles fit one per compute
-            // unit and fill at least three quarters of them (the block's
-            // 2048 x 2560 product: 256 tiles).
-            const int64_t t160 = p.N % 160 == 0 ? (int64_t)((p.M + 127) / 128) * (p.N / 160) : 0;
-            if (t160 > 0 && t160 <= dl.cus && 4 * t160 >= 3 * (int64_t)dl.cus && p.resid == nullptr &&
-                p.out_bf16 == nullptr && p.bias2 == nullptr && p.seg >= p.N && p.w_seg_rows == 0 &&
-                p.seg_stride == 0 && 2 * (int64_t)p.N < 4 * (int64_t)p.M) {
-                kind = GK_GEGLU160;
+            // 128 (else 64) tokens x 160 outputs when those tiles fit one per
+            // compute unit and fill at least three quarters of them (the
+            // block's 2048 x 2560 product, the level-2 512 x 5120 one: 256
+            // tiles); the 64-token tiles run XCD-contiguous when W has four
+            // times X's rows.
+            const bool gg_form = p.N % 160 == 0 && p.resid == nullptr && p.out_bf16 == nullptr &&
+                                 p.bias2 == nullptr && p.seg >= p.N && p.w_seg_rows == 0 && p.seg_stride == 0;
+            const int64_t t128 = gg_form ? (int64_t)((p.M + 127) / 128) * (p.N / 160) : 0;
+            const int64_t t64 = gg_form ? (int64_t)((p.M + 63) / 64) * (p.N / 160) : 0;
+            const bool wide_w = 2 * (int64_t)p.N >= 4 * (int64_t)p.M;
+            auto fits = [&](int64_t t) { return t > 0 && t <= dl.cus && 4 * t >= 3 * (int64_t)dl.cus; };
+            const int64_t tg = fits(t128) ? t128 : (fits(t64) ? t64 : 0);
+            if (tg > 0) {
+                if (wide_w && dl.xcd_merge && tg >= dl.n_xcd) {
+                    p.n_xcd = dl.n_xcd;
+                    p.tpx = (int)((tg + dl.n_xcd - 1) / dl.n_xcd);
+                    p.n_tiles = (int)tg;
+                }
+                kind = tg == t128 ? GK_GEGLU160 : GK_GEGLU160_64;
                 return hipSuccess;
             }
             // value/gate pairs on 64-token tiles at two stages (48 KB of LDS: three
@@ -1433,8 +1502,16 @@ hipError_t launch_planned(const GemmParams& p, GemmKind kind, hipStream_t s) {
         }
         case GK_DMA_GEGLU: return launch_dma<64, 128, 2, true>(p, s);
         case GK_GEGLU160:
-            geglu160_kernel<<<dim3((unsigned)((p.M + GG_BM - 1) / GG_BM), (unsigned)(p.N / GG_BN)), 512, 0, s>>>(p);
+        case GK_GEGLU160_64: {
+            const int bm = kind == GK_GEGLU160 ? 128 : 64;
+            const dim3 grid = p.tpx > 0 ? dim3((unsigned)(p.n_xcd * p.tpx), 1)
+                                        : dim3((unsigned)((p.M + bm - 1) / bm), (unsigned)(p.N / GG_BN));
+            if (kind == GK_GEGLU160)
+                geglu160_kernel<128><<<grid, 512, 0, s>>>(p);
+            else
+                geglu160_kernel<64><<<grid, 512, 0, s>>>(p);
             return hipGetLastError();
+        }
         case GK_REG_22: return launch_shape<2, 2>(p, s);
         case GK_REG_12: return launch_shape<1, 2>(p, s);
         default: return launch_shape<1, 1>(p, s);

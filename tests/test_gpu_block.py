@@ -159,6 +159,20 @@ def test_block_balanced_tiles_with_a_ragged_last_tile():
     _check_kv(gu.to_f64(v), want_v, "v export")
 
 
+def test_block_level2_geglu_tiles_with_a_ragged_last_tile():
+    """A level-2 band of 8 x 62 = 496 tokens of 1280 channels: the GEGLU
+    product (2 x 5120 outputs) runs on 64-token x 160-output tiles in
+    XCD-contiguous order, the last token tile ragged (496 = 7 x 64 + 48)."""
+    attn = synth.AttnConfig(name="blk", H=64, W=62, n=8, i=3, p=0.25, heads=20, d=64, dtype="bf16", seed_id=62)
+    bc = synth.BlockConfig(name="blk", attn=attn, ff_inner=5120, seed_id=63)
+    _say("block level-2 ragged GEGLU tiles")
+    inp = synth.block_inputs(bc)
+    y, k, v = _run_block(bc, inp, 1)
+    want_y, want_k, want_v = _oracle_block(bc, inp)
+    _check(gu.to_f64(y), want_y)
+    _check_kv(gu.to_f64(k), want_k, "k export")
+
+
 def test_block_workspace_is_reusable():
     """Workspace contract: no clearing needed.  The attention's and the split
     GEMMs' counters live there (the level-2 block splits FF-out and the text
