@@ -187,7 +187,15 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
     const int kv_end = p.kv.n_kv;
     const int end0 = p.kv.end0, end1 = p.kv.end1;
     const float sl2 = p.scale_log2;
-    const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
+    // (1, 1) in a register the compiler cannot see through: the row-sum dots
+    // then take it as an operand, and the first dot of a half can take the
+    // inline constant 0 as its addend instead of a register cleared by a move.
+    bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
+    {
+        uint32_t ou = __builtin_bit_cast(uint32_t, ones);
+        asm volatile("" : "+v"(ou));
+        ones = __builtin_bit_cast(bf16x2, ou);
+    }
     const int n_tiles = sc.n_tiles;
 
     const int x = blockIdx.x % sc.n_xcd;
@@ -335,9 +343,13 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
         // Mask the scores of half-tile h past the last key.
         auto mask_half = [&](int h, f32x16& sv) {
             if ((h >> 1) * KT + KT > kv_end) {
+                // (hidden from the compiler, which otherwise computes the
+                // lane's key offset before the branch, in every half-tile)
+                int hl = 4 * half;
+                asm volatile("" : "+v"(hl));
 #pragma unroll
                 for (int rr = 0; rr < 16; ++rr) {
-                    const int jk = (h >> 1) * KT + 32 * (h & 1) + 8 * (rr >> 2) + 4 * half + (rr & 3);
+                    const int jk = (h >> 1) * KT + 32 * (h & 1) + 8 * (rr >> 2) + hl + (rr & 3);
                     if (jk >= kv_end) sv[rr] = -INFINITY;
                 }
             }
@@ -374,19 +386,24 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
         auto step = [&](int h, f32x16& s_cur, f32x16& s_nxt, bf16x8 (&p_prev)[2], bf16x8 (&p_cur)[2],
                         Operands& op_cur, Operands& op_nxt, const char* nk, int nk_half, const char* nv, int nv_half) {
             SCHED_FENCE();
-            float acc0 = 0.f, acc1 = 0.f;
+            float acc0 = 0.f;
             float mneg = -m_run;
-            // probabilities of elements 2i, 2i+1 and their bf16 sum
+            // probabilities of elements 2i, 2i+1 and their bf16 sum (one chain
+            // of dots in pair order)
             auto pair = [&](int i) {
                 const float e0 = fast_exp2(fmaf(s_cur[2 * i], sl2, mneg));
                 const float e1 = fast_exp2(fmaf(s_cur[2 * i + 1], sl2, mneg));
                 const bf16x2 pk = {f32_to_bf16(e0), f32_to_bf16(e1)};
                 p_cur[i >> 2][2 * (i & 3)] = pk[0];
                 p_cur[i >> 2][2 * (i & 3) + 1] = pk[1];
-                if (i & 1)
-                    acc1 = __builtin_amdgcn_fdot2_f32_bf16(pk, ones, acc1, false);
-                else
+                if (i == 0) {
+                    // the first pair starts the chain with the inline constant 0 as addend
+                    asm("v_dot2_f32_bf16 %0, %1, %2, 0"
+                        : "=v"(acc0)
+                        : "v"(__builtin_bit_cast(uint32_t, pk)), "v"(__builtin_bit_cast(uint32_t, ones)));
+                } else {
                     acc0 = __builtin_amdgcn_fdot2_f32_bf16(pk, ones, acc0, false);
+                }
             };
             SCHED_FENCE();
             pair(0);
@@ -415,7 +432,7 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
                 if (i < 6) pair(i + 2);
                 SCHED_FENCE();
             }
-            float lt = acc0 + acc1;
+            float lt = acc0;
             if (__any(!(lt < P_LIMIT))) {
                 // Only when a lane's 16 probabilities of the half sum to 2^20
                 // or more (or to inf / NaN: the first half, where m is -inf)
@@ -435,11 +452,9 @@ __global__ __launch_bounds__(NTHREADS, WG_PER_CU) void attn_bf16_kernel(AttnPara
                 for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
                     for (int rr = 0; rr < 16; ++rr) o[mb][rr] *= alpha;
-                acc0 = 0.f;
-                acc1 = 0.f;
 #pragma unroll
                 for (int i = 0; i < 8; ++i) pair(i);
-                lt = acc0 + acc1;
+                lt = acc0;
             }
             l_run += lt;
             mask_half(h + 1, s_nxt);
