@@ -83,6 +83,58 @@ def test_attention_f32_at_workload_shape():
     gu.assert_close(cfg, got, gu.oracle_attention(cfg, inp), "f32 big")
 
 
+def _monotone_score_inputs(cfg, slope, rng):
+    """Inputs whose scores rise (slope > 0) or fall (slope < 0) along the
+    image rows of the key context: every query of head h points along one
+    unit direction u_h, and the keys of image row R are slope * R * u_h plus
+    noise, so each later row's scores exceed the earlier ones' by a fixed
+    margin.  float64 draws, returned in the stored dtype."""
+    from paper_2412_02962_amd import synth as sy
+    h_rows, W, C, d = cfg.h, cfg.W, cfg.C, cfg.d
+    u = rng.standard_normal((cfg.heads, d))
+    u /= np.linalg.norm(u, axis=1, keepdims=True)
+    u_full = u.reshape(C)
+
+    def band(j, kind):
+        x = 0.3 * rng.standard_normal((cfg.batch, h_rows * W, C))
+        if kind == "q":
+            x += 3.0 * u_full
+        elif kind == "k":
+            rows = j * h_rows + np.arange(h_rows * W) // W      # image row of each token
+            base = abs(slope) * (rows if slope > 0 else (cfg.H - 1 - rows))
+            x += base[None, :, None] * u_full[None, None, :]
+        return sy.store(x, cfg.dtype)
+
+    i = cfg.i
+    out = {"q": band(i, "q"), "k_fresh": band(i, "k"), "v_fresh": band(i, "v")}
+    for tag, j in (("up", i - 1), ("dn", i + 1)):
+        ok = 0 <= j < cfg.n
+        out["k_" + tag] = band(j, "k") if ok else None
+        out["v_" + tag] = band(j, "v") if ok else None
+    return out
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("slope", [10.0, -10.0])
+def test_running_max_rises_across_the_keys(dtype, slope):
+    """The online softmax's late rescale: with slope 10 the scores of each key
+    row exceed the row before by about 5.4 in log2 units, so within a key piece
+    the running maximum taken from its first half-tile is passed by 20 and more
+    several times (each time the maximum is raised and O and l are rescaled),
+    and the key pieces of a block end with maxima tens of log2 units apart
+    before they are merged.  With slope -10 the first keys dominate and the
+    later probabilities underflow.  Both against the float64 oracle."""
+    cfg = synth.AttnConfig(name="rise", H=32, W=64, n=4, i=1, p=0.5, heads=2, d=64, dtype=dtype, seed_id=77)
+    _say("monotone scores", dtype, slope)
+    rng = np.random.default_rng(4100 + int(slope) + (0 if dtype == "bf16" else 1))
+    inp = _monotone_score_inputs(cfg, slope, rng)
+    got = gu.to_f64(gu.run_attention(cfg, inp))
+    want = gu.oracle_attention(cfg, inp)
+    assert np.isfinite(got).all()
+    mx, mean = gu.assert_close(cfg, got, want, f"monotone {slope} {dtype}")
+    print(f"monotone scores slope {slope} {dtype}: max {mx:.2e} mean {mean:.2e}")
+
+
 def test_step_does_not_change_the_result():
     import torch
     cfg = synth.ATTN_CONFIGS["sdxl1024_l1"]
