@@ -13,8 +13,8 @@
 //   gn_apply  every workgroup first merges its image's chunk records with
 //             Chan et al.'s pairwise update in a fixed order (so all of them
 //             get the same statistics), then the bands, then applies the
-//             per-channel scale and shift to 8 tokens with 16-byte vectors
-//             (optionally SiLU).  Workgroup 0 of an image writes the band's
+//             per-channel scale and shift to 2, 4 or 8 tokens with 16-byte
+//             vectors (optionally SiLU).  Workgroup 0 of an image writes the band's
 //             own statistics.  In framed mode (the input of a 3x3
 //             convolution) it writes into [B][rows+2][W+2][C], and the
 //             workgroups also fill the frame (neighbour edge rows or zeros)
@@ -27,6 +27,7 @@
 #include "common.h"
 #include "gemm.h"
 #include "gn_merge.h"
+#include "kernels.h"
 
 namespace pcpp {
 
@@ -35,7 +36,6 @@ namespace {
 constexpr int GN_THREADS = 256;
 constexpr int GN_MAX_C = 2560;     // channels (LDS tables of gn_apply; the U-Net's widest concatenation)
 constexpr int GN_MAX_G = 256;
-constexpr int GN_TOKENS_PER_APPLY = 8;
 // Tokens per statistics workgroup: 32, or 8 when a band has fewer than
 // 2048 tokens (so that it still gives about 64 or more workgroups per image
 // while the apply merges few chunk records).
@@ -149,6 +149,7 @@ __global__ __launch_bounds__(GN_THREADS) void gn_stats(GroupNormParams p) {
     }
 }
 
+template <int TPW>  // tokens per workgroup
 __global__ __launch_bounds__(GN_THREADS) void gn_apply(GroupNormParams p) {
     __shared__ float sc[GN_MAX_C];
     __shared__ float sh[GN_MAX_C];
@@ -157,12 +158,12 @@ __global__ __launch_bounds__(GN_THREADS) void gn_apply(GroupNormParams p) {
     const int b = blockIdx.y;
     const int tid = threadIdx.x;
     const int C = p.C, G = p.G, cg = C / G;
-    const int tok0 = blockIdx.x * GN_TOKENS_PER_APPLY;
-    const int ntok = min(GN_TOKENS_PER_APPLY, p.N - tok0);
+    const int tok0 = blockIdx.x * TPW;
+    const int ntok = min(TPW, p.N - tok0);
     const int vpr = C / 8;  // 16-byte vectors per token row
     const int64_t base = ((int64_t)b * p.N + tok0) * C;
     // The tile's vectors are loaded first, the statistics merged meanwhile.
-    constexpr int VPT = GN_TOKENS_PER_APPLY * GN_MAX_C / 8 / GN_THREADS;
+    constexpr int VPT = (TPW * GN_MAX_C / 8 + GN_THREADS - 1) / GN_THREADS;
     bf16x8 xv[VPT];
 #pragma unroll
     for (int k = 0; k < VPT; ++k) {
@@ -371,7 +372,21 @@ hipError_t launch_group_norm_stats(GroupNormParams& p, hipStream_t s) {
 hipError_t launch_group_norm(GroupNormParams p, hipStream_t s) {
     const hipError_t e = launch_group_norm_stats(p, s);
     if (e != hipSuccess) return e;
-    gn_apply<<<dim3((p.N + GN_TOKENS_PER_APPLY - 1) / GN_TOKENS_PER_APPLY, p.B), GN_THREADS, 0, s>>>(p);
+    // Tokens per apply workgroup: the most of 8, 4 and 2 that still give four
+    // workgroups per compute unit over the images (each workgroup merges the
+    // statistics records itself, so larger tiles where there are enough of
+    // them).  2048 x 640 and 512 x 1280: 2 tokens (the ResNets 2-5 us faster
+    // than with 8); 8192 x 320: 8.
+    const int cus = device_layout(s).cus;
+    int tpw = 8;
+    while (tpw > 2 && (int64_t)((p.N + tpw - 1) / tpw) * p.B < 4 * (int64_t)cus) tpw /= 2;
+    const dim3 grid((unsigned)((p.N + tpw - 1) / tpw), (unsigned)p.B);
+    if (tpw == 8)
+        gn_apply<8><<<grid, GN_THREADS, 0, s>>>(p);
+    else if (tpw == 4)
+        gn_apply<4><<<grid, GN_THREADS, 0, s>>>(p);
+    else
+        gn_apply<2><<<grid, GN_THREADS, 0, s>>>(p);
     return hipGetLastError();
 }
 
