@@ -59,11 +59,14 @@ def test_layer_norm_matches_oracle(rows, C):
 
 
 @pytest.mark.parametrize("B,N,C,G,silu,sync", [
-    (1, 2048, 640, 32, 0, False),
+    (1, 2048, 640, 32, 0, False),    # 2 tokens per apply workgroup
     (2, 512, 1280, 32, 1, False),
     (1, 100, 64, 8, 0, False),
     (2, 256, 320, 32, 0, True),
-    (1, 8192, 320, 32, 1, True),
+    (1, 8192, 320, 32, 1, True),     # 8 tokens per apply workgroup
+    (2, 2048, 640, 32, 0, False),    # 4 tokens per apply workgroup
+    (1, 4098, 320, 32, 1, False),    # 4 tokens, a ragged last workgroup of 2
+    (1, 8199, 64, 8, 0, True),       # 8 tokens, a ragged last workgroup of 7
 ])
 def test_group_norm_matches_oracle(B, N, C, G, silu, sync):
     import torch
