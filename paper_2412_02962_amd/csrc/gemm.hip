@@ -1299,8 +1299,10 @@ SplitPlan split_plan(int M, int N, int K, const DeviceLayout& d) {
 // compute units (one workgroup per compute unit and the rest idle): about
 // kSplitTarget workgroups per compute unit, each piece at least
 // kSplitMinTiles k-tiles long.  Measured at 512 x 1280 (2048 px level 2):
-// K = 5120 in 3 pieces 21.4 us against 25.8 unsplit; K = 1280 in 2 pieces
-// of 10 k-tiles 10.6 against 9.4, hence the minimum length.  A deeper LDS
+// K = 5120 in 3 pieces 21.4 us against 25.8 unsplit (4 or 5 pieces, from a
+// target of 3 or 4 workgroups per compute unit: the level-2 block 4-8 us
+// slower); K = 1280 in 2 pieces of 10 k-tiles 10.6 against 9.4, hence the
+// minimum length.  A deeper LDS
 // ring (4, 6 or 8 stages) for the unsplit small launches gained nothing.
 constexpr int kSplitTarget = 2;
 constexpr int kSplitMinTiles = 16;
